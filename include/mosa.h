@@ -1,0 +1,157 @@
+/*
+ * mosa.h -- C ABI of the MI355X (gfx950) Mixture of Sparse Attention layer.
+ *
+ * The layer (paper, Section 2.2 and Eq. 3): every MoSA head h scores all T
+ * tokens of a sequence with a sigmoid router r = sigma(X W^r_h), keeps its k
+ * highest-scoring tokens I (expert-choice TopK, chosen independently for each
+ * batch element), computes Q, K, V only for those tokens, runs attention
+ * among them under the index-aware causal mask M_ij = 0 iff I_i >= I_j
+ * (Eq. 1), scales output row i by r_{I_i}, projects it with W^O_h and adds it
+ * back at position I_i of the T-long output.  The layer output is the sum
+ * over heads.  Optional dense heads (the hybrid layer of the "Hybridization"
+ * paragraph, standard causal heads of Eq. 2) are added to the same output.
+ *
+ * Conventions shared by every entry point
+ *   - All tensor pointers are DEVICE pointers, row-major, owned by the
+ *     caller.  The library allocates no memory and keeps no global state;
+ *     temporary memory comes in through `scratch`, state kept from the
+ *     forward for the backward through `saved`.
+ *   - `stream` is a hipStream_t (NULL: the default stream).  Calls only
+ *     enqueue work; errors raised while kernels execute surface at the next
+ *     synchronisation of that stream.
+ *   - Storage type (`dtype`): MOSA_BF16 or MOSA_F32 for X, dY, every weight,
+ *     Y, dX and every weight gradient.  Accumulation is always fp32.
+ *     Router logits, r and log-sum-exp values are fp32.
+ *   - Every tensor pointer must be 16-byte aligned; `saved` and `scratch`
+ *     256-byte aligned.
+ *   - Return value: MOSA_OK (0) or a negative status, see mosa_status_string.
+ *     Arguments are validated before any work is enqueued; no exception
+ *     crosses the ABI.
+ *   - Results are bitwise deterministic for identical inputs and shapes,
+ *     independent of stream and of the previous contents of scratch.
+ *
+ * Selection contract (Section 2.2 TopK, read as): the key of token t for
+ * head h is the exact value s_t = sum_c X[b,t,c] W^r[h,c] rounded once to
+ * double; the k tokens that come first under (key descending, token index
+ * ascending) are selected -- ties go to the lower index -- and I is returned
+ * in ascending order.  sigma is strictly increasing, so this is the TopK of
+ * r.  r_i = sigma(s_{I_i}) is computed in fp32 from the fp32 logit.
+ */
+#ifndef MOSA_H
+#define MOSA_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+enum {
+    MOSA_OK = 0,
+    MOSA_ERR_INVALID_ARG = -1, /* bad size, null required pointer, misalignment */
+    MOSA_ERR_UNSUPPORTED = -2, /* valid but not implemented (d_head, d_model, T range) */
+    MOSA_ERR_WORKSPACE = -3,   /* saved or scratch smaller than mosa_workspace_size */
+    MOSA_ERR_HIP = -4          /* a HIP launch or query failed */
+};
+
+typedef enum { MOSA_F32 = 0, MOSA_BF16 = 1 } mosa_dtype;
+
+/* Shape of one layer call.  Limits: batch >= 1; 1 <= seq_len <= 16384;
+ * d_model a multiple of 64; d_head 32 or 64; heads >= 0 and dense_heads >= 0
+ * with heads + dense_heads >= 1; 1 <= k <= seq_len when heads > 0
+ * (k = seq_len selects every token); causal 0 or 1. */
+typedef struct mosa_shape {
+    int32_t batch;       /* B */
+    int32_t seq_len;     /* T */
+    int32_t d_model;     /* d, the paper's h */
+    int32_t heads;       /* H, MoSA heads */
+    int32_t d_head;      /* dh, the paper's h' */
+    int32_t k;           /* tokens kept per MoSA head and batch element */
+    int32_t causal;      /* 1: M_ij = 0 iff I_i >= I_j; 0: no mask */
+    int32_t dense_heads; /* Hd, dense heads (all T tokens, r = 1) */
+    int32_t dtype;       /* mosa_dtype */
+} mosa_shape;
+
+/* Layer parameters, theta_h = (W^Q, W^K, W^V, W^O, W^r) per head (Section 2.2),
+ * in the paper's X W orientation:
+ *   Wr [H, d]; Wq, Wk, Wv [H, d, dh]; Wo [H, dh, d];
+ *   dense heads: Wq_d, Wk_d, Wv_d [Hd, d, dh]; Wo_d [Hd, dh, d] (NULL iff Hd == 0). */
+typedef struct mosa_weights {
+    const void* Wr;
+    const void* Wq;
+    const void* Wk;
+    const void* Wv;
+    const void* Wo;
+    const void* Wq_d;
+    const void* Wk_d;
+    const void* Wv_d;
+    const void* Wo_d;
+} mosa_weights;
+
+/* Weight gradients, same shapes and storage type as mosa_weights; written
+ * (not accumulated).  Dense entries NULL iff Hd == 0. */
+typedef struct mosa_grads {
+    void* dWr;
+    void* dWq;
+    void* dWk;
+    void* dWv;
+    void* dWo;
+    void* dWq_d;
+    void* dWk_d;
+    void* dWv_d;
+    void* dWo_d;
+} mosa_grads;
+
+/* Byte offsets of the tensors the forward leaves in `saved` (read-only for
+ * the caller; documented so that tests can inspect the stages):
+ *   I [B,H,k] int32 ascending; r [B,H,k] fp32; seg [B,H,nseg] int32 where
+ *   seg[b,h,j] = number of selected tokens < 64 j (nseg = ceil(T/64) + 1);
+ *   Q, K, V, A [B,H,k,dh] storage type (A before the router scaling);
+ *   lse [B,H,k] fp32 (natural-log sum of exp of the scaled scores);
+ *   the same five for the dense heads with k = T: Qd, Kd, Vd, Ad [B,Hd,T,dh],
+ *   lsed [B,Hd,T]. */
+typedef struct mosa_saved_layout {
+    size_t I, r, seg, Q, K, V, A, lse, Qd, Kd, Vd, Ad, lsed;
+    size_t total;
+} mosa_saved_layout;
+
+/* Sizes in bytes of the two caller-provided buffers for shape `s`:
+ * `saved` (written by mosa_forward, read by mosa_backward) and `scratch`
+ * (temporary; large enough for both forward and backward). */
+int mosa_workspace_size(const mosa_shape* s, size_t* saved_bytes, size_t* scratch_bytes);
+
+/* Offsets of the saved tensors (see mosa_saved_layout). */
+int mosa_saved_offsets(const mosa_shape* s, mosa_saved_layout* out);
+
+/* Forward of the layer (Section 2.2, Eq. 1-3).
+ *   X [B,T,d]; Y [B,T,d]: Y = layer(X) if accumulate == 0, Y += layer(X)
+ *   otherwise (residual stream).  Rows of Y no head selects and no dense head
+ *   covers are exactly 0 (accumulate == 0) or unchanged.
+ *   I_out [B,H,k] int32, r_out [B,H,k] fp32: optional copies of the
+ *   selection (NULL to skip).
+ *   saved / scratch: caller buffers of at least the mosa_workspace_size
+ *   sizes; `saved` must stay unmodified until the matching mosa_backward.
+ *   When H > 0, the first B*H*T*4 bytes of `scratch` hold the fp32 router
+ *   logits z [B,H,T] after the call (until scratch is reused). */
+int mosa_forward(const mosa_shape* s, const void* X, const mosa_weights* w, void* Y,
+                 int accumulate, int32_t* I_out, float* r_out, void* saved, size_t saved_bytes,
+                 void* scratch, size_t scratch_bytes, void* stream);
+
+/* Backward of the layer with the selection I held fixed (TopK is piecewise
+ * constant; the router receives its gradient through r, Section 2.2 final
+ * paragraph).  dY [B,T,d]; X and w must be the forward's; `saved` the
+ * forward's.  dX [B,T,d]: written (accumulate_dX == 0) or added to.
+ * All weight gradients in `g` are written. */
+int mosa_backward(const mosa_shape* s, const void* X, const mosa_weights* w, const void* dY,
+                  const void* saved, size_t saved_bytes, void* dX, int accumulate_dX,
+                  const mosa_grads* g, void* scratch, size_t scratch_bytes, void* stream);
+
+/* Static text for a status code (never NULL). */
+const char* mosa_status_string(int status);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* MOSA_H */

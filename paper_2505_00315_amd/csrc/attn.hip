@@ -1,0 +1,130 @@
+// Attention among the selected tokens of one head (paper Eq. 1 with the
+// index-aware mask of Section 2.2: M_ij = 0 iff I_i >= I_j).  I is ascending,
+// so the mask is the ordinary lower triangle in slot order; without the
+// causal flag every pair is allowed.  The same kernel runs the dense heads
+// (n = T).
+//
+// Flash-style, one wave per task of 16 query rows; a workgroup of 4 waves
+// runs 4 independent tasks.  Per block of 16 keys:
+//   S^T = K Q^T        MFMA K = 32 over d_head (A = K rows, B = Q rows),
+//                      the lane then holds query (lane % 16) and keys 4g+i;
+//   online softmax     row max / row sum reduced across the 4 lane groups
+//                      with two xor-shuffles;
+//   O^T += V^T P^T     MFMA K = 16 over the 16 keys: the S^T tile is already
+//                      in the K = 16 operand layout, so P never leaves the
+//                      registers.
+// Outputs A (= O / l, storage type) and lse = m + log(l) (fp32, natural log).
+#include "common.h"
+#include "kernels.h"
+
+namespace mosa {
+
+namespace {
+
+template <typename ST, int DH>
+__global__ __launch_bounds__(256) void attn_fwd_kernel(const ST* __restrict__ Q, const ST* __restrict__ K,
+                                                       const ST* __restrict__ V, int BH, int n, int causal,
+                                                       float scale, ST* __restrict__ A, float* __restrict__ lse) {
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int g = lane >> 4, c16 = lane & 15;
+    const int nqb = (n + 15) / 16;
+    const int task = blockIdx.x * 4 + wave;
+    if (task >= BH * nqb) return;
+    const int bh = task / nqb, q0 = (task % nqb) * 16;
+    const ST* Qp = Q + (size_t)bh * n * DH;
+    const ST* Kp = K + (size_t)bh * n * DH;
+    const ST* Vp = V + (size_t)bh * n * DH;
+
+    const int q = q0 + c16;  // this lane's query
+    Frag8<ST> qf[DH / 32];
+#pragma unroll
+    for (int s = 0; s < DH / 32; ++s)
+        qf[s] = q < n ? frag8_load<ST>(Qp + (size_t)q * DH + s * 32 + 8 * g) : frag8_zero<ST>();
+
+    float m_run = -__builtin_inff(), l_run = 0.f;
+    f32x4 o[DH / 16];
+#pragma unroll
+    for (int db = 0; db < DH / 16; ++db) o[db] = zero4();
+
+    const int kv_end = causal ? min(n, q0 + 16) : n;
+    for (int j0 = 0; j0 < kv_end; j0 += 16) {
+        f32x4 s = zero4();
+        const int kr = j0 + c16;
+#pragma unroll
+        for (int st = 0; st < DH / 32; ++st) {
+            const Frag8<ST> kf = kr < n ? frag8_load<ST>(Kp + (size_t)kr * DH + st * 32 + 8 * g) : frag8_zero<ST>();
+            mma8(s, kf, qf[st]);
+        }
+        float sc[4], mloc = -__builtin_inff();
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const int j = j0 + 4 * g + i;
+            const bool ok = j < n && (!causal || j <= q);
+            sc[i] = ok ? s[i] * scale : -__builtin_inff();
+            mloc = fmaxf(mloc, sc[i]);
+        }
+        mloc = fmaxf(mloc, __shfl_xor(mloc, 16, 64));
+        mloc = fmaxf(mloc, __shfl_xor(mloc, 32, 64));
+        const float m_new = fmaxf(m_run, mloc);
+        // Every query row has at least one allowed key (j = 0), so m_new is finite.
+        const float alpha = expf(m_run - m_new);
+        float p[4], lsum = 0.f;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            p[i] = expf(sc[i] - m_new);
+            lsum += p[i];
+        }
+        lsum += __shfl_xor(lsum, 16, 64);
+        lsum += __shfl_xor(lsum, 32, 64);
+        l_run = l_run * alpha + lsum;
+        m_run = m_new;
+        const Frag4<ST> pf = frag4_from<ST>(p);
+#pragma unroll
+        for (int db = 0; db < DH / 16; ++db) {
+            o[db] *= alpha;
+            float vv[4];
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const int j = j0 + 4 * g + i;
+                vv[i] = j < n ? ld1<ST>(Vp + (size_t)j * DH + db * 16 + c16) : 0.f;
+            }
+            const Frag4<ST> vf = frag4_from<ST>(vv);
+            mma4(o[db], vf, pf);
+        }
+    }
+    if (q < n) {
+        const float inv = 1.f / l_run;
+        ST* Ap = A + ((size_t)bh * n + q) * DH;
+#pragma unroll
+        for (int db = 0; db < DH / 16; ++db)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) st1<ST>(Ap + db * 16 + 4 * g + i, o[db][i] * inv);
+        if (g == 0) lse[(size_t)bh * n + q] = m_run + logf(l_run);
+    }
+}
+
+template <typename ST>
+int launch_attn_fwd_t(const ST* Q, const ST* K, const ST* V, int BH, int n, int dh, int causal, ST* A, float* lse,
+                      hipStream_t stream) {
+    const int tasks = BH * ((n + 15) / 16);
+    dim3 grid((tasks + 3) / 4), block(256);
+    const float scale = 1.0f / sqrtf((float)dh);
+    if (dh == 64)
+        hipLaunchKernelGGL((attn_fwd_kernel<ST, 64>), grid, block, 0, stream, Q, K, V, BH, n, causal, scale, A, lse);
+    else
+        hipLaunchKernelGGL((attn_fwd_kernel<ST, 32>), grid, block, 0, stream, Q, K, V, BH, n, causal, scale, A, lse);
+    return hipGetLastError() == hipSuccess ? 0 : -1;
+}
+
+}  // namespace
+
+int launch_attn_fwd(int dtype, const void* Q, const void* K, const void* V, int BH, int n, int dh, int causal,
+                    void* A, float* lse, hipStream_t stream) {
+    if (dtype == kBF16)
+        return launch_attn_fwd_t<uint16_t>((const uint16_t*)Q, (const uint16_t*)K, (const uint16_t*)V, BH, n, dh,
+                                           causal, (uint16_t*)A, lse, stream);
+    return launch_attn_fwd_t<float>((const float*)Q, (const float*)K, (const float*)V, BH, n, dh, causal, (float*)A,
+                                    lse, stream);
+}
+
+}  // namespace mosa

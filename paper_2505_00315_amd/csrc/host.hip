@@ -1,0 +1,219 @@
+// C ABI of the MoSA layer: argument validation, workspace carve-up and the
+// launch sequence of the forward and backward passes (see include/mosa.h).
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+#include "kernels.h"
+#include "mosa.h"
+
+namespace {
+
+using namespace mosa;
+
+constexpr size_t kAlign = 256;
+inline size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
+
+struct Layout {
+    mosa_saved_layout saved;
+    // forward scratch
+    size_t z, xnorm, unc_tok, unc_key, unc_sel;
+    // backward scratch
+    size_t dAt, dr, dQ, dK, dV, dz, dQd, dKd, dVd, Dd;
+    size_t scratch_total;
+};
+
+class Carver {
+  public:
+    size_t take(size_t bytes) {
+        size_t at = off_;
+        off_ = align_up(off_ + bytes);
+        return at;
+    }
+    size_t total() const { return off_; }
+
+  private:
+    size_t off_ = 0;
+};
+
+int validate_shape(const mosa_shape* s) {
+    if (!s) return MOSA_ERR_INVALID_ARG;
+    if (s->dtype != MOSA_F32 && s->dtype != MOSA_BF16) return MOSA_ERR_INVALID_ARG;
+    if (s->batch < 1 || s->seq_len < 1 || s->d_model < 1 || s->d_head < 1) return MOSA_ERR_INVALID_ARG;
+    if (s->heads < 0 || s->dense_heads < 0 || s->heads + s->dense_heads < 1) return MOSA_ERR_INVALID_ARG;
+    if (s->causal != 0 && s->causal != 1) return MOSA_ERR_INVALID_ARG;
+    if (s->heads > 0 && (s->k < 1 || s->k > s->seq_len)) return MOSA_ERR_INVALID_ARG;
+    if (s->d_head != 32 && s->d_head != 64) return MOSA_ERR_UNSUPPORTED;
+    if (s->d_model % 64 != 0) return MOSA_ERR_UNSUPPORTED;
+    if (s->seq_len > 16384) return MOSA_ERR_UNSUPPORTED;
+    // index arithmetic inside the kernels uses 32-bit row counts
+    const double rows = (double)s->batch * s->seq_len * (double)(s->heads > s->dense_heads ? s->heads : s->dense_heads);
+    if (rows > 2.0e9) return MOSA_ERR_UNSUPPORTED;
+    return MOSA_OK;
+}
+
+Layout make_layout(const mosa_shape* s) {
+    const size_t B = s->batch, T = s->seq_len, H = s->heads, Hd = s->dense_heads, dh = s->d_head;
+    const size_t k = s->heads > 0 ? (size_t)s->k : 0;
+    const size_t es = s->dtype == MOSA_BF16 ? 2 : 4;
+    const size_t nseg = (size_t)seg_count(s->seq_len);
+    Layout L;
+    Carver sv;
+    L.saved.I = sv.take(B * H * k * 4);
+    L.saved.r = sv.take(B * H * k * 4);
+    L.saved.seg = sv.take(B * H * nseg * 4);
+    L.saved.Q = sv.take(B * H * k * dh * es);
+    L.saved.K = sv.take(B * H * k * dh * es);
+    L.saved.V = sv.take(B * H * k * dh * es);
+    L.saved.A = sv.take(B * H * k * dh * es);
+    L.saved.lse = sv.take(B * H * k * 4);
+    L.saved.Qd = sv.take(B * Hd * T * dh * es);
+    L.saved.Kd = sv.take(B * Hd * T * dh * es);
+    L.saved.Vd = sv.take(B * Hd * T * dh * es);
+    L.saved.Ad = sv.take(B * Hd * T * dh * es);
+    L.saved.lsed = sv.take(B * Hd * T * 4);
+    L.saved.total = sv.total();
+
+    // forward and backward scratch share the same buffer (used at different times)
+    Carver fw;
+    L.z = fw.take(B * H * T * 4);
+    L.xnorm = fw.take(B * T * 4);
+    L.unc_tok = fw.take(B * H * T * 4);
+    L.unc_key = fw.take(B * H * T * 8);
+    L.unc_sel = fw.take(B * H * T * 4);
+    Carver bw;
+    L.dAt = bw.take(B * H * k * dh * 4);
+    L.dr = bw.take(B * H * k * 4);
+    L.dQ = bw.take(B * H * k * dh * 4);
+    L.dK = bw.take(B * H * k * dh * 4);
+    L.dV = bw.take(B * H * k * dh * 4);
+    L.dz = bw.take(B * H * k * 4);
+    L.dQd = bw.take(B * Hd * T * dh * 4);
+    L.dKd = bw.take(B * Hd * T * dh * 4);
+    L.dVd = bw.take(B * Hd * T * dh * 4);
+    L.Dd = bw.take(B * Hd * T * 4);
+    L.scratch_total = fw.total() > bw.total() ? fw.total() : bw.total();
+    return L;
+}
+
+inline bool aligned(const void* p, size_t a) { return ((uintptr_t)p % a) == 0; }
+
+int check_weights(const mosa_shape* s, const mosa_weights* w) {
+    if (!w) return MOSA_ERR_INVALID_ARG;
+    if (s->heads > 0) {
+        const void* need[5] = {w->Wr, w->Wq, w->Wk, w->Wv, w->Wo};
+        for (const void* p : need)
+            if (!p || !aligned(p, 16)) return MOSA_ERR_INVALID_ARG;
+    }
+    if (s->dense_heads > 0) {
+        const void* need[4] = {w->Wq_d, w->Wk_d, w->Wv_d, w->Wo_d};
+        for (const void* p : need)
+            if (!p || !aligned(p, 16)) return MOSA_ERR_INVALID_ARG;
+    }
+    return MOSA_OK;
+}
+
+template <typename T>
+T* at(void* base, size_t off) {
+    return reinterpret_cast<T*>(static_cast<char*>(base) + off);
+}
+template <typename T>
+const T* at(const void* base, size_t off) {
+    return reinterpret_cast<const T*>(static_cast<const char*>(base) + off);
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* mosa_status_string(int status) {
+    switch (status) {
+        case MOSA_OK: return "ok";
+        case MOSA_ERR_INVALID_ARG: return "invalid argument (size, null pointer or alignment)";
+        case MOSA_ERR_UNSUPPORTED: return "unsupported shape (d_head must be 32 or 64, d_model a multiple of 64, seq_len <= 16384)";
+        case MOSA_ERR_WORKSPACE: return "saved or scratch buffer smaller than mosa_workspace_size";
+        case MOSA_ERR_HIP: return "HIP launch failure";
+        default: return "unknown status";
+    }
+}
+
+int mosa_workspace_size(const mosa_shape* s, size_t* saved_bytes, size_t* scratch_bytes) {
+    int st = validate_shape(s);
+    if (st) return st;
+    if (!saved_bytes || !scratch_bytes) return MOSA_ERR_INVALID_ARG;
+    Layout L = make_layout(s);
+    *saved_bytes = L.saved.total;
+    *scratch_bytes = L.scratch_total;
+    return MOSA_OK;
+}
+
+int mosa_saved_offsets(const mosa_shape* s, mosa_saved_layout* out) {
+    int st = validate_shape(s);
+    if (st) return st;
+    if (!out) return MOSA_ERR_INVALID_ARG;
+    *out = make_layout(s).saved;
+    return MOSA_OK;
+}
+
+int mosa_forward(const mosa_shape* s, const void* X, const mosa_weights* w, void* Y, int accumulate,
+                 int32_t* I_out, float* r_out, void* saved, size_t saved_bytes, void* scratch, size_t scratch_bytes,
+                 void* stream_) {
+    int st = validate_shape(s);
+    if (st) return st;
+    if ((st = check_weights(s, w))) return st;
+    if (!X || !Y || !aligned(X, 16) || !aligned(Y, 16)) return MOSA_ERR_INVALID_ARG;
+    if (!saved || !scratch || !aligned(saved, kAlign) || !aligned(scratch, kAlign)) return MOSA_ERR_INVALID_ARG;
+    if ((I_out && !aligned(I_out, 4)) || (r_out && !aligned(r_out, 4))) return MOSA_ERR_INVALID_ARG;
+    const Layout L = make_layout(s);
+    if (saved_bytes < L.saved.total || scratch_bytes < L.scratch_total) return MOSA_ERR_WORKSPACE;
+
+    hipStream_t stream = static_cast<hipStream_t>(stream_);
+    const int B = s->batch, T = s->seq_len, d = s->d_model, H = s->heads, Hd = s->dense_heads, dh = s->d_head;
+    const int k = H > 0 ? s->k : 0, dt = s->dtype, causal = s->causal;
+    int32_t* I = at<int32_t>(saved, L.saved.I);
+    float* r = at<float>(saved, L.saved.r);
+    int32_t* seg = at<int32_t>(saved, L.saved.seg);
+    void* Q = at<char>(saved, L.saved.Q);
+    void* K = at<char>(saved, L.saved.K);
+    void* V = at<char>(saved, L.saved.V);
+    void* A = at<char>(saved, L.saved.A);
+    float* lse = at<float>(saved, L.saved.lse);
+    void* Qd = at<char>(saved, L.saved.Qd);
+    void* Kd = at<char>(saved, L.saved.Kd);
+    void* Vd = at<char>(saved, L.saved.Vd);
+    void* Ad = at<char>(saved, L.saved.Ad);
+    float* lsed = at<float>(saved, L.saved.lsed);
+
+    int e = 0;
+    if (H > 0) {
+        float* z = at<float>(scratch, L.z);
+        float* xnorm = at<float>(scratch, L.xnorm);
+        e |= launch_router(dt, X, w->Wr, B, T, d, H, z, xnorm, stream);
+        e |= launch_select(dt, z, xnorm, X, w->Wr, B, T, d, H, k, I, r, seg, at<int32_t>(scratch, L.unc_tok),
+                           at<double>(scratch, L.unc_key), at<int32_t>(scratch, L.unc_sel), stream);
+        e |= launch_qkv(dt, X, I, w->Wq, w->Wk, w->Wv, B, T, d, H, dh, k, Q, K, V, stream);
+        e |= launch_attn_fwd(dt, Q, K, V, B * H, k, dh, causal, A, lse, stream);
+    }
+    if (Hd > 0) {
+        e |= launch_qkv(dt, X, nullptr, w->Wq_d, w->Wk_d, w->Wv_d, B, T, d, Hd, dh, T, Qd, Kd, Vd, stream);
+        e |= launch_attn_fwd(dt, Qd, Kd, Vd, B * Hd, T, dh, causal, Ad, lsed, stream);
+    }
+    e |= launch_out_scatter(dt, B, T, d, dh, H, k, I, r, seg, A, w->Wo, Hd, Ad, w->Wo_d, Y, accumulate, stream);
+    if (H > 0 && I_out)
+        e |= hipMemcpyAsync(I_out, I, (size_t)B * H * k * 4, hipMemcpyDeviceToDevice, stream) != hipSuccess;
+    if (H > 0 && r_out)
+        e |= hipMemcpyAsync(r_out, r, (size_t)B * H * k * 4, hipMemcpyDeviceToDevice, stream) != hipSuccess;
+    return e ? MOSA_ERR_HIP : MOSA_OK;
+}
+
+int mosa_backward(const mosa_shape* s, const void* X, const mosa_weights* w, const void* dY, const void* saved,
+                  size_t saved_bytes, void* dX, int accumulate_dX, const mosa_grads* g, void* scratch,
+                  size_t scratch_bytes, void* stream_) {
+    int st = validate_shape(s);
+    if (st) return st;
+    (void)X; (void)w; (void)dY; (void)saved; (void)saved_bytes; (void)dX; (void)accumulate_dX; (void)g;
+    (void)scratch; (void)scratch_bytes; (void)stream_;
+    return MOSA_ERR_UNSUPPORTED;
+}
+
+}  // extern "C"

@@ -1,0 +1,121 @@
+// Router logits z = X W^r^T for every MoSA head (paper Section 2.2: the
+// router of head h is a vector W^r_h in R^d and scores token t by X_t . W^r_h;
+// sigma is applied where the score is used).
+//
+// One workgroup (4 waves) owns 32 consecutive tokens of the flattened [B*T]
+// token axis and up to 256 heads.  X is read from HBM once; W^r (H x d) is
+// small and served from L2.  The contraction runs on MFMA
+// (v_mfma_f32_16x16x32_bf16, or 16x16x4_f32 for fp32 storage) in K chunks of
+// 32.  Each chunk starts from a zero accumulator and is added to the running
+// fp32 sum with one VALU add: the error of the result then has the bound
+// that the top-k certification relies on (see select.hip):
+//   |z~ - s| <= (96 u32 + 1.01 n_c u) ||x|| ||w|| + small absolute term,
+// with u = 2^-24, u32 = 2^-23 and n_c = d / 32 chunks.
+//
+// The kernel also writes an upper bound of ||x_t||_2 for every token
+// (fp64 sum of squares, rounded up to fp32) used by that error bound.
+#include "common.h"
+#include "kernels.h"
+
+namespace mosa {
+
+namespace {
+
+constexpr int kRouterTokens = 32;
+constexpr int kRouterHeads = 256;  // heads per workgroup (grid.y covers more)
+
+// Round a non-negative double up to float.
+__device__ __forceinline__ float f32_round_up(double x) {
+    float f = (float)x;
+    if ((double)f < x) f = next_up(f);
+    return f;
+}
+
+template <typename ST>
+__global__ __launch_bounds__(256) void router_kernel(const ST* __restrict__ X, const ST* __restrict__ Wr,
+                                                     int BT, int T, int d, int H,
+                                                     float* __restrict__ z, float* __restrict__ xnorm) {
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int g = lane >> 4, c16 = lane & 15;
+    const int tok0 = blockIdx.x * kRouterTokens;
+    const int h0 = blockIdx.y * kRouterHeads;
+    const int nhb = min(16, (H - h0 + 15) / 16);  // head blocks of 16 in this workgroup
+
+    // wave -> token block tb (16 tokens) and every other head block
+    const int tb = wave & 1;
+    const int tok = tok0 + tb * 16 + c16;  // token whose row this lane feeds as B
+    const bool tok_ok = tok < BT;
+    const ST* xrow = X + (size_t)(tok_ok ? tok : 0) * d;
+
+    f32x4 acc[8];
+#pragma unroll
+    for (int m = 0; m < 8; ++m) acc[m] = zero4();
+
+    for (int kc = 0; kc < d; kc += 32) {
+        Frag8<ST> bx = tok_ok ? frag8_load<ST>(xrow + kc + 8 * g) : frag8_zero<ST>();
+#pragma unroll
+        for (int m = 0; m < 8; ++m) {
+            const int hb = (wave >> 1) + 2 * m;
+            if (hb < nhb) {
+                const int h = h0 + hb * 16 + c16;
+                Frag8<ST> aw = (h < H) ? frag8_load<ST>(Wr + (size_t)h * d + kc + 8 * g) : frag8_zero<ST>();
+                f32x4 part = zero4();
+                mma8(part, aw, bx);
+                acc[m] += part;
+            }
+        }
+    }
+    // D[head][token]: lane holds token column c16, head rows 4g + i.
+    if (tok_ok) {
+        const int b = tok / T, t = tok % T;
+#pragma unroll
+        for (int m = 0; m < 8; ++m) {
+            const int hb = (wave >> 1) + 2 * m;
+            if (hb < nhb) {
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    const int h = h0 + hb * 16 + 4 * g + i;
+                    if (h < H) z[((size_t)b * H + h) * T + t] = acc[m][i];
+                }
+            }
+        }
+    }
+
+    // ||x_t||_2 upper bound: 8 threads per token, fp64 partial sums of squares.
+    if (blockIdx.y == 0) {
+        const int tt = threadIdx.x >> 3, part = threadIdx.x & 7;
+        const int tk = tok0 + tt;
+        double ss = 0.0;
+        if (tk < BT) {
+            const ST* row = X + (size_t)tk * d;
+            for (int c = part; c < d; c += 8) {
+                double v = (double)ld1<ST>(row + c);
+                ss += v * v;
+            }
+        }
+        ss += __shfl_xor(ss, 1, 64);
+        ss += __shfl_xor(ss, 2, 64);
+        ss += __shfl_xor(ss, 4, 64);
+        if (part == 0 && tk < BT) {
+            // fp64 rounding of <= d squares and the sqrt: far below 2^-30 relative.
+            xnorm[tk] = f32_round_up(sqrt(ss) * (1.0 + 0x1p-30));
+        }
+    }
+}
+
+}  // namespace
+
+int launch_router(int dtype, const void* X, const void* Wr, int B, int T, int d, int H, float* z,
+                  float* xnorm, hipStream_t stream) {
+    const int BT = B * T;
+    dim3 grid((BT + kRouterTokens - 1) / kRouterTokens, (H + kRouterHeads - 1) / kRouterHeads);
+    if (dtype == kBF16)
+        hipLaunchKernelGGL(router_kernel<uint16_t>, grid, dim3(256), 0, stream, (const uint16_t*)X,
+                           (const uint16_t*)Wr, BT, T, d, H, z, xnorm);
+    else
+        hipLaunchKernelGGL(router_kernel<float>, grid, dim3(256), 0, stream, (const float*)X,
+                           (const float*)Wr, BT, T, d, H, z, xnorm);
+    return hipGetLastError() == hipSuccess ? 0 : -1;
+}
+
+}  // namespace mosa

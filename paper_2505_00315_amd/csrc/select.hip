@@ -1,0 +1,308 @@
+// Certified expert-choice top-k (paper Section 2.2: each head keeps the k
+// tokens with the highest router score; Section 2.1 footnote: chosen
+// separately for every batch element).
+//
+// Contract: the selected set equals the k tokens that come first under
+// (exact logit s_t rounded once to double, descending; token index,
+// ascending), returned in ascending index order.  The router kernel gives an
+// fp32 logit z~_t with a proven bound |z~_t - s_t| <= beta_t, so every token
+// has an interval [lo_t, hi_t] that contains its key.  One workgroup per
+// (b, h) row:
+//   1. radix-select (4 passes of 8 bits over order-preserving uint32 keys, all
+//      in registers + LDS histograms) the k-th largest lo, A, and the
+//      (k+1)-th largest hi, B;
+//   2. hi_t < A  => at least k tokens certainly beat t: t is out;
+//      lo_t > B  => at most k-1 tokens can beat t: t is in;
+//      the rest (typically a handful of tokens near the threshold) is
+//      uncertain;
+//   3. for the uncertain tokens the exact key is computed with a long
+//      accumulator (exact_dot.h; lanes add integer digits with LDS atomics,
+//      which is order-independent), and the k - #in best of them under
+//      (key desc, index asc) are chosen by exact rank;
+//   4. an in-order block scan compacts the chosen tokens: I ascending,
+//      r = sigmoid(z~), and the per-64-token segment table seg.
+//
+// The error bound of z~ (router.hip): every K = 32 MFMA chunk starts from
+// zero; its result is taken to differ from the exact chunk sum by at most
+// (K+1) units in the last place of the largest term for any aligned-and-
+// truncated adder, doubled for margin, and covering the rounded fp32
+// products of the fp32 variant: 96 u32 sum|x_i w_i|.  The n_c chunk results
+// are added by sequential fp32 adds: at most 1.01 n_c u sum|chunk|.
+// sum|x_i w_i| <= ||x|| ||w|| (Cauchy-Schwarz).  Denormal flushing of inputs,
+// products or partial sums adds at most (d + n_c) 2^-126 (1 + ||x|| + ||w||).
+// The total is inflated by 2^-10 to absorb the fp64 evaluation of the bound.
+#include "common.h"
+#include "exact_dot.h"
+#include "kernels.h"
+
+namespace mosa {
+
+namespace {
+
+// Order-preserving map float -> uint32 (-0.0 is first made +0.0).
+__device__ __forceinline__ uint32_t order_key(float f) {
+    uint32_t u = __float_as_uint(f);
+    if (u == 0x80000000u) u = 0u;
+    return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+}
+
+__device__ __forceinline__ float f32_down(double x) {
+    float f = (float)x;
+    if ((double)f > x) f = next_down(f);
+    return f;
+}
+__device__ __forceinline__ float f32_up(double x) {
+    float f = (float)x;
+    if ((double)f < x) f = next_up(f);
+    return f;
+}
+
+template <typename ST> __device__ __forceinline__ void split_elem(const ST* p, uint32_t& s, uint32_t& M, int& E);
+template <> __device__ __forceinline__ void split_elem<uint16_t>(const uint16_t* p, uint32_t& s, uint32_t& M, int& E) {
+    split_bf16(*p, s, M, E);
+}
+template <> __device__ __forceinline__ void split_elem<float>(const float* p, uint32_t& s, uint32_t& M, int& E) {
+    split_f32(__float_as_uint(*p), s, M, E);
+}
+
+template <typename ST, int EPT>
+__global__ __launch_bounds__(256) void select_kernel(const float* __restrict__ z, const float* __restrict__ xnorm,
+                                                     const ST* __restrict__ X, const ST* __restrict__ Wr, int T,
+                                                     int d, int H, int k, int32_t* __restrict__ I,
+                                                     float* __restrict__ r, int32_t* __restrict__ seg, int nseg,
+                                                     int32_t* __restrict__ unc_tok, double* __restrict__ unc_key,
+                                                     int32_t* __restrict__ unc_sel) {
+    __shared__ double s_red[4];
+    __shared__ int s_scan[4];
+    __shared__ int s_histA[256], s_histB[256];
+    __shared__ int s_digA, s_remA, s_digB, s_remB;
+    __shared__ int64_t s_long[4][kLongDigits];
+
+    const int row = blockIdx.x, b = row / H, h = row % H;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const size_t rowT = (size_t)row * T;
+
+    // ||w_h||_2 (fp64) for the error bound.
+    const ST* w = Wr + (size_t)h * d;
+    double ss = 0.0;
+    for (int c = tid; c < d; c += 256) {
+        double v = (double)ld1<ST>(w + c);
+        ss += v * v;
+    }
+    ss = block256_sum(ss, s_red);
+    const double wn = sqrt(ss) * (1.0 + 0x1p-30);
+    const int nc = d / 32;
+    const double coef = (96.0 * 0x1p-23 + 1.01 * (double)nc * 0x1p-24) * (1.0 + 0x1p-10);
+    const double absterm = (double)(d + nc) * 0x1p-126 * (1.0 + 0x1p-10);
+
+    // Intervals [lo, hi] around every key, as order-preserving uint32.
+    const float* zr = z + rowT;
+    const float* xn = xnorm + (size_t)b * T;
+    const int t0 = tid * EPT;
+    uint32_t lo[EPT], hi[EPT];
+#pragma unroll
+    for (int e = 0; e < EPT; ++e) {
+        const int t = t0 + e;
+        if (t < T) {
+            const double zv = (double)zr[t], xv = (double)xn[t];
+            const double beta = coef * xv * wn + absterm * (1.0 + xv + wn);
+            lo[e] = order_key(f32_down(zv - beta));
+            hi[e] = order_key(f32_up(zv + beta));
+        } else {
+            lo[e] = 0u;  // below every real key
+            hi[e] = 0u;
+        }
+    }
+
+    const bool all = k >= T;
+    uint32_t A = 0u, Bk = 0u;
+    if (!all) {
+        uint32_t prefA = 0u, prefB = 0u;
+        int remA = k, remB = k + 1;
+        for (int pass = 0; pass < 4; ++pass) {
+            const int shift = 24 - 8 * pass;
+            const uint32_t himask = pass == 0 ? 0u : (0xffffffffu << (shift + 8));
+            s_histA[tid] = 0;
+            s_histB[tid] = 0;
+            __syncthreads();
+#pragma unroll
+            for (int e = 0; e < EPT; ++e) {
+                if (t0 + e < T) {
+                    if (((lo[e] ^ prefA) & himask) == 0u) atomicAdd(&s_histA[(lo[e] >> shift) & 255u], 1);
+                    if (((hi[e] ^ prefB) & himask) == 0u) atomicAdd(&s_histB[(hi[e] >> shift) & 255u], 1);
+                }
+            }
+            __syncthreads();
+            // thread tid looks at bin v = 255 - tid: the exclusive scan in thread
+            // order is the number of candidates in higher bins.
+            const int v = 255 - tid;
+            const int ca = s_histA[v], cb = s_histB[v];
+            int tot;
+            const int aboveA = block256_exclusive_scan(ca, s_scan, &tot);
+            const int aboveB = block256_exclusive_scan(cb, s_scan, &tot);
+            if (aboveA < remA && aboveA + ca >= remA) { s_digA = v; s_remA = remA - aboveA; }
+            if (aboveB < remB && aboveB + cb >= remB) { s_digB = v; s_remB = remB - aboveB; }
+            __syncthreads();
+            prefA |= (uint32_t)s_digA << shift;
+            remA = s_remA;
+            prefB |= (uint32_t)s_digB << shift;
+            remB = s_remB;
+            __syncthreads();
+        }
+        A = prefA;
+        Bk = prefB;
+    }
+
+    // Classify.
+    uint64_t inmask = 0ull, uncmask = 0ull;
+#pragma unroll
+    for (int e = 0; e < EPT; ++e) {
+        if (t0 + e < T) {
+            const bool in = all || lo[e] > Bk;
+            const bool out = !all && hi[e] < A;
+            if (in) inmask |= 1ull << e;
+            else if (!out) uncmask |= 1ull << e;
+        }
+    }
+    int tot_in, tot_unc;
+    (void)block256_exclusive_scan(__popcll(inmask), s_scan, &tot_in);
+    const int ubase = block256_exclusive_scan(__popcll(uncmask), s_scan, &tot_unc);
+    int need = k - tot_in;  // 0 <= need <= tot_unc when the bound holds
+    if (need < 0) need = 0;
+    if (need > tot_unc) need = tot_unc;
+    const bool resolve = need > 0 && need < tot_unc;
+
+    if (resolve) {
+        {
+            int pos = ubase;
+#pragma unroll
+            for (int e = 0; e < EPT; ++e)
+                if ((uncmask >> e) & 1ull) unc_tok[rowT + pos++] = t0 + e;
+        }
+        __syncthreads();
+        // Exact keys, one uncertain token per wave at a time.
+        for (int base = 0; base < tot_unc; base += 4) {
+            const int u = base + wave;
+            if (lane < kLongDigits) s_long[wave][lane] = 0;
+            __syncthreads();
+            if (u < tot_unc) {
+                const int t = unc_tok[rowT + u];
+                const ST* xr = X + ((size_t)b * T + t) * d;
+                for (int c = lane; c < d; c += 64) {
+                    uint32_t sx, Mx, sw, Mw;
+                    int Ex, Ew;
+                    split_elem<ST>(xr + c, sx, Mx, Ex);
+                    split_elem<ST>(w + c, sw, Mw, Ew);
+                    const ProductParts p = product_parts(sx, Mx, Ex, sw, Mw, Ew);
+                    if (!p.zero) {
+#pragma unroll
+                        for (int q = 0; q < 3; ++q) {
+                            if (p.v[q]) {
+                                const uint64_t add = p.negative ? (uint64_t)(-(int64_t)p.v[q]) : p.v[q];
+                                atomicAdd(reinterpret_cast<unsigned long long*>(&s_long[wave][p.j + q]),
+                                          (unsigned long long)add);
+                            }
+                        }
+                    }
+                }
+            }
+            __syncthreads();
+            if (u < tot_unc && lane == 0) unc_key[rowT + u] = long_accumulator_round(&s_long[wave][0]);
+            __syncthreads();
+        }
+        // Exact rank among the uncertain tokens.
+        for (int u = tid; u < tot_unc; u += 256) {
+            const double ku = unc_key[rowT + u];
+            const int tu = unc_tok[rowT + u];
+            int rank = 0;
+            for (int v = 0; v < tot_unc; ++v) {
+                const double kv = unc_key[rowT + v];
+                const int tv = unc_tok[rowT + v];
+                rank += (kv > ku) || (kv == ku && tv < tu);
+            }
+            unc_sel[rowT + u] = rank < need;
+        }
+        __syncthreads();
+    }
+
+    // Compact the chosen tokens in index order.
+    uint64_t selmask = inmask;
+    {
+        int pos = ubase;
+#pragma unroll
+        for (int e = 0; e < EPT; ++e) {
+            if ((uncmask >> e) & 1ull) {
+                const bool chosen = resolve ? (unc_sel[rowT + pos] != 0) : (need == tot_unc);
+                if (chosen) selmask |= 1ull << e;
+                ++pos;
+            }
+        }
+    }
+    int tot_sel;
+    const int sbase = block256_exclusive_scan(__popcll(selmask), s_scan, &tot_sel);
+    {
+        int pos = sbase;
+#pragma unroll
+        for (int e = 0; e < EPT; ++e) {
+            if ((selmask >> e) & 1ull) {
+                const int t = t0 + e;
+                if (pos < k) {
+                    I[(size_t)row * k + pos] = t;
+                    r[(size_t)row * k + pos] = 1.0f / (1.0f + expf(-zr[t]));
+                }
+                ++pos;
+            }
+        }
+    }
+    // Only reachable if the logit error bound were violated: keep every slot
+    // defined (token 0, r = 0) so that downstream kernels stay in bounds.
+    for (int pos = tot_sel + tid; pos < k; pos += 256) {
+        I[(size_t)row * k + pos] = 0;
+        r[(size_t)row * k + pos] = 0.f;
+    }
+    // seg[j] = number of chosen tokens < 64 j (never more than k).
+    for (int j = 0; j < nseg; ++j) {
+        const int bt = j * kSegWidth;
+        if (bt >= T) {
+            if (tid == 0) seg[(size_t)row * nseg + j] = min(tot_sel, k);
+        } else if (bt >= t0 && bt < t0 + EPT) {
+            const int off = bt - t0;
+            const uint64_t below = off == 0 ? 0ull : (selmask & ((off >= 64) ? ~0ull : ((1ull << off) - 1ull)));
+            seg[(size_t)row * nseg + j] = min(sbase + __popcll(below), k);
+        }
+    }
+}
+
+template <typename ST>
+int launch_select_t(const float* z, const float* xnorm, const ST* X, const ST* Wr, int B, int T, int d, int H,
+                    int k, int32_t* I, float* r, int32_t* seg, int32_t* unc_tok, double* unc_key,
+                    int32_t* unc_sel, hipStream_t stream) {
+    dim3 grid(B * H), block(256);
+    const int nseg = seg_count(T);
+#define MOSA_SELECT_CASE(E)                                                                               \
+    hipLaunchKernelGGL((select_kernel<ST, E>), grid, block, 0, stream, z, xnorm, X, Wr, T, d, H, k, I, r, \
+                       seg, nseg, unc_tok, unc_key, unc_sel)
+    if (T <= 256) MOSA_SELECT_CASE(1);
+    else if (T <= 512) MOSA_SELECT_CASE(2);
+    else if (T <= 1024) MOSA_SELECT_CASE(4);
+    else if (T <= 2048) MOSA_SELECT_CASE(8);
+    else if (T <= 4096) MOSA_SELECT_CASE(16);
+    else if (T <= 8192) MOSA_SELECT_CASE(32);
+    else MOSA_SELECT_CASE(64);
+#undef MOSA_SELECT_CASE
+    return hipGetLastError() == hipSuccess ? 0 : -1;
+}
+
+}  // namespace
+
+int launch_select(int dtype, const float* z, const float* xnorm, const void* X, const void* Wr, int B, int T,
+                  int d, int H, int k, int32_t* I, float* r, int32_t* seg, int32_t* unc_tok, double* unc_key,
+                  int32_t* unc_sel, hipStream_t stream) {
+    if (dtype == kBF16)
+        return launch_select_t<uint16_t>(z, xnorm, (const uint16_t*)X, (const uint16_t*)Wr, B, T, d, H, k, I, r,
+                                         seg, unc_tok, unc_key, unc_sel, stream);
+    return launch_select_t<float>(z, xnorm, (const float*)X, (const float*)Wr, B, T, d, H, k, I, r, seg, unc_tok,
+                                  unc_key, unc_sel, stream);
+}
+
+}  // namespace mosa

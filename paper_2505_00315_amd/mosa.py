@@ -1,0 +1,178 @@
+"""Python binding of libmosa.so (ctypes): argument marshalling only.
+
+Every step of the layer runs in the HIP kernels behind the C ABI declared in
+``include/mosa.h``; PyTorch provides device memory and the current stream.
+There is no fallback: if the library is not built, loading fails loudly.
+"""
+import ctypes
+import os
+
+import torch
+
+PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(PKG, "libmosa.so")
+
+MOSA_OK = 0
+MOSA_ERR_INVALID_ARG = -1
+MOSA_ERR_UNSUPPORTED = -2
+MOSA_ERR_WORKSPACE = -3
+MOSA_ERR_HIP = -4
+MOSA_F32 = 0
+MOSA_BF16 = 1
+
+SYMBOLS = ("mosa_workspace_size", "mosa_saved_offsets", "mosa_forward", "mosa_backward",
+           "mosa_status_string")
+
+WEIGHT_NAMES = ("Wr", "Wq", "Wk", "Wv", "Wo", "Wq_d", "Wk_d", "Wv_d", "Wo_d")
+GRAD_NAMES = tuple("d" + n for n in WEIGHT_NAMES)
+SAVED_NAMES = ("I", "r", "seg", "Q", "K", "V", "A", "lse", "Qd", "Kd", "Vd", "Ad", "lsed")
+
+
+class Shape(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_int32) for n in
+                ("batch", "seq_len", "d_model", "heads", "d_head", "k", "causal", "dense_heads", "dtype")]
+
+
+class Weights(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_void_p) for n in WEIGHT_NAMES]
+
+
+class Grads(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_void_p) for n in GRAD_NAMES]
+
+
+class SavedLayout(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_size_t) for n in SAVED_NAMES + ("total",)]
+
+
+class MosaError(RuntimeError):
+    def __init__(self, status, what):
+        self.status = status
+        super().__init__(f"{what}: {status_string(status)} (status {status})")
+
+
+_lib = None
+
+
+def lib():
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is missing: build it with __graft_entry__.build() "
+                               "(paper_2505_00315_amd/build.py); there is no fallback path")
+        L = ctypes.CDLL(LIB_PATH)
+        P = ctypes.POINTER
+        L.mosa_workspace_size.argtypes = [P(Shape), P(ctypes.c_size_t), P(ctypes.c_size_t)]
+        L.mosa_saved_offsets.argtypes = [P(Shape), P(SavedLayout)]
+        L.mosa_forward.argtypes = [P(Shape), ctypes.c_void_p, P(Weights), ctypes.c_void_p, ctypes.c_int,
+                                   ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_size_t,
+                                   ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p]
+        L.mosa_backward.argtypes = [P(Shape), ctypes.c_void_p, P(Weights), ctypes.c_void_p, ctypes.c_void_p,
+                                    ctypes.c_size_t, ctypes.c_void_p, ctypes.c_int, P(Grads), ctypes.c_void_p,
+                                    ctypes.c_size_t, ctypes.c_void_p]
+        L.mosa_status_string.argtypes = [ctypes.c_int]
+        L.mosa_status_string.restype = ctypes.c_char_p
+        for n in ("mosa_workspace_size", "mosa_saved_offsets", "mosa_forward", "mosa_backward"):
+            getattr(L, n).restype = ctypes.c_int
+        _lib = L
+    return _lib
+
+
+def status_string(status: int) -> str:
+    return lib().mosa_status_string(int(status)).decode()
+
+
+def _check(status, what):
+    if status != MOSA_OK:
+        raise MosaError(status, what)
+
+
+def make_shape(batch, seq_len, d_model, heads, d_head, k, causal=True, dense_heads=0, dtype="bf16"):
+    code = {"bf16": MOSA_BF16, "f32": MOSA_F32, torch.bfloat16: MOSA_BF16, torch.float32: MOSA_F32}[dtype]
+    return Shape(batch, seq_len, d_model, heads, d_head, k if heads > 0 else 0, int(bool(causal)),
+                 dense_heads, code)
+
+
+def torch_dtype(shape: Shape):
+    return torch.bfloat16 if shape.dtype == MOSA_BF16 else torch.float32
+
+
+def workspace_size(shape: Shape):
+    saved, scratch = ctypes.c_size_t(), ctypes.c_size_t()
+    _check(lib().mosa_workspace_size(ctypes.byref(shape), ctypes.byref(saved), ctypes.byref(scratch)),
+           "mosa_workspace_size")
+    return saved.value, scratch.value
+
+
+def saved_offsets(shape: Shape):
+    out = SavedLayout()
+    _check(lib().mosa_saved_offsets(ctypes.byref(shape), ctypes.byref(out)), "mosa_saved_offsets")
+    return {n: getattr(out, n) for n in SAVED_NAMES + ("total",)}
+
+
+def _ptr(t):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(stream):
+    s = torch.cuda.current_stream() if stream is None else stream
+    return ctypes.c_void_p(s.cuda_stream)
+
+
+def alloc_workspace(shape: Shape, device="cuda"):
+    saved, scratch = workspace_size(shape)
+    return (torch.empty(max(saved, 256), dtype=torch.uint8, device=device),
+            torch.empty(max(scratch, 256), dtype=torch.uint8, device=device))
+
+
+def _weights(w):
+    return Weights(*[_ptr(w.get(n)) for n in WEIGHT_NAMES])
+
+
+def forward(shape: Shape, X, w, Y=None, accumulate=False, saved=None, scratch=None, I_out=None, r_out=None,
+            stream=None):
+    """Run mosa_forward.  ``w`` maps weight names (see WEIGHT_NAMES) to device
+    tensors.  Returns (Y, saved, scratch)."""
+    if Y is None:
+        Y = torch.empty_like(X)
+    if saved is None or scratch is None:
+        saved, scratch = alloc_workspace(shape, X.device)
+    st = lib().mosa_forward(ctypes.byref(shape), _ptr(X), ctypes.byref(_weights(w)), _ptr(Y), int(accumulate),
+                            _ptr(I_out), _ptr(r_out), _ptr(saved), saved.numel(), _ptr(scratch), scratch.numel(),
+                            _stream(stream))
+    _check(st, "mosa_forward")
+    return Y, saved, scratch
+
+
+def backward(shape: Shape, X, w, dY, saved, grads, dX=None, accumulate_dX=False, scratch=None, stream=None):
+    """Run mosa_backward.  ``grads`` maps gradient names (see GRAD_NAMES) to
+    device tensors that are written.  Returns dX."""
+    if dX is None:
+        dX = torch.empty_like(X)
+    if scratch is None:
+        _, scratch = alloc_workspace(shape, X.device)
+    g = Grads(*[_ptr(grads.get(n)) for n in GRAD_NAMES])
+    st = lib().mosa_backward(ctypes.byref(shape), _ptr(X), ctypes.byref(_weights(w)), _ptr(dY), _ptr(saved),
+                             saved.numel(), _ptr(dX), int(accumulate_dX), ctypes.byref(g), _ptr(scratch),
+                             scratch.numel(), _stream(stream))
+    _check(st, "mosa_backward")
+    return dX
+
+
+def saved_view(shape: Shape, saved, name):
+    """Typed view of one tensor the forward keeps in ``saved`` (for inspection)."""
+    off = saved_offsets(shape)
+    B, T, H, Hd, k, dh = shape.batch, shape.seq_len, shape.heads, shape.dense_heads, shape.k, shape.d_head
+    nseg = (T + 63) // 64 + 1
+    st = torch_dtype(shape)
+    spec = {"I": (torch.int32, (B, H, k)), "r": (torch.float32, (B, H, k)), "seg": (torch.int32, (B, H, nseg)),
+            "Q": (st, (B, H, k, dh)), "K": (st, (B, H, k, dh)), "V": (st, (B, H, k, dh)),
+            "A": (st, (B, H, k, dh)), "lse": (torch.float32, (B, H, k)),
+            "Qd": (st, (B, Hd, T, dh)), "Kd": (st, (B, Hd, T, dh)), "Vd": (st, (B, Hd, T, dh)),
+            "Ad": (st, (B, Hd, T, dh)), "lsed": (torch.float32, (B, Hd, T))}[name]
+    dt, shp = spec
+    n = 1
+    for s in shp:
+        n *= s
+    nbytes = n * torch.tensor([], dtype=dt).element_size()
+    return saved[off[name]: off[name] + nbytes].view(dt).view(shp)
