@@ -147,6 +147,30 @@ int mosa_backward(const mosa_shape* s, const void* X, const mosa_weights* w, con
                   const void* saved, size_t saved_bytes, void* dX, int accumulate_dX,
                   const mosa_grads* g, void* scratch, size_t scratch_bytes, void* stream);
 
+/* Stage timing for profiling and benchmarks.  The caller creates up to
+ * MOSA_MAX_STAGES hipEvent_t handles and stores them in `events`; the timed
+ * variants below do exactly the work of mosa_forward / mosa_backward and in
+ * addition record events[0] on `stream` before the first kernel and
+ * events[j] after stage j (one kernel per stage), setting names[j] to a
+ * static stage name and `count` to the number of events recorded.  The time
+ * of stage j is hipEventElapsedTime(events[j-1], events[j]).  A NULL
+ * `ev` makes them identical to the untimed calls. */
+#define MOSA_MAX_STAGES 32
+typedef struct mosa_stage_events {
+    void* events[MOSA_MAX_STAGES];
+    const char* names[MOSA_MAX_STAGES];
+    int count;
+} mosa_stage_events;
+
+int mosa_forward_timed(const mosa_shape* s, const void* X, const mosa_weights* w, void* Y,
+                       int accumulate, int32_t* I_out, float* r_out, void* saved,
+                       size_t saved_bytes, void* scratch, size_t scratch_bytes, void* stream,
+                       mosa_stage_events* ev);
+int mosa_backward_timed(const mosa_shape* s, const void* X, const mosa_weights* w, const void* dY,
+                        const void* saved, size_t saved_bytes, void* dX, int accumulate_dX,
+                        const mosa_grads* g, void* scratch, size_t scratch_bytes, void* stream,
+                        mosa_stage_events* ev);
+
 /* Static text for a status code (never NULL). */
 const char* mosa_status_string(int status);
 

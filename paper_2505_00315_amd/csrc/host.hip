@@ -19,7 +19,7 @@ struct Layout {
     // forward scratch
     size_t z, xnorm, unc_tok, unc_key, unc_sel;
     // backward scratch
-    size_t dAt, dr, dQ, dK, dV, dz, dQd, dKd, dVd, Dd;
+    size_t dA, D, dz, dQ, dK, dV, dAd, Dd, dQd, dKd, dVd;
     size_t scratch_total;
 };
 
@@ -82,16 +82,17 @@ Layout make_layout(const mosa_shape* s) {
     L.unc_key = fw.take(B * H * T * 8);
     L.unc_sel = fw.take(B * H * T * 4);
     Carver bw;
-    L.dAt = bw.take(B * H * k * dh * 4);
-    L.dr = bw.take(B * H * k * 4);
-    L.dQ = bw.take(B * H * k * dh * 4);
-    L.dK = bw.take(B * H * k * dh * 4);
-    L.dV = bw.take(B * H * k * dh * 4);
+    L.dA = bw.take(B * H * k * dh * es);
+    L.D = bw.take(B * H * k * 4);
     L.dz = bw.take(B * H * k * 4);
-    L.dQd = bw.take(B * Hd * T * dh * 4);
-    L.dKd = bw.take(B * Hd * T * dh * 4);
-    L.dVd = bw.take(B * Hd * T * dh * 4);
+    L.dQ = bw.take(B * H * k * dh * es);
+    L.dK = bw.take(B * H * k * dh * es);
+    L.dV = bw.take(B * H * k * dh * es);
+    L.dAd = bw.take(B * Hd * T * dh * es);
     L.Dd = bw.take(B * Hd * T * 4);
+    L.dQd = bw.take(B * Hd * T * dh * es);
+    L.dKd = bw.take(B * Hd * T * dh * es);
+    L.dVd = bw.take(B * Hd * T * dh * es);
     L.scratch_total = fw.total() > bw.total() ? fw.total() : bw.total();
     return L;
 }
@@ -121,6 +122,18 @@ template <typename T>
 const T* at(const void* base, size_t off) {
     return reinterpret_cast<const T*>(static_cast<const char*>(base) + off);
 }
+
+// Records a caller-created hipEvent_t after a stage (profiling variants only).
+struct StageMarks {
+    mosa_stage_events* ev;
+    hipStream_t stream;
+    int mark(const char* name) {
+        if (!ev) return 0;
+        if (ev->count >= MOSA_MAX_STAGES || !ev->events[ev->count]) return 1;
+        ev->names[ev->count] = name;
+        return hipEventRecord(static_cast<hipEvent_t>(ev->events[ev->count++]), stream) != hipSuccess;
+    }
+};
 
 }  // namespace
 
@@ -155,9 +168,9 @@ int mosa_saved_offsets(const mosa_shape* s, mosa_saved_layout* out) {
     return MOSA_OK;
 }
 
-int mosa_forward(const mosa_shape* s, const void* X, const mosa_weights* w, void* Y, int accumulate,
-                 int32_t* I_out, float* r_out, void* saved, size_t saved_bytes, void* scratch, size_t scratch_bytes,
-                 void* stream_) {
+int mosa_forward_timed(const mosa_shape* s, const void* X, const mosa_weights* w, void* Y, int accumulate,
+                       int32_t* I_out, float* r_out, void* saved, size_t saved_bytes, void* scratch,
+                       size_t scratch_bytes, void* stream_, mosa_stage_events* ev) {
     int st = validate_shape(s);
     if (st) return st;
     if ((st = check_weights(s, w))) return st;
@@ -168,6 +181,9 @@ int mosa_forward(const mosa_shape* s, const void* X, const mosa_weights* w, void
     if (saved_bytes < L.saved.total || scratch_bytes < L.scratch_total) return MOSA_ERR_WORKSPACE;
 
     hipStream_t stream = static_cast<hipStream_t>(stream_);
+    if (ev) ev->count = 0;
+    StageMarks sm{ev, stream};
+    int e = sm.mark("start");
     const int B = s->batch, T = s->seq_len, d = s->d_model, H = s->heads, Hd = s->dense_heads, dh = s->d_head;
     const int k = H > 0 ? s->k : 0, dt = s->dtype, causal = s->causal;
     int32_t* I = at<int32_t>(saved, L.saved.I);
@@ -184,21 +200,27 @@ int mosa_forward(const mosa_shape* s, const void* X, const mosa_weights* w, void
     void* Ad = at<char>(saved, L.saved.Ad);
     float* lsed = at<float>(saved, L.saved.lsed);
 
-    int e = 0;
     if (H > 0) {
         float* z = at<float>(scratch, L.z);
         float* xnorm = at<float>(scratch, L.xnorm);
         e |= launch_router(dt, X, w->Wr, B, T, d, H, z, xnorm, stream);
+        e |= sm.mark("router");
         e |= launch_select(dt, z, xnorm, X, w->Wr, B, T, d, H, k, I, r, seg, at<int32_t>(scratch, L.unc_tok),
                            at<double>(scratch, L.unc_key), at<int32_t>(scratch, L.unc_sel), stream);
+        e |= sm.mark("select");
         e |= launch_qkv(dt, X, I, w->Wq, w->Wk, w->Wv, B, T, d, H, dh, k, Q, K, V, stream);
+        e |= sm.mark("qkv");
         e |= launch_attn_fwd(dt, Q, K, V, B * H, k, dh, causal, A, lse, stream);
+        e |= sm.mark("attn");
     }
     if (Hd > 0) {
         e |= launch_qkv(dt, X, nullptr, w->Wq_d, w->Wk_d, w->Wv_d, B, T, d, Hd, dh, T, Qd, Kd, Vd, stream);
+        e |= sm.mark("qkv_dense");
         e |= launch_attn_fwd(dt, Qd, Kd, Vd, B * Hd, T, dh, causal, Ad, lsed, stream);
+        e |= sm.mark("attn_dense");
     }
     e |= launch_out_scatter(dt, B, T, d, dh, H, k, I, r, seg, A, w->Wo, Hd, Ad, w->Wo_d, Y, accumulate, stream);
+    e |= sm.mark("out_scatter");
     if (H > 0 && I_out)
         e |= hipMemcpyAsync(I_out, I, (size_t)B * H * k * 4, hipMemcpyDeviceToDevice, stream) != hipSuccess;
     if (H > 0 && r_out)
@@ -206,14 +228,104 @@ int mosa_forward(const mosa_shape* s, const void* X, const mosa_weights* w, void
     return e ? MOSA_ERR_HIP : MOSA_OK;
 }
 
-int mosa_backward(const mosa_shape* s, const void* X, const mosa_weights* w, const void* dY, const void* saved,
-                  size_t saved_bytes, void* dX, int accumulate_dX, const mosa_grads* g, void* scratch,
-                  size_t scratch_bytes, void* stream_) {
+int mosa_forward(const mosa_shape* s, const void* X, const mosa_weights* w, void* Y, int accumulate,
+                 int32_t* I_out, float* r_out, void* saved, size_t saved_bytes, void* scratch, size_t scratch_bytes,
+                 void* stream) {
+    return mosa_forward_timed(s, X, w, Y, accumulate, I_out, r_out, saved, saved_bytes, scratch, scratch_bytes,
+                              stream, nullptr);
+}
+
+int mosa_backward_timed(const mosa_shape* s, const void* X, const mosa_weights* w, const void* dY, const void* saved,
+                        size_t saved_bytes, void* dX, int accumulate_dX, const mosa_grads* g, void* scratch,
+                        size_t scratch_bytes, void* stream_, mosa_stage_events* ev) {
     int st = validate_shape(s);
     if (st) return st;
-    (void)X; (void)w; (void)dY; (void)saved; (void)saved_bytes; (void)dX; (void)accumulate_dX; (void)g;
-    (void)scratch; (void)scratch_bytes; (void)stream_;
-    return MOSA_ERR_UNSUPPORTED;
+    if ((st = check_weights(s, w))) return st;
+    if (!X || !dY || !dX || !g || !aligned(X, 16) || !aligned(dY, 16) || !aligned(dX, 16)) return MOSA_ERR_INVALID_ARG;
+    if (!saved || !scratch || !aligned(saved, kAlign) || !aligned(scratch, kAlign)) return MOSA_ERR_INVALID_ARG;
+    if (s->heads > 0) {
+        const void* need[5] = {g->dWr, g->dWq, g->dWk, g->dWv, g->dWo};
+        for (const void* p : need)
+            if (!p || !aligned(p, 16)) return MOSA_ERR_INVALID_ARG;
+    }
+    if (s->dense_heads > 0) {
+        const void* need[4] = {g->dWq_d, g->dWk_d, g->dWv_d, g->dWo_d};
+        for (const void* p : need)
+            if (!p || !aligned(p, 16)) return MOSA_ERR_INVALID_ARG;
+    }
+    const Layout L = make_layout(s);
+    if (saved_bytes < L.saved.total || scratch_bytes < L.scratch_total) return MOSA_ERR_WORKSPACE;
+
+    hipStream_t stream = static_cast<hipStream_t>(stream_);
+    if (ev) ev->count = 0;
+    StageMarks sm{ev, stream};
+    int e = sm.mark("start");
+    const int B = s->batch, T = s->seq_len, d = s->d_model, H = s->heads, Hd = s->dense_heads, dh = s->d_head;
+    const int k = H > 0 ? s->k : 0, dt = s->dtype, causal = s->causal;
+    const int32_t* I = at<int32_t>(saved, L.saved.I);
+    const float* r = at<float>(saved, L.saved.r);
+    const int32_t* seg = at<int32_t>(saved, L.saved.seg);
+    const void* Q = at<char>(saved, L.saved.Q);
+    const void* K = at<char>(saved, L.saved.K);
+    const void* V = at<char>(saved, L.saved.V);
+    const void* A = at<char>(saved, L.saved.A);
+    const float* lse = at<float>(saved, L.saved.lse);
+    const void* Qd = at<char>(saved, L.saved.Qd);
+    const void* Kd = at<char>(saved, L.saved.Kd);
+    const void* Vd = at<char>(saved, L.saved.Vd);
+    const void* Ad = at<char>(saved, L.saved.Ad);
+    const float* lsed = at<float>(saved, L.saved.lsed);
+    void* dA = at<char>(scratch, L.dA);
+    float* D = at<float>(scratch, L.D);
+    float* dz = at<float>(scratch, L.dz);
+    void* dQ = at<char>(scratch, L.dQ);
+    void* dK = at<char>(scratch, L.dK);
+    void* dV = at<char>(scratch, L.dV);
+    void* dAd = at<char>(scratch, L.dAd);
+    float* Dd = at<float>(scratch, L.Dd);
+    void* dQd = at<char>(scratch, L.dQd);
+    void* dKd = at<char>(scratch, L.dKd);
+    void* dVd = at<char>(scratch, L.dVd);
+
+    if (H > 0) {
+        e |= launch_dattn_out(dt, dY, I, r, w->Wo, A, B, T, d, H, dh, k, dA, D, dz, stream);
+        e |= sm.mark("bwd_out");
+        e |= launch_attn_bwd(dt, Q, K, V, dA, lse, D, B * H, k, dh, causal, dQ, dK, dV, 0, stream);
+        e |= sm.mark("attn_bwd_kv");
+        e |= launch_attn_bwd(dt, Q, K, V, dA, lse, D, B * H, k, dh, causal, dQ, dK, dV, 1, stream);
+        e |= sm.mark("attn_bwd_q");
+        e |= launch_wgrad(dt, X, dY, I, r, A, dQ, dK, dV, dz, B, T, d, H, dh, k, g->dWq, g->dWk, g->dWv, g->dWr,
+                          g->dWo, 0, stream);
+        e |= sm.mark("wgrad_qkv");
+        e |= launch_wgrad(dt, X, dY, I, r, A, dQ, dK, dV, dz, B, T, d, H, dh, k, g->dWq, g->dWk, g->dWv, g->dWr,
+                          g->dWo, 1, stream);
+        e |= sm.mark("wgrad_o");
+    }
+    if (Hd > 0) {
+        e |= launch_dattn_out(dt, dY, nullptr, nullptr, w->Wo_d, Ad, B, T, d, Hd, dh, T, dAd, Dd, nullptr, stream);
+        e |= sm.mark("bwd_out_dense");
+        e |= launch_attn_bwd(dt, Qd, Kd, Vd, dAd, lsed, Dd, B * Hd, T, dh, causal, dQd, dKd, dVd, 0, stream);
+        e |= sm.mark("attn_bwd_kv_dense");
+        e |= launch_attn_bwd(dt, Qd, Kd, Vd, dAd, lsed, Dd, B * Hd, T, dh, causal, dQd, dKd, dVd, 1, stream);
+        e |= sm.mark("attn_bwd_q_dense");
+        e |= launch_wgrad(dt, X, dY, nullptr, nullptr, Ad, dQd, dKd, dVd, nullptr, B, T, d, Hd, dh, T, g->dWq_d,
+                          g->dWk_d, g->dWv_d, nullptr, g->dWo_d, 0, stream);
+        e |= sm.mark("wgrad_qkv_dense");
+        e |= launch_wgrad(dt, X, dY, nullptr, nullptr, Ad, dQd, dKd, dVd, nullptr, B, T, d, Hd, dh, T, g->dWq_d,
+                          g->dWk_d, g->dWv_d, nullptr, g->dWo_d, 1, stream);
+        e |= sm.mark("wgrad_o_dense");
+    }
+    e |= launch_dx_scatter(dt, B, T, d, dh, H, k, I, seg, dQ, dK, dV, dz, w->Wq, w->Wk, w->Wv, w->Wr, Hd, dQd, dKd,
+                           dVd, w->Wq_d, w->Wk_d, w->Wv_d, dX, accumulate_dX, stream);
+    e |= sm.mark("dx_scatter");
+    return e ? MOSA_ERR_HIP : MOSA_OK;
+}
+
+int mosa_backward(const mosa_shape* s, const void* X, const mosa_weights* w, const void* dY, const void* saved,
+                  size_t saved_bytes, void* dX, int accumulate_dX, const mosa_grads* g, void* scratch,
+                  size_t scratch_bytes, void* stream) {
+    return mosa_backward_timed(s, X, w, dY, saved, saved_bytes, dX, accumulate_dX, g, scratch, scratch_bytes, stream,
+                               nullptr);
 }
 
 }  // extern "C"

@@ -43,4 +43,26 @@ int launch_out_scatter(int dtype, int B, int T, int d, int dh, int H, int k, con
                        const float* r, const int32_t* seg, const void* A, const void* Wo, int Hd,
                        const void* Ad, const void* Wo_d, void* Y, int accumulate, hipStream_t stream);
 
+// Backward, output side of a head: dA~ = dY[I] Wo^T; dA = r dA~;
+// D = r <dA~, A>; dz = <dA~, A> r (1 - r) (dz may be null: dense heads, r null).
+int launch_dattn_out(int dtype, const void* dY, const int32_t* I, const float* r, const void* Wo, const void* A,
+                     int B, int T, int d, int H, int dh, int n, void* dA, float* D, float* dz, hipStream_t stream);
+
+// Attention backward; pass 0 writes dK, dV, pass 1 writes dQ.
+int launch_attn_bwd(int dtype, const void* Q, const void* K, const void* V, const void* dA, const float* lse,
+                    const float* D, int BH, int n, int dh, int causal, void* dQ, void* dK, void* dV, int pass,
+                    hipStream_t stream);
+
+// Weight gradients; which 0: dWq, dWk, dWv (+ dWr when non-null), which 1: dWo.
+int launch_wgrad(int dtype, const void* X, const void* dY, const int32_t* I, const float* r, const void* A,
+                 const void* dQ, const void* dK, const void* dV, const float* dz, int B, int T, int d, int H, int dh,
+                 int n, void* dWq, void* dWk, void* dWv, void* dWr, void* dWo, int which, hipStream_t stream);
+
+// dX[b,t,:] (+)= sum_h sum_{i: I=t} (dQ Wq^T + dK Wk^T + dV Wv^T + dz Wr)_i + dense heads.
+int launch_dx_scatter(int dtype, int B, int T, int d, int dh, int H, int k, const int32_t* I, const int32_t* seg,
+                      const void* dQ, const void* dK, const void* dV, const float* dz, const void* Wq, const void* Wk,
+                      const void* Wv, const void* Wr, int Hd, const void* dQd, const void* dKd, const void* dVd,
+                      const void* Wq_d, const void* Wk_d, const void* Wv_d, void* dX, int accumulate,
+                      hipStream_t stream);
+
 }  // namespace mosa

@@ -21,7 +21,8 @@ MOSA_F32 = 0
 MOSA_BF16 = 1
 
 SYMBOLS = ("mosa_workspace_size", "mosa_saved_offsets", "mosa_forward", "mosa_backward",
-           "mosa_status_string")
+           "mosa_forward_timed", "mosa_backward_timed", "mosa_status_string")
+MAX_STAGES = 32
 
 WEIGHT_NAMES = ("Wr", "Wq", "Wk", "Wv", "Wo", "Wq_d", "Wk_d", "Wv_d", "Wo_d")
 GRAD_NAMES = tuple("d" + n for n in WEIGHT_NAMES)
@@ -43,6 +44,11 @@ class Grads(ctypes.Structure):
 
 class SavedLayout(ctypes.Structure):
     _fields_ = [(n, ctypes.c_size_t) for n in SAVED_NAMES + ("total",)]
+
+
+class StageEvents(ctypes.Structure):
+    _fields_ = [("events", ctypes.c_void_p * MAX_STAGES), ("names", ctypes.c_char_p * MAX_STAGES),
+                ("count", ctypes.c_int)]
 
 
 class MosaError(RuntimeError):
@@ -70,9 +76,12 @@ def lib():
         L.mosa_backward.argtypes = [P(Shape), ctypes.c_void_p, P(Weights), ctypes.c_void_p, ctypes.c_void_p,
                                     ctypes.c_size_t, ctypes.c_void_p, ctypes.c_int, P(Grads), ctypes.c_void_p,
                                     ctypes.c_size_t, ctypes.c_void_p]
+        L.mosa_forward_timed.argtypes = L.mosa_forward.argtypes + [P(StageEvents)]
+        L.mosa_backward_timed.argtypes = L.mosa_backward.argtypes + [P(StageEvents)]
         L.mosa_status_string.argtypes = [ctypes.c_int]
         L.mosa_status_string.restype = ctypes.c_char_p
-        for n in ("mosa_workspace_size", "mosa_saved_offsets", "mosa_forward", "mosa_backward"):
+        for n in ("mosa_workspace_size", "mosa_saved_offsets", "mosa_forward", "mosa_backward",
+                  "mosa_forward_timed", "mosa_backward_timed"):
             getattr(L, n).restype = ctypes.c_int
         _lib = L
     return _lib
@@ -130,32 +139,39 @@ def _weights(w):
 
 
 def forward(shape: Shape, X, w, Y=None, accumulate=False, saved=None, scratch=None, I_out=None, r_out=None,
-            stream=None):
-    """Run mosa_forward.  ``w`` maps weight names (see WEIGHT_NAMES) to device
-    tensors.  Returns (Y, saved, scratch)."""
+            stream=None, events=None):
+    """Run mosa_forward (mosa_forward_timed when ``events`` is a StageEvents).
+    ``w`` maps weight names (see WEIGHT_NAMES) to device tensors.
+    Returns (Y, saved, scratch)."""
     if Y is None:
         Y = torch.empty_like(X)
     if saved is None or scratch is None:
         saved, scratch = alloc_workspace(shape, X.device)
-    st = lib().mosa_forward(ctypes.byref(shape), _ptr(X), ctypes.byref(_weights(w)), _ptr(Y), int(accumulate),
-                            _ptr(I_out), _ptr(r_out), _ptr(saved), saved.numel(), _ptr(scratch), scratch.numel(),
-                            _stream(stream))
-    _check(st, "mosa_forward")
+    args = [ctypes.byref(shape), _ptr(X), ctypes.byref(_weights(w)), _ptr(Y), int(accumulate), _ptr(I_out),
+            _ptr(r_out), _ptr(saved), saved.numel(), _ptr(scratch), scratch.numel(), _stream(stream)]
+    if events is None:
+        _check(lib().mosa_forward(*args), "mosa_forward")
+    else:
+        _check(lib().mosa_forward_timed(*args, ctypes.byref(events)), "mosa_forward_timed")
     return Y, saved, scratch
 
 
-def backward(shape: Shape, X, w, dY, saved, grads, dX=None, accumulate_dX=False, scratch=None, stream=None):
-    """Run mosa_backward.  ``grads`` maps gradient names (see GRAD_NAMES) to
-    device tensors that are written.  Returns dX."""
+def backward(shape: Shape, X, w, dY, saved, grads, dX=None, accumulate_dX=False, scratch=None, stream=None,
+             events=None):
+    """Run mosa_backward (mosa_backward_timed when ``events`` is given).
+    ``grads`` maps gradient names (see GRAD_NAMES) to device tensors that are
+    written.  Returns dX."""
     if dX is None:
         dX = torch.empty_like(X)
     if scratch is None:
         _, scratch = alloc_workspace(shape, X.device)
     g = Grads(*[_ptr(grads.get(n)) for n in GRAD_NAMES])
-    st = lib().mosa_backward(ctypes.byref(shape), _ptr(X), ctypes.byref(_weights(w)), _ptr(dY), _ptr(saved),
-                             saved.numel(), _ptr(dX), int(accumulate_dX), ctypes.byref(g), _ptr(scratch),
-                             scratch.numel(), _stream(stream))
-    _check(st, "mosa_backward")
+    args = [ctypes.byref(shape), _ptr(X), ctypes.byref(_weights(w)), _ptr(dY), _ptr(saved), saved.numel(), _ptr(dX),
+            int(accumulate_dX), ctypes.byref(g), _ptr(scratch), scratch.numel(), _stream(stream)]
+    if events is None:
+        _check(lib().mosa_backward(*args), "mosa_backward")
+    else:
+        _check(lib().mosa_backward_timed(*args, ctypes.byref(events)), "mosa_backward_timed")
     return dX
 
 
