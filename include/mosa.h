@@ -105,14 +105,15 @@ typedef struct mosa_grads {
 
 /* Byte offsets of the tensors the forward leaves in `saved` (read-only for
  * the caller; documented so that tests can inspect the stages):
- *   I [B,H,k] int32 ascending; r [B,H,k] fp32; seg [B,H,nseg] int32 where
- *   seg[b,h,j] = number of selected tokens < 64 j (nseg = ceil(T/64) + 1);
- *   Q, K, V, A [B,H,k,dh] storage type (A before the router scaling);
+ *   I [B,H,k] int32 ascending; r [B,H,k] fp32;
+ *   slot [B,H,T] int16: position of token t in I[b,h,:], or -1;
+ *   QKV [B,H,k,3,dh] storage type: packed rows q | k | v of the selected tokens;
+ *   A [B,H,k,dh] storage type (attention output before the router scaling);
  *   lse [B,H,k] fp32 (natural-log sum of exp of the scaled scores);
- *   the same five for the dense heads with k = T: Qd, Kd, Vd, Ad [B,Hd,T,dh],
+ *   the same for the dense heads with k = T: QKVd [B,Hd,T,3,dh], Ad [B,Hd,T,dh],
  *   lsed [B,Hd,T]. */
 typedef struct mosa_saved_layout {
-    size_t I, r, seg, Q, K, V, A, lse, Qd, Kd, Vd, Ad, lsed;
+    size_t I, r, slot, QKV, A, lse, QKVd, Ad, lsed;
     size_t total;
 } mosa_saved_layout;
 

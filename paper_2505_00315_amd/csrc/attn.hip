@@ -22,24 +22,24 @@ namespace mosa {
 namespace {
 
 template <typename ST, int DH>
-__global__ __launch_bounds__(256) void attn_fwd_kernel(const ST* __restrict__ Q, const ST* __restrict__ K,
-                                                       const ST* __restrict__ V, int BH, int n, int causal,
+__global__ __launch_bounds__(256) void attn_fwd_kernel(const ST* __restrict__ QKV, int BH, int n, int causal,
                                                        float scale, ST* __restrict__ A, float* __restrict__ lse) {
+    constexpr int RS = 3 * DH;  // row stride of the packed Q | K | V rows
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int g = lane >> 4, c16 = lane & 15;
     const int nqb = (n + 15) / 16;
     const int task = blockIdx.x * 4 + wave;
     if (task >= BH * nqb) return;
     const int bh = task / nqb, q0 = (task % nqb) * 16;
-    const ST* Qp = Q + (size_t)bh * n * DH;
-    const ST* Kp = K + (size_t)bh * n * DH;
-    const ST* Vp = V + (size_t)bh * n * DH;
+    const ST* Qp = QKV + (size_t)bh * n * RS;
+    const ST* Kp = Qp + DH;
+    const ST* Vp = Qp + 2 * DH;
 
     const int q = q0 + c16;  // this lane's query
     Frag8<ST> qf[DH / 32];
 #pragma unroll
     for (int s = 0; s < DH / 32; ++s)
-        qf[s] = q < n ? frag8_load<ST>(Qp + (size_t)q * DH + s * 32 + 8 * g) : frag8_zero<ST>();
+        qf[s] = q < n ? frag8_load<ST>(Qp + (size_t)q * RS + s * 32 + 8 * g) : frag8_zero<ST>();
 
     float m_run = -__builtin_inff(), l_run = 0.f;
     f32x4 o[DH / 16];
@@ -52,7 +52,7 @@ __global__ __launch_bounds__(256) void attn_fwd_kernel(const ST* __restrict__ Q,
         const int kr = j0 + c16;
 #pragma unroll
         for (int st = 0; st < DH / 32; ++st) {
-            const Frag8<ST> kf = kr < n ? frag8_load<ST>(Kp + (size_t)kr * DH + st * 32 + 8 * g) : frag8_zero<ST>();
+            const Frag8<ST> kf = kr < n ? frag8_load<ST>(Kp + (size_t)kr * RS + st * 32 + 8 * g) : frag8_zero<ST>();
             mma8(s, kf, qf[st]);
         }
         float sc[4], mloc = -__builtin_inff();
@@ -86,7 +86,7 @@ __global__ __launch_bounds__(256) void attn_fwd_kernel(const ST* __restrict__ Q,
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
                 const int j = j0 + 4 * g + i;
-                vv[i] = j < n ? ld1<ST>(Vp + (size_t)j * DH + db * 16 + c16) : 0.f;
+                vv[i] = j < n ? ld1<ST>(Vp + (size_t)j * RS + db * 16 + c16) : 0.f;
             }
             const Frag4<ST> vf = frag4_from<ST>(vv);
             mma4(o[db], vf, pf);
@@ -104,27 +104,24 @@ __global__ __launch_bounds__(256) void attn_fwd_kernel(const ST* __restrict__ Q,
 }
 
 template <typename ST>
-int launch_attn_fwd_t(const ST* Q, const ST* K, const ST* V, int BH, int n, int dh, int causal, ST* A, float* lse,
-                      hipStream_t stream) {
+int launch_attn_fwd_t(const ST* QKV, int BH, int n, int dh, int causal, ST* A, float* lse, hipStream_t stream) {
     const int tasks = BH * ((n + 15) / 16);
     dim3 grid((tasks + 3) / 4), block(256);
     const float scale = 1.0f / sqrtf((float)dh);
     if (dh == 64)
-        hipLaunchKernelGGL((attn_fwd_kernel<ST, 64>), grid, block, 0, stream, Q, K, V, BH, n, causal, scale, A, lse);
+        hipLaunchKernelGGL((attn_fwd_kernel<ST, 64>), grid, block, 0, stream, QKV, BH, n, causal, scale, A, lse);
     else
-        hipLaunchKernelGGL((attn_fwd_kernel<ST, 32>), grid, block, 0, stream, Q, K, V, BH, n, causal, scale, A, lse);
+        hipLaunchKernelGGL((attn_fwd_kernel<ST, 32>), grid, block, 0, stream, QKV, BH, n, causal, scale, A, lse);
     return hipGetLastError() == hipSuccess ? 0 : -1;
 }
 
 }  // namespace
 
-int launch_attn_fwd(int dtype, const void* Q, const void* K, const void* V, int BH, int n, int dh, int causal,
-                    void* A, float* lse, hipStream_t stream) {
+int launch_attn_fwd(int dtype, const void* QKV, int BH, int n, int dh, int causal, void* A, float* lse,
+                    hipStream_t stream) {
     if (dtype == kBF16)
-        return launch_attn_fwd_t<uint16_t>((const uint16_t*)Q, (const uint16_t*)K, (const uint16_t*)V, BH, n, dh,
-                                           causal, (uint16_t*)A, lse, stream);
-    return launch_attn_fwd_t<float>((const float*)Q, (const float*)K, (const float*)V, BH, n, dh, causal, (float*)A,
-                                    lse, stream);
+        return launch_attn_fwd_t<uint16_t>((const uint16_t*)QKV, BH, n, dh, causal, (uint16_t*)A, lse, stream);
+    return launch_attn_fwd_t<float>((const float*)QKV, BH, n, dh, causal, (float*)A, lse, stream);
 }
 
 }  // namespace mosa

@@ -21,11 +21,11 @@ namespace mosa {
 namespace {
 
 template <typename ST, int DH>
-__global__ __launch_bounds__(256) void attn_bwd_kv_kernel(const ST* __restrict__ Q, const ST* __restrict__ K,
-                                                          const ST* __restrict__ V, const ST* __restrict__ dA,
+__global__ __launch_bounds__(256) void attn_bwd_kv_kernel(const ST* __restrict__ QKV, const ST* __restrict__ dA,
                                                           const float* __restrict__ lse, const float* __restrict__ D,
                                                           int BH, int n, int causal, float scale,
-                                                          ST* __restrict__ dK, ST* __restrict__ dV) {
+                                                          ST* __restrict__ dQKV) {
+    constexpr int RS = 3 * DH;  // row stride of the packed Q | K | V (and dQ | dK | dV) rows
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int g = lane >> 4, c16 = lane & 15;
     const int nb = (n + 15) / 16;
@@ -33,17 +33,17 @@ __global__ __launch_bounds__(256) void attn_bwd_kv_kernel(const ST* __restrict__
     if (task >= BH * nb) return;
     const int bh = task / nb, j0 = (task % nb) * 16;
     const size_t base = (size_t)bh * n;
-    const ST* Qp = Q + base * DH;
-    const ST* Kp = K + base * DH;
-    const ST* Vp = V + base * DH;
+    const ST* Qp = QKV + base * RS;
+    const ST* Kp = Qp + DH;
+    const ST* Vp = Qp + 2 * DH;
     const ST* dAp = dA + base * DH;
 
     const int key = j0 + c16;  // this lane's key (as MFMA column)
     Frag8<ST> kf[DH / 32], vf[DH / 32];
 #pragma unroll
     for (int s = 0; s < DH / 32; ++s) {
-        kf[s] = key < n ? frag8_load<ST>(Kp + (size_t)key * DH + s * 32 + 8 * g) : frag8_zero<ST>();
-        vf[s] = key < n ? frag8_load<ST>(Vp + (size_t)key * DH + s * 32 + 8 * g) : frag8_zero<ST>();
+        kf[s] = key < n ? frag8_load<ST>(Kp + (size_t)key * RS + s * 32 + 8 * g) : frag8_zero<ST>();
+        vf[s] = key < n ? frag8_load<ST>(Vp + (size_t)key * RS + s * 32 + 8 * g) : frag8_zero<ST>();
     }
     f32x4 dKt[DH / 16], dVt[DH / 16];
 #pragma unroll
@@ -54,7 +54,7 @@ __global__ __launch_bounds__(256) void attn_bwd_kv_kernel(const ST* __restrict__
         f32x4 s = zero4(), dp = zero4();
 #pragma unroll
         for (int st = 0; st < DH / 32; ++st) {
-            const Frag8<ST> qa_f = qa < n ? frag8_load<ST>(Qp + (size_t)qa * DH + st * 32 + 8 * g) : frag8_zero<ST>();
+            const Frag8<ST> qa_f = qa < n ? frag8_load<ST>(Qp + (size_t)qa * RS + st * 32 + 8 * g) : frag8_zero<ST>();
             const Frag8<ST> da_f = qa < n ? frag8_load<ST>(dAp + (size_t)qa * DH + st * 32 + 8 * g) : frag8_zero<ST>();
             mma8(s, qa_f, kf[st]);
             mma8(dp, da_f, vf[st]);
@@ -79,7 +79,7 @@ __global__ __launch_bounds__(256) void attn_bwd_kv_kernel(const ST* __restrict__
             for (int i = 0; i < 4; ++i) {
                 const int q = i0 + 4 * g + i;
                 at[i] = q < n ? ld1<ST>(dAp + (size_t)q * DH + db * 16 + c16) : 0.f;
-                qt[i] = q < n ? ld1<ST>(Qp + (size_t)q * DH + db * 16 + c16) : 0.f;
+                qt[i] = q < n ? ld1<ST>(Qp + (size_t)q * RS + db * 16 + c16) : 0.f;
             }
             mma4(dVt[db], frag4_from<ST>(at), pf);
             mma4(dKt[db], frag4_from<ST>(qt), dsf);
@@ -91,18 +91,18 @@ __global__ __launch_bounds__(256) void attn_bwd_kv_kernel(const ST* __restrict__
         for (int db = 0; db < DH / 16; ++db)
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
-                st1<ST>(dV + (base + key) * DH + db * 16 + 4 * g + i, dVt[db][i]);
-                st1<ST>(dK + (base + key) * DH + db * 16 + 4 * g + i, dKt[db][i] * scale);
+                st1<ST>(dQKV + (base + key) * RS + 2 * DH + db * 16 + 4 * g + i, dVt[db][i]);
+                st1<ST>(dQKV + (base + key) * RS + DH + db * 16 + 4 * g + i, dKt[db][i] * scale);
             }
     }
 }
 
 template <typename ST, int DH>
-__global__ __launch_bounds__(256) void attn_bwd_q_kernel(const ST* __restrict__ Q, const ST* __restrict__ K,
-                                                         const ST* __restrict__ V, const ST* __restrict__ dA,
+__global__ __launch_bounds__(256) void attn_bwd_q_kernel(const ST* __restrict__ QKV, const ST* __restrict__ dA,
                                                          const float* __restrict__ lse, const float* __restrict__ D,
                                                          int BH, int n, int causal, float scale,
-                                                         ST* __restrict__ dQ) {
+                                                         ST* __restrict__ dQKV) {
+    constexpr int RS = 3 * DH;
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int g = lane >> 4, c16 = lane & 15;
     const int nb = (n + 15) / 16;
@@ -110,16 +110,16 @@ __global__ __launch_bounds__(256) void attn_bwd_q_kernel(const ST* __restrict__ 
     if (task >= BH * nb) return;
     const int bh = task / nb, i0 = (task % nb) * 16;
     const size_t base = (size_t)bh * n;
-    const ST* Qp = Q + base * DH;
-    const ST* Kp = K + base * DH;
-    const ST* Vp = V + base * DH;
+    const ST* Qp = QKV + base * RS;
+    const ST* Kp = Qp + DH;
+    const ST* Vp = Qp + 2 * DH;
     const ST* dAp = dA + base * DH;
 
     const int q = i0 + c16;  // this lane's query (MFMA column)
     Frag8<ST> qf[DH / 32], daf[DH / 32];
 #pragma unroll
     for (int s = 0; s < DH / 32; ++s) {
-        qf[s] = q < n ? frag8_load<ST>(Qp + (size_t)q * DH + s * 32 + 8 * g) : frag8_zero<ST>();
+        qf[s] = q < n ? frag8_load<ST>(Qp + (size_t)q * RS + s * 32 + 8 * g) : frag8_zero<ST>();
         daf[s] = q < n ? frag8_load<ST>(dAp + (size_t)q * DH + s * 32 + 8 * g) : frag8_zero<ST>();
     }
     const float lq = q < n ? lse[base + q] : 0.f;
@@ -134,8 +134,8 @@ __global__ __launch_bounds__(256) void attn_bwd_q_kernel(const ST* __restrict__ 
         f32x4 s = zero4(), dp = zero4();
 #pragma unroll
         for (int st = 0; st < DH / 32; ++st) {
-            const Frag8<ST> k_f = kr < n ? frag8_load<ST>(Kp + (size_t)kr * DH + st * 32 + 8 * g) : frag8_zero<ST>();
-            const Frag8<ST> v_f = kr < n ? frag8_load<ST>(Vp + (size_t)kr * DH + st * 32 + 8 * g) : frag8_zero<ST>();
+            const Frag8<ST> k_f = kr < n ? frag8_load<ST>(Kp + (size_t)kr * RS + st * 32 + 8 * g) : frag8_zero<ST>();
+            const Frag8<ST> v_f = kr < n ? frag8_load<ST>(Vp + (size_t)kr * RS + st * 32 + 8 * g) : frag8_zero<ST>();
             mma8(s, k_f, qf[st]);
             mma8(dp, v_f, daf[st]);
         }
@@ -155,7 +155,7 @@ __global__ __launch_bounds__(256) void attn_bwd_q_kernel(const ST* __restrict__ 
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
                 const int j = j0 + 4 * g + i;
-                kt[i] = j < n ? ld1<ST>(Kp + (size_t)j * DH + db * 16 + c16) : 0.f;
+                kt[i] = j < n ? ld1<ST>(Kp + (size_t)j * RS + db * 16 + c16) : 0.f;
             }
             mma4(dQt[db], frag4_from<ST>(kt), dsf);
         }
@@ -164,45 +164,38 @@ __global__ __launch_bounds__(256) void attn_bwd_q_kernel(const ST* __restrict__ 
 #pragma unroll
         for (int db = 0; db < DH / 16; ++db)
 #pragma unroll
-            for (int i = 0; i < 4; ++i) st1<ST>(dQ + (base + q) * DH + db * 16 + 4 * g + i, dQt[db][i] * scale);
+            for (int i = 0; i < 4; ++i) st1<ST>(dQKV + (base + q) * RS + db * 16 + 4 * g + i, dQt[db][i] * scale);
     }
 }
 
 template <typename ST>
-int launch_t(const ST* Q, const ST* K, const ST* V, const ST* dA, const float* lse, const float* D, int BH, int n,
-             int dh, int causal, ST* dQ, ST* dK, ST* dV, int pass, hipStream_t stream) {
+int launch_t(const ST* QKV, const ST* dA, const float* lse, const float* D, int BH, int n, int dh, int causal,
+             ST* dQKV, int pass, hipStream_t stream) {
     const int tasks = BH * ((n + 15) / 16);
     dim3 grid((tasks + 3) / 4), block(256);
     const float scale = 1.0f / sqrtf((float)dh);
+#define MOSA_ATTN_BWD(KERN, DHV) \
+    hipLaunchKernelGGL((KERN<ST, DHV>), grid, block, 0, stream, QKV, dA, lse, D, BH, n, causal, scale, dQKV)
     if (pass == 0) {
-        if (dh == 64)
-            hipLaunchKernelGGL((attn_bwd_kv_kernel<ST, 64>), grid, block, 0, stream, Q, K, V, dA, lse, D, BH, n,
-                               causal, scale, dK, dV);
-        else
-            hipLaunchKernelGGL((attn_bwd_kv_kernel<ST, 32>), grid, block, 0, stream, Q, K, V, dA, lse, D, BH, n,
-                               causal, scale, dK, dV);
+        if (dh == 64) MOSA_ATTN_BWD(attn_bwd_kv_kernel, 64);
+        else MOSA_ATTN_BWD(attn_bwd_kv_kernel, 32);
     } else {
-        if (dh == 64)
-            hipLaunchKernelGGL((attn_bwd_q_kernel<ST, 64>), grid, block, 0, stream, Q, K, V, dA, lse, D, BH, n,
-                               causal, scale, dQ);
-        else
-            hipLaunchKernelGGL((attn_bwd_q_kernel<ST, 32>), grid, block, 0, stream, Q, K, V, dA, lse, D, BH, n,
-                               causal, scale, dQ);
+        if (dh == 64) MOSA_ATTN_BWD(attn_bwd_q_kernel, 64);
+        else MOSA_ATTN_BWD(attn_bwd_q_kernel, 32);
     }
+#undef MOSA_ATTN_BWD
     return hipGetLastError() == hipSuccess ? 0 : -1;
 }
 
 }  // namespace
 
-int launch_attn_bwd(int dtype, const void* Q, const void* K, const void* V, const void* dA, const float* lse,
-                    const float* D, int BH, int n, int dh, int causal, void* dQ, void* dK, void* dV, int pass,
-                    hipStream_t stream) {
+int launch_attn_bwd(int dtype, const void* QKV, const void* dA, const float* lse, const float* D, int BH, int n,
+                    int dh, int causal, void* dQKV, int pass, hipStream_t stream) {
     if (dtype == kBF16)
-        return launch_t<uint16_t>((const uint16_t*)Q, (const uint16_t*)K, (const uint16_t*)V, (const uint16_t*)dA,
-                                  lse, D, BH, n, dh, causal, (uint16_t*)dQ, (uint16_t*)dK, (uint16_t*)dV, pass,
-                                  stream);
-    return launch_t<float>((const float*)Q, (const float*)K, (const float*)V, (const float*)dA, lse, D, BH, n, dh,
-                           causal, (float*)dQ, (float*)dK, (float*)dV, pass, stream);
+        return launch_t<uint16_t>((const uint16_t*)QKV, (const uint16_t*)dA, lse, D, BH, n, dh, causal,
+                                  (uint16_t*)dQKV, pass, stream);
+    return launch_t<float>((const float*)QKV, (const float*)dA, lse, D, BH, n, dh, causal, (float*)dQKV, pass,
+                           stream);
 }
 
 }  // namespace mosa

@@ -1,17 +1,20 @@
 // Backward of the output side of a head (chain rule through Section 2.2's
 // X^o = diag(r) A W^O and the scatter Y_{I_i} = X^o_i, with I held fixed):
 //   dX^o_i   = dY[b, I_i]                      (gather)
-//   dA~_i    = dX^o_i W^O^T                    (MFMA, K = d)
+//   dA~_i    = dX^o_i W^O^T                    (GEMM, K = d)
 //   dr_i     = <dA~_i, A_i>                    (router gradient through r)
 //   dA_i     = r_i dA~_i                       (into the attention backward)
 //   D_i      = <dA_i, A_i> = r_i dr_i          (softmax row term of Eq. 1's backward)
 //   dz_i     = dr_i r_i (1 - r_i)              (sigma'(s) = r (1 - r))
 // Dense heads are the case I = identity, r = 1 (no dz).
 //
-// Workgroup = 64 gathered rows of one head (4 waves x 16 rows) x all dh
-// columns.  W^O rows are contiguous along d, which is the K index here, so
-// both MFMA operands are read straight from memory as 16-byte fragments.
-#include "common.h"
+// One GEMM per head on the tiled MFMA engine: M = B*n gathered dY rows,
+// N = dh, K = d; W^O_h rows are contiguous along d (the K index), so both
+// operands are staged without transposes.  The epilogue holds whole rows of
+// dA~ and finishes dr, dA, D, dz there; dz is also written as a 16-wide row
+// (dz, 0, ..., 0) so the weight-gradient GEMM can treat W^r as a 16-column
+// block of its B operand.
+#include "gemm.h"
 #include "kernels.h"
 
 namespace mosa {
@@ -19,93 +22,125 @@ namespace mosa {
 namespace {
 
 template <typename ST, int DH>
-__global__ __launch_bounds__(256) void dattn_out_kernel(const ST* __restrict__ dY, const int32_t* __restrict__ I,
-                                                        const float* __restrict__ r, const ST* __restrict__ Wo,
-                                                        const ST* __restrict__ A, int T, int d, int H, int n,
-                                                        int nrows, int ntiles, ST* __restrict__ dA,
-                                                        float* __restrict__ D, float* __restrict__ dz) {
-    constexpr int NCB = DH / 16;
-    const int logical = xcd_logical_id(blockIdx.x, gridDim.x);
-    const int tile = logical % ntiles, h = logical / ntiles;
-    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-    const int g = lane >> 4, c16 = lane & 15;
-
-    const int arow = tile * 64 + wave * 16 + c16;
-    const bool arow_ok = arow < nrows;
-    const ST* yrow = dY;
-    if (arow_ok) {
-        const int b = arow / n, i = arow % n;
-        const int t = I ? I[((size_t)b * H + h) * n + i] : i;
-        yrow = dY + ((size_t)b * T + t) * d;
+struct BwdOutPolicy {
+    static constexpr int MT = 64, NT = DH, KC = sizeof(ST) == 2 ? 64 : 32, WM = 4, WN = 1;
+    static constexpr size_t EPI_LDS = 0;
+    static constexpr bool A_KCONTIG = true, B_KCONTIG = true, A_SCALED = false;
+    struct Args {
+        const ST* dY;
+        const int32_t* I;  // nullptr: dense head
+        const float* r;    // nullptr: dense head
+        const ST* Wo;      // [H, DH, d]
+        const ST* A;       // [B, H, n, DH]
+        ST* dA;
+        float* D;
+        float* dz;         // nullptr: dense head
+        ST* dz16;          // [B, H, n, 16]
+        int T, d, H, n, M, mtiles;
+    };
+    struct ARef {
+        const ST* p;
+    };
+    struct BRef {
+        const ST* p;
+    };
+    struct RowInfo {
+        int unused;
+    };
+    __device__ static const ST* a_fallback(const Args& a) { return a.dY; }
+    __device__ static const ST* b_fallback(const Args& a) { return a.Wo; }
+    __device__ static void tile(const Args& a, int logical, int& h, int& m0, int& n0) {
+        h = logical / a.mtiles;
+        m0 = (logical % a.mtiles) * MT;
+        n0 = 0;
     }
-    const ST* Wh = Wo + (size_t)h * DH * d;
-
-    f32x4 acc[NCB];
-#pragma unroll
-    for (int c = 0; c < NCB; ++c) acc[c] = zero4();
-    for (int kc = 0; kc < d; kc += 32) {
-        const Frag8<ST> a = arow_ok ? frag8_load<ST>(yrow + kc + 8 * g) : frag8_zero<ST>();
-#pragma unroll
-        for (int cb = 0; cb < NCB; ++cb) {
-            const Frag8<ST> bw = frag8_load<ST>(Wh + (size_t)(cb * 16 + c16) * d + kc + 8 * g);
-            mma8(acc[cb], a, bw);
-        }
+    __device__ static int k_size(const Args& a, int) { return a.d; }
+    __device__ static ARef a_row(const Args& a, int h, int m, float&) {
+        if (m < 0 || m >= a.M) return {nullptr};
+        const int b = m / a.n, i = m % a.n;
+        const int t = a.I ? a.I[((size_t)b * a.H + h) * a.n + i] : i;
+        return {a.dY + ((size_t)b * a.T + t) * a.d};
     }
+    __device__ static const ST* a_elem(const Args&, int, const ARef& r, int k) { return r.p ? r.p + k : nullptr; }
+    __device__ static BRef b_row(const Args& a, int h, int n) {
+        return {n >= 0 && n < DH ? a.Wo + ((size_t)h * DH + n) * a.d : nullptr};
+    }
+    __device__ static const ST* b_elem(const Args&, int, const BRef& r, int k) { return r.p ? r.p + k : nullptr; }
+    __device__ static RowInfo row_info(const Args&, int, int) { return {0}; }
+    __device__ static const ST* a_kaddr(const Args& a, int, const RowInfo&, int) { return a_fallback(a); }
+    __device__ static bool a_kok(const Args&, int, const RowInfo&, int) { return false; }
+    __device__ static float a_kscale(const Args&, int, const RowInfo&) { return 1.f; }
+    __device__ static const ST* b_kaddr(const Args& a, int, const RowInfo&, int) { return b_fallback(a); }
+    __device__ static bool b_kok(const Args&, int, const RowInfo&, int) { return false; }
 
-    // lane holds dA~[row 4g+i][col cb*16 + c16]
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-        const int row = tile * 64 + wave * 16 + 4 * g + i;
-        const bool ok = row < nrows;
-        size_t ridx = 0;
+    // 4 threads per row, DH / 4 columns each.
+    __device__ static void epilogue(const Args& a, int h, int m0, int, const float* Cs, int ldc, int tid, unsigned char*) {
+        constexpr int CW = DH / 4;
+        const int ml = tid >> 2, cq = (tid & 3) * CW;
+        const int m = m0 + ml;
+        const bool ok = m < a.M;
+        size_t ri = 0;
+        float c[CW], part = 0.f;
         if (ok) {
-            const int b = row / n, ii = row % n;
-            ridx = ((size_t)b * H + h) * n + ii;
-        }
-        float part = 0.f;
-        if (ok) {
+            ri = ((size_t)(m / a.n) * a.H + h) * a.n + (m % a.n);
 #pragma unroll
-            for (int cb = 0; cb < NCB; ++cb) part += acc[cb][i] * ld1<ST>(A + ridx * DH + cb * 16 + c16);
+            for (int q = 0; q < CW / 8; ++q) {
+                float x[8];
+                vec8_to_f32<ST>(vec8_load<ST>(a.A + ri * DH + cq + 8 * q), x);
+#pragma unroll
+                for (int j = 0; j < 8; ++j) {
+                    c[8 * q + j] = Cs[ml * ldc + cq + 8 * q + j];
+                    part += c[8 * q + j] * x[j];
+                }
+            }
         }
         part += __shfl_xor(part, 1, 64);
         part += __shfl_xor(part, 2, 64);
-        part += __shfl_xor(part, 4, 64);
-        part += __shfl_xor(part, 8, 64);
-        if (ok) {
-            const float rr = r ? r[ridx] : 1.f;
+        if (!ok) return;
+        const float rr = a.r ? a.r[ri] : 1.f;
 #pragma unroll
-            for (int cb = 0; cb < NCB; ++cb) st1<ST>(dA + ridx * DH + cb * 16 + c16, rr * acc[cb][i]);
-            if (c16 == 0) {
-                D[ridx] = rr * part;
-                if (dz) dz[ridx] = part * rr * (1.f - rr);
+        for (int q = 0; q < CW / 8; ++q) {
+            float x[8];
+#pragma unroll
+            for (int j = 0; j < 8; ++j) x[j] = rr * c[8 * q + j];
+            vec8_store<ST>(a.dA + ri * DH + cq + 8 * q, vec8_from_f32<ST>(x));
+        }
+        if ((tid & 3) == 0) {
+            a.D[ri] = rr * part;
+            if (a.dz) {
+                const float dzv = part * rr * (1.f - rr);
+                a.dz[ri] = dzv;
+                float x[8] = {dzv, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f}, zz[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+                vec8_store<ST>(a.dz16 + ri * 16, vec8_from_f32<ST>(x));
+                vec8_store<ST>(a.dz16 + ri * 16 + 8, vec8_from_f32<ST>(zz));
             }
         }
     }
-}
+};
 
-template <typename ST>
-int launch_t(const ST* dY, const int32_t* I, const float* r, const ST* Wo, const ST* A, int B, int T, int d, int H,
-             int dh, int n, ST* dA, float* D, float* dz, hipStream_t stream) {
-    const int nrows = B * n, ntiles = (nrows + 63) / 64;
-    dim3 grid(ntiles * H), block(256);
-    if (dh == 64)
-        hipLaunchKernelGGL((dattn_out_kernel<ST, 64>), grid, block, 0, stream, dY, I, r, Wo, A, T, d, H, n, nrows,
-                           ntiles, dA, D, dz);
-    else
-        hipLaunchKernelGGL((dattn_out_kernel<ST, 32>), grid, block, 0, stream, dY, I, r, Wo, A, T, d, H, n, nrows,
-                           ntiles, dA, D, dz);
-    return hipGetLastError() == hipSuccess ? 0 : -1;
+template <typename ST, int DH>
+int run(const ST* dY, const int32_t* I, const float* r, const ST* Wo, const ST* A, int B, int T, int d, int H, int n,
+        ST* dA, float* D, float* dz, ST* dz16, hipStream_t stream) {
+    using P = BwdOutPolicy<ST, DH>;
+    const int M = B * n;
+    typename P::Args a{dY, I, r, Wo, A, dA, D, dz, dz16, T, d, H, n, M, (M + P::MT - 1) / P::MT};
+    return launch_gemm<ST, P>(a, H * a.mtiles, stream);
 }
 
 }  // namespace
 
 int launch_dattn_out(int dtype, const void* dY, const int32_t* I, const float* r, const void* Wo, const void* A,
-                     int B, int T, int d, int H, int dh, int n, void* dA, float* D, float* dz, hipStream_t stream) {
-    if (dtype == kBF16)
-        return launch_t<uint16_t>((const uint16_t*)dY, I, r, (const uint16_t*)Wo, (const uint16_t*)A, B, T, d, H, dh,
-                                  n, (uint16_t*)dA, D, dz, stream);
-    return launch_t<float>((const float*)dY, I, r, (const float*)Wo, (const float*)A, B, T, d, H, dh, n, (float*)dA,
-                           D, dz, stream);
+                     int B, int T, int d, int H, int dh, int n, void* dA, float* D, float* dz, void* dz16,
+                     hipStream_t stream) {
+    if (H == 0) return 0;
+    if (dtype == kBF16) {
+        auto f = dh == 64 ? run<uint16_t, 64> : run<uint16_t, 32>;
+        return f((const uint16_t*)dY, I, r, (const uint16_t*)Wo, (const uint16_t*)A, B, T, d, H, n, (uint16_t*)dA, D,
+                 dz, (uint16_t*)dz16, stream);
+    }
+    auto f = dh == 64 ? run<float, 64> : run<float, 32>;
+    return f((const float*)dY, I, r, (const float*)Wo, (const float*)A, B, T, d, H, n, (float*)dA, D, dz,
+             (float*)dz16, stream);
 }
 
 }  // namespace mosa

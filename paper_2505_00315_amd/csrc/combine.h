@@ -1,0 +1,117 @@
+// Deterministic head-ordered combination of per-head rows into a [B, T, d]
+// output tile (used by the epilogues of out_combine and dx_combine).
+//
+// The output tile is 64 tokens x 128 columns; 4 threads own one token row, 32
+// columns each, starting from the fp32 tile value the GEMM left in LDS.  The
+// MoSA heads that selected token t are found from the slot map
+// slot[b, h, t] (position of t among head h's selected tokens, or -1): the
+// map for 64 tokens x 256 heads is staged in LDS token-major, each thread
+// scans its token's heads 8 at a time, and the rows of the hits are fetched
+// four at a time (16 loads in flight) and added in ascending head order.
+// Every output element is thus produced by one thread in a fixed order
+// (bitwise reproducible, no atomics), and tokens no head selected keep the
+// GEMM value exactly.
+#pragma once
+
+#include "gemm.h"
+
+namespace mosa {
+
+constexpr int kCombineHeads = 256;              // heads staged per pass
+constexpr int kCombineLdh = kCombineHeads + 8;  // padded LDS row (int16)
+constexpr size_t kCombineLds = (size_t)64 * kCombineLdh * sizeof(int16_t);
+
+template <typename ST>
+__device__ __forceinline__ void combine_tile(const float* Cs, int ldc, int tid, int b, int m0, int n0, int T, int d,
+                                             int H, int k, const int16_t* __restrict__ slot,
+                                             const ST* __restrict__ rows, ST* __restrict__ out, int accumulate,
+                                             int16_t* s_slot) {
+    const int ml = tid >> 2, cq = (tid & 3) * 32;
+    const int t = m0 + ml;
+    const bool active = t < T && n0 + cq < d;  // d is a multiple of 64: 32-column groups are all in or all out
+    float acc[32];
+#pragma unroll
+    for (int j = 0; j < 32; ++j) acc[j] = active ? Cs[ml * ldc + cq + j] : 0.f;
+
+    const ST* rbase = rows + (size_t)b * H * k * d + n0 + cq;
+    int q = 0, qh0 = 0, qh1 = 0, qh2 = 0, qh3 = 0, qs0 = 0, qs1 = 0, qs2 = 0, qs3 = 0;
+    auto flush = [&]() {
+        const int hh[4] = {qh0, qh1, qh2, qh3}, ss[4] = {qs0, qs1, qs2, qs3};
+        Vec8<ST> v[4][4];
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            const ST* p = j < q ? rbase + ((size_t)hh[j] * k + ss[j]) * d : rbase;
+#pragma unroll
+            for (int c = 0; c < 4; ++c) v[j][c] = vec8_load<ST>(p + 8 * c);
+        }
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            if (j < q) {
+#pragma unroll
+                for (int c = 0; c < 4; ++c) {
+                    float x[8];
+                    vec8_to_f32<ST>(v[j][c], x);
+#pragma unroll
+                    for (int e = 0; e < 8; ++e) acc[8 * c + e] += x[e];
+                }
+            }
+        }
+        q = 0;
+    };
+    auto push = [&](int h, int s) {
+        if (q == 0) { qh0 = h; qs0 = s; }
+        else if (q == 1) { qh1 = h; qs1 = s; }
+        else if (q == 2) { qh2 = h; qs2 = s; }
+        else { qh3 = h; qs3 = s; }
+        if (++q == 4) flush();
+    };
+
+    for (int h0 = 0; h0 < H; h0 += kCombineHeads) {
+        const int hn = min(kCombineHeads, H - h0);
+        __syncthreads();  // the previous pass's readers are done with s_slot
+        for (int e = tid; e < hn * 64; e += 256) {
+            const int hh = e >> 6, tl = e & 63;
+            const int tt = m0 + tl;
+            s_slot[tl * kCombineLdh + hh] = tt < T ? slot[((size_t)b * H + h0 + hh) * T + tt] : (int16_t)-1;
+        }
+        __syncthreads();
+        if (active) {
+            const int16_t* mine = s_slot + ml * kCombineLdh;
+            for (int hh = 0; hh < hn; hh += 8) {
+                int16_t sv[8];
+                if (hh + 8 <= hn) {
+                    const uint4 u = *reinterpret_cast<const uint4*>(mine + hh);
+                    sv[0] = (int16_t)(u.x & 0xffff); sv[1] = (int16_t)(u.x >> 16);
+                    sv[2] = (int16_t)(u.y & 0xffff); sv[3] = (int16_t)(u.y >> 16);
+                    sv[4] = (int16_t)(u.z & 0xffff); sv[5] = (int16_t)(u.z >> 16);
+                    sv[6] = (int16_t)(u.w & 0xffff); sv[7] = (int16_t)(u.w >> 16);
+                } else {
+#pragma unroll
+                    for (int j = 0; j < 8; ++j) sv[j] = hh + j < hn ? mine[hh + j] : (int16_t)-1;
+                }
+#pragma unroll
+                for (int j = 0; j < 8; ++j)
+                    if (sv[j] >= 0) push(h0 + hh + j, sv[j]);
+            }
+        }
+    }
+    if (active) {
+        if (q > 0) flush();
+        ST* y = out + ((size_t)b * T + t) * d + n0 + cq;
+#pragma unroll
+        for (int c = 0; c < 4; ++c) {
+            float x[8];
+            if (accumulate) {
+                vec8_to_f32<ST>(vec8_load<ST>(y + 8 * c), x);
+#pragma unroll
+                for (int e = 0; e < 8; ++e) x[e] += acc[8 * c + e];
+            } else {
+#pragma unroll
+                for (int e = 0; e < 8; ++e) x[e] = acc[8 * c + e];
+            }
+            vec8_store<ST>(y + 8 * c, vec8_from_f32<ST>(x));
+        }
+    }
+}
+
+}  // namespace mosa

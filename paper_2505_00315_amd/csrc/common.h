@@ -160,6 +160,25 @@ __device__ __forceinline__ void mma4(f32x4& acc, const Frag4<float>& a, const Fr
 
 __device__ __forceinline__ f32x4 zero4() { return f32x4{0.f, 0.f, 0.f, 0.f}; }
 
+// Division of non-negative x < 2^24 by a runtime n via a float reciprocal and
+// a one-step correction (exact in that range).
+struct FastDiv {
+    int n;
+    float inv;
+};
+inline FastDiv make_fastdiv(int n) { return {n, 1.0f / (float)n}; }
+__device__ __forceinline__ void fast_divmod(const FastDiv& f, int x, int& q, int& r) {
+    q = (int)((float)x * f.inv);
+    r = x - q * f.n;
+    if (r < 0) {
+        --q;
+        r += f.n;
+    } else if (r >= f.n) {
+        ++q;
+        r -= f.n;
+    }
+}
+
 // ---------------------------------------------------------------------------
 // Launch-order helper: the hardware dispatches workgroup b to XCD b % 8.
 // Renumber so that consecutive logical ids run on the same XCD and share

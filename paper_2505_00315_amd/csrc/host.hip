@@ -17,9 +17,9 @@ inline size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
 struct Layout {
     mosa_saved_layout saved;
     // forward scratch
-    size_t z, xnorm, unc_tok, unc_key, unc_sel;
+    size_t z, xnorm, unc_tok, unc_key, unc_sel, Xo;
     // backward scratch
-    size_t dA, D, dz, dQ, dK, dV, dAd, Dd, dQd, dKd, dVd;
+    size_t dA, D, dz, dz16, dQKV, dXs, dAd, Dd, dQKVd;
     size_t scratch_total;
 };
 
@@ -49,27 +49,24 @@ int validate_shape(const mosa_shape* s) {
     // index arithmetic inside the kernels uses 32-bit row counts
     const double rows = (double)s->batch * s->seq_len * (double)(s->heads > s->dense_heads ? s->heads : s->dense_heads);
     if (rows > 2.0e9) return MOSA_ERR_UNSUPPORTED;
+    // row counts of one head (B * k or B * T) are divided with a float reciprocal
+    if ((double)s->batch * s->seq_len >= 16777216.0) return MOSA_ERR_UNSUPPORTED;
     return MOSA_OK;
 }
 
 Layout make_layout(const mosa_shape* s) {
-    const size_t B = s->batch, T = s->seq_len, H = s->heads, Hd = s->dense_heads, dh = s->d_head;
+    const size_t B = s->batch, T = s->seq_len, d = s->d_model, H = s->heads, Hd = s->dense_heads, dh = s->d_head;
     const size_t k = s->heads > 0 ? (size_t)s->k : 0;
     const size_t es = s->dtype == MOSA_BF16 ? 2 : 4;
-    const size_t nseg = (size_t)seg_count(s->seq_len);
     Layout L;
     Carver sv;
     L.saved.I = sv.take(B * H * k * 4);
     L.saved.r = sv.take(B * H * k * 4);
-    L.saved.seg = sv.take(B * H * nseg * 4);
-    L.saved.Q = sv.take(B * H * k * dh * es);
-    L.saved.K = sv.take(B * H * k * dh * es);
-    L.saved.V = sv.take(B * H * k * dh * es);
+    L.saved.slot = sv.take(B * H * T * 2);
+    L.saved.QKV = sv.take(B * H * k * 3 * dh * es);
     L.saved.A = sv.take(B * H * k * dh * es);
     L.saved.lse = sv.take(B * H * k * 4);
-    L.saved.Qd = sv.take(B * Hd * T * dh * es);
-    L.saved.Kd = sv.take(B * Hd * T * dh * es);
-    L.saved.Vd = sv.take(B * Hd * T * dh * es);
+    L.saved.QKVd = sv.take(B * Hd * T * 3 * dh * es);
     L.saved.Ad = sv.take(B * Hd * T * dh * es);
     L.saved.lsed = sv.take(B * Hd * T * 4);
     L.saved.total = sv.total();
@@ -81,18 +78,17 @@ Layout make_layout(const mosa_shape* s) {
     L.unc_tok = fw.take(B * H * T * 4);
     L.unc_key = fw.take(B * H * T * 8);
     L.unc_sel = fw.take(B * H * T * 4);
+    L.Xo = fw.take(B * H * k * d * es);
     Carver bw;
     L.dA = bw.take(B * H * k * dh * es);
     L.D = bw.take(B * H * k * 4);
     L.dz = bw.take(B * H * k * 4);
-    L.dQ = bw.take(B * H * k * dh * es);
-    L.dK = bw.take(B * H * k * dh * es);
-    L.dV = bw.take(B * H * k * dh * es);
+    L.dz16 = bw.take(B * H * k * 16 * es);
+    L.dQKV = bw.take(B * H * k * 3 * dh * es);
+    L.dXs = bw.take(B * H * k * d * es);
     L.dAd = bw.take(B * Hd * T * dh * es);
     L.Dd = bw.take(B * Hd * T * 4);
-    L.dQd = bw.take(B * Hd * T * dh * es);
-    L.dKd = bw.take(B * Hd * T * dh * es);
-    L.dVd = bw.take(B * Hd * T * dh * es);
+    L.dQKVd = bw.take(B * Hd * T * 3 * dh * es);
     L.scratch_total = fw.total() > bw.total() ? fw.total() : bw.total();
     return L;
 }
@@ -188,39 +184,38 @@ int mosa_forward_timed(const mosa_shape* s, const void* X, const mosa_weights* w
     const int k = H > 0 ? s->k : 0, dt = s->dtype, causal = s->causal;
     int32_t* I = at<int32_t>(saved, L.saved.I);
     float* r = at<float>(saved, L.saved.r);
-    int32_t* seg = at<int32_t>(saved, L.saved.seg);
-    void* Q = at<char>(saved, L.saved.Q);
-    void* K = at<char>(saved, L.saved.K);
-    void* V = at<char>(saved, L.saved.V);
+    int16_t* slot = at<int16_t>(saved, L.saved.slot);
+    void* QKV = at<char>(saved, L.saved.QKV);
     void* A = at<char>(saved, L.saved.A);
     float* lse = at<float>(saved, L.saved.lse);
-    void* Qd = at<char>(saved, L.saved.Qd);
-    void* Kd = at<char>(saved, L.saved.Kd);
-    void* Vd = at<char>(saved, L.saved.Vd);
+    void* QKVd = at<char>(saved, L.saved.QKVd);
     void* Ad = at<char>(saved, L.saved.Ad);
     float* lsed = at<float>(saved, L.saved.lsed);
+    void* Xo = at<char>(scratch, L.Xo);
 
     if (H > 0) {
         float* z = at<float>(scratch, L.z);
         float* xnorm = at<float>(scratch, L.xnorm);
         e |= launch_router(dt, X, w->Wr, B, T, d, H, z, xnorm, stream);
         e |= sm.mark("router");
-        e |= launch_select(dt, z, xnorm, X, w->Wr, B, T, d, H, k, I, r, seg, at<int32_t>(scratch, L.unc_tok),
+        e |= launch_select(dt, z, xnorm, X, w->Wr, B, T, d, H, k, I, r, slot, at<int32_t>(scratch, L.unc_tok),
                            at<double>(scratch, L.unc_key), at<int32_t>(scratch, L.unc_sel), stream);
         e |= sm.mark("select");
-        e |= launch_qkv(dt, X, I, w->Wq, w->Wk, w->Wv, B, T, d, H, dh, k, Q, K, V, stream);
+        e |= launch_qkv(dt, X, I, w->Wq, w->Wk, w->Wv, B, T, d, H, dh, k, QKV, stream);
         e |= sm.mark("qkv");
-        e |= launch_attn_fwd(dt, Q, K, V, B * H, k, dh, causal, A, lse, stream);
+        e |= launch_attn_fwd(dt, QKV, B * H, k, dh, causal, A, lse, stream);
         e |= sm.mark("attn");
+        e |= launch_out_proj(dt, A, r, w->Wo, B, d, H, dh, k, Xo, stream);
+        e |= sm.mark("out_proj");
     }
     if (Hd > 0) {
-        e |= launch_qkv(dt, X, nullptr, w->Wq_d, w->Wk_d, w->Wv_d, B, T, d, Hd, dh, T, Qd, Kd, Vd, stream);
+        e |= launch_qkv(dt, X, nullptr, w->Wq_d, w->Wk_d, w->Wv_d, B, T, d, Hd, dh, T, QKVd, stream);
         e |= sm.mark("qkv_dense");
-        e |= launch_attn_fwd(dt, Qd, Kd, Vd, B * Hd, T, dh, causal, Ad, lsed, stream);
+        e |= launch_attn_fwd(dt, QKVd, B * Hd, T, dh, causal, Ad, lsed, stream);
         e |= sm.mark("attn_dense");
     }
-    e |= launch_out_scatter(dt, B, T, d, dh, H, k, I, r, seg, A, w->Wo, Hd, Ad, w->Wo_d, Y, accumulate, stream);
-    e |= sm.mark("out_scatter");
+    e |= launch_out_combine(dt, Ad, w->Wo_d, slot, Xo, B, T, d, H, dh, k, Hd, Y, accumulate, stream);
+    e |= sm.mark("out_combine");
     if (H > 0 && I_out)
         e |= hipMemcpyAsync(I_out, I, (size_t)B * H * k * 4, hipMemcpyDeviceToDevice, stream) != hipSuccess;
     if (H > 0 && r_out)
@@ -264,60 +259,57 @@ int mosa_backward_timed(const mosa_shape* s, const void* X, const mosa_weights* 
     const int k = H > 0 ? s->k : 0, dt = s->dtype, causal = s->causal;
     const int32_t* I = at<int32_t>(saved, L.saved.I);
     const float* r = at<float>(saved, L.saved.r);
-    const int32_t* seg = at<int32_t>(saved, L.saved.seg);
-    const void* Q = at<char>(saved, L.saved.Q);
-    const void* K = at<char>(saved, L.saved.K);
-    const void* V = at<char>(saved, L.saved.V);
+    const int16_t* slot = at<int16_t>(saved, L.saved.slot);
+    const void* QKV = at<char>(saved, L.saved.QKV);
     const void* A = at<char>(saved, L.saved.A);
     const float* lse = at<float>(saved, L.saved.lse);
-    const void* Qd = at<char>(saved, L.saved.Qd);
-    const void* Kd = at<char>(saved, L.saved.Kd);
-    const void* Vd = at<char>(saved, L.saved.Vd);
+    const void* QKVd = at<char>(saved, L.saved.QKVd);
     const void* Ad = at<char>(saved, L.saved.Ad);
     const float* lsed = at<float>(saved, L.saved.lsed);
     void* dA = at<char>(scratch, L.dA);
     float* D = at<float>(scratch, L.D);
     float* dz = at<float>(scratch, L.dz);
-    void* dQ = at<char>(scratch, L.dQ);
-    void* dK = at<char>(scratch, L.dK);
-    void* dV = at<char>(scratch, L.dV);
+    void* dz16 = at<char>(scratch, L.dz16);
+    void* dQKV = at<char>(scratch, L.dQKV);
+    void* dXs = at<char>(scratch, L.dXs);
     void* dAd = at<char>(scratch, L.dAd);
     float* Dd = at<float>(scratch, L.Dd);
-    void* dQd = at<char>(scratch, L.dQd);
-    void* dKd = at<char>(scratch, L.dKd);
-    void* dVd = at<char>(scratch, L.dVd);
+    void* dQKVd = at<char>(scratch, L.dQKVd);
 
     if (H > 0) {
-        e |= launch_dattn_out(dt, dY, I, r, w->Wo, A, B, T, d, H, dh, k, dA, D, dz, stream);
+        e |= launch_dattn_out(dt, dY, I, r, w->Wo, A, B, T, d, H, dh, k, dA, D, dz, dz16, stream);
         e |= sm.mark("bwd_out");
-        e |= launch_attn_bwd(dt, Q, K, V, dA, lse, D, B * H, k, dh, causal, dQ, dK, dV, 0, stream);
+        e |= launch_attn_bwd(dt, QKV, dA, lse, D, B * H, k, dh, causal, dQKV, 0, stream);
         e |= sm.mark("attn_bwd_kv");
-        e |= launch_attn_bwd(dt, Q, K, V, dA, lse, D, B * H, k, dh, causal, dQ, dK, dV, 1, stream);
+        e |= launch_attn_bwd(dt, QKV, dA, lse, D, B * H, k, dh, causal, dQKV, 1, stream);
         e |= sm.mark("attn_bwd_q");
-        e |= launch_wgrad(dt, X, dY, I, r, A, dQ, dK, dV, dz, B, T, d, H, dh, k, g->dWq, g->dWk, g->dWv, g->dWr,
-                          g->dWo, 0, stream);
+        e |= launch_wgrad(dt, X, dY, I, r, A, dQKV, dz16, B, T, d, H, dh, k, g->dWq, g->dWk, g->dWv, g->dWr, g->dWo,
+                          0, stream);
         e |= sm.mark("wgrad_qkv");
-        e |= launch_wgrad(dt, X, dY, I, r, A, dQ, dK, dV, dz, B, T, d, H, dh, k, g->dWq, g->dWk, g->dWv, g->dWr,
-                          g->dWo, 1, stream);
+        e |= launch_wgrad(dt, X, dY, I, r, A, dQKV, dz16, B, T, d, H, dh, k, g->dWq, g->dWk, g->dWv, g->dWr, g->dWo,
+                          1, stream);
         e |= sm.mark("wgrad_o");
+        e |= launch_dx_proj(dt, dQKV, dz, w->Wq, w->Wk, w->Wv, w->Wr, B, d, H, dh, k, dXs, stream);
+        e |= sm.mark("dx_proj");
     }
     if (Hd > 0) {
-        e |= launch_dattn_out(dt, dY, nullptr, nullptr, w->Wo_d, Ad, B, T, d, Hd, dh, T, dAd, Dd, nullptr, stream);
+        e |= launch_dattn_out(dt, dY, nullptr, nullptr, w->Wo_d, Ad, B, T, d, Hd, dh, T, dAd, Dd, nullptr, nullptr,
+                              stream);
         e |= sm.mark("bwd_out_dense");
-        e |= launch_attn_bwd(dt, Qd, Kd, Vd, dAd, lsed, Dd, B * Hd, T, dh, causal, dQd, dKd, dVd, 0, stream);
+        e |= launch_attn_bwd(dt, QKVd, dAd, lsed, Dd, B * Hd, T, dh, causal, dQKVd, 0, stream);
         e |= sm.mark("attn_bwd_kv_dense");
-        e |= launch_attn_bwd(dt, Qd, Kd, Vd, dAd, lsed, Dd, B * Hd, T, dh, causal, dQd, dKd, dVd, 1, stream);
+        e |= launch_attn_bwd(dt, QKVd, dAd, lsed, Dd, B * Hd, T, dh, causal, dQKVd, 1, stream);
         e |= sm.mark("attn_bwd_q_dense");
-        e |= launch_wgrad(dt, X, dY, nullptr, nullptr, Ad, dQd, dKd, dVd, nullptr, B, T, d, Hd, dh, T, g->dWq_d,
-                          g->dWk_d, g->dWv_d, nullptr, g->dWo_d, 0, stream);
+        e |= launch_wgrad(dt, X, dY, nullptr, nullptr, Ad, dQKVd, nullptr, B, T, d, Hd, dh, T, g->dWq_d, g->dWk_d,
+                          g->dWv_d, nullptr, g->dWo_d, 0, stream);
         e |= sm.mark("wgrad_qkv_dense");
-        e |= launch_wgrad(dt, X, dY, nullptr, nullptr, Ad, dQd, dKd, dVd, nullptr, B, T, d, Hd, dh, T, g->dWq_d,
-                          g->dWk_d, g->dWv_d, nullptr, g->dWo_d, 1, stream);
+        e |= launch_wgrad(dt, X, dY, nullptr, nullptr, Ad, dQKVd, nullptr, B, T, d, Hd, dh, T, g->dWq_d, g->dWk_d,
+                          g->dWv_d, nullptr, g->dWo_d, 1, stream);
         e |= sm.mark("wgrad_o_dense");
     }
-    e |= launch_dx_scatter(dt, B, T, d, dh, H, k, I, seg, dQ, dK, dV, dz, w->Wq, w->Wk, w->Wv, w->Wr, Hd, dQd, dKd,
-                           dVd, w->Wq_d, w->Wk_d, w->Wv_d, dX, accumulate_dX, stream);
-    e |= sm.mark("dx_scatter");
+    e |= launch_dx_combine(dt, dQKVd, w->Wq_d, w->Wk_d, w->Wv_d, slot, dXs, B, T, d, H, dh, k, Hd, dX, accumulate_dX,
+                           stream);
+    e |= sm.mark("dx_combine");
     return e ? MOSA_ERR_HIP : MOSA_OK;
 }
 

@@ -20,7 +20,7 @@
 //      which is order-independent), and the k - #in best of them under
 //      (key desc, index asc) are chosen by exact rank;
 //   4. an in-order block scan compacts the chosen tokens: I ascending,
-//      r = sigmoid(z~), and the per-64-token segment table seg.
+//      r = sigmoid(z~), and the token -> slot map (slot of t in I, or -1).
 //
 // The error bound of z~ (router.hip): every K = 32 MFMA chunk starts from
 // zero; its result is taken to differ from the exact chunk sum by at most
@@ -69,7 +69,7 @@ template <typename ST, int EPT>
 __global__ __launch_bounds__(256) void select_kernel(const float* __restrict__ z, const float* __restrict__ xnorm,
                                                      const ST* __restrict__ X, const ST* __restrict__ Wr, int T,
                                                      int d, int H, int k, int32_t* __restrict__ I,
-                                                     float* __restrict__ r, int32_t* __restrict__ seg, int nseg,
+                                                     float* __restrict__ r, int16_t* __restrict__ slot,
                                                      int32_t* __restrict__ unc_tok, double* __restrict__ unc_key,
                                                      int32_t* __restrict__ unc_sel) {
     __shared__ double s_red[4];
@@ -244,14 +244,18 @@ __global__ __launch_bounds__(256) void select_kernel(const float* __restrict__ z
         int pos = sbase;
 #pragma unroll
         for (int e = 0; e < EPT; ++e) {
+            const int t = t0 + e;
+            if (t >= T) break;
+            int16_t sl = -1;
             if ((selmask >> e) & 1ull) {
-                const int t = t0 + e;
                 if (pos < k) {
                     I[(size_t)row * k + pos] = t;
                     r[(size_t)row * k + pos] = 1.0f / (1.0f + expf(-zr[t]));
+                    sl = (int16_t)pos;
                 }
                 ++pos;
             }
+            slot[rowT + t] = sl;
         }
     }
     // Only reachable if the logit error bound were violated: keep every slot
@@ -260,28 +264,16 @@ __global__ __launch_bounds__(256) void select_kernel(const float* __restrict__ z
         I[(size_t)row * k + pos] = 0;
         r[(size_t)row * k + pos] = 0.f;
     }
-    // seg[j] = number of chosen tokens < 64 j (never more than k).
-    for (int j = 0; j < nseg; ++j) {
-        const int bt = j * kSegWidth;
-        if (bt >= T) {
-            if (tid == 0) seg[(size_t)row * nseg + j] = min(tot_sel, k);
-        } else if (bt >= t0 && bt < t0 + EPT) {
-            const int off = bt - t0;
-            const uint64_t below = off == 0 ? 0ull : (selmask & ((off >= 64) ? ~0ull : ((1ull << off) - 1ull)));
-            seg[(size_t)row * nseg + j] = min(sbase + __popcll(below), k);
-        }
-    }
 }
 
 template <typename ST>
 int launch_select_t(const float* z, const float* xnorm, const ST* X, const ST* Wr, int B, int T, int d, int H,
-                    int k, int32_t* I, float* r, int32_t* seg, int32_t* unc_tok, double* unc_key,
+                    int k, int32_t* I, float* r, int16_t* slot, int32_t* unc_tok, double* unc_key,
                     int32_t* unc_sel, hipStream_t stream) {
     dim3 grid(B * H), block(256);
-    const int nseg = seg_count(T);
 #define MOSA_SELECT_CASE(E)                                                                               \
     hipLaunchKernelGGL((select_kernel<ST, E>), grid, block, 0, stream, z, xnorm, X, Wr, T, d, H, k, I, r, \
-                       seg, nseg, unc_tok, unc_key, unc_sel)
+                       slot, unc_tok, unc_key, unc_sel)
     if (T <= 256) MOSA_SELECT_CASE(1);
     else if (T <= 512) MOSA_SELECT_CASE(2);
     else if (T <= 1024) MOSA_SELECT_CASE(4);
@@ -296,12 +288,12 @@ int launch_select_t(const float* z, const float* xnorm, const ST* X, const ST* W
 }  // namespace
 
 int launch_select(int dtype, const float* z, const float* xnorm, const void* X, const void* Wr, int B, int T,
-                  int d, int H, int k, int32_t* I, float* r, int32_t* seg, int32_t* unc_tok, double* unc_key,
+                  int d, int H, int k, int32_t* I, float* r, int16_t* slot, int32_t* unc_tok, double* unc_key,
                   int32_t* unc_sel, hipStream_t stream) {
     if (dtype == kBF16)
         return launch_select_t<uint16_t>(z, xnorm, (const uint16_t*)X, (const uint16_t*)Wr, B, T, d, H, k, I, r,
-                                         seg, unc_tok, unc_key, unc_sel, stream);
-    return launch_select_t<float>(z, xnorm, (const float*)X, (const float*)Wr, B, T, d, H, k, I, r, seg, unc_tok,
+                                         slot, unc_tok, unc_key, unc_sel, stream);
+    return launch_select_t<float>(z, xnorm, (const float*)X, (const float*)Wr, B, T, d, H, k, I, r, slot, unc_tok,
                                   unc_key, unc_sel, stream);
 }
 

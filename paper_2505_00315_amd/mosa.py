@@ -26,7 +26,7 @@ MAX_STAGES = 32
 
 WEIGHT_NAMES = ("Wr", "Wq", "Wk", "Wv", "Wo", "Wq_d", "Wk_d", "Wv_d", "Wo_d")
 GRAD_NAMES = tuple("d" + n for n in WEIGHT_NAMES)
-SAVED_NAMES = ("I", "r", "seg", "Q", "K", "V", "A", "lse", "Qd", "Kd", "Vd", "Ad", "lsed")
+SAVED_NAMES = ("I", "r", "slot", "QKV", "A", "lse", "QKVd", "Ad", "lsed")
 
 
 class Shape(ctypes.Structure):
@@ -176,16 +176,18 @@ def backward(shape: Shape, X, w, dY, saved, grads, dX=None, accumulate_dX=False,
 
 
 def saved_view(shape: Shape, saved, name):
-    """Typed view of one tensor the forward keeps in ``saved`` (for inspection)."""
+    """Typed view of one tensor the forward keeps in ``saved`` (for inspection).
+    "Q", "K", "V" (and "Qd", "Kd", "Vd") are slices of the packed QKV rows."""
+    part = {"Q": 0, "K": 1, "V": 2, "Qd": 0, "Kd": 1, "Vd": 2}
+    if name in part:
+        whole = saved_view(shape, saved, "QKV" if len(name) == 1 else "QKVd")
+        return whole[..., part[name], :]
     off = saved_offsets(shape)
     B, T, H, Hd, k, dh = shape.batch, shape.seq_len, shape.heads, shape.dense_heads, shape.k, shape.d_head
-    nseg = (T + 63) // 64 + 1
     st = torch_dtype(shape)
-    spec = {"I": (torch.int32, (B, H, k)), "r": (torch.float32, (B, H, k)), "seg": (torch.int32, (B, H, nseg)),
-            "Q": (st, (B, H, k, dh)), "K": (st, (B, H, k, dh)), "V": (st, (B, H, k, dh)),
-            "A": (st, (B, H, k, dh)), "lse": (torch.float32, (B, H, k)),
-            "Qd": (st, (B, Hd, T, dh)), "Kd": (st, (B, Hd, T, dh)), "Vd": (st, (B, Hd, T, dh)),
-            "Ad": (st, (B, Hd, T, dh)), "lsed": (torch.float32, (B, Hd, T))}[name]
+    spec = {"I": (torch.int32, (B, H, k)), "r": (torch.float32, (B, H, k)), "slot": (torch.int16, (B, H, T)),
+            "QKV": (st, (B, H, k, 3, dh)), "A": (st, (B, H, k, dh)), "lse": (torch.float32, (B, H, k)),
+            "QKVd": (st, (B, Hd, T, 3, dh)), "Ad": (st, (B, Hd, T, dh)), "lsed": (torch.float32, (B, Hd, T))}[name]
     dt, shp = spec
     n = 1
     for s in shp:

@@ -26,10 +26,14 @@ def _pairs(n, causal):
 
 
 def stage_work(w, with_backward=True):
-    """Algorithmic work of every stage the library times, keyed by stage name."""
+    """Algorithmic work of every kernel the library times, keyed by stage name.
+    The output side (out_proj + out_combine) and the dX side (dx_proj +
+    dx_combine) are accounted as one stage each (GROUPS): their algorithmic
+    bytes are those of the paper's operation (A, W^O and Y once; the per-head
+    k x d rows that the two-kernel design writes and reads back are not
+    algorithmic traffic)."""
     es = 2 if w.dtype == "bf16" else 4
     B, T, d, H, dh, k, Hd = w.batch, w.seq_len, w.d_model, w.heads, w.d_head, w.k, w.dense_heads
-    nseg = (T + 63) // 64 + 1
     X = B * T * d * es
     rows = B * H * k  # selected rows over all heads
     out = {}
@@ -39,7 +43,7 @@ def stage_work(w, with_backward=True):
 
     if H:
         add("router", X + H * d * es + B * H * T * 4 + B * T * 4, 2.0 * B * T * H * d)
-        add("select", B * H * T * 4 + B * T * 4 + H * d * es + rows * 8 + B * H * nseg * 4, 0.0)
+        add("select", B * H * T * 4 + B * T * 4 + H * d * es + rows * 8 + B * H * T * 2, 0.0)
         add("qkv", X + 3 * H * d * dh * es + 3 * rows * dh * es + rows * 4, 2.0 * rows * d * 3 * dh)
         add("attn", 4 * rows * dh * es + rows * 4, 4.0 * dh * _pairs(k, w.causal) * B * H)
     if Hd:
@@ -68,6 +72,23 @@ def stage_work(w, with_backward=True):
         3 * rows * dh * es + rows * 8 + 3 * H * d * dh * es + H * d * es
         + 3 * B * Hd * T * dh * es + 3 * Hd * d * dh * es + X,
         2.0 * rows * 3 * dh * d + 2.0 * rows * d + 2.0 * B * Hd * T * 3 * dh * d)
+    return out
+
+
+# Stages made of two kernels (the library records one event per kernel).
+GROUPS = {"out_scatter": ("out_proj", "out_combine"), "dx_scatter": ("dx_proj", "dx_combine")}
+
+
+def group_stage_times(kernel_ms):
+    """Per-stage times from per-kernel times: a group is the sum of its kernels."""
+    out = {}
+    for name, ms in kernel_ms.items():
+        for g, members in GROUPS.items():
+            if name in members:
+                out[g] = out.get(g, 0.0) + ms
+                break
+        else:
+            out[name] = ms
     return out
 
 

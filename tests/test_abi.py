@@ -39,7 +39,7 @@ def test_workspace_size_and_layout():
     off = mosa.saved_offsets(s)
     assert off["total"] == saved
     B, T, H, Hd, k, dh = 8, 1024, 256, 4, 16, 64
-    assert off["Q"] >= B * H * k * 4 * 2  # after I and r
+    assert off["QKV"] >= B * H * k * 4 * 2 + B * H * T * 2  # after I, r and the slot map
     assert saved >= 4 * B * H * k * dh * 2 + 4 * B * Hd * T * dh * 2
     assert scratch >= B * H * T * 4
     for v in off.values():
