@@ -108,7 +108,8 @@ typedef struct mosa_grads {
  *   I [B,H,k] int32 ascending; r [B,H,k] fp32;
  *   slot [B,H,T] int16: position of token t in I[b,h,:], or -1;
  *   QKV [B,H,k,3,dh] storage type: packed rows q | k | v of the selected tokens;
- *   A [B,H,k,dh] storage type (attention output before the router scaling);
+ *   A [B,H,k,dh] storage type (attention output rows already scaled by the
+ *     router value: r_i (softmax(Q K^T / sqrt(dh) + M) V)_i);
  *   lse [B,H,k] fp32 (natural-log sum of exp of the scaled scores);
  *   the same for the dense heads with k = T: QKVd [B,Hd,T,3,dh], Ad [B,Hd,T,dh],
  *   lsed [B,Hd,T]. */

@@ -13,7 +13,9 @@
 //   O^T += V^T P^T     MFMA K = 16 over the 16 keys: the S^T tile is already
 //                      in the K = 16 operand layout, so P never leaves the
 //                      registers.
-// Outputs A (= O / l, storage type) and lse = m + log(l) (fp32, natural log).
+// Outputs A = r_i O_i / l_i (storage type; the router value r_i of the row
+// applied once here, as Section 2.2's diag(r), so later stages read a scaled
+// row; r = 1 for dense heads) and lse = m + log(l) (fp32, natural log).
 #include "common.h"
 #include "kernels.h"
 
@@ -23,7 +25,8 @@ namespace {
 
 template <typename ST, int DH>
 __global__ __launch_bounds__(256) void attn_fwd_kernel(const ST* __restrict__ QKV, int BH, int n, int causal,
-                                                       float scale, ST* __restrict__ A, float* __restrict__ lse) {
+                                                       float scale, const float* __restrict__ rw, ST* __restrict__ A,
+                                                       float* __restrict__ lse) {
     constexpr int RS = 3 * DH;  // row stride of the packed Q | K | V rows
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int g = lane >> 4, c16 = lane & 15;
@@ -93,7 +96,7 @@ __global__ __launch_bounds__(256) void attn_fwd_kernel(const ST* __restrict__ QK
         }
     }
     if (q < n) {
-        const float inv = 1.f / l_run;
+        const float inv = (rw ? rw[(size_t)bh * n + q] : 1.f) / l_run;
         ST* Ap = A + ((size_t)bh * n + q) * DH;
 #pragma unroll
         for (int db = 0; db < DH / 16; ++db)
@@ -104,24 +107,25 @@ __global__ __launch_bounds__(256) void attn_fwd_kernel(const ST* __restrict__ QK
 }
 
 template <typename ST>
-int launch_attn_fwd_t(const ST* QKV, int BH, int n, int dh, int causal, ST* A, float* lse, hipStream_t stream) {
+int launch_attn_fwd_t(const ST* QKV, const float* r, int BH, int n, int dh, int causal, ST* A, float* lse,
+                     hipStream_t stream) {
     const int tasks = BH * ((n + 15) / 16);
     dim3 grid((tasks + 3) / 4), block(256);
     const float scale = 1.0f / sqrtf((float)dh);
     if (dh == 64)
-        hipLaunchKernelGGL((attn_fwd_kernel<ST, 64>), grid, block, 0, stream, QKV, BH, n, causal, scale, A, lse);
+        hipLaunchKernelGGL((attn_fwd_kernel<ST, 64>), grid, block, 0, stream, QKV, BH, n, causal, scale, r, A, lse);
     else
-        hipLaunchKernelGGL((attn_fwd_kernel<ST, 32>), grid, block, 0, stream, QKV, BH, n, causal, scale, A, lse);
+        hipLaunchKernelGGL((attn_fwd_kernel<ST, 32>), grid, block, 0, stream, QKV, BH, n, causal, scale, r, A, lse);
     return hipGetLastError() == hipSuccess ? 0 : -1;
 }
 
 }  // namespace
 
-int launch_attn_fwd(int dtype, const void* QKV, int BH, int n, int dh, int causal, void* A, float* lse,
+int launch_attn_fwd(int dtype, const void* QKV, const float* r, int BH, int n, int dh, int causal, void* A, float* lse,
                     hipStream_t stream) {
     if (dtype == kBF16)
-        return launch_attn_fwd_t<uint16_t>((const uint16_t*)QKV, BH, n, dh, causal, (uint16_t*)A, lse, stream);
-    return launch_attn_fwd_t<float>((const float*)QKV, BH, n, dh, causal, (float*)A, lse, stream);
+        return launch_attn_fwd_t<uint16_t>((const uint16_t*)QKV, r, BH, n, dh, causal, (uint16_t*)A, lse, stream);
+    return launch_attn_fwd_t<float>((const float*)QKV, r, BH, n, dh, causal, (float*)A, lse, stream);
 }
 
 }  // namespace mosa

@@ -6,6 +6,8 @@
 //   dA_i     = r_i dA~_i                       (into the attention backward)
 //   D_i      = <dA_i, A_i> = r_i dr_i          (softmax row term of Eq. 1's backward)
 //   dz_i     = dr_i r_i (1 - r_i)              (sigma'(s) = r (1 - r))
+// The forward saved the scaled rows S_i = r_i A_i, so D_i = <dA~_i, S_i> and
+// dz_i = D_i (1 - r_i): no division by r, and r = 0 gives dz = D = 0.
 // Dense heads are the case I = identity, r = 1 (no dz).
 //
 // One GEMM per head on the tiled MFMA engine: M = B*n gathered dY rows,
@@ -31,7 +33,7 @@ struct BwdOutPolicy {
         const int32_t* I;  // nullptr: dense head
         const float* r;    // nullptr: dense head
         const ST* Wo;      // [H, DH, d]
-        const ST* A;       // [B, H, n, DH]
+        const ST* A;       // [B, H, n, DH], rows scaled by r
         ST* dA;
         float* D;
         float* dz;         // nullptr: dense head
@@ -87,9 +89,11 @@ struct BwdOutPolicy {
             for (int q = 0; q < CW / 8; ++q) {
                 float x[8];
                 vec8_to_f32<ST>(vec8_load<ST>(a.A + ri * DH + cq + 8 * q), x);
+                float cv[8];
+                cs_load8(Cs, ldc, ml, cq + 8 * q, cv);
 #pragma unroll
                 for (int j = 0; j < 8; ++j) {
-                    c[8 * q + j] = Cs[ml * ldc + cq + 8 * q + j];
+                    c[8 * q + j] = cv[j];
                     part += c[8 * q + j] * x[j];
                 }
             }
@@ -106,9 +110,9 @@ struct BwdOutPolicy {
             vec8_store<ST>(a.dA + ri * DH + cq + 8 * q, vec8_from_f32<ST>(x));
         }
         if ((tid & 3) == 0) {
-            a.D[ri] = rr * part;
+            a.D[ri] = part;
             if (a.dz) {
-                const float dzv = part * rr * (1.f - rr);
+                const float dzv = part * (1.f - rr);
                 a.dz[ri] = dzv;
                 float x[8] = {dzv, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f}, zz[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
                 vec8_store<ST>(a.dz16 + ri * 16, vec8_from_f32<ST>(x));

@@ -5,7 +5,8 @@
 // columns each, starting from the fp32 tile value the GEMM left in LDS.  The
 // MoSA heads that selected token t are found from the slot map
 // slot[b, h, t] (position of t among head h's selected tokens, or -1): the
-// map for 64 tokens x 256 heads is staged in LDS token-major, each thread
+// map for 64 tokens x 256 heads is staged in LDS token-major (16-byte loads
+// of 8 tokens when T % 8 == 0), each thread
 // scans its token's heads 8 at a time, and the rows of the hits are fetched
 // four at a time (16 loads in flight) and added in ascending head order.
 // Every output element is thus produced by one thread in a fixed order
@@ -69,10 +70,38 @@ __device__ __forceinline__ void combine_tile(const float* Cs, int ldc, int tid, 
     for (int h0 = 0; h0 < H; h0 += kCombineHeads) {
         const int hn = min(kCombineHeads, H - h0);
         __syncthreads();  // the previous pass's readers are done with s_slot
-        for (int e = tid; e < hn * 64; e += 256) {
-            const int hh = e >> 6, tl = e & 63;
-            const int tt = m0 + tl;
-            s_slot[tl * kCombineLdh + hh] = tt < T ? slot[((size_t)b * H + h0 + hh) * T + tt] : (int16_t)-1;
+        if ((T & 7) == 0) {
+            // 8 tokens of one head per 16-byte load (rows of the map are
+            // 16-byte aligned when T % 8 == 0); up to 8 loads in flight per
+            // thread, then transposed into the token-major table.
+            for (int e0 = 0; e0 < hn * 8; e0 += 8 * 256) {
+                uint4 v[8];
+#pragma unroll
+                for (int u = 0; u < 8; ++u) {
+                    const int e = e0 + u * 256 + tid, hh = e >> 3, q = e & 7;
+                    const bool in = e < hn * 8 && m0 + 8 * q < T;
+                    const size_t off = in ? ((size_t)b * H + h0 + hh) * T + m0 + 8 * q : 0;
+                    v[u] = *reinterpret_cast<const uint4*>(slot + off);
+                    if (!in) v[u] = make_uint4(0xffffffffu, 0xffffffffu, 0xffffffffu, 0xffffffffu);
+                }
+#pragma unroll
+                for (int u = 0; u < 8; ++u) {
+                    const int e = e0 + u * 256 + tid, hh = e >> 3, q = e & 7;
+                    if (e < hn * 8) {
+                        const uint32_t w[4] = {v[u].x, v[u].y, v[u].z, v[u].w};
+                        int16_t* dst = s_slot + (8 * q) * kCombineLdh + hh;
+#pragma unroll
+                        for (int j = 0; j < 8; ++j)
+                            dst[j * kCombineLdh] = (int16_t)((j & 1) ? (w[j >> 1] >> 16) : (w[j >> 1] & 0xffffu));
+                    }
+                }
+            }
+        } else {
+            for (int e = tid; e < hn * 64; e += 256) {
+                const int hh = e >> 6, tl = e & 63;
+                const int tt = m0 + tl;
+                s_slot[tl * kCombineLdh + hh] = tt < T ? slot[((size_t)b * H + h0 + hh) * T + tt] : (int16_t)-1;
+            }
         }
         __syncthreads();
         if (active) {

@@ -19,17 +19,20 @@ namespace mosa {
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef short s16x4 __attribute__((ext_vector_type(4)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x2 __attribute__((ext_vector_type(2)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 
 constexpr int kWave = 64;
 
 __device__ __forceinline__ float bf16_to_f32(uint16_t b) { return __uint_as_float((uint32_t)b << 16); }
 
 // Round to nearest, ties to even (NaN stays NaN).
-__device__ __forceinline__ uint16_t f32_to_bf16(float f) {
-    uint32_t u = __float_as_uint(f);
-    if ((u & 0x7fffffffu) > 0x7f800000u) return (uint16_t)((u >> 16) | 0x40u);
-    u += 0x7fffu + ((u >> 16) & 1u);
-    return (uint16_t)(u >> 16);
+// Round to nearest even (gfx950 converts in hardware: v_cvt_pk_bf16_f32).
+__device__ __forceinline__ uint16_t f32_to_bf16(float f) { return __builtin_bit_cast(uint16_t, (__bf16)f); }
+// Two floats to a packed pair of bf16 (lo in bits 0..15), one instruction.
+__device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
+    const f32x2 f = {lo, hi};
+    return __builtin_bit_cast(uint32_t, __builtin_convertvector(f, bf16x2));
 }
 
 // Neighbouring floats of a finite value (toward +inf / -inf).
@@ -88,10 +91,10 @@ template <> __device__ __forceinline__ Frag8<float> frag8_load<float>(const floa
 template <typename ST> __device__ __forceinline__ Frag8<ST> frag8_from(const float (&x)[8]);
 template <> __device__ __forceinline__ Frag8<uint16_t> frag8_from<uint16_t>(const float (&x)[8]) {
     uint4 u;
-    u.x = (uint32_t)f32_to_bf16(x[0]) | ((uint32_t)f32_to_bf16(x[1]) << 16);
-    u.y = (uint32_t)f32_to_bf16(x[2]) | ((uint32_t)f32_to_bf16(x[3]) << 16);
-    u.z = (uint32_t)f32_to_bf16(x[4]) | ((uint32_t)f32_to_bf16(x[5]) << 16);
-    u.w = (uint32_t)f32_to_bf16(x[6]) | ((uint32_t)f32_to_bf16(x[7]) << 16);
+    u.x = pack_bf16x2(x[0], x[1]);
+    u.y = pack_bf16x2(x[2], x[3]);
+    u.z = pack_bf16x2(x[4], x[5]);
+    u.w = pack_bf16x2(x[6], x[7]);
     Frag8<uint16_t> f;
     f.v = __builtin_bit_cast(bf16x8, u);
     return f;
@@ -136,11 +139,9 @@ template <> struct Frag4<float> { float v[4]; };
 
 template <typename ST> __device__ __forceinline__ Frag4<ST> frag4_from(const float (&x)[4]);
 template <> __device__ __forceinline__ Frag4<uint16_t> frag4_from<uint16_t>(const float (&x)[4]) {
+    const uint32_t lo = pack_bf16x2(x[0], x[1]), hi = pack_bf16x2(x[2], x[3]);
     Frag4<uint16_t> f;
-    f.v[0] = (short)f32_to_bf16(x[0]);
-    f.v[1] = (short)f32_to_bf16(x[1]);
-    f.v[2] = (short)f32_to_bf16(x[2]);
-    f.v[3] = (short)f32_to_bf16(x[3]);
+    f.v = __builtin_bit_cast(s16x4, make_uint2(lo, hi));
     return f;
 }
 template <> __device__ __forceinline__ Frag4<float> frag4_from<float>(const float (&x)[4]) {

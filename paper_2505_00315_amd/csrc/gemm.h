@@ -79,10 +79,10 @@ template <> __device__ __forceinline__ void vec8_to_f32<float>(const Vec8<float>
 template <typename ST> __device__ __forceinline__ Vec8<ST> vec8_from_f32(const float (&x)[8]);
 template <> __device__ __forceinline__ Vec8<uint16_t> vec8_from_f32<uint16_t>(const float (&x)[8]) {
     uint4 u;
-    u.x = (uint32_t)f32_to_bf16(x[0]) | ((uint32_t)f32_to_bf16(x[1]) << 16);
-    u.y = (uint32_t)f32_to_bf16(x[2]) | ((uint32_t)f32_to_bf16(x[3]) << 16);
-    u.z = (uint32_t)f32_to_bf16(x[4]) | ((uint32_t)f32_to_bf16(x[5]) << 16);
-    u.w = (uint32_t)f32_to_bf16(x[6]) | ((uint32_t)f32_to_bf16(x[7]) << 16);
+    u.x = pack_bf16x2(x[0], x[1]);
+    u.y = pack_bf16x2(x[2], x[3]);
+    u.z = pack_bf16x2(x[4], x[5]);
+    u.w = pack_bf16x2(x[6], x[7]);
     return {u};
 }
 template <> __device__ __forceinline__ Vec8<float> vec8_from_f32<float>(const float (&x)[8]) {
@@ -381,14 +381,7 @@ __global__ __launch_bounds__(256) void gemm_kernel(const typename P::Args args) 
         commit(0);
         __syncthreads();
     }
-    // The fetch and commit of the chunk after the last one are done too (all
-    // of its vectors are out of range and read as zeros into the unused
-    // buffer): with no conditional load in the loop body, the waits for the
-    // loads of chunk c+1 stay at the commit.
-    for (int c = 0; c < nchunks; ++c) {
-        const int buf = c & 1;
-        const typename P::RowInfo r2 = rows_load((c + 2) * KC);
-        fetch((c + 1) * KC, buf ^ 1);
+    auto mfma_chunk = [&](int buf) {
         const ST* a = As + buf * MT * LDK;
         const ST* b = Bs + buf * NT * LDK;
 #pragma unroll
@@ -405,9 +398,26 @@ __global__ __launch_bounds__(256) void gemm_kernel(const typename P::Args args) 
 #pragma unroll
                 for (int j = 0; j < S::FN; ++j) mma8(acc[i][j], fa[i], fb[j]);
         }
+    };
+    // Every chunk but the last: the loop body has no conditional load, so the
+    // waits for the loads of chunk c+1 stay at the commit.  The last chunk's
+    // MFMAs are peeled off below.
+    for (int c = 0; c < nchunks - 1; ++c) {
+        const int buf = c & 1;
+        const typename P::RowInfo r2 = rows_load((c + 2) * KC);
+        // keep the compiler from sinking these loads towards their uses: the
+        // row-info load goes first, the chunk's data loads before the MFMAs
+        __builtin_amdgcn_sched_barrier(0);
+        fetch((c + 1) * KC, buf ^ 1);
+        __builtin_amdgcn_sched_barrier(0);
+        mfma_chunk(buf);
         rows_store(r2, buf);  // rows of chunk c were consumed by fetch(c) one step earlier
         commit(buf ^ 1);
         __syncthreads();
+    }
+    if (nchunks > 0) {
+        mfma_chunk((nchunks - 1) & 1);
+        __syncthreads();  // the C tile below reuses the operand buffers
     }
 
     // C tile to LDS: Cs[m][n], row stride NT + 4 floats

@@ -203,15 +203,15 @@ int mosa_forward_timed(const mosa_shape* s, const void* X, const mosa_weights* w
         e |= sm.mark("select");
         e |= launch_qkv(dt, X, I, w->Wq, w->Wk, w->Wv, B, T, d, H, dh, k, QKV, stream);
         e |= sm.mark("qkv");
-        e |= launch_attn_fwd(dt, QKV, B * H, k, dh, causal, A, lse, stream);
+        e |= launch_attn_fwd(dt, QKV, r, B * H, k, dh, causal, A, lse, stream);
         e |= sm.mark("attn");
-        e |= launch_out_proj(dt, A, r, w->Wo, B, d, H, dh, k, Xo, stream);
+        e |= launch_out_proj(dt, A, w->Wo, B, d, H, dh, k, Xo, stream);
         e |= sm.mark("out_proj");
     }
     if (Hd > 0) {
         e |= launch_qkv(dt, X, nullptr, w->Wq_d, w->Wk_d, w->Wv_d, B, T, d, Hd, dh, T, QKVd, stream);
         e |= sm.mark("qkv_dense");
-        e |= launch_attn_fwd(dt, QKVd, B * Hd, T, dh, causal, Ad, lsed, stream);
+        e |= launch_attn_fwd(dt, QKVd, nullptr, B * Hd, T, dh, causal, Ad, lsed, stream);
         e |= sm.mark("attn_dense");
     }
     e |= launch_out_combine(dt, Ad, w->Wo_d, slot, Xo, B, T, d, H, dh, k, Hd, Y, accumulate, stream);
@@ -283,10 +283,10 @@ int mosa_backward_timed(const mosa_shape* s, const void* X, const mosa_weights* 
         e |= sm.mark("attn_bwd_kv");
         e |= launch_attn_bwd(dt, QKV, dA, lse, D, B * H, k, dh, causal, dQKV, 1, stream);
         e |= sm.mark("attn_bwd_q");
-        e |= launch_wgrad(dt, X, dY, I, r, A, dQKV, dz16, B, T, d, H, dh, k, g->dWq, g->dWk, g->dWv, g->dWr, g->dWo,
+        e |= launch_wgrad(dt, X, dY, I, A, dQKV, dz16, B, T, d, H, dh, k, g->dWq, g->dWk, g->dWv, g->dWr, g->dWo,
                           0, stream);
         e |= sm.mark("wgrad_qkv");
-        e |= launch_wgrad(dt, X, dY, I, r, A, dQKV, dz16, B, T, d, H, dh, k, g->dWq, g->dWk, g->dWv, g->dWr, g->dWo,
+        e |= launch_wgrad(dt, X, dY, I, A, dQKV, dz16, B, T, d, H, dh, k, g->dWq, g->dWk, g->dWv, g->dWr, g->dWo,
                           1, stream);
         e |= sm.mark("wgrad_o");
         e |= launch_dx_proj(dt, dQKV, dz, w->Wq, w->Wk, w->Wv, w->Wr, B, d, H, dh, k, dXs, stream);
@@ -300,10 +300,10 @@ int mosa_backward_timed(const mosa_shape* s, const void* X, const mosa_weights* 
         e |= sm.mark("attn_bwd_kv_dense");
         e |= launch_attn_bwd(dt, QKVd, dAd, lsed, Dd, B * Hd, T, dh, causal, dQKVd, 1, stream);
         e |= sm.mark("attn_bwd_q_dense");
-        e |= launch_wgrad(dt, X, dY, nullptr, nullptr, Ad, dQKVd, nullptr, B, T, d, Hd, dh, T, g->dWq_d, g->dWk_d,
+        e |= launch_wgrad(dt, X, dY, nullptr, Ad, dQKVd, nullptr, B, T, d, Hd, dh, T, g->dWq_d, g->dWk_d,
                           g->dWv_d, nullptr, g->dWo_d, 0, stream);
         e |= sm.mark("wgrad_qkv_dense");
-        e |= launch_wgrad(dt, X, dY, nullptr, nullptr, Ad, dQKVd, nullptr, B, T, d, Hd, dh, T, g->dWq_d, g->dWk_d,
+        e |= launch_wgrad(dt, X, dY, nullptr, Ad, dQKVd, nullptr, B, T, d, Hd, dh, T, g->dWq_d, g->dWk_d,
                           g->dWv_d, nullptr, g->dWo_d, 1, stream);
         e |= sm.mark("wgrad_o_dense");
     }

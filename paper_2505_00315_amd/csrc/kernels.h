@@ -28,23 +28,24 @@ int launch_select(int dtype, const float* z, const float* xnorm, const void* X, 
 int launch_qkv(int dtype, const void* X, const int32_t* I, const void* Wq, const void* Wk,
                const void* Wv, int B, int T, int d, int H, int dh, int n, void* QKV, hipStream_t stream);
 
-// A = softmax(Q K^T / sqrt(dh) + causal mask in slot order) V per (b,h);
-// lse = log-sum-exp of the scaled scores (natural log).
-int launch_attn_fwd(int dtype, const void* QKV, int BH, int n, int dh, int causal, void* A, float* lse,
-                    hipStream_t stream);
+// A = diag(r) softmax(Q K^T / sqrt(dh) + causal mask in slot order) V per
+// (b,h) (r == nullptr: r = 1); lse = log-sum-exp of the scaled scores
+// (natural log).
+int launch_attn_fwd(int dtype, const void* QKV, const float* r, int BH, int n, int dh, int causal, void* A,
+                    float* lse, hipStream_t stream);
 
-// Xo[b,h,i,:] = r[b,h,i] A[b,h,i,:] Wo[h].
-int launch_out_proj(int dtype, const void* A, const float* r, const void* Wo, int B, int d, int H, int dh,
-                    int k, void* Xo, hipStream_t stream);
+// Xo[b,h,i,:] = A[b,h,i,:] Wo[h]  (A already scaled by r).
+int launch_out_proj(int dtype, const void* A, const void* Wo, int B, int d, int H, int dh, int k, void* Xo,
+                    hipStream_t stream);
 
 // Y[b,t,:] (+)= sum_hd Ad[b,hd,t,:] Wo_d[hd] + sum_h (ascending) Xo[b,h,slot[b,h,t],:].
 int launch_out_combine(int dtype, const void* Ad, const void* Wo_d, const int16_t* slot, const void* Xo,
                        int B, int T, int d, int H, int dh, int k, int Hd, void* Y, int accumulate,
                        hipStream_t stream);
 
-// Backward, output side of a head: dA~ = dY[I] Wo^T; dA = r dA~;
-// D = r <dA~, A>; dz = <dA~, A> r (1 - r) (also as 16-wide rows dz16);
-// dz, dz16 may be null and I, r null for dense heads.
+// Backward, output side of a head (A is the r-scaled attention output):
+// dA~ = dY[I] Wo^T; dA = r dA~; D = <dA~, A>; dz = D (1 - r) (also as 16-wide
+// rows dz16); dz, dz16 may be null and I, r null for dense heads.
 int launch_dattn_out(int dtype, const void* dY, const int32_t* I, const float* r, const void* Wo,
                      const void* A, int B, int T, int d, int H, int dh, int n, void* dA, float* D, float* dz,
                      void* dz16, hipStream_t stream);
@@ -54,7 +55,7 @@ int launch_attn_bwd(int dtype, const void* QKV, const void* dA, const float* lse
                     int n, int dh, int causal, void* dQKV, int pass, hipStream_t stream);
 
 // Weight gradients; which 0: dWq, dWk, dWv (+ dWr when non-null), which 1: dWo.
-int launch_wgrad(int dtype, const void* X, const void* dY, const int32_t* I, const float* r, const void* A,
+int launch_wgrad(int dtype, const void* X, const void* dY, const int32_t* I, const void* A,
                  const void* dQKV, const void* dz16, int B, int T, int d, int H, int dh, int n, void* dWq,
                  void* dWk, void* dWv, void* dWr, void* dWo, int which, hipStream_t stream);
 

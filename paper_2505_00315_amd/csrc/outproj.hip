@@ -6,6 +6,7 @@
 // Two GEMMs on the tiled MFMA engine (gemm.h):
 //   out_proj    per MoSA head h: X^o[b,h,i,:] = (r_i A_i) W^O_h, M = B*k
 //               selected rows, N = d, K = dh, written once (storage type);
+//               the attention kernel already stored the rows as r_i A_i;
 //   out_combine per batch element b: a tile of 64 tokens x 128 columns of
 //               Y = A_dense W^O_dense (dense heads concatenated along K,
 //               K = Hd*dh, possibly 0) and then, in the epilogue, the MoSA
@@ -26,10 +27,9 @@ template <typename ST, int DH>
 struct OutProjPolicy {
     static constexpr int MT = 64, NT = 128, KC = sizeof(ST) == 2 ? DH : 32, WM = 2, WN = 2;
     static constexpr size_t EPI_LDS = 0;
-    static constexpr bool A_KCONTIG = true, B_KCONTIG = false, A_SCALED = true;
+    static constexpr bool A_KCONTIG = true, B_KCONTIG = false, A_SCALED = false;
     struct Args {
-        const ST* A;   // [B, H, k, DH]
-        const float* r;
+        const ST* A;   // [B, H, k, DH], rows scaled by r
         const ST* Wo;  // [H, DH, d]
         ST* Xo;        // [B, H, k, d]
         int d, H, k, M, mtiles, ntiles;
@@ -54,11 +54,9 @@ struct OutProjPolicy {
     __device__ static size_t ridx(const Args& a, int h, int m) {
         return ((size_t)(m / a.k) * a.H + h) * a.k + (m % a.k);
     }
-    __device__ static ARef a_row(const Args& a, int h, int m, float& sc) {
+    __device__ static ARef a_row(const Args& a, int h, int m, float&) {
         if (m < 0 || m >= a.M) return {nullptr};
-        const size_t ri = ridx(a, h, m);
-        sc = a.r[ri];
-        return {a.A + ri * DH};
+        return {a.A + ridx(a, h, m) * DH};
     }
     __device__ static const ST* a_elem(const Args&, int, const ARef& r, int k) { return r.p ? r.p + k : nullptr; }
     __device__ static BRef b_row(const Args&, int, int) { return {}; }
@@ -78,8 +76,7 @@ struct OutProjPolicy {
             const int m = m0 + ml;
             if (m >= a.M || n0 + c >= a.d) continue;
             float x[8];
-#pragma unroll
-            for (int j = 0; j < 8; ++j) x[j] = Cs[ml * ldc + c + j];
+            cs_load8(Cs, ldc, ml, c, x);
             vec8_store<ST>(a.Xo + ridx(a, h, m) * a.d + n0 + c, vec8_from_f32<ST>(x));
         }
     }
@@ -143,10 +140,10 @@ struct OutCombinePolicy {
 };
 
 template <typename ST, int DH>
-int run_proj(const ST* A, const float* r, const ST* Wo, int B, int d, int H, int k, ST* Xo, hipStream_t stream) {
+int run_proj(const ST* A, const ST* Wo, int B, int d, int H, int k, ST* Xo, hipStream_t stream) {
     using P = OutProjPolicy<ST, DH>;
     const int M = B * k;
-    typename P::Args a{A, r, Wo, Xo, d, H, k, M, (M + P::MT - 1) / P::MT, (d + P::NT - 1) / P::NT};
+    typename P::Args a{A, Wo, Xo, d, H, k, M, (M + P::MT - 1) / P::MT, (d + P::NT - 1) / P::NT};
     return launch_gemm<ST, P>(a, H * a.mtiles * a.ntiles, stream);
 }
 
@@ -161,15 +158,15 @@ int run_combine(const ST* Ad, const ST* Wod, const int16_t* slot, const ST* Xo, 
 
 }  // namespace
 
-int launch_out_proj(int dtype, const void* A, const float* r, const void* Wo, int B, int d, int H, int dh, int k,
-                    void* Xo, hipStream_t stream) {
+int launch_out_proj(int dtype, const void* A, const void* Wo, int B, int d, int H, int dh, int k, void* Xo,
+                    hipStream_t stream) {
     if (H == 0) return 0;
     if (dtype == kBF16) {
         auto f = dh == 64 ? run_proj<uint16_t, 64> : run_proj<uint16_t, 32>;
-        return f((const uint16_t*)A, r, (const uint16_t*)Wo, B, d, H, k, (uint16_t*)Xo, stream);
+        return f((const uint16_t*)A, (const uint16_t*)Wo, B, d, H, k, (uint16_t*)Xo, stream);
     }
     auto f = dh == 64 ? run_proj<float, 64> : run_proj<float, 32>;
-    return f((const float*)A, r, (const float*)Wo, B, d, H, k, (float*)Xo, stream);
+    return f((const float*)A, (const float*)Wo, B, d, H, k, (float*)Xo, stream);
 }
 
 int launch_out_combine(int dtype, const void* Ad, const void* Wo_d, const int16_t* slot, const void* Xo, int B,

@@ -3,6 +3,7 @@
 //   dW^Q_h = sum_r X[b, I_r]^T dQ_r   (likewise W^K, W^V)    [d x dh]
 //   dW^r_h = sum_r dz_r X[b, I_r]                             [d]
 //   dW^O_h = sum_r (r_r A_r)^T dY[b, I_r]                     [dh x d]
+//            (the forward saved the rows r_r A_r already scaled)
 // Dense heads: the same with I = identity and r = 1 (no W^r).
 //
 // On the tiled MFMA engine the contraction index K is the row r, which is
@@ -81,8 +82,7 @@ struct WgradQkvPolicy {
             const int c = m0 + ml;
             if (c >= a.d) continue;
             float x[8];
-#pragma unroll
-            for (int j = 0; j < 8; ++j) x[j] = Cs[ml * ldc + nn + j];
+            cs_load8(Cs, ldc, ml, nn, x);
             ST* W = nn < DH ? a.dWq : (nn < 2 * DH ? a.dWk : a.dWv);
             vec8_store<ST>(W + ((size_t)h * a.d + c) * DH + (nn % DH), vec8_from_f32<ST>(x));
         }
@@ -94,12 +94,11 @@ template <typename ST, int DH, bool GATHER>
 struct WgradOPolicy {
     static constexpr int MT = DH, NT = 128, KC = sizeof(ST) == 2 ? 64 : 32, WM = 2, WN = 2;
     static constexpr size_t EPI_LDS = 0;
-    static constexpr bool A_KCONTIG = false, B_KCONTIG = false, A_SCALED = true;
+    static constexpr bool A_KCONTIG = false, B_KCONTIG = false, A_SCALED = false;
     struct Args {
         const ST* dY;
         const int32_t* I;
-        const float* rw;  // router values (nullptr: dense)
-        const ST* A;      // [B, H, n, DH]
+        const ST* A;      // [B, H, n, DH], rows scaled by r
         ST* dWo;          // [H, DH, d]
         int T, d, H, n, R, ntiles;
         FastDiv nd;
@@ -107,10 +106,9 @@ struct WgradOPolicy {
     struct ARef {};
     struct BRef {};
     struct RowInfo {
-        int b;     // batch element, or -1 past the last row
-        int t;     // token I_r (gathered) or i (dense), as loaded
-        int ri;    // selected-row index
-        float sc;  // router value of the row (1 for dense heads)
+        int b;   // batch element, or -1 past the last row
+        int t;   // token I_r (gathered) or i (dense), as loaded
+        int ri;  // selected-row index
     };
     __device__ static const ST* a_fallback(const Args& a) { return a.A; }
     __device__ static const ST* b_fallback(const Args& a) { return a.dY; }
@@ -128,14 +126,14 @@ struct WgradOPolicy {
         int b, i;
         fast_divmod(a.nd, r < 0 ? 0 : r, b, i);
         const int ri = (b * a.H + h) * a.n + i;
-        return {r < 0 ? -1 : b, GATHER ? a.I[ri] : i, ri, GATHER ? a.rw[ri] : 1.f};
+        return {r < 0 ? -1 : b, GATHER ? a.I[ri] : i, ri};
     }
-    // A[e][r] = r_r A[r][e]
+    // A[e][r] = (r_r A_r)[e]
     __device__ static const ST* a_kaddr(const Args& a, int, const RowInfo& r, int m8) {
         return a.A + (size_t)r.ri * DH + m8;
     }
     __device__ static bool a_kok(const Args&, int, const RowInfo& r, int) { return r.b >= 0; }
-    __device__ static float a_kscale(const Args&, int, const RowInfo& r) { return r.sc; }
+    __device__ static float a_kscale(const Args&, int, const RowInfo&) { return 1.f; }
     // B[r][c] = dY[b, I_r, c]
     __device__ static const ST* b_kaddr(const Args& a, int, const RowInfo& r, int n8) {
         return a.dY + ((size_t)max(r.b, 0) * a.T + r.t) * a.d + min(n8, a.d - 8);
@@ -147,8 +145,7 @@ struct WgradOPolicy {
             const int e = v / VPR, c = (v % VPR) * 8;
             if (n0 + c >= a.d) continue;
             float x[8];
-#pragma unroll
-            for (int j = 0; j < 8; ++j) x[j] = Cs[e * ldc + c + j];
+            cs_load8(Cs, ldc, e, c, x);
             vec8_store<ST>(a.dWo + ((size_t)h * DH + e) * a.d + n0 + c, vec8_from_f32<ST>(x));
         }
     }
@@ -170,24 +167,24 @@ int run_qkv(const ST* X, const int32_t* I, const ST* dQKV, const ST* dz16, int B
 }
 
 template <typename ST, int DH>
-int run_o(const ST* dY, const int32_t* I, const float* r, const ST* A, int B, int T, int d, int H, int n, ST* dWo,
+int run_o(const ST* dY, const int32_t* I, const ST* A, int B, int T, int d, int H, int n, ST* dWo,
           hipStream_t stream) {
     const FastDiv nd = make_fastdiv(n);
     if (I) {
         using P = WgradOPolicy<ST, DH, true>;
         const int ntiles = (d + P::NT - 1) / P::NT;
-        typename P::Args a{dY, I, r, A, dWo, T, d, H, n, B * n, ntiles, nd};
+        typename P::Args a{dY, I, A, dWo, T, d, H, n, B * n, ntiles, nd};
         return launch_gemm<ST, P>(a, H * ntiles, stream);
     }
     using P = WgradOPolicy<ST, DH, false>;
     const int ntiles = (d + P::NT - 1) / P::NT;
-    typename P::Args a{dY, I, r, A, dWo, T, d, H, n, B * n, ntiles, nd};
+    typename P::Args a{dY, I, A, dWo, T, d, H, n, B * n, ntiles, nd};
     return launch_gemm<ST, P>(a, H * ntiles, stream);
 }
 
 }  // namespace
 
-int launch_wgrad(int dtype, const void* X, const void* dY, const int32_t* I, const float* r, const void* A,
+int launch_wgrad(int dtype, const void* X, const void* dY, const int32_t* I, const void* A,
                  const void* dQKV, const void* dz16, int B, int T, int d, int H, int dh, int n, void* dWq, void* dWk,
                  void* dWv, void* dWr, void* dWo, int which, hipStream_t stream) {
     if (H == 0) return 0;
@@ -199,7 +196,7 @@ int launch_wgrad(int dtype, const void* X, const void* dY, const int32_t* I, con
                      (ST*)dWr, stream);
         }
         auto f = dh == 64 ? run_o<ST, 64> : run_o<ST, 32>;
-        return f((const ST*)dY, I, r, (const ST*)A, B, T, d, H, n, (ST*)dWo, stream);
+        return f((const ST*)dY, I, (const ST*)A, B, T, d, H, n, (ST*)dWo, stream);
     }
     using ST = float;
     if (which == 0) {
@@ -208,7 +205,7 @@ int launch_wgrad(int dtype, const void* X, const void* dY, const int32_t* I, con
                  (ST*)dWr, stream);
     }
     auto f = dh == 64 ? run_o<ST, 64> : run_o<ST, 32>;
-    return f((const ST*)dY, I, r, (const ST*)A, B, T, d, H, n, (ST*)dWo, stream);
+    return f((const ST*)dY, I, (const ST*)A, B, T, d, H, n, (ST*)dWo, stream);
 }
 
 }  // namespace mosa

@@ -122,13 +122,15 @@ def test_deterministic_and_scratch_independent(orc):
 
 
 def test_stage_intermediates(orc):
-    """Q, K, V and A of the MoSA heads against the oracle's intermediates."""
+    """Q, K, V and the router-scaled attention rows r_i A_i of the MoSA heads
+    against the oracle's intermediates."""
     w = wl.small(batch=2, seq_len=200, heads=3, k=50, d_head=64, d_model=128)
     inp = wl.make_inputs(w)
     out = run_forward(w, inp)
     ref = orc.forward(inp, w.k, intermediates=True)
-    for n in ("Q", "K", "V", "A"):
-        e = rel_err(to_f64(mosa.saved_view(out["shape"], out["saved"], n)), ref[n])
+    want = {"Q": ref["Q"], "K": ref["K"], "V": ref["V"], "A": ref["A"] * ref["r"][..., None]}
+    for n, v in want.items():
+        e = rel_err(to_f64(mosa.saved_view(out["shape"], out["saved"], n)), v)
         assert e <= TOL[w.dtype], (n, e)
 
 
