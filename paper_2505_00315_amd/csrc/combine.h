@@ -32,22 +32,30 @@ __device__ __forceinline__ void combine_tile(const float* Cs, int ldc, int tid, 
     const bool active = t < T && n0 + cq < d;  // d is a multiple of 64: 32-column groups are all in or all out
     float acc[32];
 #pragma unroll
-    for (int j = 0; j < 32; ++j) acc[j] = active ? Cs[ml * ldc + cq + j] : 0.f;
+    for (int c = 0; c < 4; ++c) {
+        float x[8];
+        cs_load8(Cs, ldc, ml, cq + 8 * c, x);
+#pragma unroll
+        for (int e = 0; e < 8; ++e) acc[8 * c + e] = active ? x[e] : 0.f;
+    }
 
     const ST* rbase = rows + (size_t)b * H * k * d + n0 + cq;
+    // Queue of up to 4 pending hits as a shift register (newest in qh3/qs3),
+    // so that every access uses a fixed register and nothing spills to
+    // scratch memory; the valid entries are the last q.
     int q = 0, qh0 = 0, qh1 = 0, qh2 = 0, qh3 = 0, qs0 = 0, qs1 = 0, qs2 = 0, qs3 = 0;
     auto flush = [&]() {
         const int hh[4] = {qh0, qh1, qh2, qh3}, ss[4] = {qs0, qs1, qs2, qs3};
         Vec8<ST> v[4][4];
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
-            const ST* p = j < q ? rbase + ((size_t)hh[j] * k + ss[j]) * d : rbase;
+            const ST* p = j >= 4 - q ? rbase + ((size_t)hh[j] * k + ss[j]) * d : rbase;
 #pragma unroll
             for (int c = 0; c < 4; ++c) v[j][c] = vec8_load<ST>(p + 8 * c);
         }
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
-            if (j < q) {
+            if (j >= 4 - q) {
 #pragma unroll
                 for (int c = 0; c < 4; ++c) {
                     float x[8];
@@ -60,10 +68,8 @@ __device__ __forceinline__ void combine_tile(const float* Cs, int ldc, int tid, 
         q = 0;
     };
     auto push = [&](int h, int s) {
-        if (q == 0) { qh0 = h; qs0 = s; }
-        else if (q == 1) { qh1 = h; qs1 = s; }
-        else if (q == 2) { qh2 = h; qs2 = s; }
-        else { qh3 = h; qs3 = s; }
+        qh0 = qh1; qh1 = qh2; qh2 = qh3; qh3 = h;
+        qs0 = qs1; qs1 = qs2; qs2 = qs3; qs3 = s;
         if (++q == 4) flush();
     };
 
@@ -107,20 +113,31 @@ __device__ __forceinline__ void combine_tile(const float* Cs, int ldc, int tid, 
         if (active) {
             const int16_t* mine = s_slot + ml * kCombineLdh;
             for (int hh = 0; hh < hn; hh += 8) {
-                int16_t sv[8];
+                uint4 u;
                 if (hh + 8 <= hn) {
-                    const uint4 u = *reinterpret_cast<const uint4*>(mine + hh);
-                    sv[0] = (int16_t)(u.x & 0xffff); sv[1] = (int16_t)(u.x >> 16);
-                    sv[2] = (int16_t)(u.y & 0xffff); sv[3] = (int16_t)(u.y >> 16);
-                    sv[4] = (int16_t)(u.z & 0xffff); sv[5] = (int16_t)(u.z >> 16);
-                    sv[6] = (int16_t)(u.w & 0xffff); sv[7] = (int16_t)(u.w >> 16);
+                    u = *reinterpret_cast<const uint4*>(mine + hh);
                 } else {
+                    uint32_t w[4];
 #pragma unroll
-                    for (int j = 0; j < 8; ++j) sv[j] = hh + j < hn ? mine[hh + j] : (int16_t)-1;
+                    for (int j = 0; j < 4; ++j) {
+                        const uint32_t lo = hh + 2 * j < hn ? (uint16_t)mine[hh + 2 * j] : 0xffffu;
+                        const uint32_t hi = hh + 2 * j + 1 < hn ? (uint16_t)mine[hh + 2 * j + 1] : 0xffffu;
+                        w[j] = lo | (hi << 16);
+                    }
+                    u = make_uint4(w[0], w[1], w[2], w[3]);
                 }
+                // bit j set: head hh + j selected the token (slot >= 0)
+                const uint32_t words[4] = {u.x, u.y, u.z, u.w};
+                uint32_t mask = 0;
 #pragma unroll
-                for (int j = 0; j < 8; ++j)
-                    if (sv[j] >= 0) push(h0 + hh + j, sv[j]);
+                for (int j = 0; j < 8; ++j) mask |= ((words[j >> 1] >> (16 * (j & 1) + 15)) & 1u ? 0u : 1u) << j;
+                const uint64_t lo64 = ((uint64_t)u.y << 32) | u.x, hi64 = ((uint64_t)u.w << 32) | u.z;
+                while (mask) {
+                    const int j = __builtin_ctz(mask);
+                    mask &= mask - 1;
+                    const int sl = (int)(((j < 4 ? lo64 : hi64) >> (16 * (j & 3))) & 0xffffu);
+                    push(h0 + hh + j, sl);
+                }
             }
         }
     }
