@@ -32,6 +32,8 @@
 // LDS after the C tile are the epilogue's own).
 #pragma once
 
+#include <type_traits>
+
 #include "common.h"
 
 namespace mosa {
@@ -177,6 +179,15 @@ __device__ __forceinline__ void cs_load8(const float* Cs, int ldc, int row, int 
     x[4] = b.x; x[5] = b.y; x[6] = b.z; x[7] = b.w;
 }
 
+// Split-K policies (P::SPLITK defined) map a workgroup to (batch, tile,
+// split) with tile_split, restrict it to k_range(split) (a multiple of KC
+// wide) and finish with epilogue_split, which writes an fp32 partial tile;
+// a separate pass adds the partials in split order, so the result stays
+// bitwise reproducible.
+template <class P, class = void> struct SplitKTrait { static constexpr bool value = false; };
+template <class P> struct SplitKTrait<P, std::void_t<decltype(P::SPLITK)>> { static constexpr bool value = P::SPLITK; };
+template <class P> constexpr bool kSplitK = SplitKTrait<P>::value;
+
 // s_waitcnt immediate for vmcnt(0) with expcnt and lgkmcnt left at their
 // maxima (gfx9 encoding: vmcnt [3:0] and [15:14], expcnt [6:4], lgkmcnt [11:8]).
 constexpr int kWaitVm0 = 0x0F70;
@@ -191,10 +202,15 @@ __global__ __launch_bounds__(256) void gemm_kernel(const typename P::Args args) 
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int g = lane >> 4, c16 = lane & 15;
-    int batch, m0, n0;
-    P::tile(args, xcd_logical_id(blockIdx.x, gridDim.x), batch, m0, n0);
+    int batch, m0, n0, split = 0;
+    const int logical = xcd_logical_id(blockIdx.x, gridDim.x);
+    if constexpr (kSplitK<P>) P::tile_split(args, logical, batch, m0, n0, split);
+    else P::tile(args, logical, batch, m0, n0);
     const int K = P::k_size(args, batch);
-    const int nchunks = (K + KC - 1) / KC;
+    // this workgroup's share of the K range (the whole range unless split)
+    int kbeg = 0, kend = K;
+    if constexpr (kSplitK<P>) P::k_range(args, split, K, kbeg, kend);
+    const int nchunks = kend > kbeg ? (kend - kbeg + KC - 1) / KC : 0;
 
     // Per-thread row references of the k-contiguous operands (fixed across chunks).
     typename P::ARef arow[S::A_PER > 0 ? S::A_PER : 1];
@@ -232,7 +248,7 @@ __global__ __launch_bounds__(256) void gemm_kernel(const typename P::Args args) 
         typename P::RowInfo info{};
         if constexpr (S::ROWS) {
             const int kk = k0 + (tid & (KC - 1));
-            info = P::row_info(args, batch, kk < K ? kk : -1);
+            info = P::row_info(args, batch, kk < kend ? kk : -1);
         }
         return info;
     };
@@ -248,7 +264,7 @@ __global__ __launch_bounds__(256) void gemm_kernel(const typename P::Args args) 
             for (int j = 0; j < S::A_PER; ++j) {
                 const int v = tid + 256 * j;
                 const int kk = k0 + (v % (KC / 8)) * 8;
-                const ST* p = (v < S::A_VECS && kk < K) ? P::a_elem(args, batch, arow[j], kk) : nullptr;
+                const ST* p = (v < S::A_VECS && kk < kend) ? P::a_elem(args, batch, arow[j], kk) : nullptr;
                 sa.ok[j] = p != nullptr;
                 sa.v[j] = vec8_load<ST>(p ? p : P::a_fallback(args));
             }
@@ -278,7 +294,7 @@ __global__ __launch_bounds__(256) void gemm_kernel(const typename P::Args args) 
             for (int j = 0; j < S::B_PER; ++j) {
                 const int v = tid + 256 * j;
                 const int kk = k0 + (v % (KC / 8)) * 8;
-                const ST* p = (v < S::B_VECS && kk < K) ? P::b_elem(args, batch, brow[j], kk) : nullptr;
+                const ST* p = (v < S::B_VECS && kk < kend) ? P::b_elem(args, batch, brow[j], kk) : nullptr;
                 sb.ok[j] = p != nullptr;
                 sb.v[j] = vec8_load<ST>(p ? p : P::b_fallback(args));
             }
@@ -372,13 +388,23 @@ __global__ __launch_bounds__(256) void gemm_kernel(const typename P::Args args) 
 
     // Pipeline: row infos of chunk c+2 and data of chunk c+1 are in flight
     // while the MFMAs of chunk c run.
+    // The MFMAs of the last chunk below run unconditionally: the accumulators
+    // are read right after them, and no branch may separate an MFMA from the
+    // VALU reads of its result (the compiler's wait-state insertion for that
+    // hazard has been seen to miss a path through such a branch).  An empty
+    // K range (e.g. no dense heads, whose operand pointers are then null)
+    // issues no global load at all: buffer 0 is cleared in LDS instead.
     if (nchunks > 0) {
-        rows_store(rows_load(0), 0);
+        rows_store(rows_load(kbeg), 0);
         __syncthreads();
-        const typename P::RowInfo r1 = rows_load(KC);
-        fetch(0, 0);
+        const typename P::RowInfo r1 = rows_load(kbeg + KC);
+        fetch(kbeg, 0);
         rows_store(r1, 1);
         commit(0);
+        __syncthreads();
+    } else {
+        // both operand buffers (A at As, B at Bs = As + 2 MT LDK), all in LDS
+        for (int e = tid; e < 2 * (MT + NT) * LDK / 8; e += 256) vec8_store<ST>(As + 8 * e, vec8_zero<ST>());
         __syncthreads();
     }
     auto mfma_chunk = [&](int buf) {
@@ -404,21 +430,22 @@ __global__ __launch_bounds__(256) void gemm_kernel(const typename P::Args args) 
     // MFMAs are peeled off below.
     for (int c = 0; c < nchunks - 1; ++c) {
         const int buf = c & 1;
-        const typename P::RowInfo r2 = rows_load((c + 2) * KC);
+        const typename P::RowInfo r2 = rows_load(kbeg + (c + 2) * KC);
         // keep the compiler from sinking these loads towards their uses: the
         // row-info load goes first, the chunk's data loads before the MFMAs
         __builtin_amdgcn_sched_barrier(0);
-        fetch((c + 1) * KC, buf ^ 1);
+        fetch(kbeg + (c + 1) * KC, buf ^ 1);
         __builtin_amdgcn_sched_barrier(0);
         mfma_chunk(buf);
         rows_store(r2, buf);  // rows of chunk c were consumed by fetch(c) one step earlier
         commit(buf ^ 1);
         __syncthreads();
     }
-    if (nchunks > 0) {
-        mfma_chunk((nchunks - 1) & 1);
-        __syncthreads();  // the C tile below reuses the operand buffers
-    }
+    mfma_chunk(nchunks > 0 ? (nchunks - 1) & 1 : 0);
+    // explicit wait states before the accumulators are read (see above)
+    __builtin_amdgcn_sched_barrier(0);
+    asm volatile("s_nop 7\n\ts_nop 7\n\ts_nop 7" ::: "memory");
+    __syncthreads();  // the C tile below reuses the operand buffers
 
     // C tile to LDS: Cs[m][n], row stride NT + 4 floats
     float* Cs = reinterpret_cast<float*>(smem);
@@ -431,7 +458,8 @@ __global__ __launch_bounds__(256) void gemm_kernel(const typename P::Args args) 
             for (int r = 0; r < 4; ++r)
                 Cs[(wm * S::WTM + i * 16 + 4 * g + r) * LDC + wn * S::WTN + j * 16 + c16] = acc[i][j][r];
     __syncthreads();
-    P::epilogue(args, batch, m0, n0, Cs, LDC, tid, smem + S::ctile_bytes);
+    if constexpr (kSplitK<P>) P::epilogue_split(args, batch, split, m0, n0, Cs, LDC, tid);
+    else P::epilogue(args, batch, m0, n0, Cs, LDC, tid, smem + S::ctile_bytes);
 }
 
 template <typename ST, class P>

@@ -19,7 +19,7 @@ struct Layout {
     // forward scratch
     size_t z, xnorm, unc_tok, unc_key, unc_sel, Xo;
     // backward scratch
-    size_t dA, D, dz, dz16, dQKV, dXs, dAd, Dd, dQKVd;
+    size_t dA, D, dz, dz16, dQKV, dXs, dAd, Dd, dQKVd, wpart;
     size_t scratch_total;
 };
 
@@ -89,6 +89,12 @@ Layout make_layout(const mosa_shape* s) {
     L.dAd = bw.take(B * Hd * T * dh * es);
     L.Dd = bw.take(B * Hd * T * 4);
     L.dQKVd = bw.take(B * Hd * T * 3 * dh * es);
+    {
+        const int dt = s->dtype == MOSA_BF16 ? kBF16 : kF32;
+        const size_t pm = wgrad_partial_bytes(dt, (int)B, (int)d, (int)H, (int)dh, (int)k, 1);
+        const size_t pd = wgrad_partial_bytes(dt, (int)B, (int)d, (int)Hd, (int)dh, (int)T, 0);
+        L.wpart = bw.take(pm > pd ? pm : pd);
+    }
     L.scratch_total = fw.total() > bw.total() ? fw.total() : bw.total();
     return L;
 }
@@ -275,6 +281,7 @@ int mosa_backward_timed(const mosa_shape* s, const void* X, const mosa_weights* 
     void* dAd = at<char>(scratch, L.dAd);
     float* Dd = at<float>(scratch, L.Dd);
     void* dQKVd = at<char>(scratch, L.dQKVd);
+    float* wpart = at<float>(scratch, L.wpart);
 
     if (H > 0) {
         e |= launch_dattn_out(dt, dY, I, r, w->Wo, A, B, T, d, H, dh, k, dA, D, dz, dz16, stream);
@@ -284,10 +291,10 @@ int mosa_backward_timed(const mosa_shape* s, const void* X, const mosa_weights* 
         e |= launch_attn_bwd(dt, QKV, dA, lse, D, B * H, k, dh, causal, dQKV, 1, stream);
         e |= sm.mark("attn_bwd_q");
         e |= launch_wgrad(dt, X, dY, I, A, dQKV, dz16, B, T, d, H, dh, k, g->dWq, g->dWk, g->dWv, g->dWr, g->dWo,
-                          0, stream);
+                          wpart, 0, stream);
         e |= sm.mark("wgrad_qkv");
         e |= launch_wgrad(dt, X, dY, I, A, dQKV, dz16, B, T, d, H, dh, k, g->dWq, g->dWk, g->dWv, g->dWr, g->dWo,
-                          1, stream);
+                          wpart, 1, stream);
         e |= sm.mark("wgrad_o");
         e |= launch_dx_proj(dt, dQKV, dz, w->Wq, w->Wk, w->Wv, w->Wr, B, d, H, dh, k, dXs, stream);
         e |= sm.mark("dx_proj");
@@ -301,10 +308,10 @@ int mosa_backward_timed(const mosa_shape* s, const void* X, const mosa_weights* 
         e |= launch_attn_bwd(dt, QKVd, dAd, lsed, Dd, B * Hd, T, dh, causal, dQKVd, 1, stream);
         e |= sm.mark("attn_bwd_q_dense");
         e |= launch_wgrad(dt, X, dY, nullptr, Ad, dQKVd, nullptr, B, T, d, Hd, dh, T, g->dWq_d, g->dWk_d,
-                          g->dWv_d, nullptr, g->dWo_d, 0, stream);
+                          g->dWv_d, nullptr, g->dWo_d, wpart, 0, stream);
         e |= sm.mark("wgrad_qkv_dense");
         e |= launch_wgrad(dt, X, dY, nullptr, Ad, dQKVd, nullptr, B, T, d, Hd, dh, T, g->dWq_d, g->dWk_d,
-                          g->dWv_d, nullptr, g->dWo_d, 1, stream);
+                          g->dWv_d, nullptr, g->dWo_d, wpart, 1, stream);
         e |= sm.mark("wgrad_o_dense");
     }
     e |= launch_dx_combine(dt, dQKVd, w->Wq_d, w->Wk_d, w->Wv_d, slot, dXs, B, T, d, H, dh, k, Hd, dX, accumulate_dX,

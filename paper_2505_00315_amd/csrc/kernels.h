@@ -55,9 +55,11 @@ int launch_attn_bwd(int dtype, const void* QKV, const void* dA, const float* lse
                     int n, int dh, int causal, void* dQKV, int pass, hipStream_t stream);
 
 // Weight gradients; which 0: dWq, dWk, dWv (+ dWr when non-null), which 1: dWo.
+// part: fp32 scratch of wgrad_partial_bytes(...) bytes for split row ranges.
 int launch_wgrad(int dtype, const void* X, const void* dY, const int32_t* I, const void* A,
                  const void* dQKV, const void* dz16, int B, int T, int d, int H, int dh, int n, void* dWq,
-                 void* dWk, void* dWv, void* dWr, void* dWo, int which, hipStream_t stream);
+                 void* dWk, void* dWv, void* dWr, void* dWo, float* part, int which, hipStream_t stream);
+size_t wgrad_partial_bytes(int dtype, int B, int d, int H, int dh, int n, int router);
 
 // dXs[b,h,i,:] = dQ Wq^T + dK Wk^T + dV Wv^T + dz Wr  (per selected row).
 int launch_dx_proj(int dtype, const void* dQKV, const float* dz, const void* Wq, const void* Wk,

@@ -11,7 +11,12 @@
 // register transpose.  wgrad_qkv: M = d, N = 3 dh (+ a 16-column block whose
 // first column is dz, so dW^r falls out of the same MFMAs), one workgroup per
 // (head, 64 rows of d).  wgrad_o: M = dh, N = d.  The K loop runs over the rows
-// in order, so the sums are bitwise reproducible.
+// in order, so the sums are bitwise reproducible.  When there are too few
+// (head, tile) pairs to fill the chip the rows are split into S contiguous
+// ranges: each workgroup writes an fp32 partial tile and a second kernel adds
+// the S partials in range order (still reproducible).
+#include <algorithm>
+
 #include "gemm.h"
 #include "kernels.h"
 
@@ -23,7 +28,7 @@ template <typename ST, int DH, bool ROUTER, bool GATHER>
 struct WgradQkvPolicy {
     static constexpr int MT = 64, NT = 3 * DH + (ROUTER ? 16 : 0), KC = sizeof(ST) == 2 ? 64 : 32, WM = 4, WN = 1;
     static constexpr size_t EPI_LDS = 0;
-    static constexpr bool A_KCONTIG = false, B_KCONTIG = false, A_SCALED = false;
+    static constexpr bool A_KCONTIG = false, B_KCONTIG = false, A_SCALED = false, SPLITK = true;
     struct Args {
         const ST* X;
         const int32_t* I;
@@ -33,7 +38,8 @@ struct WgradQkvPolicy {
         ST* dWk;
         ST* dWv;         // [H, d, DH]
         ST* dWr;         // [H, d]
-        int T, d, H, n, R, mtiles;
+        float* part;     // [S, H, d, NT] fp32 partial sums (S > 1)
+        int T, d, H, n, R, mtiles, S, cps;
         FastDiv nd;
     };
     struct ARef {};
@@ -48,10 +54,17 @@ struct WgradQkvPolicy {
     };
     __device__ static const ST* a_fallback(const Args& a) { return a.X; }
     __device__ static const ST* b_fallback(const Args& a) { return a.dQKV; }
-    __device__ static void tile(const Args& a, int logical, int& h, int& m0, int& n0) {
-        h = logical / a.mtiles;
-        m0 = (logical % a.mtiles) * MT;
+    __device__ static void tile_split(const Args& a, int logical, int& h, int& m0, int& n0, int& split) {
+        const int per = a.H * a.mtiles;
+        split = logical / per;
+        const int rem = logical % per;
+        h = rem / a.mtiles;
+        m0 = (rem % a.mtiles) * MT;
         n0 = 0;
+    }
+    __device__ static void k_range(const Args& a, int split, int K, int& kbeg, int& kend) {
+        kbeg = split * a.cps * KC;
+        kend = min(K, kbeg + a.cps * KC);
     }
     __device__ static int k_size(const Args& a, int) { return a.R; }
     __device__ static ARef a_row(const Args&, int, int, float&) { return {}; }
@@ -88,19 +101,60 @@ struct WgradQkvPolicy {
         }
         if (ROUTER && tid < MT && m0 + tid < a.d) st1<ST>(a.dWr + (size_t)h * a.d + m0 + tid, Cs[tid * ldc + 3 * DH]);
     }
+    __device__ static void epilogue_split(const Args& a, int h, int split, int m0, int n0, const float* Cs, int ldc,
+                                          int tid) {
+        if (a.S == 1) {
+            epilogue(a, h, m0, n0, Cs, ldc, tid, nullptr);
+            return;
+        }
+        constexpr int VPR = NT / 4;  // float4 per row
+        for (int v = tid; v < MT * VPR; v += 256) {
+            const int ml = v / VPR, nn = (v % VPR) * 4;
+            const int c = m0 + ml;
+            if (c >= a.d) continue;
+            const float4 x = *reinterpret_cast<const float4*>(Cs + ml * ldc + nn);
+            *reinterpret_cast<float4*>(a.part + (((size_t)split * a.H + h) * a.d + c) * NT + nn) = x;
+        }
+    }
 };
+
+// Sum of the S partial tiles in split order, then the final stores.
+template <typename ST, int DH, bool ROUTER>
+__global__ __launch_bounds__(256) void wgrad_qkv_reduce_kernel(const float* __restrict__ part, int S, int H, int d,
+                                                               ST* dWq, ST* dWk, ST* dWv, ST* dWr) {
+    constexpr int NT = 3 * DH + (ROUTER ? 16 : 0);
+    constexpr int G = 3 * DH / 8 + (ROUTER ? 1 : 0);  // 8-column groups written
+    const int idx = blockIdx.x * 256 + threadIdx.x;
+    if (idx >= H * d * G) return;
+    const int gq = idx % G, hc = idx / G;  // hc = h * d + c
+    float x[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+    for (int sp = 0; sp < S; ++sp) {
+        const float* p = part + ((size_t)sp * H * d + hc) * NT + gq * 8;
+        const float4 u = reinterpret_cast<const float4*>(p)[0], w = reinterpret_cast<const float4*>(p)[1];
+        x[0] += u.x; x[1] += u.y; x[2] += u.z; x[3] += u.w;
+        x[4] += w.x; x[5] += w.y; x[6] += w.z; x[7] += w.w;
+    }
+    const int nn = gq * 8;
+    if (nn < 3 * DH) {
+        ST* W = nn < DH ? dWq : (nn < 2 * DH ? dWk : dWv);
+        vec8_store<ST>(W + (size_t)hc * DH + (nn % DH), vec8_from_f32<ST>(x));
+    } else {
+        st1<ST>(dWr + hc, x[0]);
+    }
+}
 
 template <typename ST, int DH, bool GATHER>
 struct WgradOPolicy {
     static constexpr int MT = DH, NT = 128, KC = sizeof(ST) == 2 ? 64 : 32, WM = 2, WN = 2;
     static constexpr size_t EPI_LDS = 0;
-    static constexpr bool A_KCONTIG = false, B_KCONTIG = false, A_SCALED = false;
+    static constexpr bool A_KCONTIG = false, B_KCONTIG = false, A_SCALED = false, SPLITK = true;
     struct Args {
         const ST* dY;
         const int32_t* I;
         const ST* A;      // [B, H, n, DH], rows scaled by r
         ST* dWo;          // [H, DH, d]
-        int T, d, H, n, R, ntiles;
+        float* part;      // [S, H, DH, d] fp32 partial sums (S > 1)
+        int T, d, H, n, R, ntiles, S, cps;
         FastDiv nd;
     };
     struct ARef {};
@@ -112,10 +166,17 @@ struct WgradOPolicy {
     };
     __device__ static const ST* a_fallback(const Args& a) { return a.A; }
     __device__ static const ST* b_fallback(const Args& a) { return a.dY; }
-    __device__ static void tile(const Args& a, int logical, int& h, int& m0, int& n0) {
-        h = logical / a.ntiles;
+    __device__ static void tile_split(const Args& a, int logical, int& h, int& m0, int& n0, int& split) {
+        const int per = a.H * a.ntiles;
+        split = logical / per;
+        const int rem = logical % per;
+        h = rem / a.ntiles;
         m0 = 0;
-        n0 = (logical % a.ntiles) * NT;
+        n0 = (rem % a.ntiles) * NT;
+    }
+    __device__ static void k_range(const Args& a, int split, int K, int& kbeg, int& kend) {
+        kbeg = split * a.cps * KC;
+        kend = min(K, kbeg + a.cps * KC);
     }
     __device__ static int k_size(const Args& a, int) { return a.R; }
     __device__ static ARef a_row(const Args&, int, int, float&) { return {}; }
@@ -149,63 +210,146 @@ struct WgradOPolicy {
             vec8_store<ST>(a.dWo + ((size_t)h * DH + e) * a.d + n0 + c, vec8_from_f32<ST>(x));
         }
     }
+    __device__ static void epilogue_split(const Args& a, int h, int split, int m0, int n0, const float* Cs, int ldc,
+                                          int tid) {
+        if (a.S == 1) {
+            epilogue(a, h, m0, n0, Cs, ldc, tid, nullptr);
+            return;
+        }
+        constexpr int VPR = NT / 4;
+        for (int v = tid; v < MT * VPR; v += 256) {
+            const int e = v / VPR, c = (v % VPR) * 4;
+            if (n0 + c >= a.d) continue;
+            const float4 x = *reinterpret_cast<const float4*>(Cs + e * ldc + c);
+            *reinterpret_cast<float4*>(a.part + (((size_t)split * a.H + h) * DH + e) * a.d + n0 + c) = x;
+        }
+    }
 };
 
-template <typename ST, int DH>
-int run_qkv(const ST* X, const int32_t* I, const ST* dQKV, const ST* dz16, int B, int T, int d, int H, int n, ST* dWq,
-            ST* dWk, ST* dWv, ST* dWr, hipStream_t stream) {
-    const int mtiles = (d + 63) / 64;
-    const FastDiv nd = make_fastdiv(n);
-    if (I) {  // MoSA heads: gathered rows and the router column
-        using P = WgradQkvPolicy<ST, DH, true, true>;
-        typename P::Args a{X, I, dQKV, dz16, dWq, dWk, dWv, dWr, T, d, H, n, B * n, mtiles, nd};
-        return launch_gemm<ST, P>(a, H * mtiles, stream);
+template <typename ST>
+__global__ __launch_bounds__(256) void wgrad_o_reduce_kernel(const float* __restrict__ part, int S, size_t n8,
+                                                             ST* dWo) {
+    const size_t idx = (size_t)blockIdx.x * 256 + threadIdx.x;
+    if (idx >= n8) return;
+    float x[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+    for (int sp = 0; sp < S; ++sp) {
+        const float* p = part + ((size_t)sp * n8 + idx) * 8;
+        const float4 u = reinterpret_cast<const float4*>(p)[0], w = reinterpret_cast<const float4*>(p)[1];
+        x[0] += u.x; x[1] += u.y; x[2] += u.z; x[3] += u.w;
+        x[4] += w.x; x[5] += w.y; x[6] += w.z; x[7] += w.w;
     }
-    using P = WgradQkvPolicy<ST, DH, false, false>;
-    typename P::Args a{X, I, dQKV, dz16, dWq, dWk, dWv, dWr, T, d, H, n, B * n, mtiles, nd};
-    return launch_gemm<ST, P>(a, H * mtiles, stream);
+    vec8_store<ST>(dWo + idx * 8, vec8_from_f32<ST>(x));
+}
+
+// Split of the row range: enough workgroups to fill the chip (about 512),
+// at least 4 chunks per split.
+int choose_splits(int base_tiles, int nchunks, int& cps) {
+    int sp = (512 + base_tiles - 1) / base_tiles;
+    sp = std::min(sp, std::max(1, nchunks / 4));
+    sp = std::max(1, std::min(sp, 64));
+    cps = (nchunks + sp - 1) / sp;
+    return nchunks > 0 ? (nchunks + cps - 1) / cps : 1;
+}
+
+template <typename ST, int DH, bool ROUTER, bool GATHER>
+int run_qkv_t(const ST* X, const int32_t* I, const ST* dQKV, const ST* dz16, int B, int T, int d, int H, int n,
+              ST* dWq, ST* dWk, ST* dWv, ST* dWr, float* part, hipStream_t stream) {
+    using P = WgradQkvPolicy<ST, DH, ROUTER, GATHER>;
+    const int mtiles = (d + P::MT - 1) / P::MT, R = B * n;
+    int cps;
+    const int S = choose_splits(H * mtiles, (R + P::KC - 1) / P::KC, cps);
+    typename P::Args a{X, I, dQKV, dz16, dWq, dWk, dWv, dWr, part, T, d, H, n, R, mtiles, S, cps, make_fastdiv(n)};
+    int e = launch_gemm<ST, P>(a, S * H * mtiles, stream);
+    if (S > 1 && e == 0) {
+        const int total = H * d * (3 * DH / 8 + (ROUTER ? 1 : 0));
+        hipLaunchKernelGGL((wgrad_qkv_reduce_kernel<ST, DH, ROUTER>), dim3((total + 255) / 256), dim3(256), 0, stream,
+                           part, S, H, d, dWq, dWk, dWv, dWr);
+        e = hipGetLastError() == hipSuccess ? 0 : -1;
+    }
+    return e;
 }
 
 template <typename ST, int DH>
-int run_o(const ST* dY, const int32_t* I, const ST* A, int B, int T, int d, int H, int n, ST* dWo,
-          hipStream_t stream) {
-    const FastDiv nd = make_fastdiv(n);
-    if (I) {
-        using P = WgradOPolicy<ST, DH, true>;
-        const int ntiles = (d + P::NT - 1) / P::NT;
-        typename P::Args a{dY, I, A, dWo, T, d, H, n, B * n, ntiles, nd};
-        return launch_gemm<ST, P>(a, H * ntiles, stream);
+int run_qkv(const ST* X, const int32_t* I, const ST* dQKV, const ST* dz16, int B, int T, int d, int H, int n, ST* dWq,
+            ST* dWk, ST* dWv, ST* dWr, float* part, hipStream_t stream) {
+    if (I)  // MoSA heads: gathered rows and the router column
+        return run_qkv_t<ST, DH, true, true>(X, I, dQKV, dz16, B, T, d, H, n, dWq, dWk, dWv, dWr, part, stream);
+    return run_qkv_t<ST, DH, false, false>(X, I, dQKV, dz16, B, T, d, H, n, dWq, dWk, dWv, dWr, part, stream);
+}
+
+template <typename ST, int DH, bool GATHER>
+int run_o_t(const ST* dY, const int32_t* I, const ST* A, int B, int T, int d, int H, int n, ST* dWo, float* part,
+            hipStream_t stream) {
+    using P = WgradOPolicy<ST, DH, GATHER>;
+    const int ntiles = (d + P::NT - 1) / P::NT, R = B * n;
+    int cps;
+    const int S = choose_splits(H * ntiles, (R + P::KC - 1) / P::KC, cps);
+    typename P::Args a{dY, I, A, dWo, part, T, d, H, n, R, ntiles, S, cps, make_fastdiv(n)};
+    int e = launch_gemm<ST, P>(a, S * H * ntiles, stream);
+    if (S > 1 && e == 0) {
+        const size_t n8 = (size_t)H * DH * d / 8;
+        hipLaunchKernelGGL((wgrad_o_reduce_kernel<ST>), dim3((unsigned)((n8 + 255) / 256)), dim3(256), 0, stream, part,
+                           S, n8, dWo);
+        e = hipGetLastError() == hipSuccess ? 0 : -1;
     }
-    using P = WgradOPolicy<ST, DH, false>;
-    const int ntiles = (d + P::NT - 1) / P::NT;
-    typename P::Args a{dY, I, A, dWo, T, d, H, n, B * n, ntiles, nd};
-    return launch_gemm<ST, P>(a, H * ntiles, stream);
+    return e;
+}
+
+template <typename ST, int DH>
+int run_o(const ST* dY, const int32_t* I, const ST* A, int B, int T, int d, int H, int n, ST* dWo, float* part,
+          hipStream_t stream) {
+    if (I) return run_o_t<ST, DH, true>(dY, I, A, B, T, d, H, n, dWo, part, stream);
+    return run_o_t<ST, DH, false>(dY, I, A, B, T, d, H, n, dWo, part, stream);
+}
+
+// Bytes of fp32 partial sums the two launches of one head group need.
+template <typename ST, int DH>
+size_t partial_bytes(int B, int d, int H, int n, bool router) {
+    using PQ = WgradQkvPolicy<ST, DH, true, true>;
+    using PO = WgradOPolicy<ST, DH, true>;
+    const int R = B * n;
+    int cps;
+    const int mtiles = (d + PQ::MT - 1) / PQ::MT, ntiles = (d + PO::NT - 1) / PO::NT;
+    const int sq = choose_splits(H * mtiles, (R + PQ::KC - 1) / PQ::KC, cps);
+    const int so = choose_splits(H * ntiles, (R + PO::KC - 1) / PO::KC, cps);
+    const size_t nq = 3 * DH + (router ? 16 : 0);
+    const size_t bq = sq > 1 ? (size_t)sq * H * d * nq * 4 : 0;
+    const size_t bo = so > 1 ? (size_t)so * H * DH * d * 4 : 0;
+    return bq > bo ? bq : bo;
 }
 
 }  // namespace
 
-int launch_wgrad(int dtype, const void* X, const void* dY, const int32_t* I, const void* A,
-                 const void* dQKV, const void* dz16, int B, int T, int d, int H, int dh, int n, void* dWq, void* dWk,
-                 void* dWv, void* dWr, void* dWo, int which, hipStream_t stream) {
+int launch_wgrad(int dtype, const void* X, const void* dY, const int32_t* I, const void* A, const void* dQKV,
+                 const void* dz16, int B, int T, int d, int H, int dh, int n, void* dWq, void* dWk, void* dWv,
+                 void* dWr, void* dWo, float* part, int which, hipStream_t stream) {
     if (H == 0) return 0;
     if (dtype == kBF16) {
         using ST = uint16_t;
         if (which == 0) {
             auto f = dh == 64 ? run_qkv<ST, 64> : run_qkv<ST, 32>;
             return f((const ST*)X, I, (const ST*)dQKV, (const ST*)dz16, B, T, d, H, n, (ST*)dWq, (ST*)dWk, (ST*)dWv,
-                     (ST*)dWr, stream);
+                     (ST*)dWr, part, stream);
         }
         auto f = dh == 64 ? run_o<ST, 64> : run_o<ST, 32>;
-        return f((const ST*)dY, I, (const ST*)A, B, T, d, H, n, (ST*)dWo, stream);
+        return f((const ST*)dY, I, (const ST*)A, B, T, d, H, n, (ST*)dWo, part, stream);
     }
     using ST = float;
     if (which == 0) {
         auto f = dh == 64 ? run_qkv<ST, 64> : run_qkv<ST, 32>;
         return f((const ST*)X, I, (const ST*)dQKV, (const ST*)dz16, B, T, d, H, n, (ST*)dWq, (ST*)dWk, (ST*)dWv,
-                 (ST*)dWr, stream);
+                 (ST*)dWr, part, stream);
     }
     auto f = dh == 64 ? run_o<ST, 64> : run_o<ST, 32>;
-    return f((const ST*)dY, I, (const ST*)A, B, T, d, H, n, (ST*)dWo, stream);
+    return f((const ST*)dY, I, (const ST*)A, B, T, d, H, n, (ST*)dWo, part, stream);
+}
+
+size_t wgrad_partial_bytes(int dtype, int B, int d, int H, int dh, int n, int router) {
+    if (H == 0 || n == 0) return 0;
+    if (dtype == kBF16)
+        return dh == 64 ? partial_bytes<uint16_t, 64>(B, d, H, n, router)
+                        : partial_bytes<uint16_t, 32>(B, d, H, n, router);
+    return dh == 64 ? partial_bytes<float, 64>(B, d, H, n, router) : partial_bytes<float, 32>(B, d, H, n, router);
 }
 
 }  // namespace mosa
