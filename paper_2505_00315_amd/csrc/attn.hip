@@ -17,6 +17,7 @@
 // applied once here, as Section 2.2's diag(r), so later stages read a scaled
 // row; r = 1 for dense heads) and lse = m + log(l) (fp32, natural log).
 #include "common.h"
+#include "gemm.h"
 #include "kernels.h"
 
 namespace mosa {
@@ -94,6 +95,7 @@ __global__ __launch_bounds__(256) void attn_fwd_kernel(const ST* __restrict__ QK
             const Frag4<ST> vf = frag4_from<ST>(vv);
             mma4(o[db], vf, pf);
         }
+        mfma_drain();  // the loop may exit right here
     }
     if (q < n) {
         const float inv = (rw ? rw[(size_t)bh * n + q] : 1.f) / l_run;
@@ -106,12 +108,205 @@ __global__ __launch_bounds__(256) void attn_fwd_kernel(const ST* __restrict__ QK
     }
 }
 
+// Element j of 8 packed storage elements, as raw storage.
+template <typename ST> __device__ __forceinline__ ST vec8_elem(const Vec8<ST>& v, int j);
+template <> __device__ __forceinline__ uint16_t vec8_elem<uint16_t>(const Vec8<uint16_t>& v, int j) {
+    const uint32_t w = j < 2 ? v.v.x : j < 4 ? v.v.y : j < 6 ? v.v.z : v.v.w;
+    return (uint16_t)((j & 1) ? (w >> 16) : (w & 0xffffu));
+}
+template <> __device__ __forceinline__ float vec8_elem<float>(const Vec8<float>& v, int j) {
+    return j == 0 ? v.a.x : j == 1 ? v.a.y : j == 2 ? v.a.z : j == 3 ? v.a.w
+         : j == 4 ? v.b.x : j == 5 ? v.b.y : j == 6 ? v.b.z : v.b.w;
+}
+
+// Four consecutive storage elements from LDS as MFMA operand halves.
+template <typename ST> struct Quad;
+template <> struct Quad<uint16_t> { uint2 v; };
+template <> struct Quad<float> { float4 v; };
+template <typename ST> __device__ __forceinline__ Quad<ST> quad_load(const ST* p) {
+    Quad<ST> q;
+    q.v = *reinterpret_cast<const decltype(q.v)*>(p);
+    return q;
+}
+// Frag8 from two quads (slots 0..3 and 4..7 of the lane).
+template <typename ST> __device__ __forceinline__ Frag8<ST> frag8_from_quads(const Quad<ST>& lo, const Quad<ST>& hi);
+template <> __device__ __forceinline__ Frag8<uint16_t> frag8_from_quads<uint16_t>(const Quad<uint16_t>& lo,
+                                                                                const Quad<uint16_t>& hi) {
+    Frag8<uint16_t> f;
+    f.v = __builtin_bit_cast(bf16x8, make_uint4(lo.v.x, lo.v.y, hi.v.x, hi.v.y));
+    return f;
+}
+template <> __device__ __forceinline__ Frag8<float> frag8_from_quads<float>(const Quad<float>& lo,
+                                                                          const Quad<float>& hi) {
+    Frag8<float> f;
+    f.v[0] = lo.v.x; f.v[1] = lo.v.y; f.v[2] = lo.v.z; f.v[3] = lo.v.w;
+    f.v[4] = hi.v.x; f.v[5] = hi.v.y; f.v[6] = hi.v.z; f.v[7] = hi.v.w;
+    return f;
+}
+
+// Tiled variant for n > 32: a workgroup owns 64 query rows of one (b,h)
+// (16 per wave) and walks the keys in tiles of 64 staged in LDS once for all
+// four waves: K row-major (A operand of S^T = K Q^T) and V transposed
+// (A operand of O^T += V^T P^T, K = 32 keys per MFMA, P^T straight from the
+// S^T registers).  The next tile's global loads are in flight while the
+// current one is processed.  Causal blocks are launched heaviest first.
+template <typename ST, int DH>
+__global__ __launch_bounds__(256) void attn_fwd_tiled_kernel(const ST* __restrict__ QKV, int BH, int n, int causal,
+                                                             float scale, const float* __restrict__ rw,
+                                                             ST* __restrict__ A, float* __restrict__ lse) {
+    constexpr int QB = 64, KB = 64, RS = 3 * DH;
+    constexpr int PAD = 16 / (int)sizeof(ST);
+    constexpr int LDR = DH + PAD;   // row-major K rows (and the output staging)
+    constexpr int LDT = KB + 4;     // transposed V rows (keys), quad reads stay aligned
+    constexpr int VPR = DH / 8;     // Vec8 per row
+    constexpr int PER = KB * VPR / 256;
+    static_assert(PER >= 1 && KB * VPR % 256 == 0, "tile shape");
+    __shared__ __attribute__((aligned(16))) ST Ks[KB * LDR];
+    __shared__ __attribute__((aligned(16))) ST Vt[DH * LDT];
+
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int g = lane >> 4, c16 = lane & 15;
+    const int nqb = (n + QB - 1) / QB;
+    const int bh = blockIdx.x / nqb;
+    const int qb = causal ? nqb - 1 - blockIdx.x % nqb : blockIdx.x % nqb;
+    const int q0 = qb * QB, wq0 = q0 + 16 * wave;
+    const ST* Qp = QKV + (size_t)bh * n * RS;
+    const ST* Kp = Qp + DH;
+    const ST* Vp = Qp + 2 * DH;
+
+    const int q = wq0 + c16;  // this lane's query (MFMA column)
+    Frag8<ST> qf[DH / 32];
+#pragma unroll
+    for (int st = 0; st < DH / 32; ++st) qf[st] = frag8_load<ST>(Qp + (size_t)min(q, n - 1) * RS + st * 32 + 8 * g);
+
+    float m_run = -__builtin_inff(), l_run = 0.f;
+    f32x4 o[DH / 16];
+#pragma unroll
+    for (int db = 0; db < DH / 16; ++db) o[db] = zero4();
+
+    const int kv_end = causal ? min(n, q0 + QB) : n;
+    const int ntiles = (kv_end + KB - 1) / KB;
+    Vec8<ST> kreg[PER], vreg[PER];
+    // rows past n are clamped to row n-1 (finite values whose scores are masked)
+    auto load_tile = [&](int j0) {
+#pragma unroll
+        for (int p = 0; p < PER; ++p) {
+            const int v = tid + 256 * p, key = v / VPR, dc = (v % VPR) * 8;
+            const size_t row = (size_t)min(j0 + key, n - 1);
+            kreg[p] = vec8_load<ST>(Kp + row * RS + dc);
+            vreg[p] = vec8_load<ST>(Vp + row * RS + dc);
+        }
+    };
+    auto store_tile = [&]() {
+#pragma unroll
+        for (int p = 0; p < PER; ++p) {
+            const int v = tid + 256 * p, key = v / VPR, dc = (v % VPR) * 8;
+            vec8_store<ST>(Ks + key * LDR + dc, kreg[p]);
+#pragma unroll
+            for (int j = 0; j < 8; ++j) Vt[(dc + j) * LDT + key] = vec8_elem<ST>(vreg[p], j);
+        }
+    };
+
+    load_tile(0);
+    for (int t = 0; t < ntiles; ++t) {
+        const int j0 = t * KB;
+        __syncthreads();  // every wave is done with the previous tile
+        store_tile();
+        __syncthreads();
+        load_tile(min(t + 1, ntiles - 1) * KB);  // the last tile is simply loaded again
+
+        // S^T for the 4 sub-blocks of 16 keys: lane = query c16, rows = keys 4g + i
+        f32x4 s[4];
+#pragma unroll
+        for (int sb = 0; sb < 4; ++sb) {
+            s[sb] = zero4();
+#pragma unroll
+            for (int st = 0; st < DH / 32; ++st)
+                mma8(s[sb], frag8_load<ST>(Ks + (sb * 16 + c16) * LDR + st * 32 + 8 * g), qf[st]);
+        }
+        float mloc = -__builtin_inff();
+#pragma unroll
+        for (int sb = 0; sb < 4; ++sb)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const int key = j0 + sb * 16 + 4 * g + i;
+                const bool ok = key < n && (!causal || key <= q);
+                s[sb][i] = ok ? s[sb][i] * scale : -__builtin_inff();
+                mloc = fmaxf(mloc, s[sb][i]);
+            }
+        mloc = fmaxf(mloc, __shfl_xor(mloc, 16, 64));
+        mloc = fmaxf(mloc, __shfl_xor(mloc, 32, 64));
+        // tile 0 always holds key 0, allowed for every query: m_new is finite
+        const float m_new = fmaxf(m_run, mloc);
+        const float alpha = expf(m_run - m_new);
+        float p[4][4], lsum = 0.f;
+#pragma unroll
+        for (int sb = 0; sb < 4; ++sb)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                p[sb][i] = expf(s[sb][i] - m_new);
+                lsum += p[sb][i];
+            }
+        lsum += __shfl_xor(lsum, 16, 64);
+        lsum += __shfl_xor(lsum, 32, 64);
+        l_run = l_run * alpha + lsum;
+        m_run = m_new;
+#pragma unroll
+        for (int db = 0; db < DH / 16; ++db) o[db] *= alpha;
+        // O^T += V^T P^T, 32 keys per MFMA: lane slots 0..3 = keys 4g+i of
+        // sub-block 2u, slots 4..7 = the same of sub-block 2u+1
+#pragma unroll
+        for (int u = 0; u < 2; ++u) {
+            const float pv[8] = {p[2 * u][0], p[2 * u][1], p[2 * u][2], p[2 * u][3],
+                                 p[2 * u + 1][0], p[2 * u + 1][1], p[2 * u + 1][2], p[2 * u + 1][3]};
+            const Frag8<ST> pf = frag8_from<ST>(pv);
+#pragma unroll
+            for (int db = 0; db < DH / 16; ++db) {
+                const ST* vrow = Vt + (db * 16 + c16) * LDT + 32 * u + 4 * g;
+                mma8(o[db], frag8_from_quads<ST>(quad_load<ST>(vrow), quad_load<ST>(vrow + 16)), pf);
+            }
+        }
+        mfma_drain();  // the loop may exit right here
+    }
+
+    // O^T (lane: query c16, d rows db*16 + 4g + i) through LDS to 16-byte row stores
+    __syncthreads();
+    const float inv = (rw && q < n ? rw[(size_t)bh * n + q] : 1.f) / l_run;
+    ST* Os = Ks + wave * 16 * LDR;
+#pragma unroll
+    for (int db = 0; db < DH / 16; ++db)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const float x = o[db][i] * inv;
+            if constexpr (sizeof(ST) == 2) Os[c16 * LDR + db * 16 + 4 * g + i] = f32_to_bf16(x);
+            else Os[c16 * LDR + db * 16 + 4 * g + i] = x;
+        }
+    if (g == 0 && q < n) lse[(size_t)bh * n + q] = m_run + logf(l_run);
+    __syncthreads();
+#pragma unroll
+    for (int e = lane; e < 16 * VPR; e += 64) {
+        const int r = e / VPR, dc = (e % VPR) * 8;
+        if (wq0 + r < n)
+            vec8_store<ST>(A + ((size_t)bh * n + wq0 + r) * DH + dc, vec8_load<ST>(Os + r * LDR + dc));
+    }
+}
+
 template <typename ST>
 int launch_attn_fwd_t(const ST* QKV, const float* r, int BH, int n, int dh, int causal, ST* A, float* lse,
                      hipStream_t stream) {
+    const float scale = 1.0f / sqrtf((float)dh);
+    if (n > 32) {
+        const dim3 grid(BH * ((n + 63) / 64)), block(256);
+        if (dh == 64)
+            hipLaunchKernelGGL((attn_fwd_tiled_kernel<ST, 64>), grid, block, 0, stream, QKV, BH, n, causal, scale, r, A,
+                               lse);
+        else
+            hipLaunchKernelGGL((attn_fwd_tiled_kernel<ST, 32>), grid, block, 0, stream, QKV, BH, n, causal, scale, r, A,
+                               lse);
+        return hipGetLastError() == hipSuccess ? 0 : -1;
+    }
     const int tasks = BH * ((n + 15) / 16);
     dim3 grid((tasks + 3) / 4), block(256);
-    const float scale = 1.0f / sqrtf((float)dh);
     if (dh == 64)
         hipLaunchKernelGGL((attn_fwd_kernel<ST, 64>), grid, block, 0, stream, QKV, BH, n, causal, scale, r, A, lse);
     else

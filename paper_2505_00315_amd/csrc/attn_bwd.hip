@@ -84,6 +84,7 @@ __global__ __launch_bounds__(256) void attn_bwd_kv_kernel(const ST* __restrict__
             mma4(dVt[db], frag4_from<ST>(at), pf);
             mma4(dKt[db], frag4_from<ST>(qt), dsf);
         }
+        mfma_drain();  // the loop may exit right here
     }
     if (key < n) {
         // lane: key column c16, d_head rows db*16 + 4g + i
@@ -159,6 +160,7 @@ __global__ __launch_bounds__(256) void attn_bwd_q_kernel(const ST* __restrict__ 
             }
             mma4(dQt[db], frag4_from<ST>(kt), dsf);
         }
+        mfma_drain();  // the loop may exit right here
     }
     if (q < n) {
 #pragma unroll

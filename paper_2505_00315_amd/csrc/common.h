@@ -161,6 +161,15 @@ __device__ __forceinline__ void mma4(f32x4& acc, const Frag4<float>& a, const Fr
 
 __device__ __forceinline__ f32x4 zero4() { return f32x4{0.f, 0.f, 0.f, 0.f}; }
 
+// Explicit wait states between the last MFMA of a loop and the first VALU
+// read of its accumulators after the loop: the compiler's hazard insertion
+// has been seen to miss the path that leaves a loop (or skips a block) right
+// after an MFMA, so kernels call this once after such loops.
+__device__ __forceinline__ void mfma_drain() {
+    __builtin_amdgcn_sched_barrier(0);
+    asm volatile("s_nop 7\n\ts_nop 7\n\ts_nop 7" ::: "memory");
+}
+
 // Division of non-negative x < 2^24 by a runtime n via a float reciprocal and
 // a one-step correction (exact in that range).
 struct FastDiv {

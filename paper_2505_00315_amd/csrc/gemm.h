@@ -442,9 +442,7 @@ __global__ __launch_bounds__(256) void gemm_kernel(const typename P::Args args) 
         __syncthreads();
     }
     mfma_chunk(nchunks > 0 ? (nchunks - 1) & 1 : 0);
-    // explicit wait states before the accumulators are read (see above)
-    __builtin_amdgcn_sched_barrier(0);
-    asm volatile("s_nop 7\n\ts_nop 7\n\ts_nop 7" ::: "memory");
+    mfma_drain();  // explicit wait states before the accumulators are read
     __syncthreads();  // the C tile below reuses the operand buffers
 
     // C tile to LDS: Cs[m][n], row stride NT + 4 floats
