@@ -38,7 +38,28 @@ def parse_args():
     p.add_argument("--fwd-only", action="store_true", help="time the forward pass only")
     p.add_argument("--cpu-seconds", type=float, default=15.0, help="target length of the oracle sample")
     p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
+                   help="after the timed steps, copy MIB MiB device to device once (a plain copy kernel of known "
+                        "size whose counter readings calibrate the HBM traffic counters)")
     return p.parse_args()
+
+
+def source_digest(rel):
+    """sha256[:16] of a source file, or of every file of a directory in name
+    order (any change to the kernels' sources invalidates their counters)."""
+    path = os.path.join(ROOT, rel)
+    h = hashlib.sha256()
+    if os.path.isdir(path):
+        for name in sorted(os.listdir(path)):
+            f = os.path.join(path, name)
+            if os.path.isfile(f):
+                h.update(name.encode())
+                h.update(open(f, "rb").read())
+    elif os.path.exists(path):
+        h.update(open(path, "rb").read())
+    else:
+        return None
+    return h.hexdigest()[:16]
 
 
 class HipEvents:
@@ -80,10 +101,7 @@ def traffic_for(kernel, w):
         f = dict(kv.split("=", 1) for kv in line.split())
         if f.get("stage") != kernel or f.get("workload") != w.name:
             continue
-        src = os.path.join(ROOT, f["source"])
-        if not os.path.exists(src):
-            return None
-        if hashlib.sha256(open(src, "rb").read()).hexdigest()[:16] != f["source_sha"]:
+        if source_digest(f["source"]) != f["source_sha"]:
             return None
         return float(f["hbm_bytes_per_launch"])
     return None
@@ -235,6 +253,15 @@ def main():
         "stages": stages,
         "roofline": roof,
     }
+    if args.calibrate_copy > 0:
+        nel = args.calibrate_copy * (1 << 20) // 4
+        src_t = torch.ones(nel, dtype=torch.float32, device="cuda")
+        dst_t = torch.empty_like(src_t)
+        torch.cuda.synchronize()
+        dst_t.copy_(src_t)
+        torch.cuda.synchronize()
+        line["copy_calibration_bytes"] = nel * 4
+        del src_t, dst_t
     if not args.no_cpu_baseline:
         line["cpu_baseline"] = cpu_baseline(w, inp, with_bwd, args.cpu_seconds)
     print(json.dumps(line), flush=True)

@@ -135,3 +135,86 @@ def paper_mosa_heads_for_budget(layers, h, hp, T, baseline_heads, dense_heads, s
     k = T // sparsity
     fixed = paper_flops_model(layers, h, hp, T, dense_heads)
     return int((budget - fixed) // (layers * paper_flops_mosa_head(h, hp, T, k)))
+
+
+# ---------------------------------------------------------------------------
+# Measured HBM traffic per stage from rocprofv3 counter runs
+# ---------------------------------------------------------------------------
+
+# Kernel-name patterns of each stage (MoSA heads only: dense heads reuse the
+# same kernels, so workloads with dense heads are not attributed here).
+STAGE_KERNELS = {
+    "router": (r"router_kernel",),
+    "select": (r"select_kernel",),
+    "qkv": (r"(?<!Wgrad)QkvPolicy",),
+    "attn": (r"attn_fwd",),
+    "out_scatter": (r"OutProjPolicy", r"OutCombinePolicy"),
+    "bwd_out": (r"BwdOutPolicy",),
+    "attn_bwd_kv": (r"attn_bwd_kv",),
+    "attn_bwd_q": (r"attn_bwd_q",),
+    "wgrad_qkv": (r"WgradQkvPolicy", r"wgrad_qkv_reduce"),
+    "wgrad_o": (r"WgradOPolicy", r"wgrad_o_reduce"),
+    "dx_scatter": (r"DxProjPolicy", r"DxCombinePolicy"),
+}
+
+
+def _read_counter_csv(run_dir):
+    import csv
+    import glob
+    import os
+    rows = []
+    for f in sorted(glob.glob(os.path.join(run_dir, "**", "*counter_collection.csv"), recursive=True)):
+        rows += list(csv.DictReader(open(f)))
+    rows.sort(key=lambda r: int(r["Dispatch_Id"]))
+    return rows
+
+
+def traffic_summary(fetch_dir, write_dir, copy_bytes):
+    """Per-stage HBM bytes per launch from a FETCH_SIZE run and a WRITE_SIZE
+    run (KiB per dispatch) of `bench.py --calibrate-copy`: the last dispatch of
+    each run is the plain copy of `copy_bytes` bytes, whose readings give the
+    scale of each counter.  Returns (per-stage dict, fetch scale, write scale)."""
+    import re
+    fetch, write = _read_counter_csv(fetch_dir), _read_counter_csv(write_dir)
+    if not fetch or not write:
+        raise ValueError("no counter rows")
+    f_scale = copy_bytes / (float(fetch[-1]["Counter_Value"]) * 1024.0)
+    w_scale = copy_bytes / (float(write[-1]["Counter_Value"]) * 1024.0)
+    out = {}
+    for rows, key, scale in ((fetch, "fetch", f_scale), (write, "write", w_scale)):
+        steps = sum(1 for r in rows if re.search(STAGE_KERNELS["router"][0], r["Kernel_Name"]))
+        for stage, pats in STAGE_KERNELS.items():
+            kib = sum(float(r["Counter_Value"]) for r in rows[:-1]
+                      if any(re.search(p, r["Kernel_Name"]) for p in pats))
+            if steps and kib:
+                d = out.setdefault(stage, {})
+                d[key + "_kib"] = kib / steps
+                d[key + "_bytes"] = kib / steps * 1024.0 * scale
+    for d in out.values():
+        d["hbm_bytes_per_launch"] = d.get("fetch_bytes", 0.0) + d.get("write_bytes", 0.0)
+    return out, f_scale, w_scale
+
+
+if __name__ == "__main__":
+    import argparse
+
+    ap = argparse.ArgumentParser(description="write the per-stage HBM traffic summary from two rocprofv3 "
+                                             "counter runs of bench.py --calibrate-copy")
+    ap.add_argument("--fetch", required=True, help="output directory of the FETCH_SIZE run")
+    ap.add_argument("--write", required=True, help="output directory of the WRITE_SIZE run")
+    ap.add_argument("--copy-bytes", type=int, required=True)
+    ap.add_argument("--workload", required=True)
+    ap.add_argument("--source", default="paper_2505_00315_amd/csrc")
+    ap.add_argument("--source-sha", required=True)
+    ap.add_argument("--command", default="")
+    a = ap.parse_args()
+    stages, fs, ws = traffic_summary(a.fetch, a.write, a.copy_bytes)
+    print(f"# HBM traffic per launch of each stage, workload {a.workload}: rocprofv3 FETCH_SIZE and WRITE_SIZE "
+          f"(KiB per dispatch, one run each), scaled by the readings of a plain {a.copy_bytes}-byte device copy "
+          f"in the same run (fetch x{fs:.4f}, write x{ws:.4f}).")
+    if a.command:
+        print(f"# command: {a.command}")
+    for name, d in stages.items():
+        print(f"stage={name} workload={a.workload} source={a.source} source_sha={a.source_sha} "
+              f"fetch_kib={d.get('fetch_kib', 0):.1f} write_kib={d.get('write_kib', 0):.1f} "
+              f"hbm_bytes_per_launch={d['hbm_bytes_per_launch']:.0f}")
