@@ -51,17 +51,50 @@ __global__ __launch_bounds__(256) void router_kernel(const ST* __restrict__ X, c
 #pragma unroll
     for (int m = 0; m < 8; ++m) acc[m] = zero4();
 
-    for (int kc = 0; kc < d; kc += 32) {
-        Frag8<ST> bx = tok_ok ? frag8_load<ST>(xrow + kc + 8 * g) : frag8_zero<ST>();
+    // ||x_t||^2 in fp64 from the same fragments (waves 0 and 1 of the first
+    // head group see every token of the workgroup exactly once).
+    const bool do_norm = blockIdx.y == 0 && (wave >> 1) == 0;
+    double ss = 0.0;
+    // Groups of U chunks: all loads of a group are issued before its MFMAs;
+    // out-of-range rows and chunks load a clamped address and are zeroed.
+    constexpr int U = 8;
+    for (int kc0 = 0; kc0 < d; kc0 += 32 * U) {
+        Frag8<ST> bx[U];
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const int kc = min(kc0 + 32 * u, d - 32);
+            const Frag8<ST> v = frag8_load<ST>(xrow + kc + 8 * g);
+            bx[u] = (tok_ok && kc0 + 32 * u < d) ? v : frag8_zero<ST>();
+        }
+        if (do_norm) {
+#pragma unroll
+            for (int u = 0; u < U; ++u) {
+                float x[8];
+                frag8_to_f32<ST>(bx[u], x);
+#pragma unroll
+                for (int j = 0; j < 8; ++j) ss += (double)x[j] * (double)x[j];
+            }
+        }
 #pragma unroll
         for (int m = 0; m < 8; ++m) {
             const int hb = (wave >> 1) + 2 * m;
             if (hb < nhb) {
                 const int h = h0 + hb * 16 + c16;
-                Frag8<ST> aw = (h < H) ? frag8_load<ST>(Wr + (size_t)h * d + kc + 8 * g) : frag8_zero<ST>();
-                f32x4 part = zero4();
-                mma8(part, aw, bx);
-                acc[m] += part;
+                const ST* wrow = Wr + (size_t)min(h, H - 1) * d;
+                Frag8<ST> aw[U];
+#pragma unroll
+                for (int u = 0; u < U; ++u) {
+                    const int kc = min(kc0 + 32 * u, d - 32);
+                    const Frag8<ST> v = frag8_load<ST>(wrow + kc + 8 * g);
+                    aw[u] = (h < H && kc0 + 32 * u < d) ? v : frag8_zero<ST>();
+                }
+                // every chunk starts from zero and is added with one fp32 add
+#pragma unroll
+                for (int u = 0; u < U; ++u) {
+                    f32x4 part = zero4();
+                    mma8(part, aw[u], bx[u]);
+                    acc[m] += part;
+                }
             }
         }
     }
@@ -81,24 +114,13 @@ __global__ __launch_bounds__(256) void router_kernel(const ST* __restrict__ X, c
         }
     }
 
-    // ||x_t||_2 upper bound: 8 threads per token, fp64 partial sums of squares.
-    if (blockIdx.y == 0) {
-        const int tt = threadIdx.x >> 3, part = threadIdx.x & 7;
-        const int tk = tok0 + tt;
-        double ss = 0.0;
-        if (tk < BT) {
-            const ST* row = X + (size_t)tk * d;
-            for (int c = part; c < d; c += 8) {
-                double v = (double)ld1<ST>(row + c);
-                ss += v * v;
-            }
-        }
-        ss += __shfl_xor(ss, 1, 64);
-        ss += __shfl_xor(ss, 2, 64);
-        ss += __shfl_xor(ss, 4, 64);
-        if (part == 0 && tk < BT) {
+    // ||x_t||_2 upper bound (lanes g = 0..3 hold disjoint quarters of the row)
+    if (do_norm) {
+        ss += __shfl_xor(ss, 16, 64);
+        ss += __shfl_xor(ss, 32, 64);
+        if (g == 0 && tok_ok) {
             // fp64 rounding of <= d squares and the sqrt: far below 2^-30 relative.
-            xnorm[tk] = f32_round_up(sqrt(ss) * (1.0 + 0x1p-30));
+            xnorm[tok] = f32_round_up(sqrt(ss) * (1.0 + 0x1p-30));
         }
     }
 }

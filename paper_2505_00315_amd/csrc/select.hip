@@ -33,6 +33,7 @@
 // The total is inflated by 2^-10 to absorb the fp64 evaluation of the bound.
 #include "common.h"
 #include "exact_dot.h"
+#include "gemm.h"
 #include "kernels.h"
 
 namespace mosa {
@@ -266,10 +267,333 @@ __global__ __launch_bounds__(256) void select_kernel(const float* __restrict__ z
     }
 }
 
+// One wave per (b, h) row for T <= 64 * EPT <= 2048: the same contract and
+// steps, with no block barriers and no LDS histograms.  Token t = 64 e + lane
+// (coalesced loads); the two order statistics are found bit by bit from the
+// top: the keys of a lane are transposed once into bit planes, and at each
+// bit the candidates that share the prefix and have the bit set are counted
+// with one popcount per lane and one DPP wave sum (both selections packed in
+// one 32-bit sum).  The in-order compaction is a running ballot count.
+// Uncertain tokens are first re-scored in fp64 (exact products, bounded
+// summation error), which separates them unless keys (nearly) tie; only then
+// are exact keys computed with the long accumulator in this wave's LDS.
+__device__ __forceinline__ uint64_t lanes_below() {
+    return (1ull << (threadIdx.x & 63)) - 1ull;
+}
+
+// In-place transpose of the two 16 x 16 bit matrices held in the low and high
+// halves of 16 registers (row = register index, column = bit): afterwards
+// bit e of the low (high) half of r[b] is bit b (b + 16) of the original r[e].
+__device__ __forceinline__ void transpose16x2(uint32_t (&r)[16]) {
+    uint32_t m = 0x00FF00FFu;
+#pragma unroll
+    for (int j = 8; j != 0; j >>= 1, m ^= (m << j)) {
+#pragma unroll
+        for (int k = 0; k < 16; k = (k + j + 1) & ~j) {
+            const uint32_t t = ((r[k] >> j) ^ r[k + j]) & m;
+            r[k + j] ^= t;
+            r[k] ^= t << j;
+        }
+    }
+}
+
+// Bit planes of EPT keys per lane: plane(b) bit e = bit b of key e.
+template <int EPT>
+struct BitPlanes {
+    static constexpr int G = (EPT + 15) / 16;
+    uint32_t r[G][16];
+    __device__ __forceinline__ void build(const uint32_t (&key)[EPT]) {
+#pragma unroll
+        for (int gr = 0; gr < G; ++gr) {
+#pragma unroll
+            for (int i = 0; i < 16; ++i) r[gr][i] = gr * 16 + i < EPT ? key[gr * 16 + i] : 0u;
+            transpose16x2(r[gr]);
+        }
+    }
+    template <int B>
+    __device__ __forceinline__ uint32_t plane() const {
+        uint32_t m = 0u;
+#pragma unroll
+        for (int gr = 0; gr < G; ++gr) m |= (B >= 16 ? (r[gr][B - 16] >> 16) : (r[gr][B] & 0xffffu)) << (16 * gr);
+        return m;
+    }
+};
+
+// One bit of the two top-down selections (k-th largest lo, (k+1)-th largest hi).
+template <int B, int EPT>
+__device__ __forceinline__ void select_bit(const BitPlanes<EPT>& pa, const BitPlanes<EPT>& pb, uint32_t& candA,
+                                           uint32_t& candB, uint32_t& prefA, uint32_t& prefB, int& remA,
+                                           int& remB) {
+    const uint32_t hA = pa.template plane<B>(), hB = pb.template plane<B>();
+    // both counts in one wave sum (each <= T <= 2048)
+    const uint32_t both = wave_sum_u32((uint32_t)__popc(candA & hA) | ((uint32_t)__popc(candB & hB) << 16));
+    const int cA = (int)(both & 0xffffu), cB = (int)(both >> 16);
+    if (cA >= remA) {
+        prefA |= 1u << B;
+        candA &= hA;
+    } else {
+        remA -= cA;
+        candA &= ~hA;
+    }
+    if (cB >= remB) {
+        prefB |= 1u << B;
+        candB &= hB;
+    } else {
+        remB -= cB;
+        candB &= ~hB;
+    }
+}
+
+template <int B, int EPT>
+__device__ __forceinline__ void select_bits(const BitPlanes<EPT>& pa, const BitPlanes<EPT>& pb, uint32_t& candA,
+                                            uint32_t& candB, uint32_t& prefA, uint32_t& prefB, int& remA,
+                                            int& remB) {
+    select_bit<B, EPT>(pa, pb, candA, candB, prefA, prefB, remA, remB);
+    if constexpr (B > 0) select_bits<B - 1, EPT>(pa, pb, candA, candB, prefA, prefB, remA, remB);
+}
+
+template <typename ST, int EPT>
+__global__ __launch_bounds__(256) void select_wave_kernel(const float* __restrict__ z, const float* __restrict__ xnorm,
+                                                          const ST* __restrict__ X, const ST* __restrict__ Wr, int BH,
+                                                          int T, int d, int H, int k, int32_t* __restrict__ I,
+                                                          float* __restrict__ r, int16_t* __restrict__ slot,
+                                                          int32_t* __restrict__ unc_tok, double* __restrict__ unc_key,
+                                                          int32_t* __restrict__ unc_sel) {
+    __shared__ int64_t s_long[4][kLongDigits];
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int row = blockIdx.x * 4 + wave;
+    if (row >= BH) return;  // whole wave; nothing below synchronises across waves
+    const int b = row / H, h = row % H;
+    const size_t rowT = (size_t)row * T;
+
+    // ||w_h||_2 (fp64) for the error bound: 8 elements per lane and load
+    const ST* w = Wr + (size_t)h * d;
+    double ss = 0.0;
+    for (int c0 = 0; c0 < d; c0 += 8 * 64 * 2) {
+        Vec8<ST> v[2];
+#pragma unroll
+        for (int q = 0; q < 2; ++q) v[q] = vec8_load<ST>(w + min(c0 + 8 * (64 * q + lane), d - 8));
+#pragma unroll
+        for (int q = 0; q < 2; ++q) {
+            if (c0 + 8 * (64 * q + lane) < d) {
+                float x[8];
+                vec8_to_f32<ST>(v[q], x);
+#pragma unroll
+                for (int j = 0; j < 8; ++j) ss += (double)x[j] * (double)x[j];
+            }
+        }
+    }
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) ss += __shfl_xor(ss, o, 64);
+    const double wn = sqrt(ss) * (1.0 + 0x1p-30);
+    const int nc = d / 32;
+    const double coef = (96.0 * 0x1p-23 + 1.01 * (double)nc * 0x1p-24) * (1.0 + 0x1p-10);
+    const double absterm = (double)(d + nc) * 0x1p-126 * (1.0 + 0x1p-10);
+
+    const float* zr = z + rowT;
+    const float* xn = xnorm + (size_t)b * T;
+    uint32_t lo[EPT], hi[EPT];
+    float zv[EPT];
+#pragma unroll
+    for (int e = 0; e < EPT; ++e) {
+        const int t = 64 * e + lane;
+        const int tc = min(t, T - 1);
+        zv[e] = zr[tc];
+        const double xv = (double)xn[tc];
+        const double beta = coef * xv * wn + absterm * (1.0 + xv + wn);
+        lo[e] = t < T ? order_key(f32_down((double)zv[e] - beta)) : 0u;  // 0: below every real key
+        hi[e] = t < T ? order_key(f32_up((double)zv[e] + beta)) : 0u;
+    }
+
+    const bool all = k >= T;
+    uint32_t A = 0u, Bk = 0u;
+    if (!all) {
+        // candA / candB: bit e set while element e still matches the prefix
+        uint32_t candA = 0u, candB = 0u;
+#pragma unroll
+        for (int e = 0; e < EPT; ++e)
+            if (64 * e + lane < T) {
+                candA |= 1u << e;
+                candB |= 1u << e;
+            }
+        uint32_t prefA = 0u, prefB = 0u;
+        int remA = k, remB = k + 1;
+        BitPlanes<EPT> pa, pb;
+        pa.build(lo);
+        pb.build(hi);
+        select_bits<31, EPT>(pa, pb, candA, candB, prefA, prefB, remA, remB);
+        A = prefA;
+        Bk = prefB;
+    }
+
+    // Classify; positions of the uncertain tokens in index order.
+    uint32_t inm = 0u, uncm = 0u;
+    int tot_in = 0, tot_unc = 0;
+    int upos[EPT];
+#pragma unroll
+    for (int e = 0; e < EPT; ++e) {
+        const int t = 64 * e + lane;
+        const bool in = t < T && (all || lo[e] > Bk);
+        const bool unc = t < T && !in && !(hi[e] < A);
+        const uint64_t bi = __ballot(in), bu = __ballot(unc);
+        upos[e] = tot_unc + __popcll(bu & lanes_below());
+        if (in) inm |= 1u << e;
+        if (unc) uncm |= 1u << e;
+        tot_in += __popcll(bi);
+        tot_unc += __popcll(bu);
+    }
+    int need = k - tot_in;  // 0 <= need <= tot_unc when the bound holds
+    if (need < 0) need = 0;
+    if (need > tot_unc) need = tot_unc;
+    const bool resolve = need > 0 && need < tot_unc;
+
+    if (resolve) {
+#pragma unroll
+        for (int e = 0; e < EPT; ++e)
+            if ((uncm >> e) & 1u) unc_tok[rowT + upos[e]] = 64 * e + lane;
+        __threadfence_block();
+        __builtin_amdgcn_wave_barrier();
+        // Second level: the logits of the uncertain tokens in fp64.  Products
+        // of two stored values are exact in fp64; any order of the d - 1
+        // additions errs by at most (d - 1) u64 sum|x_i w_i| <= that times
+        // ||x|| ||w||, and the key RN64(s) is within half an ulp of s.
+        for (int u = 0; u < tot_unc; ++u) {
+            const int t = unc_tok[rowT + u];
+            const ST* xr = X + ((size_t)b * T + t) * d;
+            double acc = 0.0;
+            for (int c0 = 0; c0 < d; c0 += 8 * 64) {
+                const int c = min(c0 + 8 * lane, d - 8);
+                float xv8[8], wv8[8];
+                vec8_to_f32<ST>(vec8_load<ST>(xr + c), xv8);
+                vec8_to_f32<ST>(vec8_load<ST>(w + c), wv8);
+                if (c0 + 8 * lane < d) {
+#pragma unroll
+                    for (int j = 0; j < 8; ++j) acc += (double)xv8[j] * (double)wv8[j];
+                }
+            }
+#pragma unroll
+            for (int o = 32; o >= 1; o >>= 1) acc += __shfl_xor(acc, o, 64);
+            if (lane == 0) unc_key[rowT + u] = acc;
+        }
+        __threadfence_block();
+        __builtin_amdgcn_wave_barrier();
+        // Decide from the fp64 intervals where they separate; otherwise fall
+        // back to exact keys for all uncertain tokens.
+        bool undecided = false;
+        for (int u = lane; u < tot_unc; u += 64) {
+            const double vu = unc_key[rowT + u];
+            const double bu = 1.01 * (double)d * 0x1p-53 * (double)xn[unc_tok[rowT + u]] * wn + fabs(vu) * 0x1p-51;
+            int above = 0, maybe = 0;
+            for (int v = 0; v < tot_unc; ++v) {
+                if (v == u) continue;
+                const double vv = unc_key[rowT + v];
+                const double bv = 1.01 * (double)d * 0x1p-53 * (double)xn[unc_tok[rowT + v]] * wn + fabs(vv) * 0x1p-51;
+                if (vv - bv > vu + bu) ++above;         // certainly above u
+                else if (!(vv + bv < vu - bu)) ++maybe;  // order unknown
+            }
+            int sel = -1;
+            if (above + maybe < need) sel = 1;
+            else if (above >= need) sel = 0;
+            else undecided = true;
+            unc_sel[rowT + u] = sel;
+        }
+        undecided = __ballot(undecided) != 0ull;
+        __threadfence_block();
+        __builtin_amdgcn_wave_barrier();
+        if (undecided) {
+            // Exact keys (long accumulator in this wave's LDS digits).
+            for (int u = 0; u < tot_unc; ++u) {
+                if (lane < kLongDigits) s_long[wave][lane] = 0;
+                __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "workgroup");
+                __builtin_amdgcn_wave_barrier();
+                const int t = unc_tok[rowT + u];
+                const ST* xr = X + ((size_t)b * T + t) * d;
+                for (int c = lane; c < d; c += 64) {
+                    uint32_t sx, Mx, sw, Mw;
+                    int Ex, Ew;
+                    split_elem<ST>(xr + c, sx, Mx, Ex);
+                    split_elem<ST>(w + c, sw, Mw, Ew);
+                    const ProductParts p = product_parts(sx, Mx, Ex, sw, Mw, Ew);
+                    if (!p.zero) {
+#pragma unroll
+                        for (int q = 0; q < 3; ++q) {
+                            if (p.v[q]) {
+                                const uint64_t add = p.negative ? (uint64_t)(-(int64_t)p.v[q]) : p.v[q];
+                                atomicAdd(reinterpret_cast<unsigned long long*>(&s_long[wave][p.j + q]),
+                                          (unsigned long long)add);
+                            }
+                        }
+                    }
+                }
+                __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "workgroup");
+                __builtin_amdgcn_wave_barrier();
+                if (lane == 0) unc_key[rowT + u] = long_accumulator_round(&s_long[wave][0]);
+                __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "workgroup");
+                __builtin_amdgcn_wave_barrier();
+            }
+            __threadfence_block();
+            __builtin_amdgcn_wave_barrier();
+            // exact rank among the uncertain tokens (key desc, index asc)
+            for (int u = lane; u < tot_unc; u += 64) {
+                const double ku = unc_key[rowT + u];
+                const int tu = unc_tok[rowT + u];
+                int rank = 0;
+                for (int v = 0; v < tot_unc; ++v) {
+                    const double kv = unc_key[rowT + v];
+                    const int tv = unc_tok[rowT + v];
+                    rank += (kv > ku) || (kv == ku && tv < tu);
+                }
+                unc_sel[rowT + u] = rank < need;
+            }
+        }
+        __threadfence_block();
+        __builtin_amdgcn_wave_barrier();
+    }
+
+    // Compact the chosen tokens in index order: I ascending, r, and the slot map.
+    int pos0 = 0;
+#pragma unroll
+    for (int e = 0; e < EPT; ++e) {
+        const int t = 64 * e + lane;
+        bool sel = (inm >> e) & 1u;
+        if ((uncm >> e) & 1u) sel = resolve ? (unc_sel[rowT + upos[e]] != 0) : (need == tot_unc);
+        const uint64_t bs = __ballot(sel);
+        const int pos = pos0 + __popcll(bs & lanes_below());
+        int16_t sl = -1;
+        if (sel && pos < k) {
+            I[(size_t)row * k + pos] = t;
+            r[(size_t)row * k + pos] = 1.0f / (1.0f + expf(-zv[e]));
+            sl = (int16_t)pos;
+        }
+        if (t < T) slot[rowT + t] = sl;
+        pos0 += __popcll(bs);
+    }
+    // Only reachable if the logit error bound were violated: keep every slot
+    // defined (token 0, r = 0) so that downstream kernels stay in bounds.
+    for (int pos = pos0 + lane; pos < k; pos += 64) {
+        I[(size_t)row * k + pos] = 0;
+        r[(size_t)row * k + pos] = 0.f;
+    }
+}
+
 template <typename ST>
 int launch_select_t(const float* z, const float* xnorm, const ST* X, const ST* Wr, int B, int T, int d, int H,
                     int k, int32_t* I, float* r, int16_t* slot, int32_t* unc_tok, double* unc_key,
                     int32_t* unc_sel, hipStream_t stream) {
+    if (T <= 2048) {
+        const dim3 wgrid((B * H + 3) / 4), wblock(256);
+#define MOSA_SELECT_WAVE(E)                                                                                       \
+    hipLaunchKernelGGL((select_wave_kernel<ST, E>), wgrid, wblock, 0, stream, z, xnorm, X, Wr, B * H, T, d, H, k, I, \
+                       r, slot, unc_tok, unc_key, unc_sel)
+        if (T <= 64) MOSA_SELECT_WAVE(1);
+        else if (T <= 128) MOSA_SELECT_WAVE(2);
+        else if (T <= 256) MOSA_SELECT_WAVE(4);
+        else if (T <= 512) MOSA_SELECT_WAVE(8);
+        else if (T <= 1024) MOSA_SELECT_WAVE(16);
+        else MOSA_SELECT_WAVE(32);
+#undef MOSA_SELECT_WAVE
+        return hipGetLastError() == hipSuccess ? 0 : -1;
+    }
     dim3 grid(B * H), block(256);
 #define MOSA_SELECT_CASE(E)                                                                               \
     hipLaunchKernelGGL((select_kernel<ST, E>), grid, block, 0, stream, z, xnorm, X, Wr, T, d, H, k, I, r, \
