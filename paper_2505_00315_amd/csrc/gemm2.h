@@ -1,0 +1,301 @@
+// Multi-stage MFMA GEMM engine for bf16 storage with direct global->LDS loads.
+//
+//   C[M x N] = sum_k A[M x K] B[K x N]   (fp32 accumulation), one problem per
+//   "batch" index, tiles of MT x NT, four waves, K in chunks of KC.
+//
+// Operands are copied from global memory straight into LDS with 16-byte
+// global_load_lds instructions (no register staging): one instruction of a
+// wave fills 1 KB of LDS, lane l writing bytes 16 l .. 16 l + 15, and each
+// lane chooses the global 16 bytes that belong at its slot.  STAGES chunk
+// buffers are in flight; one barrier per chunk.
+//
+// A k-contiguous operand (rows along M or N, 8 consecutive k per 16 bytes) is
+// stored row-major [rows][KC] with the 16-byte units of a row XOR-permuted
+// (f(r) below) so that the ds_read_b128 of an MFMA fragment (16 rows, same
+// k) hits distinct banks.  An m-contiguous operand (rows along K, e.g. a
+// weight W[k][n]) is stored [KC][R] as in memory, units permuted by h(k), and
+// its MFMA fragments are read with ds_read_b64_tr_b16, which transposes 4 x 4
+// blocks of 16-bit elements across the lanes of a 16-lane group: source lane
+// s supplies the address of row kbase + s/4, columns m0 + 4 (s % 4) .. +3, and
+// lane i receives rows kbase .. kbase + 3 of column m0 + i.  Two such reads give
+// the 8 consecutive k of an MFMA operand, in the same k order as the
+// k-contiguous reads.
+//
+// Policy P (all addresses must be valid for any k in [0, K) and any row; rows
+// past the problem are clamped by the policy and their results discarded):
+//   MT, NT, KC, WM, WN, STAGES, EPI_LDS; A_KCONTIG, B_KCONTIG;
+//   tile(args, logical, batch, m0, n0), k_size(args, batch) (a multiple of KC);
+//   k-contiguous: a_row(args, batch, m) -> ARef, a_elem(args, batch, ARef, k)
+//                 (likewise b_row / b_elem);
+//   m-contiguous: a_maddr(args, batch, k, m8) / b_maddr(args, batch, k, n8) and
+//                 a_kstride(args, batch) / b_kstride(args, batch), the element
+//                 distance between consecutive k (addresses move linearly in k);
+//   epilogue(args, batch, m0, n0, Cs, ldc, tid, extra) as in gemm.h.
+#pragma once
+
+#include "gemm.h"
+
+namespace mosa {
+
+typedef __attribute__((address_space(3))) unsigned char lds_u8;
+
+// One wave's 1 KB of LDS from 64 lanes x 16 bytes of global memory
+// (global_load_lds_dwordx4: the LDS base goes in M0, lane l writes base +
+// 16 l).  Issued as inline assembly so that the compiler does not treat the
+// asynchronous LDS write as aliasing every later LDS read and wait for all
+// loads in flight; the engine waits for these loads itself (wait_vmcnt).
+// `base` is the wave-uniform LDS byte address of the 1 KB block.
+__device__ __forceinline__ void lds_load16(const void* g, uint32_t base) {
+    asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off" : : "v"(g), "s"(base) : "memory", "m0");
+}
+__device__ __forceinline__ uint32_t lds_addr(const void* p) { return (uint32_t)(size_t)(const lds_u8*)p; }
+
+// Four 16-bit elements of a transposed 4 x 4 block (see above), issued as
+// inline assembly: the compiler cannot tell which LDS bytes the builtin form
+// reads and would wait for every direct-to-LDS load in flight before it.  The
+// result is not ready until lds_wait() below; nothing may read it earlier.
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+__device__ __forceinline__ u32x2 lds_read_tr16(const unsigned char* p) {
+    const uint32_t off = (uint32_t)(size_t)(lds_u8*)p;
+    u32x2 r;
+    asm volatile("ds_read_b64_tr_b16 %0, %1" : "=v"(r) : "v"(off) : "memory");
+    return r;
+}
+// Wait for every outstanding LDS read of this wave.
+__device__ __forceinline__ void lds_wait() { asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory"); }
+// Make x depend on the preceding lds_wait() (an empty volatile statement that
+// claims to modify x keeps its consumers after the wait).
+__device__ __forceinline__ void lds_ready(u32x4& x) { asm volatile("" : "+v"(x)); }
+
+// Unit permutations (both are involutions within a row).
+__device__ __forceinline__ int kswz(int r, int lpr) {
+    return lpr == 8 ? ((r & 7) ^ ((r >> 3) & 1)) : ((r & 3) ^ ((r >> 2) & 3));
+}
+template <int U>  // units per m-contiguous row
+__device__ __forceinline__ int mswz(int k, int u) {
+    if constexpr (U % 16 == 0) return u ^ (2 * ((k & 3) | (((k >> 3) & 1) << 2)));
+    else if constexpr (U % 8 == 0) return u ^ (2 * (((k >> 1) & 1) | (((k >> 3) & 1) << 1)));
+    else return u;
+}
+
+template <class P>
+struct Gemm2Shape {
+    static constexpr int MT = P::MT, NT = P::NT, KC = P::KC, WM = P::WM, WN = P::WN, STAGES = P::STAGES;
+    static constexpr int WTM = MT / WM, WTN = NT / WN, FM = WTM / 16, FN = WTN / 16;
+    static constexpr int LPR = KC / 8;  // units per k-contiguous row
+    static constexpr int A_UNITS = P::A_KCONTIG ? MT * LPR : KC * (MT / 8);
+    static constexpr int B_UNITS = P::B_KCONTIG ? NT * LPR : KC * (NT / 8);
+    static constexpr int IA = A_UNITS / 256, IB = B_UNITS / 256;  // instructions per wave per chunk
+    static constexpr int A_BYTES = A_UNITS * 16, B_BYTES = B_UNITS * 16;
+    static constexpr int STAGE_BYTES = A_BYTES + B_BYTES;
+    static_assert(WM * WN == 4 && WTM % 16 == 0 && WTN % 16 == 0 && KC % 32 == 0, "tile shape");
+    static_assert(A_UNITS % 256 == 0 && B_UNITS % 256 == 0, "whole instructions per wave");
+    static_assert((STAGES - 2) * (IA + IB) <= 63, "vmcnt range");
+    static constexpr size_t ctile_bytes = (size_t)MT * (NT + 4) * sizeof(float);
+    static constexpr size_t lds_bytes() {
+        const size_t ops = (size_t)STAGES * STAGE_BYTES;
+        const size_t epi = ctile_bytes + P::EPI_LDS;
+        return ops > epi ? ops : epi;
+    }
+};
+
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+    static_assert(N >= 0 && N <= 63, "vmcnt");
+    // gfx9 s_waitcnt: vmcnt [3:0] and [15:14], expcnt [6:4] = 7, lgkmcnt [11:8] = 15
+    __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | 0x0F70);
+}
+
+template <class P>
+__global__ __launch_bounds__(256) void gemm2_kernel(const typename P::Args args) {
+    using ST = uint16_t;
+    using S = Gemm2Shape<P>;
+    constexpr int MT = S::MT, NT = S::NT, KC = S::KC, LPR = S::LPR, STG = S::STAGES;
+    extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
+
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int g = lane >> 4, c16 = lane & 15;
+    int batch, m0, n0;
+    P::tile(args, xcd_logical_id(blockIdx.x, gridDim.x), batch, m0, n0);
+    const int K = P::k_size(args, batch);
+    const int nchunks = K / KC;
+
+    // Where this lane's 16 bytes of each load instruction come from for chunk
+    // 0, and how far they move per chunk (KC elements along k).  Computed once
+    // so that the loop does plain pointer arithmetic.
+    const ST* asrc[S::IA > 0 ? S::IA : 1];
+    const ST* bsrc[S::IB > 0 ? S::IB : 1];
+#pragma unroll
+    for (int j = 0; j < S::IA; ++j) {
+        const int p = 64 * (wave + 4 * j) + lane;  // unit of the tile
+        if constexpr (P::A_KCONTIG) {
+            const int r = p / LPR, pos = p % LPR;
+            asrc[j] = P::a_elem(args, batch, P::a_row(args, batch, m0 + r), 8 * (pos ^ kswz(r, LPR)));
+        } else {
+            constexpr int U = MT / 8;
+            const int kr = p / U, pos = p % U;
+            asrc[j] = P::a_maddr(args, batch, kr, m0 + 8 * mswz<U>(kr, pos));
+        }
+    }
+#pragma unroll
+    for (int j = 0; j < S::IB; ++j) {
+        const int p = 64 * (wave + 4 * j) + lane;
+        if constexpr (P::B_KCONTIG) {
+            const int r = p / LPR, pos = p % LPR;
+            bsrc[j] = P::b_elem(args, batch, P::b_row(args, batch, n0 + r), 8 * (pos ^ kswz(r, LPR)));
+        } else {
+            constexpr int U = NT / 8;
+            const int kr = p / U, pos = p % U;
+            bsrc[j] = P::b_maddr(args, batch, kr, n0 + 8 * mswz<U>(kr, pos));
+        }
+    }
+    size_t astep = KC, bstep = KC;
+    if constexpr (!P::A_KCONTIG) astep *= P::a_kstride(args, batch);
+    if constexpr (!P::B_KCONTIG) bstep *= P::b_kstride(args, batch);
+
+    // LDS address of this wave's first 1 KB block of a stage (scalar).
+    const uint32_t lds_wave = __builtin_amdgcn_readfirstlane(lds_addr(smem) + 1024 * wave);
+
+    // Issue the loads of chunk c into its stage buffer (chunks past the end
+    // load valid, clamped addresses into a buffer nobody reads).
+    auto issue_buf = [&](int c, int bidx) {
+        const uint32_t buf = lds_wave + bidx * S::STAGE_BYTES;
+        const size_t kc = (size_t)min(c, nchunks - 1);
+#pragma unroll
+        for (int j = 0; j < S::IA; ++j) lds_load16(asrc[j] + kc * astep, buf + 4096 * j);
+#pragma unroll
+        for (int j = 0; j < S::IB; ++j) lds_load16(bsrc[j] + kc * bstep, buf + S::A_BYTES + 4096 * j);
+    };
+
+    const int wm = wave / S::WN, wn = wave % S::WN;
+    f32x4 acc[S::FM][S::FN];
+#pragma unroll
+    for (int i = 0; i < S::FM; ++i)
+#pragma unroll
+        for (int j = 0; j < S::FN; ++j) acc[i][j] = zero4();
+
+    // Fragment of 8 consecutive k at ks + 8g for operand row `row` (the
+    // MFMA's M or N index) from a stage buffer.
+    auto frag_k = [&](const unsigned char* t, int row, int ks) {
+        const int s = (ks >> 3) + g;
+        Frag8<ST> f;
+        f.v = __builtin_bit_cast(bf16x8, *reinterpret_cast<const uint4*>(t + (row * LPR + (s ^ kswz(row, LPR))) * 16));
+        return f;
+    };
+    // m-contiguous fragment: two transposed reads, raw (see lds_read_tr16)
+    auto frag_m = [&](const unsigned char* t, int mbase, int ks, auto u_tag) {
+        constexpr int U = decltype(u_tag)::value;
+        const int mcol = mbase + 4 * (c16 & 3);
+        const int u = mcol >> 3, half = (mcol >> 2) & 1;
+        const int k0r = ks + 8 * g + (c16 >> 2);
+        const u32x2 lo = lds_read_tr16(t + (k0r * U + mswz<U>(k0r, u)) * 16 + 8 * half);
+        const int k1r = k0r + 4;
+        const u32x2 hi = lds_read_tr16(t + (k1r * U + mswz<U>(k1r, u)) * 16 + 8 * half);
+        return u32x4{lo.x, lo.y, hi.x, hi.y};
+    };
+    auto mfma_buf = [&](int bidx) {
+        const unsigned char* ta = smem + bidx * S::STAGE_BYTES;
+        const unsigned char* tb = ta + S::A_BYTES;
+#pragma unroll
+        for (int ks = 0; ks < KC; ks += 32) {
+            Frag8<ST> fa[S::FM], fb[S::FN];
+            u32x4 ma[S::FM], mb[S::FN];  // raw m-contiguous fragments
+#pragma unroll
+            for (int i = 0; i < S::FM; ++i) {
+                if constexpr (P::A_KCONTIG) fa[i] = frag_k(ta, wm * S::WTM + i * 16 + c16, ks);
+                else ma[i] = frag_m(ta, wm * S::WTM + i * 16, ks, std::integral_constant<int, MT / 8>{});
+            }
+#pragma unroll
+            for (int j = 0; j < S::FN; ++j) {
+                if constexpr (P::B_KCONTIG) fb[j] = frag_k(tb, wn * S::WTN + j * 16 + c16, ks);
+                else mb[j] = frag_m(tb, wn * S::WTN + j * 16, ks, std::integral_constant<int, NT / 8>{});
+            }
+            if constexpr (!P::A_KCONTIG || !P::B_KCONTIG) {
+                lds_wait();
+#pragma unroll
+                for (int i = 0; i < S::FM; ++i)
+                    if constexpr (!P::A_KCONTIG) {
+                        lds_ready(ma[i]);
+                        fa[i].v = __builtin_bit_cast(bf16x8, ma[i]);
+                    }
+#pragma unroll
+                for (int j = 0; j < S::FN; ++j)
+                    if constexpr (!P::B_KCONTIG) {
+                        lds_ready(mb[j]);
+                        fb[j].v = __builtin_bit_cast(bf16x8, mb[j]);
+                    }
+            }
+#pragma unroll
+            for (int i = 0; i < S::FM; ++i)
+#pragma unroll
+                for (int j = 0; j < S::FN; ++j) mma8(acc[i][j], fa[i], fb[j]);
+        }
+    };
+
+    // Pipeline: STAGES - 1 chunks in flight; per chunk one wait, one barrier,
+    // the loads of chunk c + STAGES - 1, then the MFMAs of chunk c.  Every
+    // wave issues exactly IA + IB loads per chunk, so the wait count is a
+    // constant.  An empty K range (no dense heads) issues nothing.
+    // The loop is unrolled by STAGES so that every stage buffer has a constant
+    // LDS offset: the compiler then sees that the loads in flight write other
+    // buffers than the one being read and does not wait for them.
+    // The only way out is after the MFMAs of the last chunk, through
+    // mfma_drain(): the compiler misses the MFMA result hazard on loop-exit
+    // edges, where it moves the accumulators to other registers.
+    if (nchunks > 0) {
+#pragma unroll
+        for (int s = 0; s < STG - 1; ++s) issue_buf(s, s);
+        for (int c0 = 0;; c0 += STG) {
+#pragma unroll
+            for (int u = 0; u < STG; ++u) {
+                const int c = c0 + u;
+                wait_vmcnt<(STG - 2) * (S::IA + S::IB)>();
+                __syncthreads();  // chunk c is in LDS for every wave; chunk c-1's buffer is free
+                issue_buf(c + STG - 1, (u + STG - 1) % STG);
+                __builtin_amdgcn_sched_barrier(0);
+                mfma_buf(u);
+                if (c + 1 == nchunks) {
+                    mfma_drain();
+                    goto pipeline_done;
+                }
+            }
+        }
+    }
+pipeline_done:
+    wait_vmcnt<0>();  // the trailing loads write into the buffers the C tile reuses
+    __syncthreads();
+
+    // C tile to LDS: Cs[m][n], row stride NT + 4 floats
+    float* Cs = reinterpret_cast<float*>(smem);
+    constexpr int LDC = NT + 4;
+#pragma unroll
+    for (int i = 0; i < S::FM; ++i)
+#pragma unroll
+        for (int j = 0; j < S::FN; ++j)
+#pragma unroll
+            for (int r = 0; r < 4; ++r)
+                Cs[(wm * S::WTM + i * 16 + 4 * g + r) * LDC + wn * S::WTN + j * 16 + c16] = acc[i][j][r];
+    __syncthreads();
+    P::epilogue(args, batch, m0, n0, Cs, LDC, tid, smem + S::ctile_bytes);
+}
+
+template <class P>
+int launch_gemm2(const typename P::Args& args, int nblocks, hipStream_t stream) {
+    if (nblocks <= 0) return 0;
+    constexpr size_t lds = Gemm2Shape<P>::lds_bytes();
+    auto kern = gemm2_kernel<P>;
+    if (lds > 64 * 1024) {
+        static bool set = false;
+        if (!set) {
+            if (hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds) !=
+                hipSuccess)
+                return -1;
+            set = true;
+        }
+    }
+    hipLaunchKernelGGL(kern, dim3(nblocks), dim3(256), lds, stream, args);
+    return hipGetLastError() == hipSuccess ? 0 : -1;
+}
+
+}  // namespace mosa

@@ -11,6 +11,7 @@
 // Workgroups of one head are numbered consecutively on one XCD so the head's
 // weights are fetched from HBM once into that XCD's L2.
 #include "gemm.h"
+#include "gemm2.h"
 #include "kernels.h"
 
 namespace mosa {
@@ -74,10 +75,45 @@ struct QkvPolicy {
             if (m >= a.M) continue;
             const int b = m / a.n, i = m % a.n;
             float x[8];
-#pragma unroll
-            for (int j = 0; j < 8; ++j) x[j] = Cs[ml * ldc + c + j];
+            cs_load8(Cs, ldc, ml, c, x);
             vec8_store<ST>(a.out + (((size_t)b * a.H + h) * a.n + i) * NT + c, vec8_from_f32<ST>(x));
         }
+    }
+};
+
+// bf16 storage: the multi-stage engine with direct-to-LDS loads (gemm2.h).
+// A: gathered token rows (k-contiguous, clamped to the last row past M);
+// B: the three weights as one m-contiguous [d][3 DH] operand.
+template <int DH>
+struct QkvPolicy2 {
+    using ST = uint16_t;
+    static constexpr int MT = 64, NT = 3 * DH, KC = DH == 64 ? 32 : 64, WM = 2, WN = 2, STAGES = 4;
+    static constexpr size_t EPI_LDS = 0;
+    static constexpr bool A_KCONTIG = true, B_KCONTIG = false;
+    using Args = typename QkvPolicy<ST, DH>::Args;
+    struct ARef {
+        const ST* p;
+    };
+    __device__ static void tile(const Args& a, int logical, int& batch, int& m0, int& n0) {
+        QkvPolicy<ST, DH>::tile(a, logical, batch, m0, n0);
+    }
+    __device__ static int k_size(const Args& a, int) { return a.d; }
+    __device__ static ARef a_row(const Args& a, int h, int m) {
+        m = min(m, a.M - 1);
+        const int b = m / a.n, i = m % a.n;
+        const int t = a.I ? a.I[((size_t)b * a.H + h) * a.n + i] : i;
+        return {a.X + ((size_t)b * a.T + t) * a.d};
+    }
+    __device__ static const ST* a_elem(const Args&, int, const ARef& r, int k) { return r.p + k; }
+    __device__ static size_t b_kstride(const Args&, int) { return DH; }
+    // B[k][n] = W^{n / DH}_h[k][n % DH]
+    __device__ static const ST* b_maddr(const Args& a, int h, int k, int n8) {
+        const ST* W = n8 < DH ? a.W0 : (n8 < 2 * DH ? a.W1 : a.W2);
+        return W + ((size_t)h * a.d + k) * DH + (n8 % DH);
+    }
+    __device__ static void epilogue(const Args& a, int h, int m0, int n0, const float* Cs, int ldc, int tid,
+                                    unsigned char* extra) {
+        QkvPolicy<ST, DH>::epilogue(a, h, m0, n0, Cs, ldc, tid, extra);
     }
 };
 
@@ -86,6 +122,9 @@ int run(const ST* X, const int32_t* I, const ST* Wq, const ST* Wk, const ST* Wv,
         ST* out, hipStream_t stream) {
     using P = QkvPolicy<ST, DH>;
     typename P::Args a{X, I, Wq, Wk, Wv, out, T, d, H, n, B * n, (B * n + P::MT - 1) / P::MT};
+    if constexpr (sizeof(ST) == 2) {
+        if (d % QkvPolicy2<DH>::KC == 0) return launch_gemm2<QkvPolicy2<DH>>(a, a.mtiles * H, stream);
+    }
     return launch_gemm<ST, P>(a, a.mtiles * H, stream);
 }
 
