@@ -17,6 +17,7 @@
 // (dz, 0, ..., 0) so the weight-gradient GEMM can treat W^r as a 16-column
 // block of its B operand.
 #include "gemm.h"
+#include "gemm2.h"
 #include "kernels.h"
 
 namespace mosa {
@@ -122,12 +123,42 @@ struct BwdOutPolicy {
     }
 };
 
+// bf16 storage: the multi-stage engine (gemm2.h); both operands k-contiguous,
+// the gathered dY rows clamped to the last row past M.
+template <int DH>
+struct BwdOutPolicy2 {
+    using ST = uint16_t;
+    using P1 = BwdOutPolicy<ST, DH>;
+    static constexpr int MT = 64, NT = DH, KC = 64, WM = 4, WN = 1, STAGES = 4;
+    static constexpr size_t EPI_LDS = 0;
+    static constexpr bool A_KCONTIG = true, B_KCONTIG = true;
+    using Args = typename P1::Args;
+    using ARef = typename P1::ARef;
+    using BRef = typename P1::BRef;
+    __device__ static void tile(const Args& a, int logical, int& h, int& m0, int& n0) { P1::tile(a, logical, h, m0, n0); }
+    __device__ static int k_size(const Args& a, int) { return a.d; }
+    __device__ static ARef a_row(const Args& a, int h, int m) {
+        float unused;
+        return P1::a_row(a, h, min(m, a.M - 1), unused);
+    }
+    __device__ static const ST* a_elem(const Args&, int, const ARef& r, int k) { return r.p + k; }
+    __device__ static BRef b_row(const Args& a, int h, int n) { return {a.Wo + ((size_t)h * DH + n) * a.d}; }
+    __device__ static const ST* b_elem(const Args&, int, const BRef& r, int k) { return r.p + k; }
+    __device__ static void epilogue(const Args& a, int h, int m0, int n0, const float* Cs, int ldc, int tid,
+                                    unsigned char* extra) {
+        P1::epilogue(a, h, m0, n0, Cs, ldc, tid, extra);
+    }
+};
+
 template <typename ST, int DH>
 int run(const ST* dY, const int32_t* I, const float* r, const ST* Wo, const ST* A, int B, int T, int d, int H, int n,
         ST* dA, float* D, float* dz, ST* dz16, hipStream_t stream) {
     using P = BwdOutPolicy<ST, DH>;
     const int M = B * n;
     typename P::Args a{dY, I, r, Wo, A, dA, D, dz, dz16, T, d, H, n, M, (M + P::MT - 1) / P::MT};
+    if constexpr (sizeof(ST) == 2) {
+        if (d % BwdOutPolicy2<DH>::KC == 0) return launch_gemm2<BwdOutPolicy2<DH>>(a, H * a.mtiles, stream);
+    }
     return launch_gemm<ST, P>(a, H * a.mtiles, stream);
 }
 

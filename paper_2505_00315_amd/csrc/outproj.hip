@@ -18,6 +18,7 @@
 #include "combine.h"
 #include "gemm.h"
 #include "kernels.h"
+#include "rowgemm.h"
 
 namespace mosa {
 
@@ -139,10 +140,54 @@ struct OutCombinePolicy {
     }
 };
 
+// bf16 storage, d a multiple of the column block: the row-streaming kernel (rowgemm.h),
+// W^O_h[:, n0:n0+256] held in registers, the r-scaled rows streamed.
+template <int DH>
+struct OutProjRowPolicy {
+    using ST = uint16_t;
+    static constexpr int K = DH, NPAIR = 2, STAGES = 4;
+    static constexpr bool W_KCONTIG = false, ROW_SCALAR = false;
+    struct Args {
+        const ST* A;   // [B, H, k, DH], rows scaled by r
+        const ST* Wo;  // [H, DH, d]
+        ST* Xo;        // [B, H, k, d]
+        int d, H, k, M, ntiles, tiles, per, splits, out_bytes;
+    };
+    __device__ static void tile(const Args& a, int logical, int& h, int& n0, int& s_beg, int& s_end) {
+        const int unit = logical / a.splits, sp = logical % a.splits;
+        h = unit / a.ntiles;
+        n0 = (unit % a.ntiles) * (128 * NPAIR);
+        s_beg = sp * a.per;
+        s_end = min(a.tiles, s_beg + a.per);
+    }
+    __device__ static int rows(const Args& a) { return a.M; }
+    __device__ static size_t ridx(const Args& a, int h, int m) {
+        return ((size_t)(m / a.k) * a.H + h) * a.k + (m % a.k);
+    }
+    __device__ static const ST* a_row(const Args& a, int h, int m) { return a.A + ridx(a, h, m) * DH; }
+    __device__ static const ST* w_mptr(const Args& a, int h, int k, int n) { return a.Wo + ((size_t)h * DH + k) * a.d + n; }
+    __device__ static void col_init(const Args&, int, int, float (&)[8]) {}
+    __device__ static __amdgpu_buffer_rsrc_t out_rsrc(const Args& a, int) {
+        return __builtin_amdgcn_make_buffer_rsrc(a.Xo, 0, a.out_bytes, 0x00020000);
+    }
+    __device__ static int out_row(const Args& a, int h, int m) { return (int)(ridx(a, h, m) * a.d * 2); }
+    __device__ static void finish(float (&)[8], float, const float (&)[8]) {}
+};
+
 template <typename ST, int DH>
 int run_proj(const ST* A, const ST* Wo, int B, int d, int H, int k, ST* Xo, hipStream_t stream) {
     using P = OutProjPolicy<ST, DH>;
     const int M = B * k;
+    if constexpr (sizeof(ST) == 2) {
+        const long long out_bytes = (long long)M * H * d * 2;
+        using R = OutProjRowPolicy<DH>;
+        if (d % (128 * R::NPAIR) == 0 && out_bytes < (1ll << 31)) {
+            const int ntiles = d / (128 * R::NPAIR), tiles = (M + 63) / 64;
+            const int per = rowgemm_tiles_per_wg(H * ntiles, tiles, 512), splits = (tiles + per - 1) / per;
+            typename R::Args ra{A, Wo, Xo, d, H, k, M, ntiles, tiles, per, splits, (int)out_bytes};
+            return launch_rowgemm<R>(ra, H * ntiles * splits, stream);
+        }
+    }
     typename P::Args a{A, Wo, Xo, d, H, k, M, (M + P::MT - 1) / P::MT, (d + P::NT - 1) / P::NT};
     return launch_gemm<ST, P>(a, H * a.mtiles * a.ntiles, stream);
 }
