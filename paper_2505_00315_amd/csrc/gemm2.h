@@ -31,6 +31,21 @@
 //                 a_kstride(args, batch) / b_kstride(args, batch), the element
 //                 distance between consecutive k (addresses move linearly in k);
 //   epilogue(args, batch, m0, n0, Cs, ldc, tid, extra) as in gemm.h.
+//
+// Optional (all off by default):
+//   KGATHER: the rows along k are gathered (both operands m-contiguous).  The
+//     workgroup first fills an LDS table with k_row(args, batch, k, K) -> int2
+//     for every k of its range (K need not be a multiple of KC; the table
+//     covers the padded range), and a lane's address for row k is
+//     base + tab[k].{x|y} * stride with base and stride from
+//     a_mlane(args, batch, m8, base, stride) (A_TAB picks x or y; likewise
+//     b_mlane / B_TAB).  A negative table entry reads zeros.
+//   A_INTERLEAVE: an m-contiguous A operand whose 16-row MFMA blocks are taken
+//     in pairs with interleaved columns (block 2p row i is M index
+//     32 p + 8 (i / 4) + i % 4, block 2p + 1 row i is 32 p + 8 (i / 4) + 4 + i % 4),
+//     so that a lane's accumulators of a block pair are 8 consecutive M.
+//   EPI_REGS (needs A_INTERLEAVE): no C tile; the engine calls
+//     store8(args, batch, m, n, x[8]) for M indices m .. m + 7 at column n.
 #pragma once
 
 #include "gemm.h"
@@ -79,6 +94,17 @@ __device__ __forceinline__ int mswz(int k, int u) {
     else return u;
 }
 
+template <class P, class = void> struct G2Gather : std::false_type {};
+template <class P> struct G2Gather<P, std::void_t<decltype(P::KGATHER)>> : std::bool_constant<P::KGATHER> {};
+template <class P, class = void> struct G2Interleave : std::false_type {};
+template <class P>
+struct G2Interleave<P, std::void_t<decltype(P::A_INTERLEAVE)>> : std::bool_constant<P::A_INTERLEAVE> {};
+template <class P, class = void> struct G2EpiRegs : std::false_type {};
+template <class P> struct G2EpiRegs<P, std::void_t<decltype(P::EPI_REGS)>> : std::bool_constant<P::EPI_REGS> {};
+
+// Zeros for the rows past the end of a gathered range.
+static __device__ __attribute__((aligned(16))) const uint16_t g2_zero[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+
 template <class P>
 struct Gemm2Shape {
     static constexpr int MT = P::MT, NT = P::NT, KC = P::KC, WM = P::WM, WN = P::WN, STAGES = P::STAGES;
@@ -92,10 +118,16 @@ struct Gemm2Shape {
     static_assert(WM * WN == 4 && WTM % 16 == 0 && WTN % 16 == 0 && KC % 32 == 0, "tile shape");
     static_assert(A_UNITS % 256 == 0 && B_UNITS % 256 == 0, "whole instructions per wave");
     static_assert((STAGES - 2) * (IA + IB) <= 63, "vmcnt range");
-    static constexpr size_t ctile_bytes = (size_t)MT * (NT + 4) * sizeof(float);
-    static constexpr size_t lds_bytes() {
-        const size_t ops = (size_t)STAGES * STAGE_BYTES;
-        const size_t epi = ctile_bytes + P::EPI_LDS;
+    static constexpr bool KG = G2Gather<P>::value, IL = G2Interleave<P>::value, ER = G2EpiRegs<P>::value;
+    static_assert(!KG || (!P::A_KCONTIG && !P::B_KCONTIG), "gathered k needs m-contiguous operands");
+    static_assert(!IL || (!P::A_KCONTIG && FM % 2 == 0), "interleaved A needs m-contiguous pairs of blocks");
+    static_assert(!ER || IL, "register epilogue needs interleaved A");
+    static constexpr size_t ctile_bytes = ER ? 0 : (size_t)MT * (NT + 4) * sizeof(float);
+    // LDS bytes; the k-row table of a gathered range (8 bytes per row of the
+    // padded range) follows the stage buffers.
+    static constexpr size_t lds_bytes(int ktab_rows = 0) {
+        const size_t ops = (size_t)STAGES * STAGE_BYTES + (KG ? (size_t)ktab_rows * 8 : 0);
+        const size_t epi = ER ? 0 : ctile_bytes + P::EPI_LDS;
         return ops > epi ? ops : epi;
     }
 };
@@ -119,13 +151,20 @@ __global__ __launch_bounds__(256) void gemm2_kernel(const typename P::Args args)
     int batch, m0, n0;
     P::tile(args, xcd_logical_id(blockIdx.x, gridDim.x), batch, m0, n0);
     const int K = P::k_size(args, batch);
-    const int nchunks = K / KC;
+    const int nchunks = S::KG ? (K + KC - 1) / KC : K / KC;
+    int2* ktab = reinterpret_cast<int2*>(smem + STG * S::STAGE_BYTES);
+    if constexpr (S::KG) {
+        for (int i = tid; i < nchunks * KC; i += 256) ktab[i] = P::k_row(args, batch, i, K);
+        __syncthreads();
+    }
 
     // Where this lane's 16 bytes of each load instruction come from for chunk
     // 0, and how far they move per chunk (KC elements along k).  Computed once
     // so that the loop does plain pointer arithmetic.
     const ST* asrc[S::IA > 0 ? S::IA : 1];
     const ST* bsrc[S::IB > 0 ? S::IB : 1];
+    size_t astr[S::IA > 0 ? S::IA : 1], bstr[S::IB > 0 ? S::IB : 1];  // gathered: element stride per table unit
+    int akr[S::IA > 0 ? S::IA : 1], bkr[S::IB > 0 ? S::IB : 1];         // gathered: k row within the chunk
 #pragma unroll
     for (int j = 0; j < S::IA; ++j) {
         const int p = 64 * (wave + 4 * j) + lane;  // unit of the tile
@@ -135,7 +174,12 @@ __global__ __launch_bounds__(256) void gemm2_kernel(const typename P::Args args)
         } else {
             constexpr int U = MT / 8;
             const int kr = p / U, pos = p % U;
-            asrc[j] = P::a_maddr(args, batch, kr, m0 + 8 * mswz<U>(kr, pos));
+            if constexpr (S::KG) {
+                P::a_mlane(args, batch, m0 + 8 * mswz<U>(kr, pos), asrc[j], astr[j]);
+                akr[j] = kr;
+            } else {
+                asrc[j] = P::a_maddr(args, batch, kr, m0 + 8 * mswz<U>(kr, pos));
+            }
         }
     }
 #pragma unroll
@@ -147,12 +191,17 @@ __global__ __launch_bounds__(256) void gemm2_kernel(const typename P::Args args)
         } else {
             constexpr int U = NT / 8;
             const int kr = p / U, pos = p % U;
-            bsrc[j] = P::b_maddr(args, batch, kr, n0 + 8 * mswz<U>(kr, pos));
+            if constexpr (S::KG) {
+                P::b_mlane(args, batch, n0 + 8 * mswz<U>(kr, pos), bsrc[j], bstr[j]);
+                bkr[j] = kr;
+            } else {
+                bsrc[j] = P::b_maddr(args, batch, kr, n0 + 8 * mswz<U>(kr, pos));
+            }
         }
     }
     size_t astep = KC, bstep = KC;
-    if constexpr (!P::A_KCONTIG) astep *= P::a_kstride(args, batch);
-    if constexpr (!P::B_KCONTIG) bstep *= P::b_kstride(args, batch);
+    if constexpr (!P::A_KCONTIG && !S::KG) astep *= P::a_kstride(args, batch);
+    if constexpr (!P::B_KCONTIG && !S::KG) bstep *= P::b_kstride(args, batch);
 
     // LDS address of this wave's first 1 KB block of a stage (scalar).
     const uint32_t lds_wave = __builtin_amdgcn_readfirstlane(lds_addr(smem) + 1024 * wave);
@@ -161,11 +210,23 @@ __global__ __launch_bounds__(256) void gemm2_kernel(const typename P::Args args)
     // load valid, clamped addresses into a buffer nobody reads).
     auto issue_buf = [&](int c, int bidx) {
         const uint32_t buf = lds_wave + bidx * S::STAGE_BYTES;
-        const size_t kc = (size_t)min(c, nchunks - 1);
+        const int cc = min(c, nchunks - 1);
+        const size_t kc = (size_t)cc;
+        auto gathered = [&](const ST* base, size_t stride, int kr, int which) {
+            const int2 e = ktab[cc * KC + kr];
+            const int rv = which ? e.y : e.x;
+            return rv >= 0 ? base + (size_t)rv * stride : g2_zero;
+        };
 #pragma unroll
-        for (int j = 0; j < S::IA; ++j) lds_load16(asrc[j] + kc * astep, buf + 4096 * j);
+        for (int j = 0; j < S::IA; ++j) {
+            if constexpr (S::KG) lds_load16(gathered(asrc[j], astr[j], akr[j], P::A_TAB), buf + 4096 * j);
+            else lds_load16(asrc[j] + kc * astep, buf + 4096 * j);
+        }
 #pragma unroll
-        for (int j = 0; j < S::IB; ++j) lds_load16(bsrc[j] + kc * bstep, buf + S::A_BYTES + 4096 * j);
+        for (int j = 0; j < S::IB; ++j) {
+            if constexpr (S::KG) lds_load16(gathered(bsrc[j], bstr[j], bkr[j], P::B_TAB), buf + S::A_BYTES + 4096 * j);
+            else lds_load16(bsrc[j] + kc * bstep, buf + S::A_BYTES + 4096 * j);
+        }
     };
 
     const int wm = wave / S::WN, wn = wave % S::WN;
@@ -184,9 +245,10 @@ __global__ __launch_bounds__(256) void gemm2_kernel(const typename P::Args args)
         return f;
     };
     // m-contiguous fragment: two transposed reads, raw (see lds_read_tr16)
-    auto frag_m = [&](const unsigned char* t, int mbase, int ks, auto u_tag) {
+    // (colstep 8 and odd: the interleaved pairs of A_INTERLEAVE)
+    auto frag_m = [&](const unsigned char* t, int mbase, int ks, auto u_tag, int colstep = 4, int odd = 0) {
         constexpr int U = decltype(u_tag)::value;
-        const int mcol = mbase + 4 * (c16 & 3);
+        const int mcol = mbase + colstep * (c16 & 3) + 4 * odd;
         const int u = mcol >> 3, half = (mcol >> 2) & 1;
         const int k0r = ks + 8 * g + (c16 >> 2);
         const u32x2 lo = lds_read_tr16(t + (k0r * U + mswz<U>(k0r, u)) * 16 + 8 * half);
@@ -204,6 +266,8 @@ __global__ __launch_bounds__(256) void gemm2_kernel(const typename P::Args args)
 #pragma unroll
             for (int i = 0; i < S::FM; ++i) {
                 if constexpr (P::A_KCONTIG) fa[i] = frag_k(ta, wm * S::WTM + i * 16 + c16, ks);
+                else if constexpr (S::IL)
+                    ma[i] = frag_m(ta, wm * S::WTM + 32 * (i >> 1), ks, std::integral_constant<int, MT / 8>{}, 8, i & 1);
                 else ma[i] = frag_m(ta, wm * S::WTM + i * 16, ks, std::integral_constant<int, MT / 8>{});
             }
 #pragma unroll
@@ -264,34 +328,52 @@ __global__ __launch_bounds__(256) void gemm2_kernel(const typename P::Args args)
     }
 pipeline_done:
     wait_vmcnt<0>();  // the trailing loads write into the buffers the C tile reuses
-    __syncthreads();
+    if constexpr (S::ER) {
+        // lane: M indices 32 p + 8 g .. + 7 of the wave's rows, column c16 of block j
+#pragma unroll
+        for (int p = 0; p < S::FM / 2; ++p)
+#pragma unroll
+            for (int j = 0; j < S::FN; ++j) {
+                float x[8];
+#pragma unroll
+                for (int r = 0; r < 4; ++r) {
+                    x[r] = acc[2 * p][j][r];
+                    x[4 + r] = acc[2 * p + 1][j][r];
+                }
+                P::store8(args, batch, m0 + wm * S::WTM + 32 * p + 8 * g, n0 + wn * S::WTN + 16 * j + c16, x);
+            }
+    } else {
+        __syncthreads();
 
-    // C tile to LDS: Cs[m][n], row stride NT + 4 floats
-    float* Cs = reinterpret_cast<float*>(smem);
-    constexpr int LDC = NT + 4;
+        // C tile to LDS: Cs[m][n], row stride NT + 4 floats
+        float* Cs = reinterpret_cast<float*>(smem);
+        constexpr int LDC = NT + 4;
 #pragma unroll
-    for (int i = 0; i < S::FM; ++i)
+        for (int i = 0; i < S::FM; ++i)
 #pragma unroll
-        for (int j = 0; j < S::FN; ++j)
+            for (int j = 0; j < S::FN; ++j)
 #pragma unroll
-            for (int r = 0; r < 4; ++r)
-                Cs[(wm * S::WTM + i * 16 + 4 * g + r) * LDC + wn * S::WTN + j * 16 + c16] = acc[i][j][r];
-    __syncthreads();
-    P::epilogue(args, batch, m0, n0, Cs, LDC, tid, smem + S::ctile_bytes);
+                for (int r = 0; r < 4; ++r)
+                    Cs[(wm * S::WTM + i * 16 + 4 * g + r) * LDC + wn * S::WTN + j * 16 + c16] = acc[i][j][r];
+        __syncthreads();
+        P::epilogue(args, batch, m0, n0, Cs, LDC, tid, smem + S::ctile_bytes);
+    }
 }
 
+// ktab_rows: rows of the k-row table (gathered k: the padded k range).
 template <class P>
-int launch_gemm2(const typename P::Args& args, int nblocks, hipStream_t stream) {
+int launch_gemm2(const typename P::Args& args, int nblocks, hipStream_t stream, int ktab_rows = 0) {
     if (nblocks <= 0) return 0;
-    constexpr size_t lds = Gemm2Shape<P>::lds_bytes();
+    const size_t lds = Gemm2Shape<P>::lds_bytes(ktab_rows);
+    if (lds > 160 * 1024) return -1;
     auto kern = gemm2_kernel<P>;
     if (lds > 64 * 1024) {
-        static bool set = false;
-        if (!set) {
+        static size_t set = 0;
+        if (lds > set) {
             if (hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds) !=
                 hipSuccess)
                 return -1;
-            set = true;
+            set = lds;
         }
     }
     hipLaunchKernelGGL(kern, dim3(nblocks), dim3(256), lds, stream, args);

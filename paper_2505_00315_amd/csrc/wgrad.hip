@@ -18,6 +18,7 @@
 #include <algorithm>
 
 #include "gemm.h"
+#include "gemm2.h"
 #include "kernels.h"
 
 namespace mosa {
@@ -241,6 +242,110 @@ __global__ __launch_bounds__(256) void wgrad_o_reduce_kernel(const float* __rest
     vec8_store<ST>(dWo + idx * 8, vec8_from_f32<ST>(x));
 }
 
+// bf16 storage, MoSA heads: the multi-stage engine (gemm2.h) with the rows
+// gathered through an LDS table, k = r in order over the whole range (no
+// split: one workgroup owns its output tile, so the sums are reproducible
+// without partials).  Table entry of row r = (b, i): x = b T + I_r (the
+// token row of X or dY), y = (b H + h) n + i (the selected-row index), y = -1
+// past the last row (that operand then reads zeros).  The MFMA's A operand
+// is the one whose output index is contiguous in memory, interleaved so the
+// accumulators go straight to 16-byte stores.
+__device__ __forceinline__ int2 wgrad_k_row(const int32_t* I, const FastDiv& nd, int T, int H, int n, int h, int k,
+                                            int K) {
+    int b, i;
+    fast_divmod(nd, min(k, K - 1), b, i);
+    const int ri = (b * H + h) * n + i;
+    return make_int2(b * T + I[ri], k < K ? ri : -1);
+}
+
+// dW^{Q,K,V}_h and dW^r_h: M = the 3 dh + 64 output columns [dQ | dK | dV |
+// dz, 0 ...] (dz16 holds dz and 15 zeros; the rest reads the zero row),
+// N = 64 rows c of d per workgroup.
+template <int DH>
+struct WgradQkvPolicy2 {
+    using ST = uint16_t;
+    static constexpr int MT = DH == 64 ? 256 : 128, NT = 64, KC = 32, WM = 2, WN = 2, STAGES = 3;
+    static constexpr size_t EPI_LDS = 0;
+    static constexpr bool A_KCONTIG = false, B_KCONTIG = false, KGATHER = true, A_INTERLEAVE = true, EPI_REGS = true;
+    static constexpr int A_TAB = 1, B_TAB = 0;
+    using Args = typename WgradQkvPolicy<ST, DH, true, true>::Args;
+    __device__ static void tile(const Args& a, int logical, int& h, int& m0, int& n0) {
+        h = logical / a.mtiles;
+        m0 = 0;
+        n0 = (logical % a.mtiles) * NT;
+    }
+    __device__ static int k_size(const Args& a, int) { return a.R; }
+    __device__ static int2 k_row(const Args& a, int h, int k, int K) {
+        return wgrad_k_row(a.I, a.nd, a.T, a.H, a.n, h, k, K);
+    }
+    __device__ static void a_mlane(const Args& a, int, int m8, const ST*& base, size_t& stride) {
+        if (m8 < 3 * DH) {
+            base = a.dQKV + m8;
+            stride = 3 * DH;
+        } else if (m8 < 3 * DH + 16) {
+            base = a.dz16 + (m8 - 3 * DH);
+            stride = 16;
+        } else {
+            base = g2_zero;
+            stride = 0;
+        }
+    }
+    __device__ static void b_mlane(const Args& a, int, int n8, const ST*& base, size_t& stride) {
+        base = a.X + n8;
+        stride = a.d;
+    }
+    // columns m .. m + 7 of row c = n
+    __device__ static void store8(const Args& a, int h, int m, int n, const float (&x)[8]) {
+        if (m < 3 * DH) {
+            ST* W = m < DH ? a.dWq : (m < 2 * DH ? a.dWk : a.dWv);
+            vec8_store<ST>(W + ((size_t)h * a.d + n) * DH + (m % DH), vec8_from_f32<ST>(x));
+        } else if (m == 3 * DH) {
+            st1<ST>(a.dWr + (size_t)h * a.d + n, x[0]);
+        }
+    }
+};
+
+// dW^O_h: M = 64 columns c of d per workgroup (dY rows), N = dh (the scaled
+// attention rows).
+template <int DH>
+struct WgradOPolicy2 {
+    using ST = uint16_t;
+    static constexpr int MT = 64, NT = DH, KC = 64, WM = 2, WN = 2, STAGES = 4;
+    static constexpr size_t EPI_LDS = 0;
+    static constexpr bool A_KCONTIG = false, B_KCONTIG = false, KGATHER = true, A_INTERLEAVE = true, EPI_REGS = true;
+    static constexpr int A_TAB = 0, B_TAB = 1;
+    using Args = typename WgradOPolicy<ST, DH, true>::Args;
+    __device__ static void tile(const Args& a, int logical, int& h, int& m0, int& n0) {
+        h = logical / a.ntiles;
+        m0 = (logical % a.ntiles) * MT;
+        n0 = 0;
+    }
+    __device__ static int k_size(const Args& a, int) { return a.R; }
+    __device__ static int2 k_row(const Args& a, int h, int k, int K) {
+        return wgrad_k_row(a.I, a.nd, a.T, a.H, a.n, h, k, K);
+    }
+    __device__ static void a_mlane(const Args& a, int, int m8, const ST*& base, size_t& stride) {
+        base = a.dY + m8;
+        stride = a.d;
+    }
+    __device__ static void b_mlane(const Args& a, int, int n8, const ST*& base, size_t& stride) {
+        base = a.A + n8;
+        stride = DH;
+    }
+    // columns c = m .. m + 7 of row e = n
+    __device__ static void store8(const Args& a, int h, int m, int n, const float (&x)[8]) {
+        vec8_store<ST>(a.dWo + ((size_t)h * DH + n) * a.d + m, vec8_from_f32<ST>(x));
+    }
+};
+
+// Rows of the k-row table for a gathered range of R rows (0: not usable).
+template <class P2>
+int wgrad2_table_rows(int R, int d) {
+    const int rows = (R + P2::KC - 1) / P2::KC * P2::KC;
+    if (R <= 0 || rows > 4096 || d % 64 != 0) return 0;
+    return rows;
+}
+
 // Split of the row range: enough workgroups to fill the chip (about 512),
 // at least 4 chunks per split.
 int choose_splits(int base_tiles, int nchunks, int& cps) {
@@ -256,6 +361,13 @@ int run_qkv_t(const ST* X, const int32_t* I, const ST* dQKV, const ST* dz16, int
               ST* dWq, ST* dWk, ST* dWv, ST* dWr, float* part, hipStream_t stream) {
     using P = WgradQkvPolicy<ST, DH, ROUTER, GATHER>;
     const int mtiles = (d + P::MT - 1) / P::MT, R = B * n;
+    if constexpr (sizeof(ST) == 2 && ROUTER && GATHER) {
+        using P2 = WgradQkvPolicy2<DH>;
+        if (const int rows = wgrad2_table_rows<P2>(R, d)) {
+            typename P::Args a{X, I, dQKV, dz16, dWq, dWk, dWv, dWr, part, T, d, H, n, R, d / 64, 1, 0, make_fastdiv(n)};
+            return launch_gemm2<P2>(a, H * (d / 64), stream, rows);
+        }
+    }
     int cps;
     const int S = choose_splits(H * mtiles, (R + P::KC - 1) / P::KC, cps);
     typename P::Args a{X, I, dQKV, dz16, dWq, dWk, dWv, dWr, part, T, d, H, n, R, mtiles, S, cps, make_fastdiv(n)};
@@ -282,6 +394,13 @@ int run_o_t(const ST* dY, const int32_t* I, const ST* A, int B, int T, int d, in
             hipStream_t stream) {
     using P = WgradOPolicy<ST, DH, GATHER>;
     const int ntiles = (d + P::NT - 1) / P::NT, R = B * n;
+    if constexpr (sizeof(ST) == 2 && GATHER) {
+        using P2 = WgradOPolicy2<DH>;
+        if (const int rows = wgrad2_table_rows<P2>(R, d)) {
+            typename P::Args a{dY, I, A, dWo, part, T, d, H, n, R, d / 64, 1, 0, make_fastdiv(n)};
+            return launch_gemm2<P2>(a, H * (d / 64), stream, rows);
+        }
+    }
     int cps;
     const int S = choose_splits(H * ntiles, (R + P::KC - 1) / P::KC, cps);
     typename P::Args a{dY, I, A, dWo, part, T, d, H, n, R, ntiles, S, cps, make_fastdiv(n)};
@@ -308,6 +427,10 @@ size_t partial_bytes(int B, int d, int H, int n, bool router) {
     using PQ = WgradQkvPolicy<ST, DH, true, true>;
     using PO = WgradOPolicy<ST, DH, true>;
     const int R = B * n;
+    if constexpr (sizeof(ST) == 2) {  // MoSA heads on the gathered-row engine: no partials
+        if (router && wgrad2_table_rows<WgradQkvPolicy2<DH>>(R, d) && wgrad2_table_rows<WgradOPolicy2<DH>>(R, d))
+            return 0;
+    }
     int cps;
     const int mtiles = (d + PQ::MT - 1) / PQ::MT, ntiles = (d + PO::NT - 1) / PO::NT;
     const int sq = choose_splits(H * mtiles, (R + PQ::KC - 1) / PQ::KC, cps);
