@@ -160,4 +160,140 @@ __device__ __forceinline__ void combine_tile(const float* Cs, int ldc, int tid, 
     }
 }
 
+// The same combination without dense heads, as a kernel of its own: out[b, t]
+// (+)= sum over MoSA heads h (ascending) of rows[b, h, slot[b, h, t]].  A
+// workgroup takes 16 tokens of one batch element and stages their slot
+// entries for every head in LDS (head-major, padded rows); each wave then
+// handles 4 tokens, one at a time, with the whole d-wide row spread over its
+// lanes (8 consecutive columns per lane and 64-lane group, so every hit is
+// one coalesced d-element load).  The hits of a token are taken 4 at a time
+// in ascending head order (the lanes of a 64-head group ballot their slot
+// entries); the sum starts from 0 and is added to the old output value at
+// the end when accumulating, so every element is produced by one lane in a
+// fixed order.
+constexpr int kCombineTokens = 16;
+constexpr int kCombineLdt = kCombineTokens + 2;  // padded LDS row (int16) per head
+
+template <typename ST, int CH>  // CH: 8-column groups per lane (d <= 512 CH)
+__global__ __launch_bounds__(256) void combine_rows_kernel(const int16_t* __restrict__ slot,
+                                                           const ST* __restrict__ rows, ST* __restrict__ out, int T,
+                                                           int d, int H, int k, int accumulate, int tiles_per_b) {
+    extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
+    int16_t* s_slot = reinterpret_cast<int16_t*>(smem);  // [H][kCombineLdt]
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int logical = xcd_logical_id(blockIdx.x, gridDim.x);
+    const int b = logical / tiles_per_b, t0 = (logical % tiles_per_b) * kCombineTokens;
+
+    if ((T & 7) == 0) {
+        for (int e = tid; e < H * 2; e += 256) {
+            const int h = e >> 1, q = e & 1, tt = t0 + 8 * q;
+            uint4 v = make_uint4(0xffffffffu, 0xffffffffu, 0xffffffffu, 0xffffffffu);
+            if (tt < T) v = *reinterpret_cast<const uint4*>(slot + ((size_t)b * H + h) * T + tt);
+            uint32_t* dst = reinterpret_cast<uint32_t*>(s_slot + h * kCombineLdt + 8 * q);
+            dst[0] = v.x;
+            dst[1] = v.y;
+            dst[2] = v.z;
+            dst[3] = v.w;
+        }
+    } else {
+        for (int e = tid; e < H * kCombineTokens; e += 256) {
+            const int h = e / kCombineTokens, tl = e % kCombineTokens, tt = t0 + tl;
+            s_slot[h * kCombineLdt + tl] = tt < T ? slot[((size_t)b * H + h) * T + tt] : (int16_t)-1;
+        }
+    }
+    __syncthreads();
+
+    const ST* rb = rows + (size_t)b * H * k * d;
+    for (int tl = 4 * wave; tl < 4 * wave + 4; ++tl) {
+        const int t = t0 + tl;
+        if (t >= T) break;
+        float acc[CH][8];
+#pragma unroll
+        for (int c = 0; c < CH; ++c)
+#pragma unroll
+            for (int e = 0; e < 8; ++e) acc[c][e] = 0.f;
+        for (int hc = 0; hc < H; hc += 64) {
+            const int h = hc + lane;
+            const int sl = h < H ? s_slot[h * kCombineLdt + tl] : -1;
+            uint64_t mask = __ballot(sl >= 0);
+            while (mask) {
+                int hh[4], ss[4], n = 0;
+#pragma unroll
+                for (int j = 0; j < 4; ++j) {
+                    if (mask) {
+                        const int bit = __builtin_ctzll(mask);
+                        mask &= mask - 1;
+                        hh[j] = hc + bit;
+                        ss[j] = __builtin_amdgcn_readlane(sl, bit);
+                        n = j + 1;
+                    } else {  // reload the first hit; not added
+                        hh[j] = hh[0];
+                        ss[j] = ss[0];
+                    }
+                }
+                Vec8<ST> v[4][CH];
+#pragma unroll
+                for (int j = 0; j < 4; ++j) {
+                    const ST* p = rb + ((size_t)hh[j] * k + ss[j]) * d;
+#pragma unroll
+                    for (int c = 0; c < CH; ++c) {
+                        const int col = 8 * (lane + 64 * c);
+                        v[j][c] = col < d ? vec8_load<ST>(p + col) : vec8_zero<ST>();
+                    }
+                }
+#pragma unroll
+                for (int j = 0; j < 4; ++j) {
+                    if (j < n) {
+#pragma unroll
+                        for (int c = 0; c < CH; ++c) {
+                            float x[8];
+                            vec8_to_f32<ST>(v[j][c], x);
+#pragma unroll
+                            for (int e = 0; e < 8; ++e) acc[c][e] += x[e];
+                        }
+                    }
+                }
+            }
+        }
+        ST* y = out + ((size_t)b * T + t) * d;
+#pragma unroll
+        for (int c = 0; c < CH; ++c) {
+            const int col = 8 * (lane + 64 * c);
+            if (col >= d) continue;
+            float x[8];
+            if (accumulate) {
+                vec8_to_f32<ST>(vec8_load<ST>(y + col), x);
+#pragma unroll
+                for (int e = 0; e < 8; ++e) x[e] += acc[c][e];
+            } else {
+#pragma unroll
+                for (int e = 0; e < 8; ++e) x[e] = acc[c][e];
+            }
+            vec8_store<ST>(y + col, vec8_from_f32<ST>(x));
+        }
+    }
+}
+
+// out (+)= head-ordered sum of the MoSA rows (no dense heads); d a multiple of 8.
+template <typename ST>
+int launch_combine_rows(const int16_t* slot, const ST* rows, ST* out, int B, int T, int d, int H, int k,
+                        int accumulate, hipStream_t stream) {
+    if (B == 0 || T == 0) return 0;
+    if (d % 8 != 0 || d > 2048) return -1;
+    const int tiles = (T + kCombineTokens - 1) / kCombineTokens;
+    const size_t lds = (size_t)(H > 0 ? H : 1) * kCombineLdt * sizeof(int16_t);
+    if (lds > 64 * 1024) return -1;
+    const dim3 grid(B * tiles), block(256);
+    if (d <= 512)
+        hipLaunchKernelGGL((combine_rows_kernel<ST, 1>), grid, block, lds, stream, slot, rows, out, T, d, H, k,
+                           accumulate, tiles);
+    else if (d <= 1024)
+        hipLaunchKernelGGL((combine_rows_kernel<ST, 2>), grid, block, lds, stream, slot, rows, out, T, d, H, k,
+                           accumulate, tiles);
+    else
+        hipLaunchKernelGGL((combine_rows_kernel<ST, 4>), grid, block, lds, stream, slot, rows, out, T, d, H, k,
+                           accumulate, tiles);
+    return hipGetLastError() == hipSuccess ? 0 : -1;
+}
+
 }  // namespace mosa
