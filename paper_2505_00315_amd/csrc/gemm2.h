@@ -44,6 +44,7 @@
 //     in pairs with interleaved columns (block 2p row i is M index
 //     32 p + 8 (i / 4) + i % 4, block 2p + 1 row i is 32 p + 8 (i / 4) + 4 + i % 4),
 //     so that a lane's accumulators of a block pair are 8 consecutive M.
+//   MIN_WAVES: waves per SIMD the register allocation must allow.
 //   EPI_REGS (needs A_INTERLEAVE): no C tile; the engine calls
 //     store8(args, batch, m, n, x[8]) for M indices m .. m + 7 at column n.
 #pragma once
@@ -79,6 +80,26 @@ __device__ __forceinline__ u32x2 lds_read_tr16(const unsigned char* p) {
 }
 // Wait for every outstanding LDS read of this wave.
 __device__ __forceinline__ void lds_wait() { asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory"); }
+// Wait until at most N LDS operations of this wave are outstanding (LDS
+// operations complete in issue order).
+template <int N>
+__device__ __forceinline__ void lds_wait_n() {
+    static_assert(N >= 0 && N <= 15, "lgkmcnt range");
+    asm volatile("s_waitcnt lgkmcnt(%0)" ::"n"(N) : "memory");
+}
+// lds_wait_n<n>() for an n that is a constant after unrolling.
+template <int I = 0>
+__device__ __forceinline__ void lds_wait_le(int n) {
+    if constexpr (I < 15) {
+        if (n == I) {
+            lds_wait_n<I>();
+            return;
+        }
+        lds_wait_le<I + 1>(n);
+    } else {
+        lds_wait_n<15>();
+    }
+}
 // Make x depend on the preceding lds_wait() (an empty volatile statement that
 // claims to modify x keeps its consumers after the wait).
 __device__ __forceinline__ void lds_ready(u32x4& x) { asm volatile("" : "+v"(x)); }
@@ -99,6 +120,9 @@ template <class P> struct G2Gather<P, std::void_t<decltype(P::KGATHER)>> : std::
 template <class P, class = void> struct G2Interleave : std::false_type {};
 template <class P>
 struct G2Interleave<P, std::void_t<decltype(P::A_INTERLEAVE)>> : std::bool_constant<P::A_INTERLEAVE> {};
+template <class P, class = void> struct G2MinWaves : std::integral_constant<int, 1> {};
+template <class P>
+struct G2MinWaves<P, std::void_t<decltype(P::MIN_WAVES)>> : std::integral_constant<int, P::MIN_WAVES> {};
 template <class P, class = void> struct G2EpiRegs : std::false_type {};
 template <class P> struct G2EpiRegs<P, std::void_t<decltype(P::EPI_REGS)>> : std::bool_constant<P::EPI_REGS> {};
 
@@ -140,7 +164,7 @@ __device__ __forceinline__ void wait_vmcnt() {
 }
 
 template <class P>
-__global__ __launch_bounds__(256) void gemm2_kernel(const typename P::Args args) {
+__global__ __launch_bounds__(256, G2MinWaves<P>::value) void gemm2_kernel(const typename P::Args args) {
     using ST = uint16_t;
     using S = Gemm2Shape<P>;
     constexpr int MT = S::MT, NT = S::NT, KC = S::KC, LPR = S::LPR, STG = S::STAGES;
@@ -163,7 +187,7 @@ __global__ __launch_bounds__(256) void gemm2_kernel(const typename P::Args args)
     // so that the loop does plain pointer arithmetic.
     const ST* asrc[S::IA > 0 ? S::IA : 1];
     const ST* bsrc[S::IB > 0 ? S::IB : 1];
-    size_t astr[S::IA > 0 ? S::IA : 1], bstr[S::IB > 0 ? S::IB : 1];  // gathered: element stride per table unit
+    uint32_t astr[S::IA > 0 ? S::IA : 1], bstr[S::IB > 0 ? S::IB : 1];  // gathered: element stride per table unit
     int akr[S::IA > 0 ? S::IA : 1], bkr[S::IB > 0 ? S::IB : 1];         // gathered: k row within the chunk
 #pragma unroll
     for (int j = 0; j < S::IA; ++j) {
@@ -206,25 +230,44 @@ __global__ __launch_bounds__(256) void gemm2_kernel(const typename P::Args args)
     // LDS address of this wave's first 1 KB block of a stage (scalar).
     const uint32_t lds_wave = __builtin_amdgcn_readfirstlane(lds_addr(smem) + 1024 * wave);
 
+    // Gathered k: this lane's table entries for the next chunk to issue, read
+    // one iteration ahead so that the LDS latency stays off the issue path.
+    int arv[S::IA > 0 ? S::IA : 1], brv[S::IB > 0 ? S::IB : 1];
+    auto load_rows = [&](int c) {
+        if constexpr (S::KG) {
+            const int cc = min(c, nchunks - 1);
+#pragma unroll
+            for (int j = 0; j < S::IA; ++j) {
+                const int2 e = ktab[cc * KC + akr[j]];
+                arv[j] = P::A_TAB ? e.y : e.x;
+            }
+#pragma unroll
+            for (int j = 0; j < S::IB; ++j) {
+                const int2 e = ktab[cc * KC + bkr[j]];
+                brv[j] = P::B_TAB ? e.y : e.x;
+            }
+        }
+    };
+    // base + rv * stride, or the zero row for rv < 0 (branch-free)
+    auto gathered = [](const ST* base, uint32_t stride, int rv) {
+        const ST* p = base + (size_t)(uint32_t)max(rv, 0) * stride;
+        return rv >= 0 ? p : g2_zero;
+    };
+
     // Issue the loads of chunk c into its stage buffer (chunks past the end
-    // load valid, clamped addresses into a buffer nobody reads).
+    // load valid, clamped addresses into a buffer nobody reads).  Gathered k:
+    // the table entries of chunk c must be in arv / brv (load_rows(c)).
     auto issue_buf = [&](int c, int bidx) {
         const uint32_t buf = lds_wave + bidx * S::STAGE_BYTES;
-        const int cc = min(c, nchunks - 1);
-        const size_t kc = (size_t)cc;
-        auto gathered = [&](const ST* base, size_t stride, int kr, int which) {
-            const int2 e = ktab[cc * KC + kr];
-            const int rv = which ? e.y : e.x;
-            return rv >= 0 ? base + (size_t)rv * stride : g2_zero;
-        };
+        const size_t kc = (size_t)min(c, nchunks - 1);
 #pragma unroll
         for (int j = 0; j < S::IA; ++j) {
-            if constexpr (S::KG) lds_load16(gathered(asrc[j], astr[j], akr[j], P::A_TAB), buf + 4096 * j);
+            if constexpr (S::KG) lds_load16(gathered(asrc[j], astr[j], arv[j]), buf + 4096 * j);
             else lds_load16(asrc[j] + kc * astep, buf + 4096 * j);
         }
 #pragma unroll
         for (int j = 0; j < S::IB; ++j) {
-            if constexpr (S::KG) lds_load16(gathered(bsrc[j], bstr[j], bkr[j], P::B_TAB), buf + S::A_BYTES + 4096 * j);
+            if constexpr (S::KG) lds_load16(gathered(bsrc[j], bstr[j], brv[j]), buf + S::A_BYTES + 4096 * j);
             else lds_load16(bsrc[j] + kc * bstep, buf + S::A_BYTES + 4096 * j);
         }
     };
@@ -263,6 +306,11 @@ __global__ __launch_bounds__(256) void gemm2_kernel(const typename P::Args args)
         for (int ks = 0; ks < KC; ks += 32) {
             Frag8<ST> fa[S::FM], fb[S::FN];
             u32x4 ma[S::FM], mb[S::FN];  // raw m-contiguous fragments
+            if constexpr (!P::A_KCONTIG && !P::B_KCONTIG) {
+#pragma unroll
+                for (int j = 0; j < S::FN; ++j)
+                    mb[j] = frag_m(tb, wn * S::WTN + j * 16, ks, std::integral_constant<int, NT / 8>{});
+            }
 #pragma unroll
             for (int i = 0; i < S::FM; ++i) {
                 if constexpr (P::A_KCONTIG) fa[i] = frag_k(ta, wm * S::WTM + i * 16 + c16, ks);
@@ -273,7 +321,31 @@ __global__ __launch_bounds__(256) void gemm2_kernel(const typename P::Args args)
 #pragma unroll
             for (int j = 0; j < S::FN; ++j) {
                 if constexpr (P::B_KCONTIG) fb[j] = frag_k(tb, wn * S::WTN + j * 16 + c16, ks);
-                else mb[j] = frag_m(tb, wn * S::WTN + j * 16, ks, std::integral_constant<int, NT / 8>{});
+                else if constexpr (P::A_KCONTIG)
+                    mb[j] = frag_m(tb, wn * S::WTN + j * 16, ks, std::integral_constant<int, NT / 8>{});
+            }
+            if constexpr (!P::A_KCONTIG && !P::B_KCONTIG) {
+                // Both operands by transposed reads: B's were issued first, so
+                // after the wait for A fragment i (2 reads each) the MFMAs of
+                // that row block can start while later reads are in flight.
+                static_assert(2 * (S::FM - 1) <= 15, "lgkmcnt range");
+#pragma unroll
+                for (int i = 0; i < S::FM; ++i) {
+                    lds_wait_le(2 * (S::FM - 1 - i));
+                    if (i == 0) {
+#pragma unroll
+                        for (int j = 0; j < S::FN; ++j) {
+                            lds_ready(mb[j]);
+                            fb[j].v = __builtin_bit_cast(bf16x8, mb[j]);
+                        }
+                    }
+                    lds_ready(ma[i]);
+                    fa[i].v = __builtin_bit_cast(bf16x8, ma[i]);
+#pragma unroll
+                    for (int j = 0; j < S::FN; ++j) mma8(acc[i][j], fa[i], fb[j]);
+                    __builtin_amdgcn_sched_barrier(0);  // keep these MFMAs before the next wait
+                }
+                continue;
             }
             if constexpr (!P::A_KCONTIG || !P::B_KCONTIG) {
                 lds_wait();
@@ -309,7 +381,11 @@ __global__ __launch_bounds__(256) void gemm2_kernel(const typename P::Args args)
     // edges, where it moves the accumulators to other registers.
     if (nchunks > 0) {
 #pragma unroll
-        for (int s = 0; s < STG - 1; ++s) issue_buf(s, s);
+        for (int s = 0; s < STG - 1; ++s) {
+            load_rows(s);
+            issue_buf(s, s);
+        }
+        load_rows(STG - 1);
         for (int c0 = 0;; c0 += STG) {
 #pragma unroll
             for (int u = 0; u < STG; ++u) {
@@ -317,6 +393,7 @@ __global__ __launch_bounds__(256) void gemm2_kernel(const typename P::Args args)
                 wait_vmcnt<(STG - 2) * (S::IA + S::IB)>();
                 __syncthreads();  // chunk c is in LDS for every wave; chunk c-1's buffer is free
                 issue_buf(c + STG - 1, (u + STG - 1) % STG);
+                load_rows(c + STG);
                 __builtin_amdgcn_sched_barrier(0);
                 mfma_buf(u);
                 if (c + 1 == nchunks) {

@@ -267,7 +267,7 @@ struct WgradQkvPolicy2 {
     static constexpr int MT = DH == 64 ? 256 : 128, NT = 64, KC = 32, WM = 2, WN = 2, STAGES = 3;
     static constexpr size_t EPI_LDS = 0;
     static constexpr bool A_KCONTIG = false, B_KCONTIG = false, KGATHER = true, A_INTERLEAVE = true, EPI_REGS = true;
-    static constexpr int A_TAB = 1, B_TAB = 0;
+    static constexpr int A_TAB = 1, B_TAB = 0, MIN_WAVES = 2;
     using Args = typename WgradQkvPolicy<ST, DH, true, true>::Args;
     __device__ static void tile(const Args& a, int logical, int& h, int& m0, int& n0) {
         h = logical / a.mtiles;
@@ -278,7 +278,7 @@ struct WgradQkvPolicy2 {
     __device__ static int2 k_row(const Args& a, int h, int k, int K) {
         return wgrad_k_row(a.I, a.nd, a.T, a.H, a.n, h, k, K);
     }
-    __device__ static void a_mlane(const Args& a, int, int m8, const ST*& base, size_t& stride) {
+    __device__ static void a_mlane(const Args& a, int, int m8, const ST*& base, uint32_t& stride) {
         if (m8 < 3 * DH) {
             base = a.dQKV + m8;
             stride = 3 * DH;
@@ -290,7 +290,7 @@ struct WgradQkvPolicy2 {
             stride = 0;
         }
     }
-    __device__ static void b_mlane(const Args& a, int, int n8, const ST*& base, size_t& stride) {
+    __device__ static void b_mlane(const Args& a, int, int n8, const ST*& base, uint32_t& stride) {
         base = a.X + n8;
         stride = a.d;
     }
@@ -324,11 +324,11 @@ struct WgradOPolicy2 {
     __device__ static int2 k_row(const Args& a, int h, int k, int K) {
         return wgrad_k_row(a.I, a.nd, a.T, a.H, a.n, h, k, K);
     }
-    __device__ static void a_mlane(const Args& a, int, int m8, const ST*& base, size_t& stride) {
+    __device__ static void a_mlane(const Args& a, int, int m8, const ST*& base, uint32_t& stride) {
         base = a.dY + m8;
         stride = a.d;
     }
-    __device__ static void b_mlane(const Args& a, int, int n8, const ST*& base, size_t& stride) {
+    __device__ static void b_mlane(const Args& a, int, int n8, const ST*& base, uint32_t& stride) {
         base = a.A + n8;
         stride = DH;
     }
