@@ -200,19 +200,23 @@ __device__ __forceinline__ int xcd_logical_id(int b, int n) {
 }
 
 // ---------------------------------------------------------------------------
-// Sum of a 32-bit value over the 64 lanes of a wave, returned to every lane:
-// an inclusive scan with DPP row shifts (1, 2, 4, 8 within rows of 16 lanes)
-// and row broadcasts (lane 15 into rows 1 and 3, lane 31 into rows 2 and 3),
-// after which lane 63 holds the total.  The whole wave must be active.
+// Inclusive scan of a 32-bit value over the 64 lanes of a wave (lane i gets
+// the sum over lanes 0..i) with DPP row shifts (1, 2, 4, 8 within rows of 16
+// lanes) and row broadcasts (lane 15 into rows 1 and 3, lane 31 into rows 2
+// and 3), after which lane 63 holds the total; wave_sum_u32 returns that total
+// to every lane.  The whole wave must be active.
 // ---------------------------------------------------------------------------
-__device__ __forceinline__ uint32_t wave_sum_u32(uint32_t x) {
+__device__ __forceinline__ uint32_t wave_inclusive_scan_u32(uint32_t x) {
     x += __builtin_amdgcn_update_dpp(0u, x, 0x111, 0xf, 0xf, false);  // row_shr:1
     x += __builtin_amdgcn_update_dpp(0u, x, 0x112, 0xf, 0xf, false);  // row_shr:2
     x += __builtin_amdgcn_update_dpp(0u, x, 0x114, 0xf, 0xf, false);  // row_shr:4
     x += __builtin_amdgcn_update_dpp(0u, x, 0x118, 0xf, 0xf, false);  // row_shr:8
     x += __builtin_amdgcn_update_dpp(0u, x, 0x142, 0xa, 0xf, false);  // row_bcast:15
     x += __builtin_amdgcn_update_dpp(0u, x, 0x143, 0xc, 0xf, false);  // row_bcast:31
-    return __builtin_amdgcn_readlane(x, 63);
+    return x;
+}
+__device__ __forceinline__ uint32_t wave_sum_u32(uint32_t x) {
+    return __builtin_amdgcn_readlane(wave_inclusive_scan_u32(x), 63);
 }
 
 // ---------------------------------------------------------------------------

@@ -6,20 +6,21 @@
 // (exact logit s_t rounded once to double, descending; token index,
 // ascending), returned in ascending index order.  The router kernel gives an
 // fp32 logit z~_t with a proven bound |z~_t - s_t| <= beta_t, so every token
-// has an interval [lo_t, hi_t] that contains its key.  One workgroup per
-// (b, h) row:
-//   1. radix-select (4 passes of 8 bits over order-preserving uint32 keys, all
-//      in registers + LDS histograms) the k-th largest lo, A, and the
-//      (k+1)-th largest hi, B;
+// has an interval [lo_t, hi_t] that contains its key.  One workgroup of
+// several waves per (b, h) row:
+//   1. radix-select (4 passes of 8 bits over order-preserving uint32 keys held
+//      in registers, LDS histograms) the k-th largest lo, A, and the (k+1)-th
+//      largest hi, B;
 //   2. hi_t < A  => at least k tokens certainly beat t: t is out;
 //      lo_t > B  => at most k-1 tokens can beat t: t is in;
-//      the rest (typically a handful of tokens near the threshold) is
-//      uncertain;
-//   3. for the uncertain tokens the exact key is computed with a long
-//      accumulator (exact_dot.h; lanes add integer digits with LDS atomics,
-//      which is order-independent), and the k - #in best of them under
-//      (key desc, index asc) are chosen by exact rank;
-//   4. an in-order block scan compacts the chosen tokens: I ascending,
+//      the rest (typically none or two tokens at the threshold) is uncertain;
+//   3. the uncertain tokens are re-scored in fp64 (exact products, bounded
+//      summation error), which orders them unless their keys (nearly) tie;
+//      only then is the exact key computed with a long accumulator
+//      (exact_dot.h; lanes add integer digits with LDS atomics, which is
+//      order-independent); the k - #in best of them under (key desc, index
+//      asc) are chosen;
+//   4. the chosen tokens are compacted in index order: I ascending,
 //      r = sigmoid(z~), and the token -> slot map (slot of t in I, or -1).
 //
 // The error bound of z~ (router.hip): every K = 32 MFMA chunk starts from
@@ -66,536 +67,22 @@ template <> __device__ __forceinline__ void split_elem<float>(const float* p, ui
     split_f32(__float_as_uint(*p), s, M, E);
 }
 
-template <typename ST, int EPT>
-__global__ __launch_bounds__(256) void select_kernel(const float* __restrict__ z, const float* __restrict__ xnorm,
-                                                     const ST* __restrict__ X, const ST* __restrict__ Wr, int T,
-                                                     int d, int H, int k, int32_t* __restrict__ I,
-                                                     float* __restrict__ r, int16_t* __restrict__ slot,
-                                                     int32_t* __restrict__ unc_tok, double* __restrict__ unc_key,
-                                                     int32_t* __restrict__ unc_sel) {
-    __shared__ double s_red[4];
-    __shared__ int s_scan[4];
-    __shared__ int s_histA[256], s_histB[256];
-    __shared__ int s_digA, s_remA, s_digB, s_remB;
-    __shared__ int64_t s_long[4][kLongDigits];
-
-    const int row = blockIdx.x, b = row / H, h = row % H;
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const size_t rowT = (size_t)row * T;
-
-    // ||w_h||_2 (fp64) for the error bound.
-    const ST* w = Wr + (size_t)h * d;
-    double ss = 0.0;
-    for (int c = tid; c < d; c += 256) {
-        double v = (double)ld1<ST>(w + c);
-        ss += v * v;
-    }
-    ss = block256_sum(ss, s_red);
-    const double wn = sqrt(ss) * (1.0 + 0x1p-30);
-    const int nc = d / 32;
-    const double coef = (96.0 * 0x1p-23 + 1.01 * (double)nc * 0x1p-24) * (1.0 + 0x1p-10);
-    const double absterm = (double)(d + nc) * 0x1p-126 * (1.0 + 0x1p-10);
-
-    // Intervals [lo, hi] around every key, as order-preserving uint32.
-    const float* zr = z + rowT;
-    const float* xn = xnorm + (size_t)b * T;
-    const int t0 = tid * EPT;
-    uint32_t lo[EPT], hi[EPT];
-#pragma unroll
-    for (int e = 0; e < EPT; ++e) {
-        const int t = t0 + e;
-        if (t < T) {
-            const double zv = (double)zr[t], xv = (double)xn[t];
-            const double beta = coef * xv * wn + absterm * (1.0 + xv + wn);
-            lo[e] = order_key(f32_down(zv - beta));
-            hi[e] = order_key(f32_up(zv + beta));
-        } else {
-            lo[e] = 0u;  // below every real key
-            hi[e] = 0u;
-        }
-    }
-
-    const bool all = k >= T;
-    uint32_t A = 0u, Bk = 0u;
-    if (!all) {
-        uint32_t prefA = 0u, prefB = 0u;
-        int remA = k, remB = k + 1;
-        for (int pass = 0; pass < 4; ++pass) {
-            const int shift = 24 - 8 * pass;
-            const uint32_t himask = pass == 0 ? 0u : (0xffffffffu << (shift + 8));
-            s_histA[tid] = 0;
-            s_histB[tid] = 0;
-            __syncthreads();
-#pragma unroll
-            for (int e = 0; e < EPT; ++e) {
-                if (t0 + e < T) {
-                    if (((lo[e] ^ prefA) & himask) == 0u) atomicAdd(&s_histA[(lo[e] >> shift) & 255u], 1);
-                    if (((hi[e] ^ prefB) & himask) == 0u) atomicAdd(&s_histB[(hi[e] >> shift) & 255u], 1);
-                }
-            }
-            __syncthreads();
-            // thread tid looks at bin v = 255 - tid: the exclusive scan in thread
-            // order is the number of candidates in higher bins.
-            const int v = 255 - tid;
-            const int ca = s_histA[v], cb = s_histB[v];
-            int tot;
-            const int aboveA = block256_exclusive_scan(ca, s_scan, &tot);
-            const int aboveB = block256_exclusive_scan(cb, s_scan, &tot);
-            if (aboveA < remA && aboveA + ca >= remA) { s_digA = v; s_remA = remA - aboveA; }
-            if (aboveB < remB && aboveB + cb >= remB) { s_digB = v; s_remB = remB - aboveB; }
-            __syncthreads();
-            prefA |= (uint32_t)s_digA << shift;
-            remA = s_remA;
-            prefB |= (uint32_t)s_digB << shift;
-            remB = s_remB;
-            __syncthreads();
-        }
-        A = prefA;
-        Bk = prefB;
-    }
-
-    // Classify.
-    uint64_t inmask = 0ull, uncmask = 0ull;
-#pragma unroll
-    for (int e = 0; e < EPT; ++e) {
-        if (t0 + e < T) {
-            const bool in = all || lo[e] > Bk;
-            const bool out = !all && hi[e] < A;
-            if (in) inmask |= 1ull << e;
-            else if (!out) uncmask |= 1ull << e;
-        }
-    }
-    int tot_in, tot_unc;
-    (void)block256_exclusive_scan(__popcll(inmask), s_scan, &tot_in);
-    const int ubase = block256_exclusive_scan(__popcll(uncmask), s_scan, &tot_unc);
-    int need = k - tot_in;  // 0 <= need <= tot_unc when the bound holds
-    if (need < 0) need = 0;
-    if (need > tot_unc) need = tot_unc;
-    const bool resolve = need > 0 && need < tot_unc;
-
-    if (resolve) {
-        {
-            int pos = ubase;
-#pragma unroll
-            for (int e = 0; e < EPT; ++e)
-                if ((uncmask >> e) & 1ull) unc_tok[rowT + pos++] = t0 + e;
-        }
-        __syncthreads();
-        // Exact keys, one uncertain token per wave at a time.
-        for (int base = 0; base < tot_unc; base += 4) {
-            const int u = base + wave;
-            if (lane < kLongDigits) s_long[wave][lane] = 0;
-            __syncthreads();
-            if (u < tot_unc) {
-                const int t = unc_tok[rowT + u];
-                const ST* xr = X + ((size_t)b * T + t) * d;
-                for (int c = lane; c < d; c += 64) {
-                    uint32_t sx, Mx, sw, Mw;
-                    int Ex, Ew;
-                    split_elem<ST>(xr + c, sx, Mx, Ex);
-                    split_elem<ST>(w + c, sw, Mw, Ew);
-                    const ProductParts p = product_parts(sx, Mx, Ex, sw, Mw, Ew);
-                    if (!p.zero) {
-#pragma unroll
-                        for (int q = 0; q < 3; ++q) {
-                            if (p.v[q]) {
-                                const uint64_t add = p.negative ? (uint64_t)(-(int64_t)p.v[q]) : p.v[q];
-                                atomicAdd(reinterpret_cast<unsigned long long*>(&s_long[wave][p.j + q]),
-                                          (unsigned long long)add);
-                            }
-                        }
-                    }
-                }
-            }
-            __syncthreads();
-            if (u < tot_unc && lane == 0) unc_key[rowT + u] = long_accumulator_round(&s_long[wave][0]);
-            __syncthreads();
-        }
-        // Exact rank among the uncertain tokens.
-        for (int u = tid; u < tot_unc; u += 256) {
-            const double ku = unc_key[rowT + u];
-            const int tu = unc_tok[rowT + u];
-            int rank = 0;
-            for (int v = 0; v < tot_unc; ++v) {
-                const double kv = unc_key[rowT + v];
-                const int tv = unc_tok[rowT + v];
-                rank += (kv > ku) || (kv == ku && tv < tu);
-            }
-            unc_sel[rowT + u] = rank < need;
-        }
-        __syncthreads();
-    }
-
-    // Compact the chosen tokens in index order.
-    uint64_t selmask = inmask;
-    {
-        int pos = ubase;
-#pragma unroll
-        for (int e = 0; e < EPT; ++e) {
-            if ((uncmask >> e) & 1ull) {
-                const bool chosen = resolve ? (unc_sel[rowT + pos] != 0) : (need == tot_unc);
-                if (chosen) selmask |= 1ull << e;
-                ++pos;
-            }
-        }
-    }
-    int tot_sel;
-    const int sbase = block256_exclusive_scan(__popcll(selmask), s_scan, &tot_sel);
-    {
-        int pos = sbase;
-#pragma unroll
-        for (int e = 0; e < EPT; ++e) {
-            const int t = t0 + e;
-            if (t >= T) break;
-            int16_t sl = -1;
-            if ((selmask >> e) & 1ull) {
-                if (pos < k) {
-                    I[(size_t)row * k + pos] = t;
-                    r[(size_t)row * k + pos] = 1.0f / (1.0f + expf(-zr[t]));
-                    sl = (int16_t)pos;
-                }
-                ++pos;
-            }
-            slot[rowT + t] = sl;
-        }
-    }
-    // Only reachable if the logit error bound were violated: keep every slot
-    // defined (token 0, r = 0) so that downstream kernels stay in bounds.
-    for (int pos = tot_sel + tid; pos < k; pos += 256) {
-        I[(size_t)row * k + pos] = 0;
-        r[(size_t)row * k + pos] = 0.f;
-    }
-}
-
-// One wave per (b, h) row for T <= 64 * EPT <= 2048: the same contract and
-// steps, with no block barriers and no LDS histograms.  Token t = 64 e + lane
-// (coalesced loads); the two order statistics are found bit by bit from the
-// top: the keys of a lane are transposed once into bit planes, and at each
-// bit the candidates that share the prefix and have the bit set are counted
-// with one popcount per lane and one DPP wave sum (both selections packed in
-// one 32-bit sum).  The in-order compaction is a running ballot count.
-// Uncertain tokens are first re-scored in fp64 (exact products, bounded
-// summation error), which separates them unless keys (nearly) tie; only then
-// are exact keys computed with the long accumulator in this wave's LDS.
 __device__ __forceinline__ uint64_t lanes_below() {
     return (1ull << (threadIdx.x & 63)) - 1ull;
 }
 
-// In-place transpose of the two 16 x 16 bit matrices held in the low and high
-// halves of 16 registers (row = register index, column = bit): afterwards
-// bit e of the low (high) half of r[b] is bit b (b + 16) of the original r[e].
-__device__ __forceinline__ void transpose16x2(uint32_t (&r)[16]) {
-    uint32_t m = 0x00FF00FFu;
-#pragma unroll
-    for (int j = 8; j != 0; j >>= 1, m ^= (m << j)) {
-#pragma unroll
-        for (int k = 0; k < 16; k = (k + j + 1) & ~j) {
-            const uint32_t t = ((r[k] >> j) ^ r[k + j]) & m;
-            r[k + j] ^= t;
-            r[k] ^= t << j;
-        }
-    }
-}
-
-// Bit planes of EPT keys per lane: plane(b) bit e = bit b of key e.
-template <int EPT>
-struct BitPlanes {
-    static constexpr int G = (EPT + 15) / 16;
-    uint32_t r[G][16];
-    __device__ __forceinline__ void build(const uint32_t (&key)[EPT]) {
-#pragma unroll
-        for (int gr = 0; gr < G; ++gr) {
-#pragma unroll
-            for (int i = 0; i < 16; ++i) r[gr][i] = gr * 16 + i < EPT ? key[gr * 16 + i] : 0u;
-            transpose16x2(r[gr]);
-        }
-    }
-    template <int B>
-    __device__ __forceinline__ uint32_t plane() const {
-        uint32_t m = 0u;
-#pragma unroll
-        for (int gr = 0; gr < G; ++gr) m |= (B >= 16 ? (r[gr][B - 16] >> 16) : (r[gr][B] & 0xffffu)) << (16 * gr);
-        return m;
-    }
-};
-
-// One bit of the two top-down selections (k-th largest lo, (k+1)-th largest hi).
-template <int B, int EPT>
-__device__ __forceinline__ void select_bit(const BitPlanes<EPT>& pa, const BitPlanes<EPT>& pb, uint32_t& candA,
-                                           uint32_t& candB, uint32_t& prefA, uint32_t& prefB, int& remA,
-                                           int& remB) {
-    const uint32_t hA = pa.template plane<B>(), hB = pb.template plane<B>();
-    // both counts in one wave sum (each <= T <= 2048)
-    const uint32_t both = wave_sum_u32((uint32_t)__popc(candA & hA) | ((uint32_t)__popc(candB & hB) << 16));
-    const int cA = (int)(both & 0xffffu), cB = (int)(both >> 16);
-    if (cA >= remA) {
-        prefA |= 1u << B;
-        candA &= hA;
-    } else {
-        remA -= cA;
-        candA &= ~hA;
-    }
-    if (cB >= remB) {
-        prefB |= 1u << B;
-        candB &= hB;
-    } else {
-        remB -= cB;
-        candB &= ~hB;
-    }
-}
-
-template <int B, int EPT>
-__device__ __forceinline__ void select_bits(const BitPlanes<EPT>& pa, const BitPlanes<EPT>& pb, uint32_t& candA,
-                                            uint32_t& candB, uint32_t& prefA, uint32_t& prefB, int& remA,
-                                            int& remB) {
-    select_bit<B, EPT>(pa, pb, candA, candB, prefA, prefB, remA, remB);
-    if constexpr (B > 0) select_bits<B - 1, EPT>(pa, pb, candA, candB, prefA, prefB, remA, remB);
-}
-
-template <typename ST, int EPT>
-__global__ __launch_bounds__(256) void select_wave_kernel(const float* __restrict__ z, const float* __restrict__ xnorm,
-                                                          const ST* __restrict__ X, const ST* __restrict__ Wr, int BH,
-                                                          int T, int d, int H, int k, int32_t* __restrict__ I,
-                                                          float* __restrict__ r, int16_t* __restrict__ slot,
-                                                          int32_t* __restrict__ unc_tok, double* __restrict__ unc_key,
-                                                          int32_t* __restrict__ unc_sel) {
-    __shared__ int64_t s_long[4][kLongDigits];
-    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-    const int row = blockIdx.x * 4 + wave;
-    if (row >= BH) return;  // whole wave; nothing below synchronises across waves
-    const int b = row / H, h = row % H;
-    const size_t rowT = (size_t)row * T;
-
-    // ||w_h||_2 (fp64) for the error bound: 8 elements per lane and load
-    const ST* w = Wr + (size_t)h * d;
-    double ss = 0.0;
-    for (int c0 = 0; c0 < d; c0 += 8 * 64 * 2) {
-        Vec8<ST> v[2];
-#pragma unroll
-        for (int q = 0; q < 2; ++q) v[q] = vec8_load<ST>(w + min(c0 + 8 * (64 * q + lane), d - 8));
-#pragma unroll
-        for (int q = 0; q < 2; ++q) {
-            if (c0 + 8 * (64 * q + lane) < d) {
-                float x[8];
-                vec8_to_f32<ST>(v[q], x);
-#pragma unroll
-                for (int j = 0; j < 8; ++j) ss += (double)x[j] * (double)x[j];
-            }
-        }
-    }
-#pragma unroll
-    for (int o = 32; o >= 1; o >>= 1) ss += __shfl_xor(ss, o, 64);
-    const double wn = sqrt(ss) * (1.0 + 0x1p-30);
-    const int nc = d / 32;
-    const double coef = (96.0 * 0x1p-23 + 1.01 * (double)nc * 0x1p-24) * (1.0 + 0x1p-10);
-    const double absterm = (double)(d + nc) * 0x1p-126 * (1.0 + 0x1p-10);
-
-    const float* zr = z + rowT;
-    const float* xn = xnorm + (size_t)b * T;
-    uint32_t lo[EPT], hi[EPT];
-    float zv[EPT];
-#pragma unroll
-    for (int e = 0; e < EPT; ++e) {
-        const int t = 64 * e + lane;
-        const int tc = min(t, T - 1);
-        zv[e] = zr[tc];
-        const double xv = (double)xn[tc];
-        const double beta = coef * xv * wn + absterm * (1.0 + xv + wn);
-        lo[e] = t < T ? order_key(f32_down((double)zv[e] - beta)) : 0u;  // 0: below every real key
-        hi[e] = t < T ? order_key(f32_up((double)zv[e] + beta)) : 0u;
-    }
-
-    const bool all = k >= T;
-    uint32_t A = 0u, Bk = 0u;
-    if (!all) {
-        // candA / candB: bit e set while element e still matches the prefix
-        uint32_t candA = 0u, candB = 0u;
-#pragma unroll
-        for (int e = 0; e < EPT; ++e)
-            if (64 * e + lane < T) {
-                candA |= 1u << e;
-                candB |= 1u << e;
-            }
-        uint32_t prefA = 0u, prefB = 0u;
-        int remA = k, remB = k + 1;
-        BitPlanes<EPT> pa, pb;
-        pa.build(lo);
-        pb.build(hi);
-        select_bits<31, EPT>(pa, pb, candA, candB, prefA, prefB, remA, remB);
-        A = prefA;
-        Bk = prefB;
-    }
-
-    // Classify; positions of the uncertain tokens in index order.
-    uint32_t inm = 0u, uncm = 0u;
-    int tot_in = 0, tot_unc = 0;
-    int upos[EPT];
-#pragma unroll
-    for (int e = 0; e < EPT; ++e) {
-        const int t = 64 * e + lane;
-        const bool in = t < T && (all || lo[e] > Bk);
-        const bool unc = t < T && !in && !(hi[e] < A);
-        const uint64_t bi = __ballot(in), bu = __ballot(unc);
-        upos[e] = tot_unc + __popcll(bu & lanes_below());
-        if (in) inm |= 1u << e;
-        if (unc) uncm |= 1u << e;
-        tot_in += __popcll(bi);
-        tot_unc += __popcll(bu);
-    }
-    int need = k - tot_in;  // 0 <= need <= tot_unc when the bound holds
-    if (need < 0) need = 0;
-    if (need > tot_unc) need = tot_unc;
-    const bool resolve = need > 0 && need < tot_unc;
-
-    if (resolve) {
-#pragma unroll
-        for (int e = 0; e < EPT; ++e)
-            if ((uncm >> e) & 1u) unc_tok[rowT + upos[e]] = 64 * e + lane;
-        __threadfence_block();
-        __builtin_amdgcn_wave_barrier();
-        // Second level: the logits of the uncertain tokens in fp64.  Products
-        // of two stored values are exact in fp64; any order of the d - 1
-        // additions errs by at most (d - 1) u64 sum|x_i w_i| <= that times
-        // ||x|| ||w||, and the key RN64(s) is within half an ulp of s.
-        for (int u = 0; u < tot_unc; ++u) {
-            const int t = unc_tok[rowT + u];
-            const ST* xr = X + ((size_t)b * T + t) * d;
-            double acc = 0.0;
-            for (int c0 = 0; c0 < d; c0 += 8 * 64) {
-                const int c = min(c0 + 8 * lane, d - 8);
-                float xv8[8], wv8[8];
-                vec8_to_f32<ST>(vec8_load<ST>(xr + c), xv8);
-                vec8_to_f32<ST>(vec8_load<ST>(w + c), wv8);
-                if (c0 + 8 * lane < d) {
-#pragma unroll
-                    for (int j = 0; j < 8; ++j) acc += (double)xv8[j] * (double)wv8[j];
-                }
-            }
-#pragma unroll
-            for (int o = 32; o >= 1; o >>= 1) acc += __shfl_xor(acc, o, 64);
-            if (lane == 0) unc_key[rowT + u] = acc;
-        }
-        __threadfence_block();
-        __builtin_amdgcn_wave_barrier();
-        // Decide from the fp64 intervals where they separate; otherwise fall
-        // back to exact keys for all uncertain tokens.
-        bool undecided = false;
-        for (int u = lane; u < tot_unc; u += 64) {
-            const double vu = unc_key[rowT + u];
-            const double bu = 1.01 * (double)d * 0x1p-53 * (double)xn[unc_tok[rowT + u]] * wn + fabs(vu) * 0x1p-51;
-            int above = 0, maybe = 0;
-            for (int v = 0; v < tot_unc; ++v) {
-                if (v == u) continue;
-                const double vv = unc_key[rowT + v];
-                const double bv = 1.01 * (double)d * 0x1p-53 * (double)xn[unc_tok[rowT + v]] * wn + fabs(vv) * 0x1p-51;
-                if (vv - bv > vu + bu) ++above;         // certainly above u
-                else if (!(vv + bv < vu - bu)) ++maybe;  // order unknown
-            }
-            int sel = -1;
-            if (above + maybe < need) sel = 1;
-            else if (above >= need) sel = 0;
-            else undecided = true;
-            unc_sel[rowT + u] = sel;
-        }
-        undecided = __ballot(undecided) != 0ull;
-        __threadfence_block();
-        __builtin_amdgcn_wave_barrier();
-        if (undecided) {
-            // Exact keys (long accumulator in this wave's LDS digits).
-            for (int u = 0; u < tot_unc; ++u) {
-                if (lane < kLongDigits) s_long[wave][lane] = 0;
-                __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "workgroup");
-                __builtin_amdgcn_wave_barrier();
-                const int t = unc_tok[rowT + u];
-                const ST* xr = X + ((size_t)b * T + t) * d;
-                for (int c = lane; c < d; c += 64) {
-                    uint32_t sx, Mx, sw, Mw;
-                    int Ex, Ew;
-                    split_elem<ST>(xr + c, sx, Mx, Ex);
-                    split_elem<ST>(w + c, sw, Mw, Ew);
-                    const ProductParts p = product_parts(sx, Mx, Ex, sw, Mw, Ew);
-                    if (!p.zero) {
-#pragma unroll
-                        for (int q = 0; q < 3; ++q) {
-                            if (p.v[q]) {
-                                const uint64_t add = p.negative ? (uint64_t)(-(int64_t)p.v[q]) : p.v[q];
-                                atomicAdd(reinterpret_cast<unsigned long long*>(&s_long[wave][p.j + q]),
-                                          (unsigned long long)add);
-                            }
-                        }
-                    }
-                }
-                __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "workgroup");
-                __builtin_amdgcn_wave_barrier();
-                if (lane == 0) unc_key[rowT + u] = long_accumulator_round(&s_long[wave][0]);
-                __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "workgroup");
-                __builtin_amdgcn_wave_barrier();
-            }
-            __threadfence_block();
-            __builtin_amdgcn_wave_barrier();
-            // exact rank among the uncertain tokens (key desc, index asc)
-            for (int u = lane; u < tot_unc; u += 64) {
-                const double ku = unc_key[rowT + u];
-                const int tu = unc_tok[rowT + u];
-                int rank = 0;
-                for (int v = 0; v < tot_unc; ++v) {
-                    const double kv = unc_key[rowT + v];
-                    const int tv = unc_tok[rowT + v];
-                    rank += (kv > ku) || (kv == ku && tv < tu);
-                }
-                unc_sel[rowT + u] = rank < need;
-            }
-        }
-        __threadfence_block();
-        __builtin_amdgcn_wave_barrier();
-    }
-
-    // Compact the chosen tokens in index order: I ascending, r, and the slot map.
-    int pos0 = 0;
-#pragma unroll
-    for (int e = 0; e < EPT; ++e) {
-        const int t = 64 * e + lane;
-        bool sel = (inm >> e) & 1u;
-        if ((uncm >> e) & 1u) sel = resolve ? (unc_sel[rowT + upos[e]] != 0) : (need == tot_unc);
-        const uint64_t bs = __ballot(sel);
-        const int pos = pos0 + __popcll(bs & lanes_below());
-        int16_t sl = -1;
-        if (sel && pos < k) {
-            I[(size_t)row * k + pos] = t;
-            r[(size_t)row * k + pos] = 1.0f / (1.0f + expf(-zv[e]));
-            sl = (int16_t)pos;
-        }
-        if (t < T) slot[rowT + t] = sl;
-        pos0 += __popcll(bs);
-    }
-    // Only reachable if the logit error bound were violated: keep every slot
-    // defined (token 0, r = 0) so that downstream kernels stay in bounds.
-    for (int pos = pos0 + lane; pos < k; pos += 64) {
-        I[(size_t)row * k + pos] = 0;
-        r[(size_t)row * k + pos] = 0.f;
-    }
-}
-
-// Several waves per (b, h) row (NW waves, EPT tokens per thread; token
-// t = e * 64 NW + tid, so loads and stores are coalesced).  The same contract
-// and steps as above, arranged for parallelism: the two order statistics by
-// four 8-bit radix passes over LDS histograms (both selections share one
-// packed 32-bit block scan per pass); the in-order positions from per-wave,
-// per-stripe ballot counts; the uncertain tokens (if any) re-scored in fp64
-// one token per wave in parallel, their list kept in LDS when short, and the
-// exact long-accumulator keys only where the fp64 intervals still overlap.
+// NW waves per row, EPT tokens per thread (token t = e * 64 NW + tid, so loads
+// and stores are coalesced).  Both selections share one packed 32-bit block
+// scan per radix pass; the in-order positions come from per-wave, per-stripe
+// ballot counts; the uncertain tokens (if any) are re-scored one per wave in
+// parallel, their list kept in LDS when short.
 constexpr int kSelectLdsUnc = 64;  // uncertain tokens held in LDS (more: the global scratch arrays)
 
 template <int NW>
 __device__ __forceinline__ uint32_t block_exclusive_scan_u32(uint32_t v, uint32_t* tmp, uint32_t& total) {
-    // inclusive wave scan with shuffles, then the wave totals through LDS
+    // inclusive wave scan (DPP), then the wave totals through LDS
     const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-    uint32_t inc = v;
-#pragma unroll
-    for (int o = 1; o < 64; o <<= 1) {
-        const uint32_t u = __shfl_up(inc, o, 64);
-        if (lane >= o) inc += u;
-    }
+    const uint32_t inc = wave_inclusive_scan_u32(v);
     if (lane == 63) tmp[w] = inc;
     __syncthreads();
     uint32_t base = 0, all = 0;
@@ -913,7 +400,7 @@ int launch_select_t(const float* z, const float* xnorm, const ST* X, const ST* W
                        k, I, r, slot, unc_tok, unc_key, unc_sel)
     if (T <= 256) MOSA_SELECT_ROWS(4, 1);
     else if (T <= 512) MOSA_SELECT_ROWS(4, 2);
-    else if (T <= 1024) MOSA_SELECT_ROWS(4, 4);
+    else if (T <= 1024) MOSA_SELECT_ROWS(8, 2);
     else if (T <= 2048) MOSA_SELECT_ROWS(4, 8);
     else if (T <= 8192) MOSA_SELECT_ROWS(16, 8);
     else if (T <= 16384) MOSA_SELECT_ROWS(16, 16);
