@@ -174,7 +174,9 @@ __device__ __forceinline__ void combine_tile(const float* Cs, int ldc, int tid, 
 constexpr int kCombineTokens = 16;
 constexpr int kCombineLdt = kCombineTokens + 2;  // padded LDS row (int16) per head
 
-template <typename ST, int CH>  // CH: 8-column groups per lane (d <= 512 CH)
+// CH: 8-column groups per lane (d <= 512 CH).  USE only names the caller
+// (0: the layer output, 1: dX) so that profiles tell the two launches apart.
+template <typename ST, int CH, int USE>
 __global__ __launch_bounds__(256) void combine_rows_kernel(const int16_t* __restrict__ slot,
                                                            const ST* __restrict__ rows, ST* __restrict__ out, int T,
                                                            int d, int H, int k, int accumulate, int tiles_per_b) {
@@ -275,7 +277,7 @@ __global__ __launch_bounds__(256) void combine_rows_kernel(const int16_t* __rest
 }
 
 // out (+)= head-ordered sum of the MoSA rows (no dense heads); d a multiple of 8.
-template <typename ST>
+template <typename ST, int USE>
 int launch_combine_rows(const int16_t* slot, const ST* rows, ST* out, int B, int T, int d, int H, int k,
                         int accumulate, hipStream_t stream) {
     if (B == 0 || T == 0) return 0;
@@ -285,13 +287,13 @@ int launch_combine_rows(const int16_t* slot, const ST* rows, ST* out, int B, int
     if (lds > 64 * 1024) return -1;
     const dim3 grid(B * tiles), block(256);
     if (d <= 512)
-        hipLaunchKernelGGL((combine_rows_kernel<ST, 1>), grid, block, lds, stream, slot, rows, out, T, d, H, k,
+        hipLaunchKernelGGL((combine_rows_kernel<ST, 1, USE>), grid, block, lds, stream, slot, rows, out, T, d, H, k,
                            accumulate, tiles);
     else if (d <= 1024)
-        hipLaunchKernelGGL((combine_rows_kernel<ST, 2>), grid, block, lds, stream, slot, rows, out, T, d, H, k,
+        hipLaunchKernelGGL((combine_rows_kernel<ST, 2, USE>), grid, block, lds, stream, slot, rows, out, T, d, H, k,
                            accumulate, tiles);
     else
-        hipLaunchKernelGGL((combine_rows_kernel<ST, 4>), grid, block, lds, stream, slot, rows, out, T, d, H, k,
+        hipLaunchKernelGGL((combine_rows_kernel<ST, 4, USE>), grid, block, lds, stream, slot, rows, out, T, d, H, k,
                            accumulate, tiles);
     return hipGetLastError() == hipSuccess ? 0 : -1;
 }

@@ -228,7 +228,7 @@ int run_combine(const ST* dQKVd, const ST* Wq, const ST* Wk, const ST* Wv, const
                 int T, int d, int H, int k, int Hd, ST* dX, int accumulate, hipStream_t stream) {
     using P = DxCombinePolicy<ST, DH>;
     if (Hd == 0 && d % 8 == 0 && d <= 2048 && (size_t)H * kCombineLdt * 2 <= 64 * 1024)
-        return launch_combine_rows<ST>(slot, dXs, dX, B, T, d, H, k, accumulate, stream);
+        return launch_combine_rows<ST, 1>(slot, dXs, dX, B, T, d, H, k, accumulate, stream);
     typename P::Args a{dQKVd, Wq, Wk, Wv, slot, dXs, dX, T, d, H, k, Hd, accumulate, (T + P::MT - 1) / P::MT,
                        (d + P::NT - 1) / P::NT};
     return launch_gemm<ST, P>(a, B * a.mtiles * a.ntiles, stream);

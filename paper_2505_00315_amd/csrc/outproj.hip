@@ -197,7 +197,7 @@ int run_combine(const ST* Ad, const ST* Wod, const int16_t* slot, const ST* Xo, 
                 int Hd, ST* Y, int accumulate, hipStream_t stream) {
     using P = OutCombinePolicy<ST, DH>;
     if (Hd == 0 && d % 8 == 0 && d <= 2048 && (size_t)H * kCombineLdt * 2 <= 64 * 1024)
-        return launch_combine_rows<ST>(slot, Xo, Y, B, T, d, H, k, accumulate, stream);
+        return launch_combine_rows<ST, 0>(slot, Xo, Y, B, T, d, H, k, accumulate, stream);
     typename P::Args a{Ad, Wod, slot, Xo, Y, T, d, H, k, Hd, accumulate, (T + P::MT - 1) / P::MT,
                        (d + P::NT - 1) / P::NT};
     return launch_gemm<ST, P>(a, B * a.mtiles * a.ntiles, stream);

@@ -145,16 +145,16 @@ def paper_mosa_heads_for_budget(layers, h, hp, T, baseline_heads, dense_heads, s
 # same kernels, so workloads with dense heads are not attributed here).
 STAGE_KERNELS = {
     "router": (r"router_kernel",),
-    "select": (r"select_kernel",),
+    "select": (r"select_\w*kernel",),
     "qkv": (r"(?<!Wgrad)QkvPolicy",),
     "attn": (r"attn_fwd",),
-    "out_scatter": (r"OutProjPolicy", r"OutCombinePolicy"),
+    "out_scatter": (r"OutProj\w*Policy", r"OutCombinePolicy", r"combine_rows_kernel<[^>]*, 0>"),
     "bwd_out": (r"BwdOutPolicy",),
     "attn_bwd_kv": (r"attn_bwd_kv",),
     "attn_bwd_q": (r"attn_bwd_q",),
     "wgrad_qkv": (r"WgradQkvPolicy", r"wgrad_qkv_reduce"),
     "wgrad_o": (r"WgradOPolicy", r"wgrad_o_reduce"),
-    "dx_scatter": (r"DxProjPolicy", r"DxCombinePolicy"),
+    "dx_scatter": (r"DxProj\w*Policy", r"DxCombinePolicy", r"combine_rows_kernel<[^>]*, 1>"),
 }
 
 
