@@ -163,21 +163,22 @@ __device__ __forceinline__ void combine_tile(const float* Cs, int ldc, int tid, 
 // The same combination without dense heads, as a kernel of its own: out[b, t]
 // (+)= sum over MoSA heads h (ascending) of rows[b, h, slot[b, h, t]].  A
 // workgroup takes 16 tokens of one batch element and stages their slot
-// entries for every head in LDS (head-major, padded rows); each wave then
-// handles 4 tokens, one at a time, with the whole d-wide row spread over its
+// entries for every head in LDS (head-major, padded rows); each of its 16
+// waves then handles one token, with the whole d-wide row spread over its
 // lanes (8 consecutive columns per lane and 64-lane group, so every hit is
 // one coalesced d-element load).  The hits of a token are taken 4 at a time
 // in ascending head order (the lanes of a 64-head group ballot their slot
 // entries); the sum starts from 0 and is added to the old output value at
 // the end when accumulating, so every element is produced by one lane in a
 // fixed order.
-constexpr int kCombineTokens = 16;
+constexpr int kCombineTokens = 16;               // one per wave
+constexpr int kCombineThreads = 64 * kCombineTokens;
 constexpr int kCombineLdt = kCombineTokens + 2;  // padded LDS row (int16) per head
 
 // CH: 8-column groups per lane (d <= 512 CH).  USE only names the caller
 // (0: the layer output, 1: dX) so that profiles tell the two launches apart.
 template <typename ST, int CH, int USE>
-__global__ __launch_bounds__(256) void combine_rows_kernel(const int16_t* __restrict__ slot,
+__global__ __launch_bounds__(kCombineThreads) void combine_rows_kernel(const int16_t* __restrict__ slot,
                                                            const ST* __restrict__ rows, ST* __restrict__ out, int T,
                                                            int d, int H, int k, int accumulate, int tiles_per_b) {
     extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
@@ -187,7 +188,7 @@ __global__ __launch_bounds__(256) void combine_rows_kernel(const int16_t* __rest
     const int b = logical / tiles_per_b, t0 = (logical % tiles_per_b) * kCombineTokens;
 
     if ((T & 7) == 0) {
-        for (int e = tid; e < H * 2; e += 256) {
+        for (int e = tid; e < H * 2; e += kCombineThreads) {
             const int h = e >> 1, q = e & 1, tt = t0 + 8 * q;
             uint4 v = make_uint4(0xffffffffu, 0xffffffffu, 0xffffffffu, 0xffffffffu);
             if (tt < T) v = *reinterpret_cast<const uint4*>(slot + ((size_t)b * H + h) * T + tt);
@@ -198,7 +199,7 @@ __global__ __launch_bounds__(256) void combine_rows_kernel(const int16_t* __rest
             dst[3] = v.w;
         }
     } else {
-        for (int e = tid; e < H * kCombineTokens; e += 256) {
+        for (int e = tid; e < H * kCombineTokens; e += kCombineThreads) {
             const int h = e / kCombineTokens, tl = e % kCombineTokens, tt = t0 + tl;
             s_slot[h * kCombineLdt + tl] = tt < T ? slot[((size_t)b * H + h) * T + tt] : (int16_t)-1;
         }
@@ -206,9 +207,9 @@ __global__ __launch_bounds__(256) void combine_rows_kernel(const int16_t* __rest
     __syncthreads();
 
     const ST* rb = rows + (size_t)b * H * k * d;
-    for (int tl = 4 * wave; tl < 4 * wave + 4; ++tl) {
-        const int t = t0 + tl;
-        if (t >= T) break;
+    {
+        const int tl = wave, t = t0 + tl;
+        if (t >= T) return;
         float acc[CH][8];
 #pragma unroll
         for (int c = 0; c < CH; ++c)
@@ -285,7 +286,7 @@ int launch_combine_rows(const int16_t* slot, const ST* rows, ST* out, int B, int
     const int tiles = (T + kCombineTokens - 1) / kCombineTokens;
     const size_t lds = (size_t)(H > 0 ? H : 1) * kCombineLdt * sizeof(int16_t);
     if (lds > 64 * 1024) return -1;
-    const dim3 grid(B * tiles), block(256);
+    const dim3 grid(B * tiles), block(kCombineThreads);
     if (d <= 512)
         hipLaunchKernelGGL((combine_rows_kernel<ST, 1, USE>), grid, block, lds, stream, slot, rows, out, T, d, H, k,
                            accumulate, tiles);
