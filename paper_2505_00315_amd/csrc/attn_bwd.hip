@@ -14,6 +14,7 @@
 //   q pass:  one wave per block of 16 queries, loop over allowed key blocks;
 //            S^T and dP^T tiles (query in the lane) feed dQ^T += K^T dS^T.
 #include "common.h"
+#include "gemm2.h"
 #include "kernels.h"
 #include "tiles.h"
 
@@ -447,11 +448,239 @@ __global__ __launch_bounds__(256) void attn_bwd_q_tiled_kernel(const ST* __restr
     }
 }
 
+// bf16, n <= 128: both passes in one workgroup of 8 waves per (b, h).  Q, K,
+// V and dA of all n rows go into LDS once (direct global->LDS loads, rows
+// with XOR-permuted 16-byte units), with lse and D.  Phase 1, wave w owns key
+// block w: S and dP with the key in the lane (B operands K and V from
+// registers), P and dS, dV^T += dA^T P and dK^T += Q^T dS 32 queries per MFMA
+// (dA^T and Q^T by transposed LDS reads in the query order of the P and dS
+// registers), and dS (bf16, the MFMA operand value) into an LDS tile
+// [query][key].  Phase 2, wave w owns query block w: dQ^T += K^T dS^T 32 keys
+// per MFMA from that tile.  No value is accumulated by more than one lane, so
+// the result is reproducible; the roundings are those of the two-pass kernels
+// (P and dS enter the MFMAs as bf16).
+constexpr int kAttnBwdLdsMaxN = 128;
+
+template <int DH>
+struct AttnBwdLds {
+    static constexpr int NMAX = kAttnBwdLdsMaxN, LPR = DH / 8, NW = NMAX / 16;
+    static constexpr int TILE = NMAX * DH * 2;           // Q, K, V, dA tiles
+    static constexpr int DS_BYTES = NMAX * NMAX * 2;     // dS [query][key], 16 units per row
+    static constexpr size_t lds = 4 * (size_t)TILE + DS_BYTES + 2 * NMAX * 4;
+};
+
+template <int DH>
+__global__ __launch_bounds__(512) void attn_bwd_lds_kernel(const uint16_t* __restrict__ QKV,
+                                                           const uint16_t* __restrict__ dA,
+                                                           const float* __restrict__ lse, const float* __restrict__ D,
+                                                           int BH, int n, int causal, float scale,
+                                                           uint16_t* __restrict__ dQKV) {
+    using ST = uint16_t;
+    using L = AttnBwdLds<DH>;
+    constexpr int RS = 3 * DH, NMAX = L::NMAX, LPR = L::LPR, NW = L::NW, TILE = L::TILE;
+    constexpr int PER = NMAX * LPR / (64 * NW);  // DMA instructions per wave per tile
+    static_assert(PER >= 1 && NMAX * LPR % (64 * NW) == 0, "tile shape");
+    extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
+    unsigned char* const Qs = smem;
+    unsigned char* const Ks = smem + TILE;
+    unsigned char* const Vs = smem + 2 * TILE;
+    unsigned char* const dAs = smem + 3 * TILE;
+    unsigned char* const dSs = smem + 4 * TILE;
+    float* const lse_s = reinterpret_cast<float*>(dSs + L::DS_BYTES);
+    float* const D_s = lse_s + NMAX;
+
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int g = lane >> 4, c16 = lane & 15;
+    const int bh = xcd_logical_id(blockIdx.x, gridDim.x);
+    const size_t base = (size_t)bh * n;
+    const ST* Qp = QKV + base * RS;
+    const ST* dAp = dA + base * DH;
+
+    {
+        const uint32_t lb = __builtin_amdgcn_readfirstlane(lds_addr(smem)) + 1024 * __builtin_amdgcn_readfirstlane(wave);
+#pragma unroll
+        for (int j = 0; j < PER; ++j) {
+            const int p = 64 * (wave + NW * j) + lane, row = p / LPR, pos = p % LPR;
+            const int col = 8 * (pos ^ kswz(row, LPR));
+            const size_t r = (size_t)min(row, n - 1);
+            const uint32_t off = lb + 1024 * NW * j;
+            lds_load16(Qp + r * RS + col, off);
+            lds_load16(Qp + r * RS + DH + col, off + TILE);
+            lds_load16(Qp + r * RS + 2 * DH + col, off + 2 * TILE);
+            lds_load16(dAp + r * DH + col, off + 3 * TILE);
+        }
+    }
+    if (tid < NMAX) {
+        const size_t r = base + min(tid, n - 1);
+        lse_s[tid] = lse[r];
+        D_s[tid] = D[r];
+    }
+    wait_vmcnt<0>();
+    __syncthreads();
+
+    // k-contiguous operand: row `row`, d = 32 st + 8 g .. + 7
+    auto frag_k = [&](const unsigned char* t, int row, int st) {
+        const int u = 4 * st + g;
+        Frag8<ST> f;
+        f.v = __builtin_bit_cast(bf16x8, *reinterpret_cast<const uint4*>(t + (row * LPR + (u ^ kswz(row, LPR))) * 16));
+        return f;
+    };
+    // transposed read of 4 rows k .. k + 3 (k = kb0 + (c16 >> 2) per source lane) at columns mcol .. + 3
+    auto tr4 = [&](const unsigned char* t, int k, int mcol) {
+        const int un = mcol >> 3, half = (mcol >> 2) & 1;
+        return lds_read_tr16(t + (k * LPR + (un ^ kswz(k, LPR))) * 16 + 8 * half);
+    };
+    // A operand X^T (rows d = dbase + c16) over rows {kb + 4 g + i, kb + 16 + 4 g + i}
+    // of a row-major tile: the order of two D-layout register blocks
+    auto trA_pair = [&](const unsigned char* t, int dbase, int kb) {
+        const int k0 = kb + 4 * g + (c16 >> 2), mcol = dbase + 4 * (c16 & 3);
+        const u32x2 lo = tr4(t, k0, mcol), hi = tr4(t, k0 + 16, mcol);
+        return u32x4{lo.x, lo.y, hi.x, hi.y};
+    };
+    // A operand X^T over consecutive rows kb + 8 g .. + 7
+    auto trA_run = [&](const unsigned char* t, int dbase, int kb) {
+        const int k0 = kb + 8 * g + (c16 >> 2), mcol = dbase + 4 * (c16 & 3);
+        const u32x2 lo = tr4(t, k0, mcol), hi = tr4(t, k0 + 4, mcol);
+        return u32x4{lo.x, lo.y, hi.x, hi.y};
+    };
+    auto ds_unit = [](int q, int key8) { return q * 16 + ((key8 >> 3) ^ (q & 15)); };  // dS tile, 16-byte unit
+
+    const int nb = (n + 15) / 16;
+    // Phase 1: key block kb = wave.
+    if (wave < nb) {
+        const int kb = wave, key = 16 * kb + c16;
+        Frag8<ST> kf[DH / 32], vf[DH / 32];
+#pragma unroll
+        for (int st = 0; st < DH / 32; ++st) {
+            kf[st] = frag_k(Ks, key, st);
+            vf[st] = frag_k(Vs, key, st);
+        }
+        f32x4 dKt[DH / 16], dVt[DH / 16];
+#pragma unroll
+        for (int db = 0; db < DH / 16; ++db) dKt[db] = dVt[db] = zero4();
+        for (int u = causal ? kb / 2 : 0; 2 * u < nb; ++u) {
+            float p[2][4], ds[2][4];
+#pragma unroll
+            for (int hq = 0; hq < 2; ++hq) {
+                const int qb = 2 * u + hq;
+                f32x4 s = zero4(), dp = zero4();
+                if (qb < nb) {
+#pragma unroll
+                    for (int st = 0; st < DH / 32; ++st) {
+                        mma8(s, frag_k(Qs, 16 * qb + c16, st), kf[st]);
+                        mma8(dp, frag_k(dAs, 16 * qb + c16, st), vf[st]);
+                    }
+                }
+                mfma_drain();
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    const int q = 16 * qb + 4 * g + i;
+                    const bool ok = qb < nb && q < n && key < n && (!causal || key <= q);
+                    const float pv = ok ? expf(s[i] * scale - lse_s[q & (NMAX - 1)]) : 0.f;
+                    const float dsv = pv * (dp[i] - D_s[q & (NMAX - 1)]);
+                    p[hq][i] = pv;
+                    ds[hq][i] = dsv;
+                    if (qb < nb) {
+                        ST* dst = reinterpret_cast<ST*>(dSs + ds_unit(q, key) * 16) + (key & 7);
+                        *dst = f32_to_bf16(dsv);
+                    }
+                }
+            }
+            // dV^T += dA^T P, dK^T += Q^T dS over the 32 queries 32 u + {4 g + i, 16 + 4 g + i}
+            const float pv8[8] = {p[0][0], p[0][1], p[0][2], p[0][3], p[1][0], p[1][1], p[1][2], p[1][3]};
+            const float ds8[8] = {ds[0][0], ds[0][1], ds[0][2], ds[0][3], ds[1][0], ds[1][1], ds[1][2], ds[1][3]};
+            const Frag8<ST> pf = frag8_from<ST>(pv8), dsf = frag8_from<ST>(ds8);
+            u32x4 at[DH / 16], qt[DH / 16];
+#pragma unroll
+            for (int db = 0; db < DH / 16; ++db) {
+                at[db] = trA_pair(dAs, 16 * db, 32 * u);
+                qt[db] = trA_pair(Qs, 16 * db, 32 * u);
+            }
+            lds_wait();
+#pragma unroll
+            for (int db = 0; db < DH / 16; ++db) {
+                lds_ready(at[db]);
+                lds_ready(qt[db]);
+                Frag8<ST> fa, fq;
+                fa.v = __builtin_bit_cast(bf16x8, at[db]);
+                fq.v = __builtin_bit_cast(bf16x8, qt[db]);
+                mma8(dVt[db], fa, pf);
+                mma8(dKt[db], fq, dsf);
+            }
+        }
+        mfma_drain();
+        if (key < n) {
+            ST* out = dQKV + (base + key) * RS;
+#pragma unroll
+            for (int db = 0; db < DH / 16; ++db) {
+                // lane: key c16, d = 16 db + 4 g + i
+                *reinterpret_cast<uint2*>(out + DH + 16 * db + 4 * g) =
+                    make_uint2(pack_bf16x2(dKt[db][0] * scale, dKt[db][1] * scale),
+                               pack_bf16x2(dKt[db][2] * scale, dKt[db][3] * scale));
+                *reinterpret_cast<uint2*>(out + 2 * DH + 16 * db + 4 * g) =
+                    make_uint2(pack_bf16x2(dVt[db][0], dVt[db][1]), pack_bf16x2(dVt[db][2], dVt[db][3]));
+            }
+        }
+    }
+    __syncthreads();  // the dS tile is complete
+    // Phase 2: query block qb = wave: dQ^T += K^T dS^T over 32 keys per MFMA.
+    if (wave < nb) {
+        const int qb = wave, q = 16 * qb + c16;
+        f32x4 dQt[DH / 16];
+#pragma unroll
+        for (int db = 0; db < DH / 16; ++db) dQt[db] = zero4();
+        const int nk = causal ? 16 * (qb + 1) : 16 * nb;
+        for (int u = 0; 32 * u < nk; ++u) {
+            // dS^T[keys 32 u + 8 g .. + 7][q] = dS[q][...]; key blocks past the
+            // last one were never written and count as zero
+            const int k8 = 32 * u + 8 * g;
+            Frag8<ST> sf;
+            sf.v = __builtin_bit_cast(bf16x8, k8 < 16 * nb ? *reinterpret_cast<const uint4*>(dSs + ds_unit(q, k8) * 16)
+                                                           : make_uint4(0u, 0u, 0u, 0u));
+            u32x4 kt[DH / 16];
+#pragma unroll
+            for (int db = 0; db < DH / 16; ++db) kt[db] = trA_run(Ks, 16 * db, 32 * u);
+            lds_wait();
+#pragma unroll
+            for (int db = 0; db < DH / 16; ++db) {
+                lds_ready(kt[db]);
+                Frag8<ST> fk;
+                fk.v = __builtin_bit_cast(bf16x8, kt[db]);
+                mma8(dQt[db], fk, sf);
+            }
+        }
+        mfma_drain();
+        if (q < n) {
+            ST* out = dQKV + (base + q) * RS;
+#pragma unroll
+            for (int db = 0; db < DH / 16; ++db)
+                *reinterpret_cast<uint2*>(out + 16 * db + 4 * g) =
+                    make_uint2(pack_bf16x2(dQt[db][0] * scale, dQt[db][1] * scale),
+                               pack_bf16x2(dQt[db][2] * scale, dQt[db][3] * scale));
+        }
+    }
+}
+
 template <typename ST>
 int launch_t(const ST* QKV, const ST* dA, const float* lse, const float* D, int BH, int n, int dh, int causal,
              ST* dQKV, int pass, hipStream_t stream) {
     const float scale = 1.0f / sqrtf((float)dh);
     if constexpr (sizeof(ST) == 2) {
+      if (n > 32 && n <= kAttnBwdLdsMaxN) {
+        // both passes in one launch: the second call has nothing left to do
+        if (pass != 0) return 0;
+        auto kern = dh == 64 ? attn_bwd_lds_kernel<64> : attn_bwd_lds_kernel<32>;
+        const size_t lds = dh == 64 ? AttnBwdLds<64>::lds : AttnBwdLds<32>::lds;
+        static bool attr[2] = {false, false};
+        if (!attr[dh == 64]) {
+            if (hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds) !=
+                hipSuccess)
+                return -1;
+            attr[dh == 64] = true;
+        }
+        hipLaunchKernelGGL(kern, dim3(BH), dim3(512), lds, stream, QKV, dA, lse, D, BH, n, causal, scale, dQKV);
+        return hipGetLastError() == hipSuccess ? 0 : -1;
+      }
       if (n > 32) {
         const dim3 grid(BH * ((n + 63) / 64)), block(256);
 #define MOSA_ATTN_BWD_T(KERN, DHV) \

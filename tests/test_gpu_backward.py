@@ -60,6 +60,8 @@ def test_tiny_f32_workload(orc):
     dict(dense_heads=2, dtype="f32", seq_len=130),
     dict(batch=3, seq_len=300, heads=5, k=64),
     dict(batch=1, seq_len=1000, heads=2, k=500, d_model=192),
+    dict(seq_len=256, k=128, d_head=64, d_model=128),
+    dict(seq_len=200, k=100, causal=False),
 ])
 def test_small_shapes(orc, kw):
     check_backward(orc, wl.small(**kw))
