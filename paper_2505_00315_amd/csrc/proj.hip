@@ -68,8 +68,13 @@ struct QkvPolicy {
     }
     __device__ static bool b_kok(const Args&, int, const RowInfo& r, int) { return r.k >= 0; }
     __device__ static void epilogue(const Args& a, int h, int m0, int, const float* Cs, int ldc, int tid, unsigned char*) {
+        epilogue_rows<MT>(a, h, m0, Cs, ldc, tid);
+    }
+    // rows m0 .. m0 + ROWS - 1 of the C tile to their packed Q | K | V rows
+    template <int ROWS>
+    __device__ static void epilogue_rows(const Args& a, int h, int m0, const float* Cs, int ldc, int tid) {
         constexpr int VPR = NT / 8;  // vectors per row
-        for (int v = tid; v < MT * VPR; v += 256) {
+        for (int v = tid; v < ROWS * VPR; v += 256) {
             const int ml = v / VPR, c = (v % VPR) * 8;
             const int m = m0 + ml;
             if (m >= a.M) continue;
@@ -87,15 +92,19 @@ struct QkvPolicy {
 template <int DH>
 struct QkvPolicy2 {
     using ST = uint16_t;
-    static constexpr int MT = 64, NT = 3 * DH, KC = DH == 64 ? 32 : 64, WM = 2, WN = 2, STAGES = 4;
+    static constexpr int MT = 128, NT = 3 * DH, KC = DH == 64 ? 32 : 64, WM = 2, WN = 2, STAGES = 4;
     static constexpr size_t EPI_LDS = 0;
     static constexpr bool A_KCONTIG = true, B_KCONTIG = false;
     using Args = typename QkvPolicy<ST, DH>::Args;
     struct ARef {
         const ST* p;
     };
+    static int mtiles(int M) { return (M + MT - 1) / MT; }
     __device__ static void tile(const Args& a, int logical, int& batch, int& m0, int& n0) {
-        QkvPolicy<ST, DH>::tile(a, logical, batch, m0, n0);
+        const int mt = (a.M + MT - 1) / MT;
+        batch = logical / mt;
+        m0 = (logical % mt) * MT;
+        n0 = 0;
     }
     __device__ static int k_size(const Args& a, int) { return a.d; }
     __device__ static ARef a_row(const Args& a, int h, int m) {
@@ -111,9 +120,9 @@ struct QkvPolicy2 {
         const ST* W = n8 < DH ? a.W0 : (n8 < 2 * DH ? a.W1 : a.W2);
         return W + ((size_t)h * a.d + k) * DH + (n8 % DH);
     }
-    __device__ static void epilogue(const Args& a, int h, int m0, int n0, const float* Cs, int ldc, int tid,
-                                    unsigned char* extra) {
-        QkvPolicy<ST, DH>::epilogue(a, h, m0, n0, Cs, ldc, tid, extra);
+    __device__ static void epilogue(const Args& a, int h, int m0, int, const float* Cs, int ldc, int tid,
+                                    unsigned char*) {
+        QkvPolicy<ST, DH>::template epilogue_rows<MT>(a, h, m0, Cs, ldc, tid);
     }
 };
 
@@ -123,7 +132,7 @@ int run(const ST* X, const int32_t* I, const ST* Wq, const ST* Wk, const ST* Wv,
     using P = QkvPolicy<ST, DH>;
     typename P::Args a{X, I, Wq, Wk, Wv, out, T, d, H, n, B * n, (B * n + P::MT - 1) / P::MT};
     if constexpr (sizeof(ST) == 2) {
-        if (d % QkvPolicy2<DH>::KC == 0) return launch_gemm2<QkvPolicy2<DH>>(a, a.mtiles * H, stream);
+        if (d % QkvPolicy2<DH>::KC == 0) return launch_gemm2<QkvPolicy2<DH>>(a, QkvPolicy2<DH>::mtiles(B * n) * H, stream);
     }
     return launch_gemm<ST, P>(a, a.mtiles * H, stream);
 }
