@@ -163,17 +163,17 @@ __device__ __forceinline__ void wait_vmcnt() {
     __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | 0x0F70);
 }
 
+// One workgroup's tile of logical index `logical`.
 template <class P>
-__global__ __launch_bounds__(256, G2MinWaves<P>::value) void gemm2_kernel(const typename P::Args args) {
+__device__ __forceinline__ void gemm2_body(const typename P::Args& args, int logical, unsigned char* smem) {
     using ST = uint16_t;
     using S = Gemm2Shape<P>;
     constexpr int MT = S::MT, NT = S::NT, KC = S::KC, LPR = S::LPR, STG = S::STAGES;
-    extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int g = lane >> 4, c16 = lane & 15;
     int batch, m0, n0;
-    P::tile(args, xcd_logical_id(blockIdx.x, gridDim.x), batch, m0, n0);
+    P::tile(args, logical, batch, m0, n0);
     const int K = P::k_size(args, batch);
     const int nchunks = S::KG ? (K + KC - 1) / KC : K / KC;
     int2* ktab = reinterpret_cast<int2*>(smem + STG * S::STAGE_BYTES);
@@ -437,6 +437,42 @@ pipeline_done:
     }
 }
 
+template <class P>
+__global__ __launch_bounds__(256, G2MinWaves<P>::value) void gemm2_kernel(const typename P::Args args) {
+    extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
+    gemm2_body<P>(args, xcd_logical_id(blockIdx.x, gridDim.x), smem);
+}
+
+// Two independent GEMMs in one launch (n1 workgroups of P1, the rest P2),
+// mixed on every XCD so that both kinds share its CUs: the blocks an XCD
+// receives (every eighth) are its share of P1 first, in index order, then
+// its share of P2.
+__device__ __forceinline__ void xcd_dual_id(int b, int nb, int n1, int& which, int& idx) {
+    const int x = b % 8, j = b / 8;
+    const int q = nb / 8, r = nb % 8, q1 = n1 / 8, r1 = n1 % 8;
+    const int cnt1 = q1 + (x < r1 ? 1 : 0);
+    const int s1 = x * q1 + (x < r1 ? x : r1);                // P1 blocks on lower XCDs
+    const int sall = x * q + (x < r ? x : r);                // all blocks on lower XCDs
+    if (j < cnt1) {
+        which = 0;
+        idx = s1 + j;
+    } else {
+        which = 1;
+        idx = (sall - s1) + (j - cnt1);
+    }
+}
+
+template <class P1, class P2>
+__global__ __launch_bounds__(256, (G2MinWaves<P1>::value > G2MinWaves<P2>::value ? G2MinWaves<P1>::value
+                                                                                  : G2MinWaves<P2>::value))
+void gemm2_dual_kernel(const typename P1::Args a1, const typename P2::Args a2, int n1) {
+    extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
+    int which, idx;
+    xcd_dual_id(blockIdx.x, gridDim.x, n1, which, idx);
+    if (which == 0) gemm2_body<P1>(a1, idx, smem);
+    else gemm2_body<P2>(a2, idx, smem);
+}
+
 // ktab_rows: rows of the k-row table (gathered k: the padded k range).
 template <class P>
 int launch_gemm2(const typename P::Args& args, int nblocks, hipStream_t stream, int ktab_rows = 0) {
@@ -454,6 +490,33 @@ int launch_gemm2(const typename P::Args& args, int nblocks, hipStream_t stream, 
         }
     }
     hipLaunchKernelGGL(kern, dim3(nblocks), dim3(256), lds, stream, args);
+    return hipGetLastError() == hipSuccess ? 0 : -1;
+}
+
+// Both GEMMs in one launch (see gemm2_dual_kernel); requires every XCD's
+// share of the blocks to hold its share of P1.
+template <class P1, class P2>
+int launch_gemm2_dual(const typename P1::Args& a1, int n1, int rows1, const typename P2::Args& a2, int n2, int rows2,
+                      hipStream_t stream) {
+    if (n1 <= 0) return launch_gemm2<P2>(a2, n2, stream, rows2);
+    if (n2 <= 0) return launch_gemm2<P1>(a1, n1, stream, rows1);
+    const size_t l1 = Gemm2Shape<P1>::lds_bytes(rows1), l2 = Gemm2Shape<P2>::lds_bytes(rows2);
+    const size_t lds = l1 > l2 ? l1 : l2;
+    if (lds > 160 * 1024) return -1;
+    const int nb = n1 + n2;
+    for (int x = 0; x < 8; ++x)  // xcd_dual_id's assumption
+        if (nb / 8 + (x < nb % 8 ? 1 : 0) < n1 / 8 + (x < n1 % 8 ? 1 : 0)) return -1;
+    auto kern = gemm2_dual_kernel<P1, P2>;
+    if (lds > 64 * 1024) {
+        static size_t set = 0;
+        if (lds > set) {
+            if (hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds) !=
+                hipSuccess)
+                return -1;
+            set = lds;
+        }
+    }
+    hipLaunchKernelGGL(kern, dim3(nb), dim3(256), lds, stream, a1, a2, n1);
     return hipGetLastError() == hipSuccess ? 0 : -1;
 }
 

@@ -291,11 +291,8 @@ int mosa_backward_timed(const mosa_shape* s, const void* X, const mosa_weights* 
         e |= launch_attn_bwd(dt, QKV, dA, lse, D, B * H, k, dh, causal, dQKV, 1, stream);
         e |= sm.mark("attn_bwd_q");
         e |= launch_wgrad(dt, X, dY, I, A, dQKV, dz16, B, T, d, H, dh, k, g->dWq, g->dWk, g->dWv, g->dWr, g->dWo,
-                          wpart, 0, stream);
-        e |= sm.mark("wgrad_qkv");
-        e |= launch_wgrad(dt, X, dY, I, A, dQKV, dz16, B, T, d, H, dh, k, g->dWq, g->dWk, g->dWv, g->dWr, g->dWo,
-                          wpart, 1, stream);
-        e |= sm.mark("wgrad_o");
+                          wpart, 2, stream);
+        e |= sm.mark("wgrad");
         e |= launch_dx_proj(dt, dQKV, dz, w->Wq, w->Wk, w->Wv, w->Wr, B, d, H, dh, k, dXs, stream);
         e |= sm.mark("dx_proj");
     }

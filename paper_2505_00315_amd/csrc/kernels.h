@@ -54,7 +54,8 @@ int launch_dattn_out(int dtype, const void* dY, const int32_t* I, const float* r
 int launch_attn_bwd(int dtype, const void* QKV, const void* dA, const float* lse, const float* D, int BH,
                     int n, int dh, int causal, void* dQKV, int pass, hipStream_t stream);
 
-// Weight gradients; which 0: dWq, dWk, dWv (+ dWr when non-null), which 1: dWo.
+// Weight gradients; which 0: dWq, dWk, dWv (+ dWr when non-null), which 1: dWo,
+// which 2: both (in one launch where the gathered-row engine applies).
 // part: fp32 scratch of wgrad_partial_bytes(...) bytes for split row ranges.
 int launch_wgrad(int dtype, const void* X, const void* dY, const int32_t* I, const void* A,
                  const void* dQKV, const void* dz16, int B, int T, int d, int H, int dh, int n, void* dWq,

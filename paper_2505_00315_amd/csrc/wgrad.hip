@@ -421,6 +421,24 @@ int run_o(const ST* dY, const int32_t* I, const ST* A, int B, int T, int d, int 
     return run_o_t<ST, DH, false>(dY, I, A, B, T, d, H, n, dWo, part, stream);
 }
 
+// dW^{Q,K,V,r} and dW^O of the MoSA heads in one launch of the gathered-row
+// engine (the two kinds of workgroups share the CUs); 1: not applicable.
+template <int DH>
+int run_both(const uint16_t* X, const uint16_t* dY, const int32_t* I, const uint16_t* A, const uint16_t* dQKV,
+             const uint16_t* dz16, int B, int T, int d, int H, int n, uint16_t* dWq, uint16_t* dWk, uint16_t* dWv,
+             uint16_t* dWr, uint16_t* dWo, hipStream_t stream) {
+    using ST = uint16_t;
+    using PQ = WgradQkvPolicy2<DH>;
+    using PO = WgradOPolicy2<DH>;
+    const int R = B * n;
+    const int rq = wgrad2_table_rows<PQ>(R, d), ro = wgrad2_table_rows<PO>(R, d);
+    if (!rq || !ro) return 1;
+    typename PQ::Args aq{X, I, dQKV, dz16, dWq, dWk, dWv, dWr, nullptr, T, d, H, n, R, d / 64, 1, 0, make_fastdiv(n)};
+    typename PO::Args ao{dY, I, A, dWo, nullptr, T, d, H, n, R, d / 64, 1, 0, make_fastdiv(n)};
+    const int e = launch_gemm2_dual<PQ, PO>(aq, H * (d / 64), rq, ao, H * (d / 64), ro, stream);
+    return e == -1 ? 1 : e;  // a shape the grouped launch cannot take falls back to two launches
+}
+
 // Bytes of fp32 partial sums the two launches of one head group need.
 template <typename ST, int DH>
 size_t partial_bytes(int B, int d, int H, int n, bool router) {
@@ -447,6 +465,20 @@ int launch_wgrad(int dtype, const void* X, const void* dY, const int32_t* I, con
                  const void* dz16, int B, int T, int d, int H, int dh, int n, void* dWq, void* dWk, void* dWv,
                  void* dWr, void* dWo, float* part, int which, hipStream_t stream) {
     if (H == 0) return 0;
+    if (which == 2) {
+        // both: one launch on the gathered-row engine where it applies
+        if (dtype == kBF16 && I) {
+            using ST = uint16_t;
+            auto both = dh == 64 ? run_both<64> : run_both<32>;
+            const int e = both((const ST*)X, (const ST*)dY, I, (const ST*)A, (const ST*)dQKV, (const ST*)dz16, B, T, d,
+                               H, n, (ST*)dWq, (ST*)dWk, (ST*)dWv, (ST*)dWr, (ST*)dWo, stream);
+            if (e != 1) return e;
+        }
+        const int e0 = launch_wgrad(dtype, X, dY, I, A, dQKV, dz16, B, T, d, H, dh, n, dWq, dWk, dWv, dWr, dWo, part,
+                                    0, stream);
+        return e0 | launch_wgrad(dtype, X, dY, I, A, dQKV, dz16, B, T, d, H, dh, n, dWq, dWk, dWv, dWr, dWo, part, 1,
+                                 stream);
+    }
     if (dtype == kBF16) {
         using ST = uint16_t;
         if (which == 0) {

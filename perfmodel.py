@@ -58,9 +58,10 @@ def stage_work(w, with_backward=True):
         add("bwd_out", X + H * dh * d * es + 2 * rows * dh * es + rows * 16, 2.0 * rows * d * dh)
         add("attn_bwd_kv", 6 * rows * dh * es + rows * 8, 8.0 * dh * _pairs(k, w.causal) * B * H)
         add("attn_bwd_q", 5 * rows * dh * es + rows * 8, 6.0 * dh * _pairs(k, w.causal) * B * H)
-        add("wgrad_qkv", X + 3 * rows * dh * es + rows * 4 + 3 * H * d * dh * es + H * d * es,
-            2.0 * rows * d * (3 * dh + 1))
-        add("wgrad_o", X + rows * dh * es + rows * 4 + H * dh * d * es, 2.0 * rows * dh * d)
+        # dW^{Q,K,V,r} and dW^O (one grouped launch): X and dY read, the
+        # selected rows' dQ|dK|dV and r A, I, the gradients written once
+        add("wgrad", 2 * X + 4 * rows * dh * es + rows * 4 + 4 * H * d * dh * es + H * d * es,
+            2.0 * rows * d * (3 * dh + 1) + 2.0 * rows * dh * d)
     if Hd:
         R = B * Hd * T
         add("bwd_out_dense", X + Hd * dh * d * es + 2 * R * dh * es + R * 4, 2.0 * R * d * dh)
@@ -152,8 +153,8 @@ STAGE_KERNELS = {
     "bwd_out": (r"BwdOutPolicy",),
     "attn_bwd_kv": (r"attn_bwd_kv",),
     "attn_bwd_q": (r"attn_bwd_q",),
-    "wgrad_qkv": (r"WgradQkvPolicy", r"wgrad_qkv_reduce"),
-    "wgrad_o": (r"WgradOPolicy", r"wgrad_o_reduce"),
+    "wgrad": (r"WgradQkvPolicy<[^>]*, true, true>", r"WgradQkvPolicy2", r"WgradOPolicy<[^>]*, true>",
+              r"WgradOPolicy2", r"wgrad_qkv_reduce", r"wgrad_o_reduce"),
     "dx_scatter": (r"DxProj\w*Policy", r"DxCombinePolicy", r"combine_rows_kernel<[^>]*, 1>"),
 }
 
