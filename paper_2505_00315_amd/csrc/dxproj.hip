@@ -13,9 +13,9 @@
 //              K = Hd * 3 dh, then the MoSA rows of each token added in head
 //              order from the slot map (bitwise reproducible), then written.
 #include "combine.h"
+#include "dxrow.h"
 #include "gemm.h"
 #include "kernels.h"
-#include "rowgemm.h"
 
 namespace mosa {
 
@@ -155,69 +155,17 @@ struct DxCombinePolicy {
     }
 };
 
-// bf16 storage, d a multiple of the column block: the row-streaming kernel (rowgemm.h);
-// the three weights' rows for 256 columns of dX held in registers, the packed
-// dQ | dK | dV rows streamed, dz through LDS for the rank-1 router term.
-template <int DH>
-struct DxProjRowPolicy {
-    using ST = uint16_t;
-    static constexpr int K = 3 * DH, NPAIR = 1, STAGES = 3;
-    static constexpr bool W_KCONTIG = true, ROW_SCALAR = true;
-    struct Args {
-        const ST* dQKV;  // [B, H, k, 3*DH]
-        const float* dz; // [B, H, k]
-        const ST* Wq;
-        const ST* Wk;
-        const ST* Wv;    // [H, d, DH]
-        const ST* Wr;    // [H, d]
-        ST* dXs;         // [B, H, k, d]
-        int d, H, k, M, ntiles, tiles, per, splits, out_bytes;
-    };
-    __device__ static void tile(const Args& a, int logical, int& h, int& n0, int& s_beg, int& s_end) {
-        const int unit = logical / a.splits, sp = logical % a.splits;
-        h = unit / a.ntiles;
-        n0 = (unit % a.ntiles) * (128 * NPAIR);
-        s_beg = sp * a.per;
-        s_end = min(a.tiles, s_beg + a.per);
-    }
-    __device__ static int rows(const Args& a) { return a.M; }
-    __device__ static size_t ridx(const Args& a, int h, int m) {
-        return ((size_t)(m / a.k) * a.H + h) * a.k + (m % a.k);
-    }
-    __device__ static const ST* a_row(const Args& a, int h, int m) { return a.dQKV + ridx(a, h, m) * (3 * DH); }
-    // W[k][n] = W^{k / DH}_h[n][k % DH]: 8 consecutive k of column n
-    __device__ static const ST* w_kptr(const Args& a, int h, int n, int k) {
-        const ST* W = k < DH ? a.Wq : (k < 2 * DH ? a.Wk : a.Wv);
-        return W + ((size_t)h * a.d + n) * DH + (k % DH);
-    }
-    __device__ static const float* z_ptr(const Args& a, int h, int m) { return a.dz + ridx(a, h, m); }
-    __device__ static void col_init(const Args& a, int h, int n, float (&cv)[8]) {
-        vec8_to_f32<ST>(vec8_load<ST>(a.Wr + (size_t)h * a.d + n), cv);
-    }
-    __device__ static __amdgpu_buffer_rsrc_t out_rsrc(const Args& a, int) {
-        return __builtin_amdgcn_make_buffer_rsrc(a.dXs, 0, a.out_bytes, 0x00020000);
-    }
-    __device__ static int out_row(const Args& a, int h, int m) { return (int)(ridx(a, h, m) * a.d * 2); }
-    __device__ static void finish(float (&x)[8], float z, const float (&cv)[8]) {
-#pragma unroll
-        for (int j = 0; j < 8; ++j) x[j] += z * cv[j];
-    }
-};
-
 template <typename ST, int DH>
 int run_proj(const ST* dQKV, const float* dz, const ST* Wq, const ST* Wk, const ST* Wv, const ST* Wr, int B, int d,
              int H, int k, ST* dXs, hipStream_t stream) {
     using P = DxProjPolicy<ST, DH>;
     const int M = B * k;
     if constexpr (sizeof(ST) == 2) {
-        const long long out_bytes = (long long)M * H * d * 2;
         using R = DxProjRowPolicy<DH>;
-        if (d % (128 * R::NPAIR) == 0 && out_bytes < (1ll << 31)) {
-            const int ntiles = d / (128 * R::NPAIR), tiles = (M + 63) / 64;
-            const int per = rowgemm_tiles_per_wg(H * ntiles, tiles, 512), splits = (tiles + per - 1) / per;
-            typename R::Args ra{dQKV, dz, Wq, Wk, Wv, Wr, dXs, d, H, k, M, ntiles, tiles, per, splits, (int)out_bytes};
-            return launch_rowgemm<R>(ra, H * ntiles * splits, stream);
-        }
+        typename R::Args ra;
+        int nblocks;
+        if (dx_row_args<DH>(dQKV, dz, Wq, Wk, Wv, Wr, B, d, H, k, dXs, ra, nblocks))
+            return launch_rowgemm<R>(ra, nblocks, stream);
     }
     typename P::Args a{dQKV, dz, Wq, Wk, Wv, Wr, dXs, d, H, k, M, (M + P::MT - 1) / P::MT, (d + P::NT - 1) / P::NT};
     return launch_gemm<ST, P>(a, H * a.mtiles * a.ntiles, stream);

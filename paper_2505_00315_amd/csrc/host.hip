@@ -290,11 +290,18 @@ int mosa_backward_timed(const mosa_shape* s, const void* X, const mosa_weights* 
         e |= sm.mark("attn_bwd_kv");
         e |= launch_attn_bwd(dt, QKV, dA, lse, D, B * H, k, dh, causal, dQKV, 1, stream);
         e |= sm.mark("attn_bwd_q");
-        e |= launch_wgrad(dt, X, dY, I, A, dQKV, dz16, B, T, d, H, dh, k, g->dWq, g->dWk, g->dWv, g->dWr, g->dWo,
-                          wpart, 2, stream);
-        e |= sm.mark("wgrad");
-        e |= launch_dx_proj(dt, dQKV, dz, w->Wq, w->Wk, w->Wv, w->Wr, B, d, H, dh, k, dXs, stream);
-        e |= sm.mark("dx_proj");
+        // untimed: the weight gradients and the dX rows in one grouped launch
+        const int grouped = ev ? 1
+                               : launch_bwd_proj(dt, X, dY, I, A, dQKV, dz16, dz, w->Wq, w->Wk, w->Wv, w->Wr, B, T, d,
+                                                 H, dh, k, g->dWq, g->dWk, g->dWv, g->dWr, g->dWo, dXs, stream);
+        if (grouped < 0) e |= 1;
+        if (grouped == 1) {
+            e |= launch_wgrad(dt, X, dY, I, A, dQKV, dz16, B, T, d, H, dh, k, g->dWq, g->dWk, g->dWv, g->dWr,
+                              g->dWo, wpart, 2, stream);
+            e |= sm.mark("wgrad");
+            e |= launch_dx_proj(dt, dQKV, dz, w->Wq, w->Wk, w->Wv, w->Wr, B, d, H, dh, k, dXs, stream);
+            e |= sm.mark("dx_proj");
+        }
     }
     if (Hd > 0) {
         e |= launch_dattn_out(dt, dY, nullptr, nullptr, w->Wo_d, Ad, B, T, d, Hd, dh, T, dAd, Dd, nullptr, nullptr,

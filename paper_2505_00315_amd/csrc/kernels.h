@@ -61,6 +61,12 @@ int launch_wgrad(int dtype, const void* X, const void* dY, const int32_t* I, con
                  const void* dQKV, const void* dz16, int B, int T, int d, int H, int dh, int n, void* dWq,
                  void* dWk, void* dWv, void* dWr, void* dWo, float* part, int which, hipStream_t stream);
 size_t wgrad_partial_bytes(int dtype, int B, int d, int H, int dh, int n, int router);
+// The MoSA heads' dW^{Q,K,V,r}, dW^O and per-head dX rows (launch_dx_proj) in
+// one grouped launch; returns 1, launching nothing, where that does not apply.
+int launch_bwd_proj(int dtype, const void* X, const void* dY, const int32_t* I, const void* A, const void* dQKV,
+                    const void* dz16, const float* dz, const void* Wq, const void* Wk, const void* Wv, const void* Wr,
+                    int B, int T, int d, int H, int dh, int n, void* dWq, void* dWk, void* dWv, void* dWr, void* dWo,
+                    void* dXs, hipStream_t stream);
 
 // dXs[b,h,i,:] = dQ Wq^T + dK Wk^T + dV Wv^T + dz Wr  (per selected row).
 int launch_dx_proj(int dtype, const void* dQKV, const float* dz, const void* Wq, const void* Wk,

@@ -77,17 +77,17 @@ struct RowGemmShape {
     }
 };
 
+// One workgroup's run of row tiles, logical index `logical`.
 template <class P>
-__global__ __launch_bounds__(256) void rowgemm_kernel(const typename P::Args args) {
+__device__ __forceinline__ void rowgemm_body(const typename P::Args& args, int logical, unsigned char* smem) {
     using ST = uint16_t;
     using S = RowGemmShape<P>;
     constexpr int K = S::K, LPR = S::LPR, SLAB = S::SLAB, KS = S::KS, STG = S::STG, NB = S::NB, NC = S::NC;
-    extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int g = lane >> 4, c16 = lane & 15;
     int h, n0, s_beg, s_end;
-    P::tile(args, xcd_logical_id(blockIdx.x, gridDim.x), h, n0, s_beg, s_end);
+    P::tile(args, logical, h, n0, s_beg, s_end);
     const int nsteps = s_end - s_beg, M = P::rows(args);
     const int wcol = n0 + 32 * S::NPAIR * wave;            // this wave's columns
     const int icol = 8 * (c16 >> 2) + (c16 & 3);           // column of MFMA row c16 in a block pair
@@ -243,6 +243,12 @@ __global__ __launch_bounds__(256) void rowgemm_kernel(const typename P::Args arg
                 if (pass(s0, std::false_type{})) break;
     }
     wait_vmcnt<0>();
+}
+
+template <class P>
+__global__ __launch_bounds__(256) void rowgemm_kernel(const typename P::Args args) {
+    extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
+    rowgemm_body<P>(args, xcd_logical_id(blockIdx.x, gridDim.x), smem);
 }
 
 // Splits the row tiles of every (head, column block) over workgroups so that

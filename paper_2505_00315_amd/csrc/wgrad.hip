@@ -17,8 +17,10 @@
 // the S partials in range order (still reproducible).
 #include <algorithm>
 
+#include "dxrow.h"
 #include "gemm.h"
 #include "gemm2.h"
+#include "group.h"
 #include "kernels.h"
 
 namespace mosa {
@@ -439,6 +441,28 @@ int run_both(const uint16_t* X, const uint16_t* dY, const int32_t* I, const uint
     return e == -1 ? 1 : e;  // a shape the grouped launch cannot take falls back to two launches
 }
 
+// The three products after the attention backward in one launch: dW^{Q,K,V,r},
+// dW^O and the per-head dX rows; 1: not applicable.
+template <int DH>
+int run_bwd_proj(const uint16_t* X, const uint16_t* dY, const int32_t* I, const uint16_t* A, const uint16_t* dQKV,
+                 const uint16_t* dz16, const float* dz, const uint16_t* Wq, const uint16_t* Wk, const uint16_t* Wv,
+                 const uint16_t* Wr, int B, int T, int d, int H, int n, uint16_t* dWq, uint16_t* dWk, uint16_t* dWv,
+                 uint16_t* dWr, uint16_t* dWo, uint16_t* dXs, hipStream_t stream) {
+    using PQ = WgradQkvPolicy2<DH>;
+    using PO = WgradOPolicy2<DH>;
+    using PX = DxProjRowPolicy<DH>;
+    const int R = B * n;
+    const int rq = wgrad2_table_rows<PQ>(R, d), ro = wgrad2_table_rows<PO>(R, d);
+    typename PX::Args ax;
+    int nx;
+    if (!rq || !ro || !dx_row_args<DH>(dQKV, dz, Wq, Wk, Wv, Wr, B, d, H, n, dXs, ax, nx)) return 1;
+    typename PQ::Args aq{X, I, dQKV, dz16, dWq, dWk, dWv, dWr, nullptr, T, d, H, n, R, d / 64, 1, 0, make_fastdiv(n)};
+    typename PO::Args ao{dY, I, A, dWo, nullptr, T, d, H, n, R, d / 64, 1, 0, make_fastdiv(n)};
+    return launch_group3<Gemm2Job<PQ>, Gemm2Job<PO>, RowGemmJob<PX>>(
+        aq, H * (d / 64), Gemm2Job<PQ>::lds(rq), ao, H * (d / 64), Gemm2Job<PO>::lds(ro), ax, nx,
+        RowGemmJob<PX>::lds(0), stream);
+}
+
 // Bytes of fp32 partial sums the two launches of one head group need.
 template <typename ST, int DH>
 size_t partial_bytes(int B, int d, int H, int n, bool router) {
@@ -497,6 +521,18 @@ int launch_wgrad(int dtype, const void* X, const void* dY, const int32_t* I, con
     }
     auto f = dh == 64 ? run_o<ST, 64> : run_o<ST, 32>;
     return f((const ST*)dY, I, (const ST*)A, B, T, d, H, n, (ST*)dWo, part, stream);
+}
+
+int launch_bwd_proj(int dtype, const void* X, const void* dY, const int32_t* I, const void* A, const void* dQKV,
+                    const void* dz16, const float* dz, const void* Wq, const void* Wk, const void* Wv, const void* Wr,
+                    int B, int T, int d, int H, int dh, int n, void* dWq, void* dWk, void* dWv, void* dWr, void* dWo,
+                    void* dXs, hipStream_t stream) {
+    if (dtype != kBF16 || H == 0 || !I) return 1;
+    using ST = uint16_t;
+    auto f = dh == 64 ? run_bwd_proj<64> : run_bwd_proj<32>;
+    return f((const ST*)X, (const ST*)dY, I, (const ST*)A, (const ST*)dQKV, (const ST*)dz16, dz, (const ST*)Wq,
+             (const ST*)Wk, (const ST*)Wv, (const ST*)Wr, B, T, d, H, n, (ST*)dWq, (ST*)dWk, (ST*)dWv, (ST*)dWr,
+             (ST*)dWo, (ST*)dXs, stream);
 }
 
 size_t wgrad_partial_bytes(int dtype, int B, int d, int H, int dh, int n, int router) {
