@@ -159,6 +159,9 @@ STAGE_KERNELS = {
 }
 
 
+GROUPED_KERNEL = r"group3_kernel"
+
+
 def _read_counter_csv(run_dir):
     import csv
     import glob
@@ -183,14 +186,19 @@ def traffic_summary(fetch_dir, write_dir, copy_bytes):
     w_scale = copy_bytes / (float(write[-1]["Counter_Value"]) * 1024.0)
     out = {}
     for rows, key, scale in ((fetch, "fetch", f_scale), (write, "write", w_scale)):
-        steps = sum(1 for r in rows if re.search(STAGE_KERNELS["router"][0], r["Kernel_Name"]))
         for stage, pats in STAGE_KERNELS.items():
-            kib = sum(float(r["Counter_Value"]) for r in rows[:-1]
-                      if any(re.search(p, r["Kernel_Name"]) for p in pats))
-            if steps and kib:
+            # grouped launches (several stages' work in one kernel) are left out;
+            # a stage's launches = its dispatches / the distinct kernels it runs
+            hit = [r for r in rows[:-1] if not re.search(GROUPED_KERNEL, r["Kernel_Name"])
+                   and any(re.search(p, r["Kernel_Name"]) for p in pats)]
+            if not hit:
+                continue
+            launches = len(hit) / len({r["Kernel_Name"] for r in hit})
+            kib = sum(float(r["Counter_Value"]) for r in hit)
+            if kib:
                 d = out.setdefault(stage, {})
-                d[key + "_kib"] = kib / steps
-                d[key + "_bytes"] = kib / steps * 1024.0 * scale
+                d[key + "_kib"] = kib / launches
+                d[key + "_bytes"] = kib / launches * 1024.0 * scale
     for d in out.values():
         d["hbm_bytes_per_launch"] = d.get("fetch_bytes", 0.0) + d.get("write_bytes", 0.0)
     return out, f_scale, w_scale
