@@ -18,6 +18,7 @@
 // row; r = 1 for dense heads) and lse = m + log(l) (fp32, natural log).
 #include "common.h"
 #include "gemm.h"
+#include "attn_lds.h"
 #include "gemm2.h"
 #include "kernels.h"
 #include "tiles.h"
@@ -258,22 +259,10 @@ __global__ __launch_bounds__(256) void attn_fwd_tiled_kernel(const ST* __restric
 }
 
 // bf16, n <= 128: one workgroup of 8 waves per (b, h), one block of 16
-// queries per wave.  K and V of all n keys go into LDS once, by direct
-// global->LDS loads (K rows with XOR-permuted 16-byte units for
+// queries per wave (attn_lds.h).  K and V of all n keys go into LDS once, by
+// direct global->LDS loads (K rows with XOR-permuted 16-byte units for
 // ds_read_b128, V rows as in memory, units permuted per key row, for
-// transposed reads); each wave's Q rows are loaded meanwhile.  A wave keeps
-// the scores of all keys of its block in registers (S^T = K Q^T, lane =
-// query), takes the row maximum and sum once, and accumulates
-// O^T += V^T P^T 32 keys per MFMA with V^T read by ds_read_b64_tr_b16 in the
-// key order of the P^T registers.
-constexpr int kAttnLdsMaxN = 128;
-
-template <int U>
-__device__ __forceinline__ int vt_swz(int k) {  // V tile unit permutation (an involution per row)
-    if constexpr (U == 8) return 2 * ((k >> 1) & 3);
-    else return 2 * ((k >> 2) & 1);
-}
-
+// transposed reads); each wave's Q rows are loaded meanwhile.
 template <int DH>
 __global__ __launch_bounds__(512) void attn_fwd_lds_kernel(const uint16_t* __restrict__ QKV, int BH, int n, int causal,
                                                            float scale, const float* __restrict__ rw,
@@ -303,98 +292,15 @@ __global__ __launch_bounds__(512) void attn_fwd_lds_kernel(const uint16_t* __res
             lds_load16(Vp + row + 8 * (pos ^ vt_swz<U>(key)), base + TILE + 1024 * NW * j);
         }
     }
-    const int nqb = (n + 15) / 16, qb = wave, q0 = 16 * qb, q = q0 + c16;
+    const int nqb = (n + 15) / 16, qb = wave, q = 16 * qb + c16;
     Frag8<ST> qf[DH / 32];
 #pragma unroll
     for (int st = 0; st < DH / 32; ++st) qf[st] = frag8_load<ST>(Qp + (size_t)min(q, n - 1) * RS + st * 32 + 8 * g);
     wait_vmcnt<0>();
     __syncthreads();
     if (qb >= nqb) return;
-    const unsigned char* Ks = smem;
-    const unsigned char* Vs = smem + TILE;
-    {
-        const int nkb = causal ? qb + 1 : nqb;
-
-        // S^T for every key block: lane = query c16, rows = keys 16 sb + 4 g + i
-        f32x4 s[NMAX / 16];
-        float m = -__builtin_inff();
-#pragma unroll
-        for (int sb = 0; sb < NMAX / 16; ++sb) {
-            s[sb] = zero4();
-            if (sb < nkb) {
-                const int row = 16 * sb + c16;
-#pragma unroll
-                for (int st = 0; st < DH / 32; ++st) {
-                    const int u = 4 * st + g;
-                    Frag8<ST> kf;
-                    kf.v = __builtin_bit_cast(
-                        bf16x8, *reinterpret_cast<const uint4*>(Ks + (row * U + (u ^ kswz(row, U))) * 16));
-                    mma8(s[sb], kf, qf[st]);
-                }
-#pragma unroll
-                for (int i = 0; i < 4; ++i) {
-                    const int key = 16 * sb + 4 * g + i;
-                    const bool ok = key < n && (!causal || key <= q);
-                    s[sb][i] = ok ? s[sb][i] * scale : -__builtin_inff();
-                    m = fmaxf(m, s[sb][i]);
-                }
-            }
-        }
-        m = fmaxf(m, __shfl_xor(m, 16, 64));
-        m = fmaxf(m, __shfl_xor(m, 32, 64));
-        float l = 0.f;
-#pragma unroll
-        for (int sb = 0; sb < NMAX / 16; ++sb)
-#pragma unroll
-            for (int i = 0; i < 4; ++i) {
-                s[sb][i] = sb < nkb ? expf(s[sb][i] - m) : 0.f;  // key 0 is allowed for every query: m finite
-                l += s[sb][i];
-            }
-        l += __shfl_xor(l, 16, 64);
-        l += __shfl_xor(l, 32, 64);
-
-        // O^T += V^T P^T, 32 keys per MFMA: slots 0..3 = keys 32 u + 4 g + i,
-        // slots 4..7 = keys 32 u + 16 + 4 g + i (the P^T registers as they are)
-        f32x4 o[DH / 16];
-#pragma unroll
-        for (int db = 0; db < DH / 16; ++db) o[db] = zero4();
-#pragma unroll
-        for (int uu = 0; uu < NMAX / 32; ++uu) {
-            if (2 * uu < nkb) {
-                const float pv[8] = {s[2 * uu][0], s[2 * uu][1], s[2 * uu][2], s[2 * uu][3],
-                                     s[2 * uu + 1][0], s[2 * uu + 1][1], s[2 * uu + 1][2], s[2 * uu + 1][3]};
-                const Frag8<ST> pf = frag8_from<ST>(pv);
-                u32x4 vt[DH / 16];
-#pragma unroll
-                for (int db = 0; db < DH / 16; ++db) {
-                    const int mcol = 16 * db + 4 * (c16 & 3), un = mcol >> 3, half = (mcol >> 2) & 1;
-                    const int k0 = 32 * uu + 4 * g + (c16 >> 2), k1 = k0 + 16;
-                    const u32x2 lo = lds_read_tr16(Vs + (k0 * U + (un ^ vt_swz<U>(k0))) * 16 + 8 * half);
-                    const u32x2 hi = lds_read_tr16(Vs + (k1 * U + (un ^ vt_swz<U>(k1))) * 16 + 8 * half);
-                    vt[db] = u32x4{lo.x, lo.y, hi.x, hi.y};
-                }
-                lds_wait();
-#pragma unroll
-                for (int db = 0; db < DH / 16; ++db) {
-                    lds_ready(vt[db]);
-                    Frag8<ST> vf;
-                    vf.v = __builtin_bit_cast(bf16x8, vt[db]);
-                    mma8(o[db], vf, pf);
-                }
-            }
-        }
-        mfma_drain();
-        // lane: query c16, d = 16 db + 4 g + i
-        if (q < n) {
-            const float inv = (rw ? rw[(size_t)bh * n + q] : 1.f) / l;
-            ST* Ap = A + ((size_t)bh * n + q) * DH;
-#pragma unroll
-            for (int db = 0; db < DH / 16; ++db)
-                *reinterpret_cast<uint2*>(Ap + 16 * db + 4 * g) =
-                    make_uint2(pack_bf16x2(o[db][0] * inv, o[db][1] * inv), pack_bf16x2(o[db][2] * inv, o[db][3] * inv));
-            if (g == 0) lse[(size_t)bh * n + q] = m + logf(l);
-        }
-    }
+    attn_lds_block<DH>(smem, smem + TILE, 0, qf, n, causal, scale, qb, rw ? rw + (size_t)bh * n : nullptr,
+                       A + (size_t)bh * n * DH, lse + (size_t)bh * n);
 }
 
 template <typename ST>

@@ -11,10 +11,22 @@
 //   D (16x16, fp32)    lane l holds column l % 16, rows 4 g + i (i = 0..3).
 #pragma once
 
+#include <type_traits>
+
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
 namespace mosa {
+
+// f(std::integral_constant<int, I>) for I = B .. E - 1, each I a constant
+// expression in f (immediate offsets, template arguments).
+template <int B, int E, class F>
+__device__ __forceinline__ void static_for(F&& f) {
+    if constexpr (B < E) {
+        f(std::integral_constant<int, B>{});
+        static_for<B + 1, E>(f);
+    }
+}
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef short s16x4 __attribute__((ext_vector_type(4)));

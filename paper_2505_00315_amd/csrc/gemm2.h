@@ -78,6 +78,15 @@ __device__ __forceinline__ u32x2 lds_read_tr16(const unsigned char* p) {
     asm volatile("ds_read_b64_tr_b16 %0, %1" : "=v"(r) : "v"(off) : "memory");
     return r;
 }
+// The same at p + OFF bytes (the instruction's immediate offset).
+template <int OFF>
+__device__ __forceinline__ u32x2 lds_read_tr16_at(const unsigned char* p) {
+    static_assert(OFF >= 0 && OFF < 65536, "ds offset field");
+    const uint32_t off = (uint32_t)(size_t)(lds_u8*)p;
+    u32x2 r;
+    asm volatile("ds_read_b64_tr_b16 %0, %1 offset:%2" : "=v"(r) : "v"(off), "i"(OFF) : "memory");
+    return r;
+}
 // Wait for every outstanding LDS read of this wave.
 __device__ __forceinline__ void lds_wait() { asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory"); }
 // Wait until at most N LDS operations of this wave are outstanding (LDS

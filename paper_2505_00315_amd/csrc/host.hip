@@ -207,10 +207,17 @@ int mosa_forward_timed(const mosa_shape* s, const void* X, const mosa_weights* w
         e |= launch_select(dt, z, xnorm, X, w->Wr, B, T, d, H, k, I, r, slot, at<int32_t>(scratch, L.unc_tok),
                            at<double>(scratch, L.unc_key), at<int32_t>(scratch, L.unc_sel), stream);
         e |= sm.mark("select");
-        e |= launch_qkv(dt, X, I, w->Wq, w->Wk, w->Wv, B, T, d, H, dh, k, QKV, stream);
-        e |= sm.mark("qkv");
-        e |= launch_attn_fwd(dt, QKV, r, B * H, k, dh, causal, A, lse, stream);
-        e |= sm.mark("attn");
+        const int fused = launch_qkv_attn(dt, X, I, w->Wq, w->Wk, w->Wv, B, T, d, H, dh, k, QKV, r, causal, A, lse,
+                                          stream);
+        if (fused == 1) {
+            e |= launch_qkv(dt, X, I, w->Wq, w->Wk, w->Wv, B, T, d, H, dh, k, QKV, stream);
+            e |= sm.mark("qkv");
+            e |= launch_attn_fwd(dt, QKV, r, B * H, k, dh, causal, A, lse, stream);
+            e |= sm.mark("attn");
+        } else {
+            e |= fused;
+            e |= sm.mark("qkv_attn");
+        }
         e |= launch_out_proj(dt, A, w->Wo, B, d, H, dh, k, Xo, stream);
         e |= sm.mark("out_proj");
     }

@@ -31,6 +31,12 @@ int launch_qkv(int dtype, const void* X, const int32_t* I, const void* Wq, const
 // A = diag(r) softmax(Q K^T / sqrt(dh) + causal mask in slot order) V per
 // (b,h) (r == nullptr: r = 1); lse = log-sum-exp of the scaled scores
 // (natural log).
+// Q/K/V projection and attention in one launch for bf16 groups of
+// n = 16, 32, 64 or 128 rows (the outputs of launch_qkv and launch_attn_fwd);
+// returns 1 without launching when the shape does not qualify.
+int launch_qkv_attn(int dtype, const void* X, const int32_t* I, const void* Wq, const void* Wk, const void* Wv,
+                    int B, int T, int d, int H, int dh, int n, void* QKV, const float* r, int causal, void* A,
+                    float* lse, hipStream_t stream);
 int launch_attn_fwd(int dtype, const void* QKV, const float* r, int BH, int n, int dh, int causal, void* A,
                     float* lse, hipStream_t stream);
 

@@ -10,6 +10,7 @@
 // token, so the attention kernels read each token's q, k, v from one row.
 // Workgroups of one head are numbered consecutively on one XCD so the head's
 // weights are fetched from HBM once into that XCD's L2.
+#include "attn_lds.h"
 #include "gemm.h"
 #include "gemm2.h"
 #include "kernels.h"
@@ -126,6 +127,73 @@ struct QkvPolicy2 {
     }
 };
 
+// QKV projection and attention in one kernel, for groups of n | 128 rows
+// (n = 16, 32, 64 or 128): every 128-row tile holds whole (b, h) groups, so
+// after the epilogue has written the packed Q | K | V rows (kept for the
+// backward pass), the same workgroup copies the tile's K and V in bf16 into
+// LDS, takes Q from the C tile, and runs the attention of its groups
+// (attn_lds.h, bit-identical to the separate attention kernel).
+template <int DH>
+struct QkvAttnPolicy : QkvPolicy2<DH> {
+    using ST = uint16_t;
+    using Base = QkvPolicy2<DH>;
+    static constexpr int MT = Base::MT, U = DH / 8, KROWS = MT, VROWS = MT + 16;
+    // bf16 K tile, then the V tile with 16 zero rows after it (the last
+    // group's odd key block reads 16 rows past its end, at weight zero)
+    static constexpr size_t EPI_LDS = (size_t)(KROWS + VROWS) * DH * 2;
+    static_assert(MT == 128 && Base::WM * Base::WN == 4, "two query blocks per wave");
+    struct Args : QkvPolicy<ST, DH>::Args {
+        const float* r;  // [B, H, n] router weights of the selected rows
+        ST* A;           // [B, H, n, DH]
+        float* lse;      // [B, H, n]
+        int causal;
+        float scale;
+    };
+    __device__ static void epilogue(const Args& a, int h, int m0, int, const float* Cs, int ldc, int tid,
+                                    unsigned char* extra) {
+        constexpr int VPR = 3 * U;  // 16-byte vectors per packed row
+        unsigned char* Ks = extra;
+        unsigned char* Vs = extra + (size_t)KROWS * DH * 2;
+        for (int v = tid; v < MT * VPR; v += 256) {
+            const int ml = v / VPR, u = v % VPR, m = m0 + ml;
+            float x[8];
+            cs_load8(Cs, ldc, ml, 8 * u, x);
+            const uint4 y = vec8_from_f32<ST>(x).v;
+            if (m < a.M) {
+                const int b = m / a.n, i = m % a.n;
+                *reinterpret_cast<uint4*>(a.out + (((size_t)b * a.H + h) * a.n + i) * (3 * DH) + 8 * u) = y;
+            }
+            // rows past M hold the clamped last row's values: finite, never used
+            if (u >= 2 * U)
+                *reinterpret_cast<uint4*>(Vs + (ml * U + ((u - 2 * U) ^ vt_swz<U>(ml))) * 16) = y;
+            else if (u >= U)
+                *reinterpret_cast<uint4*>(Ks + (ml * U + ((u - U) ^ kswz(ml, U))) * 16) = y;
+        }
+        for (int v = tid; v < (VROWS - MT) * U; v += 256)
+            *reinterpret_cast<uint4*>(Vs + (size_t)(MT * U + v) * 16) = make_uint4(0, 0, 0, 0);
+        __syncthreads();
+
+        // MT / 16 = 8 query blocks over 4 waves: blocks w and 7 - w, so that
+        // every wave's causal key blocks add up to the same count
+        const int wave = tid >> 6, lane = tid & 63, g = lane >> 4, c16 = lane & 15;
+        const int n = a.n, nqb = n / 16;
+        for (int j2 = 0; j2 < 2; ++j2) {
+            const int j = j2 ? 7 - wave : wave, gi = j / nqb, qb = j % nqb, mg = m0 + gi * n;
+            if (mg >= a.M) continue;
+            const size_t bh = (size_t)(mg / n) * a.H + h;
+            Frag8<ST> qf[DH / 32];
+#pragma unroll
+            for (int st = 0; st < DH / 32; ++st) {
+                float x[8];
+                cs_load8(Cs, ldc, gi * n + 16 * qb + c16, 32 * st + 8 * g, x);
+                qf[st] = frag8_from<ST>(x);
+            }
+            attn_lds_block<DH>(Ks, Vs, gi * n, qf, n, a.causal, a.scale, qb, a.r ? a.r + bh * n : nullptr,
+                               a.A + bh * n * DH, a.lse + bh * n);
+        }
+    }
+};
+
 template <typename ST, int DH>
 int run(const ST* X, const int32_t* I, const ST* Wq, const ST* Wk, const ST* Wv, int B, int T, int d, int H, int n,
         ST* out, hipStream_t stream) {
@@ -138,6 +206,29 @@ int run(const ST* X, const int32_t* I, const ST* Wq, const ST* Wk, const ST* Wv,
 }
 
 }  // namespace
+
+int launch_qkv_attn(int dtype, const void* X, const int32_t* I, const void* Wq, const void* Wk, const void* Wv,
+                    int B, int T, int d, int H, int dh, int n, void* QKV, const float* r, int causal, void* A,
+                    float* lse, hipStream_t stream) {
+    if (dtype != kBF16 || n < 16 || n % 16 || 128 % n || (dh != 64 && dh != 32)) return 1;
+    const float scale = 1.0f / sqrtf((float)dh);
+    auto go = [&](auto tag) {
+        constexpr int DH = decltype(tag)::value;
+        using P = QkvAttnPolicy<DH>;
+        if (d % P::KC) return 1;
+        typename P::Args a{};
+        static_cast<typename QkvPolicy<uint16_t, DH>::Args&>(a) = {
+            (const uint16_t*)X, I, (const uint16_t*)Wq, (const uint16_t*)Wk, (const uint16_t*)Wv, (uint16_t*)QKV,
+            T, d, H, n, B * n, 0};
+        a.r = r;
+        a.A = (uint16_t*)A;
+        a.lse = lse;
+        a.causal = causal;
+        a.scale = scale;
+        return launch_gemm2<P>(a, P::mtiles(B * n) * H, stream);
+    };
+    return dh == 64 ? go(std::integral_constant<int, 64>{}) : go(std::integral_constant<int, 32>{});
+}
 
 int launch_qkv(int dtype, const void* X, const int32_t* I, const void* Wq, const void* Wk, const void* Wv, int B,
                int T, int d, int H, int dh, int n, void* QKV, hipStream_t stream) {

@@ -46,6 +46,9 @@ def stage_work(w, with_backward=True):
         add("select", B * H * T * 4 + B * T * 4 + H * d * es + rows * 8 + B * H * T * 2, 0.0)
         add("qkv", X + 3 * H * d * dh * es + 3 * rows * dh * es + rows * 4, 2.0 * rows * d * 3 * dh)
         add("attn", 4 * rows * dh * es + rows * 4, 4.0 * dh * _pairs(k, w.causal) * B * H)
+        # the two in one launch (groups of k | 128 rows): Q|K|V written once
+        # and not read back, A and lse written, r read
+        add("qkv_attn", out["qkv"].bytes + rows * dh * es + rows * 8, out["qkv"].flops + out["attn"].flops)
     if Hd:
         add("qkv_dense", X + 3 * Hd * d * dh * es + 3 * B * Hd * T * dh * es, 2.0 * B * Hd * T * d * 3 * dh)
         add("attn_dense", 4 * B * Hd * T * dh * es + B * Hd * T * 4, 4.0 * dh * _pairs(T, w.causal) * B * Hd)
@@ -148,6 +151,7 @@ STAGE_KERNELS = {
     "router": (r"router_kernel",),
     "select": (r"select_\w*kernel",),
     "qkv": (r"(?<!Wgrad)QkvPolicy",),
+    "qkv_attn": (r"QkvAttnPolicy",),
     "attn": (r"attn_fwd",),
     "out_scatter": (r"OutProj\w*Policy", r"OutCombinePolicy", r"combine_rows_kernel<[^>]*, 0>"),
     "bwd_out": (r"BwdOutPolicy",),

@@ -64,6 +64,11 @@ def test_tiny_f32_workload(orc):
     dict(batch=1, seq_len=1000, heads=2, k=500, d_model=192),
     dict(seq_len=256, k=128, d_head=64, d_model=128),     # the largest single-workgroup attention
     dict(seq_len=200, k=100, causal=False),
+    # groups of 16, 32, 64 rows that tile the 128-row projection tile
+    # (projection and attention in one launch), full and partial last tiles
+    dict(batch=3, seq_len=96, k=16, heads=3, d_model=64),
+    dict(seq_len=160, k=32, d_head=32, causal=False),
+    dict(batch=1, seq_len=128, k=64, d_head=64, d_model=128),
 ])
 def test_small_shapes(orc, kw):
     check_forward(orc, wl.small(**kw))
@@ -123,10 +128,12 @@ def test_deterministic_and_scratch_independent(orc):
     assert torch.equal(mosa.saved_view(shape, a["saved"], "r"), mosa.saved_view(shape, saved2, "r"))
 
 
-def test_stage_intermediates(orc):
+@pytest.mark.parametrize("k", [50, 64])
+def test_stage_intermediates(orc, k):
     """Q, K, V and the router-scaled attention rows r_i A_i of the MoSA heads
-    against the oracle's intermediates."""
-    w = wl.small(batch=2, seq_len=200, heads=3, k=50, d_head=64, d_model=128)
+    against the oracle's intermediates (k = 64: projection and attention in
+    one launch)."""
+    w = wl.small(batch=2, seq_len=200, heads=3, k=k, d_head=64, d_model=128)
     inp = wl.make_inputs(w)
     out = run_forward(w, inp)
     ref = orc.forward(inp, w.k, intermediates=True)
