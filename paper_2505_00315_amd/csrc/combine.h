@@ -160,8 +160,9 @@ __device__ __forceinline__ void combine_tile(const float* Cs, int ldc, int tid, 
     }
 }
 
-// The same combination without dense heads, as a kernel of its own: out[b, t]
-// (+)= sum over MoSA heads h (ascending) of rows[b, h, slot[b, h, t]].  A
+// The same combination as a kernel of its own: out[b, t] (+)= base[b, t] +
+// sum over MoSA heads h (ascending) of rows[b, h, slot[b, h, t]], where base
+// (fp32, optional) holds the dense heads' part.  A
 // workgroup takes 16 tokens of one batch element and stages their slot
 // entries for every head in LDS (head-major, padded rows); each of its 16
 // waves then handles one token, with the whole d-wide row spread over its
@@ -170,7 +171,7 @@ __device__ __forceinline__ void combine_tile(const float* Cs, int ldc, int tid, 
 // in ascending head order (the lanes of a 64-head group ballot their slot
 // entries); the sum starts from 0 and is added to the old output value at
 // the end when accumulating, so every element is produced by one lane in a
-// fixed order.
+// fixed order: the dense part, then the MoSA heads in ascending order.
 constexpr int kCombineTokens = 16;               // one per wave
 constexpr int kCombineThreads = 64 * kCombineTokens;
 constexpr int kCombineLdt = kCombineTokens + 2;  // padded LDS row (int16) per head
@@ -179,8 +180,10 @@ constexpr int kCombineLdt = kCombineTokens + 2;  // padded LDS row (int16) per h
 // (0: the layer output, 1: dX) so that profiles tell the two launches apart.
 template <typename ST, int CH, int USE>
 __global__ __launch_bounds__(kCombineThreads) void combine_rows_kernel(const int16_t* __restrict__ slot,
-                                                           const ST* __restrict__ rows, ST* __restrict__ out, int T,
-                                                           int d, int H, int k, int accumulate, int tiles_per_b) {
+                                                           const ST* __restrict__ rows,
+                                                           const float* __restrict__ base, ST* __restrict__ out,
+                                                           int T, int d, int H, int k, int accumulate,
+                                                           int tiles_per_b) {
     extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
     int16_t* s_slot = reinterpret_cast<int16_t*>(smem);  // [H][kCombineLdt]
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -212,9 +215,18 @@ __global__ __launch_bounds__(kCombineThreads) void combine_rows_kernel(const int
         if (t >= T) return;
         float acc[CH][8];
 #pragma unroll
-        for (int c = 0; c < CH; ++c)
+        for (int c = 0; c < CH; ++c) {
+            const int col = 8 * (lane + 64 * c);
+            if (base && col < d) {
+                const float* bp = base + ((size_t)b * T + t) * d + col;
+                const float4 u = *reinterpret_cast<const float4*>(bp), w = *reinterpret_cast<const float4*>(bp + 4);
+                acc[c][0] = u.x, acc[c][1] = u.y, acc[c][2] = u.z, acc[c][3] = u.w;
+                acc[c][4] = w.x, acc[c][5] = w.y, acc[c][6] = w.z, acc[c][7] = w.w;
+            } else {
 #pragma unroll
-            for (int e = 0; e < 8; ++e) acc[c][e] = 0.f;
+                for (int e = 0; e < 8; ++e) acc[c][e] = 0.f;
+            }
+        }
         for (int hc = 0; hc < H; hc += 64) {
             const int h = hc + lane;
             const int sl = h < H ? s_slot[h * kCombineLdt + tl] : -1;
@@ -277,25 +289,29 @@ __global__ __launch_bounds__(kCombineThreads) void combine_rows_kernel(const int
     }
 }
 
-// out (+)= head-ordered sum of the MoSA rows (no dense heads); d a multiple of 8.
+// out (+)= base + head-ordered sum of the MoSA rows; d a multiple of 8, base
+// [B, T, d] fp32 or nullptr.
+inline bool combine_rows_fits(int d, int H) {
+    return d % 8 == 0 && d <= 2048 && (size_t)(H > 0 ? H : 1) * kCombineLdt * sizeof(int16_t) <= 64 * 1024;
+}
 template <typename ST, int USE>
-int launch_combine_rows(const int16_t* slot, const ST* rows, ST* out, int B, int T, int d, int H, int k,
-                        int accumulate, hipStream_t stream) {
+int launch_combine_rows(const int16_t* slot, const ST* rows, const float* base, ST* out, int B, int T, int d, int H,
+                        int k, int accumulate, hipStream_t stream) {
     if (B == 0 || T == 0) return 0;
-    if (d % 8 != 0 || d > 2048) return -1;
+    if (!combine_rows_fits(d, H)) return -1;
     const int tiles = (T + kCombineTokens - 1) / kCombineTokens;
     const size_t lds = (size_t)(H > 0 ? H : 1) * kCombineLdt * sizeof(int16_t);
     if (lds > 64 * 1024) return -1;
     const dim3 grid(B * tiles), block(kCombineThreads);
     if (d <= 512)
-        hipLaunchKernelGGL((combine_rows_kernel<ST, 1, USE>), grid, block, lds, stream, slot, rows, out, T, d, H, k,
-                           accumulate, tiles);
+        hipLaunchKernelGGL((combine_rows_kernel<ST, 1, USE>), grid, block, lds, stream, slot, rows, base, out, T, d, H,
+                           k, accumulate, tiles);
     else if (d <= 1024)
-        hipLaunchKernelGGL((combine_rows_kernel<ST, 2, USE>), grid, block, lds, stream, slot, rows, out, T, d, H, k,
-                           accumulate, tiles);
+        hipLaunchKernelGGL((combine_rows_kernel<ST, 2, USE>), grid, block, lds, stream, slot, rows, base, out, T, d, H,
+                           k, accumulate, tiles);
     else
-        hipLaunchKernelGGL((combine_rows_kernel<ST, 4, USE>), grid, block, lds, stream, slot, rows, out, T, d, H, k,
-                           accumulate, tiles);
+        hipLaunchKernelGGL((combine_rows_kernel<ST, 4, USE>), grid, block, lds, stream, slot, rows, base, out, T, d, H,
+                           k, accumulate, tiles);
     return hipGetLastError() == hipSuccess ? 0 : -1;
 }
 

@@ -13,6 +13,7 @@
 //              K = Hd * 3 dh, then the MoSA rows of each token added in head
 //              order from the slot map (bitwise reproducible), then written.
 #include "combine.h"
+#include "gemm2.h"
 #include "dxrow.h"
 #include "gemm.h"
 #include "kernels.h"
@@ -155,6 +156,85 @@ struct DxCombinePolicy {
     }
 };
 
+// The dense heads' part alone, kept in fp32 ([B, T, d]) for combine_rows_kernel
+// to start from.
+template <typename ST, int DH>
+struct DxDensePolicy : DxCombinePolicy<ST, DH> {
+    using Base = DxCombinePolicy<ST, DH>;
+    static constexpr size_t EPI_LDS = 0;
+    struct Args : Base::Args {
+        float* base;
+    };
+    __device__ static void epilogue(const Args& a, int b, int m0, int n0, const float* Cs, int ldc, int tid,
+                                    unsigned char*) {
+        constexpr int VPR = Base::NT / 4;
+        for (int v = tid; v < Base::MT * VPR; v += 256) {
+            const int ml = v / VPR, c = (v % VPR) * 4, t = m0 + ml;
+            if (t >= a.T || n0 + c >= a.d) continue;
+            *reinterpret_cast<float4*>(a.base + ((size_t)b * a.T + t) * a.d + n0 + c) =
+                *reinterpret_cast<const float4*>(Cs + ml * ldc + c);
+        }
+    }
+};
+
+// The same on the multi-stage engine (gemm2.h), bf16: 128 tokens x 128
+// columns per workgroup.  K runs over (head, Q|K|V, e): A = the dense heads'
+// dQ|dK|dV rows of token t, head after head; B[k][n] = W^{Q|K|V}_d[hd][n][e]
+// (k-contiguous, one of three weights per chunk, reached by its element
+// offset from W^Q_d).
+template <int DH>
+struct DxDensePolicy2 {
+    using ST = uint16_t;
+    static constexpr int MT = 128, NT = 128, KC = 32, WM = 2, WN = 2, STAGES = 4;
+    static constexpr size_t EPI_LDS = 0;
+    static constexpr bool A_KCONTIG = true, B_KCONTIG = true;
+    static_assert(DH % KC == 0, "chunks within one weight of one head");
+    struct Args {
+        const ST* dQKVd;  // [B, Hd, T, 3 DH]
+        const ST* Wq;     // [Hd, d, DH]
+        ptrdiff_t dk, dv; // W^K_d - W^Q_d, W^V_d - W^Q_d (elements)
+        float* base;      // [B, T, d]
+        int T, d, Hd, mtiles, ntiles;
+    };
+    struct ARef {
+        const ST* p;
+    };
+    struct BRef {
+        const ST* p;
+    };
+    __device__ static void tile(const Args& a, int logical, int& b, int& m0, int& n0) {
+        const int per = a.mtiles * a.ntiles, rem = logical % per;
+        b = logical / per;
+        m0 = (rem / a.ntiles) * MT;
+        n0 = (rem % a.ntiles) * NT;
+    }
+    __device__ static int k_size(const Args& a, int) { return a.Hd * 3 * DH; }
+    __device__ static ARef a_row(const Args& a, int b, int t) {
+        return {a.dQKVd + ((size_t)b * a.Hd * a.T + min(t, a.T - 1)) * (3 * DH)};
+    }
+    __device__ static const ST* a_elem(const Args&, int, const ARef& r, int k) { return r.p + k; }
+    __device__ static ptrdiff_t a_koff(const Args& a, int, int c) {
+        const int k = c * KC;
+        return (ptrdiff_t)(k / (3 * DH)) * a.T * (3 * DH) + k % (3 * DH);
+    }
+    __device__ static BRef b_row(const Args& a, int, int n) { return {a.Wq + (size_t)min(n, a.d - 1) * DH}; }
+    __device__ static const ST* b_elem(const Args&, int, const BRef& r, int k) { return r.p + k; }
+    __device__ static ptrdiff_t b_koff(const Args& a, int, int c) {
+        const int k = c * KC, hd = k / (3 * DH), j = k % (3 * DH), w = j / DH;
+        return (w == 0 ? 0 : (w == 1 ? a.dk : a.dv)) + (ptrdiff_t)hd * a.d * DH + j % DH;
+    }
+    __device__ static void epilogue(const Args& a, int b, int m0, int n0, const float* Cs, int ldc, int tid,
+                                    unsigned char*) {
+        constexpr int VPR = NT / 4;
+        for (int v = tid; v < MT * VPR; v += 256) {
+            const int ml = v / VPR, c = (v % VPR) * 4, t = m0 + ml;
+            if (t >= a.T || n0 + c >= a.d) continue;
+            *reinterpret_cast<float4*>(a.base + ((size_t)b * a.T + t) * a.d + n0 + c) =
+                *reinterpret_cast<const float4*>(Cs + ml * ldc + c);
+        }
+    }
+};
+
 template <typename ST, int DH>
 int run_proj(const ST* dQKV, const float* dz, const ST* Wq, const ST* Wk, const ST* Wv, const ST* Wr, int B, int d,
              int H, int k, ST* dXs, hipStream_t stream) {
@@ -173,12 +253,34 @@ int run_proj(const ST* dQKV, const float* dz, const ST* Wq, const ST* Wk, const 
 
 template <typename ST, int DH>
 int run_combine(const ST* dQKVd, const ST* Wq, const ST* Wk, const ST* Wv, const int16_t* slot, const ST* dXs, int B,
-                int T, int d, int H, int k, int Hd, ST* dX, int accumulate, hipStream_t stream) {
+                int T, int d, int H, int k, int Hd, ST* dX, int accumulate, float* base, hipStream_t stream) {
     using P = DxCombinePolicy<ST, DH>;
-    if (Hd == 0 && d % 8 == 0 && d <= 2048 && (size_t)H * kCombineLdt * 2 <= 64 * 1024)
-        return launch_combine_rows<ST, 1>(slot, dXs, dX, B, T, d, H, k, accumulate, stream);
     typename P::Args a{dQKVd, Wq, Wk, Wv, slot, dXs, dX, T, d, H, k, Hd, accumulate, (T + P::MT - 1) / P::MT,
                        (d + P::NT - 1) / P::NT};
+    if (combine_rows_fits(d, H) && (Hd == 0 || base)) {
+        // dense heads first (fp32 into base), then the per-token combination
+        if (Hd > 0) {
+            int e;
+            if constexpr (sizeof(ST) == 2) {
+                using P2 = DxDensePolicy2<DH>;
+                const int mt = (T + P2::MT - 1) / P2::MT, nt = (d + P2::NT - 1) / P2::NT;
+                auto dist = [&](const ST* p) {  // element distance from W^Q_d
+                    return (ptrdiff_t)(((intptr_t)p - (intptr_t)Wq) / (intptr_t)sizeof(ST));
+                };
+                typename P2::Args a2{(const uint16_t*)dQKVd, (const uint16_t*)Wq, dist(Wk), dist(Wv), base, T, d, Hd,
+                                     mt, nt};
+                e = launch_gemm2<P2>(a2, B * mt * nt, stream);
+            } else {
+                using PD = DxDensePolicy<ST, DH>;
+                typename PD::Args ad{};
+                static_cast<typename P::Args&>(ad) = a;
+                ad.base = base;
+                e = launch_gemm<ST, PD>(ad, B * a.mtiles * a.ntiles, stream);
+            }
+            if (e) return e;
+        }
+        return launch_combine_rows<ST, 1>(slot, dXs, Hd > 0 ? base : nullptr, dX, B, T, d, H, k, accumulate, stream);
+    }
     return launch_gemm<ST, P>(a, B * a.mtiles * a.ntiles, stream);
 }
 
@@ -199,15 +301,15 @@ int launch_dx_proj(int dtype, const void* dQKV, const float* dz, const void* Wq,
 
 int launch_dx_combine(int dtype, const void* dQKVd, const void* Wq_d, const void* Wk_d, const void* Wv_d,
                       const int16_t* slot, const void* dXs, int B, int T, int d, int H, int dh, int k, int Hd,
-                      void* dX, int accumulate, hipStream_t stream) {
+                      void* dX, int accumulate, float* base, hipStream_t stream) {
     if (dtype == kBF16) {
         auto f = dh == 64 ? run_combine<uint16_t, 64> : run_combine<uint16_t, 32>;
         return f((const uint16_t*)dQKVd, (const uint16_t*)Wq_d, (const uint16_t*)Wk_d, (const uint16_t*)Wv_d, slot,
-                 (const uint16_t*)dXs, B, T, d, H, k, Hd, (uint16_t*)dX, accumulate, stream);
+                 (const uint16_t*)dXs, B, T, d, H, k, Hd, (uint16_t*)dX, accumulate, base, stream);
     }
     auto f = dh == 64 ? run_combine<float, 64> : run_combine<float, 32>;
     return f((const float*)dQKVd, (const float*)Wq_d, (const float*)Wk_d, (const float*)Wv_d, slot,
-             (const float*)dXs, B, T, d, H, k, Hd, (float*)dX, accumulate, stream);
+             (const float*)dXs, B, T, d, H, k, Hd, (float*)dX, accumulate, base, stream);
 }
 
 }  // namespace mosa

@@ -135,6 +135,17 @@ struct G2MinWaves<P, std::void_t<decltype(P::MIN_WAVES)>> : std::integral_consta
 template <class P, class = void> struct G2EpiRegs : std::false_type {};
 template <class P> struct G2EpiRegs<P, std::void_t<decltype(P::EPI_REGS)>> : std::bool_constant<P::EPI_REGS> {};
 
+// a_koff(args, batch, c) / b_koff(args, batch, c): element offset of k chunk c
+// from chunk 0 (k-contiguous operands whose k axis is made of segments, e.g.
+// heads, that are not adjacent in memory; the policy keeps KC within one
+// segment).  Default: c * KC (times the k-stride of an m-contiguous operand).
+template <class P, class = void> struct G2AKoff : std::false_type {};
+template <class P>
+struct G2AKoff<P, std::void_t<decltype(P::a_koff(std::declval<const typename P::Args&>(), 0, 0))>> : std::true_type {};
+template <class P, class = void> struct G2BKoff : std::false_type {};
+template <class P>
+struct G2BKoff<P, std::void_t<decltype(P::b_koff(std::declval<const typename P::Args&>(), 0, 0))>> : std::true_type {};
+
 // Zeros for the rows past the end of a gathered range.
 static __device__ __attribute__((aligned(16))) const uint16_t g2_zero[8] = {0, 0, 0, 0, 0, 0, 0, 0};
 
@@ -269,15 +280,22 @@ __device__ __forceinline__ void gemm2_body(const typename P::Args& args, int log
     auto issue_buf = [&](int c, int bidx) {
         const uint32_t buf = lds_wave + bidx * S::STAGE_BYTES;
         const size_t kc = (size_t)min(c, nchunks - 1);
+        ptrdiff_t aoff = 0, boff = 0;
+        if constexpr (!S::KG) {
+            if constexpr (G2AKoff<P>::value) aoff = P::a_koff(args, batch, (int)kc);
+            else aoff = (ptrdiff_t)(kc * astep);
+            if constexpr (G2BKoff<P>::value) boff = P::b_koff(args, batch, (int)kc);
+            else boff = (ptrdiff_t)(kc * bstep);
+        }
 #pragma unroll
         for (int j = 0; j < S::IA; ++j) {
             if constexpr (S::KG) lds_load16(gathered(asrc[j], astr[j], arv[j]), buf + 4096 * j);
-            else lds_load16(asrc[j] + kc * astep, buf + 4096 * j);
+            else lds_load16(asrc[j] + aoff, buf + 4096 * j);
         }
 #pragma unroll
         for (int j = 0; j < S::IB; ++j) {
             if constexpr (S::KG) lds_load16(gathered(bsrc[j], bstr[j], brv[j]), buf + S::A_BYTES + 4096 * j);
-            else lds_load16(bsrc[j] + kc * bstep, buf + S::A_BYTES + 4096 * j);
+            else lds_load16(bsrc[j] + boff, buf + S::A_BYTES + 4096 * j);
         }
     };
 

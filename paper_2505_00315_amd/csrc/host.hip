@@ -17,9 +17,9 @@ inline size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
 struct Layout {
     mosa_saved_layout saved;
     // forward scratch
-    size_t z, xnorm, unc_tok, unc_key, unc_sel, Xo;
+    size_t z, xnorm, unc_tok, unc_key, unc_sel, Xo, ybase;
     // backward scratch
-    size_t dA, D, dz, dz16, dQKV, dXs, dAd, Dd, dQKVd, wpart;
+    size_t dA, D, dz, dz16, dQKV, dXs, dAd, Dd, dQKVd, wpart, dxbase;
     size_t scratch_total;
 };
 
@@ -79,6 +79,7 @@ Layout make_layout(const mosa_shape* s) {
     L.unc_key = fw.take(B * H * T * 8);
     L.unc_sel = fw.take(B * H * T * 4);
     L.Xo = fw.take(B * H * k * d * es);
+    L.ybase = fw.take(Hd > 0 ? B * T * d * 4 : 0);  // dense heads' part of Y (fp32)
     Carver bw;
     L.dA = bw.take(B * H * k * dh * es);
     L.D = bw.take(B * H * k * 4);
@@ -89,6 +90,7 @@ Layout make_layout(const mosa_shape* s) {
     L.dAd = bw.take(B * Hd * T * dh * es);
     L.Dd = bw.take(B * Hd * T * 4);
     L.dQKVd = bw.take(B * Hd * T * 3 * dh * es);
+    L.dxbase = bw.take(Hd > 0 ? B * T * d * 4 : 0);  // dense heads' part of dX (fp32)
     {
         const int dt = s->dtype == MOSA_BF16 ? kBF16 : kF32;
         const size_t pm = wgrad_partial_bytes(dt, (int)B, (int)d, (int)H, (int)dh, (int)k, 1);
@@ -227,7 +229,8 @@ int mosa_forward_timed(const mosa_shape* s, const void* X, const mosa_weights* w
         e |= launch_attn_fwd(dt, QKVd, nullptr, B * Hd, T, dh, causal, Ad, lsed, stream);
         e |= sm.mark("attn_dense");
     }
-    e |= launch_out_combine(dt, Ad, w->Wo_d, slot, Xo, B, T, d, H, dh, k, Hd, Y, accumulate, stream);
+    e |= launch_out_combine(dt, Ad, w->Wo_d, slot, Xo, B, T, d, H, dh, k, Hd, Y, accumulate,
+                            at<float>(scratch, L.ybase), stream);
     e |= sm.mark("out_combine");
     if (H > 0 && I_out)
         e |= hipMemcpyAsync(I_out, I, (size_t)B * H * k * 4, hipMemcpyDeviceToDevice, stream) != hipSuccess;
@@ -326,7 +329,7 @@ int mosa_backward_timed(const mosa_shape* s, const void* X, const mosa_weights* 
         e |= sm.mark("wgrad_o_dense");
     }
     e |= launch_dx_combine(dt, dQKVd, w->Wq_d, w->Wk_d, w->Wv_d, slot, dXs, B, T, d, H, dh, k, Hd, dX, accumulate_dX,
-                           stream);
+                           at<float>(scratch, L.dxbase), stream);
     e |= sm.mark("dx_combine");
     return e ? MOSA_ERR_HIP : MOSA_OK;
 }

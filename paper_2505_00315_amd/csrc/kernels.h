@@ -45,8 +45,9 @@ int launch_out_proj(int dtype, const void* A, const void* Wo, int B, int d, int 
                     hipStream_t stream);
 
 // Y[b,t,:] (+)= sum_hd Ad[b,hd,t,:] Wo_d[hd] + sum_h (ascending) Xo[b,h,slot[b,h,t],:].
+// base: fp32 [B, T, d] scratch for the dense heads' part (used when Hd > 0).
 int launch_out_combine(int dtype, const void* Ad, const void* Wo_d, const int16_t* slot, const void* Xo,
-                       int B, int T, int d, int H, int dh, int k, int Hd, void* Y, int accumulate,
+                       int B, int T, int d, int H, int dh, int k, int Hd, void* Y, int accumulate, float* base,
                        hipStream_t stream);
 
 // Backward, output side of a head (A is the r-scaled attention output):
@@ -80,8 +81,9 @@ int launch_dx_proj(int dtype, const void* dQKV, const float* dz, const void* Wq,
                    hipStream_t stream);
 
 // dX[b,t,:] (+)= dense heads' (dQ Wq^T + dK Wk^T + dV Wv^T) + sum_h (ascending) dXs[b,h,slot,:].
+// base: fp32 [B, T, d] scratch for the dense heads' part (used when Hd > 0).
 int launch_dx_combine(int dtype, const void* dQKVd, const void* Wq_d, const void* Wk_d, const void* Wv_d,
                       const int16_t* slot, const void* dXs, int B, int T, int d, int H, int dh, int k,
-                      int Hd, void* dX, int accumulate, hipStream_t stream);
+                      int Hd, void* dX, int accumulate, float* base, hipStream_t stream);
 
 }  // namespace mosa

@@ -16,6 +16,7 @@
 //               the result is bitwise reproducible and unselected rows are
 //               exactly the dense part (0 without dense heads).
 #include "combine.h"
+#include "gemm2.h"
 #include "gemm.h"
 #include "kernels.h"
 #include "rowgemm.h"
@@ -140,6 +141,78 @@ struct OutCombinePolicy {
     }
 };
 
+// The dense heads' part alone, kept in fp32 ([B, T, d]) for combine_rows_kernel
+// to start from.
+template <typename ST, int DH>
+struct OutDensePolicy : OutCombinePolicy<ST, DH> {
+    using Base = OutCombinePolicy<ST, DH>;
+    static constexpr size_t EPI_LDS = 0;
+    struct Args : Base::Args {
+        float* base;
+    };
+    __device__ static void epilogue(const Args& a, int b, int m0, int n0, const float* Cs, int ldc, int tid,
+                                    unsigned char*) {
+        constexpr int VPR = Base::NT / 4;
+        for (int v = tid; v < Base::MT * VPR; v += 256) {
+            const int ml = v / VPR, c = (v % VPR) * 4, t = m0 + ml;
+            if (t >= a.T || n0 + c >= a.d) continue;
+            *reinterpret_cast<float4*>(a.base + ((size_t)b * a.T + t) * a.d + n0 + c) =
+                *reinterpret_cast<const float4*>(Cs + ml * ldc + c);
+        }
+    }
+};
+
+// The same on the multi-stage engine (gemm2.h), bf16: 128 tokens x 128
+// columns per workgroup; A = the dense heads' rows of token t, head after
+// head (chunks of KC stay within a head), B = W^O_d as one [Hd DH, d]
+// m-contiguous operand.
+template <int DH>
+struct OutDensePolicy2 {
+    using ST = uint16_t;
+    static constexpr int MT = 128, NT = 128, KC = 32, WM = 2, WN = 2, STAGES = 4;
+    static constexpr size_t EPI_LDS = 0;
+    static constexpr bool A_KCONTIG = true, B_KCONTIG = false;
+    static_assert(DH % KC == 0, "chunks within a head");
+    struct Args {
+        const ST* Ad;   // [B, Hd, T, DH]
+        const ST* Wod;  // [Hd DH, d]
+        float* base;    // [B, T, d]
+        int T, d, Hd, mtiles, ntiles;
+    };
+    struct ARef {
+        const ST* p;
+    };
+    __device__ static void tile(const Args& a, int logical, int& b, int& m0, int& n0) {
+        const int per = a.mtiles * a.ntiles, rem = logical % per;
+        b = logical / per;
+        m0 = (rem / a.ntiles) * MT;
+        n0 = (rem % a.ntiles) * NT;
+    }
+    __device__ static int k_size(const Args& a, int) { return a.Hd * DH; }
+    __device__ static ARef a_row(const Args& a, int b, int t) {
+        return {a.Ad + ((size_t)b * a.Hd * a.T + min(t, a.T - 1)) * DH};
+    }
+    __device__ static const ST* a_elem(const Args&, int, const ARef& r, int k) { return r.p + k; }
+    __device__ static ptrdiff_t a_koff(const Args& a, int, int c) {
+        const int k = c * KC;
+        return (ptrdiff_t)(k / DH) * a.T * DH + k % DH;
+    }
+    __device__ static size_t b_kstride(const Args& a, int) { return a.d; }
+    __device__ static const ST* b_maddr(const Args& a, int, int k, int n8) {
+        return a.Wod + (size_t)k * a.d + min(n8, a.d - 8);
+    }
+    __device__ static void epilogue(const Args& a, int b, int m0, int n0, const float* Cs, int ldc, int tid,
+                                    unsigned char*) {
+        constexpr int VPR = NT / 4;
+        for (int v = tid; v < MT * VPR; v += 256) {
+            const int ml = v / VPR, c = (v % VPR) * 4, t = m0 + ml;
+            if (t >= a.T || n0 + c >= a.d) continue;
+            *reinterpret_cast<float4*>(a.base + ((size_t)b * a.T + t) * a.d + n0 + c) =
+                *reinterpret_cast<const float4*>(Cs + ml * ldc + c);
+        }
+    }
+};
+
 // bf16 storage, d a multiple of the column block: the row-streaming kernel (rowgemm.h),
 // W^O_h[:, n0:n0+256] held in registers, the r-scaled rows streamed.
 template <int DH>
@@ -194,12 +267,30 @@ int run_proj(const ST* A, const ST* Wo, int B, int d, int H, int k, ST* Xo, hipS
 
 template <typename ST, int DH>
 int run_combine(const ST* Ad, const ST* Wod, const int16_t* slot, const ST* Xo, int B, int T, int d, int H, int k,
-                int Hd, ST* Y, int accumulate, hipStream_t stream) {
+                int Hd, ST* Y, int accumulate, float* base, hipStream_t stream) {
     using P = OutCombinePolicy<ST, DH>;
-    if (Hd == 0 && d % 8 == 0 && d <= 2048 && (size_t)H * kCombineLdt * 2 <= 64 * 1024)
-        return launch_combine_rows<ST, 0>(slot, Xo, Y, B, T, d, H, k, accumulate, stream);
     typename P::Args a{Ad, Wod, slot, Xo, Y, T, d, H, k, Hd, accumulate, (T + P::MT - 1) / P::MT,
                        (d + P::NT - 1) / P::NT};
+    if (combine_rows_fits(d, H) && (Hd == 0 || base)) {
+        // dense heads first (fp32 into base), then the per-token combination
+        if (Hd > 0) {
+            int e;
+            if constexpr (sizeof(ST) == 2) {
+                using P2 = OutDensePolicy2<DH>;
+                const int mt = (T + P2::MT - 1) / P2::MT, nt = (d + P2::NT - 1) / P2::NT;
+                typename P2::Args a2{(const uint16_t*)Ad, (const uint16_t*)Wod, base, T, d, Hd, mt, nt};
+                e = launch_gemm2<P2>(a2, B * mt * nt, stream);
+            } else {
+                using PD = OutDensePolicy<ST, DH>;
+                typename PD::Args ad{};
+                static_cast<typename P::Args&>(ad) = a;
+                ad.base = base;
+                e = launch_gemm<ST, PD>(ad, B * a.mtiles * a.ntiles, stream);
+            }
+            if (e) return e;
+        }
+        return launch_combine_rows<ST, 0>(slot, Xo, Hd > 0 ? base : nullptr, Y, B, T, d, H, k, accumulate, stream);
+    }
     return launch_gemm<ST, P>(a, B * a.mtiles * a.ntiles, stream);
 }
 
@@ -217,15 +308,16 @@ int launch_out_proj(int dtype, const void* A, const void* Wo, int B, int d, int 
 }
 
 int launch_out_combine(int dtype, const void* Ad, const void* Wo_d, const int16_t* slot, const void* Xo, int B,
-                       int T, int d, int H, int dh, int k, int Hd, void* Y, int accumulate, hipStream_t stream) {
+                       int T, int d, int H, int dh, int k, int Hd, void* Y, int accumulate, float* base,
+                       hipStream_t stream) {
     if (dtype == kBF16) {
         auto f = dh == 64 ? run_combine<uint16_t, 64> : run_combine<uint16_t, 32>;
         return f((const uint16_t*)Ad, (const uint16_t*)Wo_d, slot, (const uint16_t*)Xo, B, T, d, H, k, Hd,
-                 (uint16_t*)Y, accumulate, stream);
+                 (uint16_t*)Y, accumulate, base, stream);
     }
     auto f = dh == 64 ? run_combine<float, 64> : run_combine<float, 32>;
     return f((const float*)Ad, (const float*)Wo_d, slot, (const float*)Xo, B, T, d, H, k, Hd, (float*)Y, accumulate,
-             stream);
+             base, stream);
 }
 
 }  // namespace mosa

@@ -67,8 +67,9 @@ def test_small_shapes(orc, kw):
     check_backward(orc, wl.small(**kw))
 
 
-def test_accumulate_dX(orc):
-    w = wl.small(seq_len=128, k=30, dtype="f32")
+@pytest.mark.parametrize("dense", [0, 2])
+def test_accumulate_dX(orc, dense):
+    w = wl.small(seq_len=128, k=30, dtype="f32", dense_heads=dense)
     inp = wl.make_inputs(w)
     dX0 = torch.randn(w.batch, w.seq_len, w.d_model, device="cuda")
     _, dX, _, _ = run_fwd_bwd(w, inp, accumulate_dX=True, dX0=dX0)

@@ -102,8 +102,9 @@ def test_unselected_rows_exactly_zero(orc):
         assert (Y[b, rest] == 0).all()
 
 
-def test_accumulate_adds_to_residual(orc):
-    w = wl.small(seq_len=128, k=30, dtype="f32")
+@pytest.mark.parametrize("dense", [0, 2])
+def test_accumulate_adds_to_residual(orc, dense):
+    w = wl.small(seq_len=128, k=30, dtype="f32", dense_heads=dense)
     inp = wl.make_inputs(w)
     Y0 = torch.randn(w.batch, w.seq_len, w.d_model, device="cuda")
     out = run_forward(w, inp, accumulate=True, Y0=Y0)
