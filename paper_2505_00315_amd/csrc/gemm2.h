@@ -45,6 +45,7 @@
 //     32 p + 8 (i / 4) + i % 4, block 2p + 1 row i is 32 p + 8 (i / 4) + 4 + i % 4),
 //     so that a lane's accumulators of a block pair are 8 consecutive M.
 //   MIN_WAVES: waves per SIMD the register allocation must allow.
+//   CHUNK_ADD (k-contiguous A and B): each MFMA from zero, then one add.
 //   EPI_REGS (needs A_INTERLEAVE): no C tile; the engine calls
 //     store8(args, batch, m, n, x[8]) for M indices m .. m + 7 at column n.
 #pragma once
@@ -132,6 +133,11 @@ struct G2Interleave<P, std::void_t<decltype(P::A_INTERLEAVE)>> : std::bool_const
 template <class P, class = void> struct G2MinWaves : std::integral_constant<int, 1> {};
 template <class P>
 struct G2MinWaves<P, std::void_t<decltype(P::MIN_WAVES)>> : std::integral_constant<int, P::MIN_WAVES> {};
+// CHUNK_ADD: every MFMA (32 k) starts from a zero accumulator and is added to
+// the running sum with one fp32 add per element (a summation whose error
+// bound does not depend on the MFMA's internal accumulation).
+template <class P, class = void> struct G2ChunkAdd : std::false_type {};
+template <class P> struct G2ChunkAdd<P, std::void_t<decltype(P::CHUNK_ADD)>> : std::bool_constant<P::CHUNK_ADD> {};
 template <class P, class = void> struct G2EpiRegs : std::false_type {};
 template <class P> struct G2EpiRegs<P, std::void_t<decltype(P::EPI_REGS)>> : std::bool_constant<P::EPI_REGS> {};
 
@@ -163,6 +169,7 @@ struct Gemm2Shape {
     static_assert(A_UNITS % 256 == 0 && B_UNITS % 256 == 0, "whole instructions per wave");
     static_assert((STAGES - 2) * (IA + IB) <= 63, "vmcnt range");
     static constexpr bool KG = G2Gather<P>::value, IL = G2Interleave<P>::value, ER = G2EpiRegs<P>::value;
+    static constexpr bool CA = G2ChunkAdd<P>::value;
     static_assert(!KG || (!P::A_KCONTIG && !P::B_KCONTIG), "gathered k needs m-contiguous operands");
     static_assert(!IL || (!P::A_KCONTIG && FM % 2 == 0), "interleaved A needs m-contiguous pairs of blocks");
     static_assert(!ER || IL, "register epilogue needs interleaved A");
@@ -392,7 +399,15 @@ __device__ __forceinline__ void gemm2_body(const typename P::Args& args, int log
 #pragma unroll
             for (int i = 0; i < S::FM; ++i)
 #pragma unroll
-                for (int j = 0; j < S::FN; ++j) mma8(acc[i][j], fa[i], fb[j]);
+                for (int j = 0; j < S::FN; ++j) {
+                    if constexpr (S::CA) {
+                        f32x4 part = zero4();
+                        mma8(part, fa[i], fb[j]);
+                        acc[i][j] += part;
+                    } else {
+                        mma8(acc[i][j], fa[i], fb[j]);
+                    }
+                }
         }
     };
 

@@ -15,6 +15,7 @@
 // The kernel also writes an upper bound of ||x_t||_2 for every token
 // (fp64 sum of squares, rounded up to fp32) used by that error bound.
 #include "common.h"
+#include "gemm2.h"
 #include "kernels.h"
 
 namespace mosa {
@@ -125,11 +126,90 @@ __global__ __launch_bounds__(256) void router_kernel(const ST* __restrict__ X, c
     }
 }
 
+// bf16: the same contraction on the multi-stage engine (gemm2.h), MT tokens x
+// NT heads per workgroup with both operands staged through LDS, so that each
+// W^r row is fetched once per workgroup rather than once per wave.  Every
+// 32-k MFMA starts from zero and is added to the running sum (CHUNK_ADD): the
+// same summation, and the same error bound, as router_kernel.  The workgroups
+// of the first head tile also write the ||x_t|| bounds of their tokens.
+template <int MT_, int NT_>
+struct RouterPolicy2 {
+    using ST = uint16_t;
+    static constexpr int MT = MT_, NT = NT_, KC = 64, WM = 2, WN = 2, STAGES = MT * NT >= 64 * 128 ? 3 : 4;
+    static constexpr size_t EPI_LDS = 0;
+    static constexpr bool A_KCONTIG = true, B_KCONTIG = true, CHUNK_ADD = true;
+    struct Args {
+        const ST* X;   // [BT, d]
+        const ST* Wr;  // [H, d]
+        float* z;      // [B, H, T]
+        float* xnorm;  // [BT]
+        int BT, T, d, H, ntiles;
+    };
+    struct ARef {
+        const ST* p;
+    };
+    struct BRef {
+        const ST* p;
+    };
+    // the head tiles of one token tile are consecutive (one XCD, X from its L2)
+    __device__ static void tile(const Args& a, int logical, int& batch, int& m0, int& n0) {
+        batch = 0;
+        m0 = (logical / a.ntiles) * MT;
+        n0 = (logical % a.ntiles) * NT;
+    }
+    __device__ static int k_size(const Args& a, int) { return a.d; }
+    __device__ static ARef a_row(const Args& a, int, int m) { return {a.X + (size_t)min(m, a.BT - 1) * a.d}; }
+    __device__ static const ST* a_elem(const Args&, int, const ARef& r, int k) { return r.p + k; }
+    __device__ static BRef b_row(const Args& a, int, int n) { return {a.Wr + (size_t)min(n, a.H - 1) * a.d}; }
+    __device__ static const ST* b_elem(const Args&, int, const BRef& r, int k) { return r.p + k; }
+    __device__ static void epilogue(const Args& a, int, int m0, int n0, const float* Cs, int ldc, int tid,
+                                    unsigned char*) {
+        for (int v = tid; v < MT * NT; v += 256) {
+            const int nl = v / MT, ml = v % MT, tok = m0 + ml, h = n0 + nl;
+            if (tok < a.BT && h < a.H) {
+                const int b = tok / a.T, t = tok % a.T;
+                a.z[((size_t)b * a.H + h) * a.T + t] = Cs[ml * ldc + nl];
+            }
+        }
+        if (n0 != 0) return;
+        // ||x_t||_2 bound: 256 / MT threads per token, fp64 sum of squares
+        constexpr int TPT = 256 / MT;
+        const int ml = tid / TPT, j = tid % TPT, tok = m0 + ml;
+        const ST* xr = a.X + (size_t)min(tok, a.BT - 1) * a.d;
+        double ss = 0.0;
+        for (int c = 8 * j; c < a.d; c += 8 * TPT) {
+            float x[8];
+            vec8_to_f32<ST>(vec8_load<ST>(xr + c), x);
+#pragma unroll
+            for (int e = 0; e < 8; ++e) ss += (double)x[e] * (double)x[e];
+        }
+#pragma unroll
+        for (int o = 1; o < TPT; o <<= 1) ss += __shfl_xor(ss, o, 64);
+        if (j == 0 && tok < a.BT) a.xnorm[tok] = f32_round_up(sqrt(ss) * (1.0 + 0x1p-30));
+    }
+};
+
+template <int MT, int NT>
+int run_router2(const uint16_t* X, const uint16_t* Wr, int BT, int T, int d, int H, float* z, float* xnorm,
+                hipStream_t stream) {
+    using P = RouterPolicy2<MT, NT>;
+    const int mt = (BT + MT - 1) / MT, nt = (H + NT - 1) / NT;
+    typename P::Args a{X, Wr, z, xnorm, BT, T, d, H, nt};
+    return launch_gemm2<P>(a, mt * nt, stream);
+}
+
 }  // namespace
 
 int launch_router(int dtype, const void* X, const void* Wr, int B, int T, int d, int H, float* z,
                   float* xnorm, hipStream_t stream) {
     const int BT = B * T;
+    if (dtype == kBF16 && d % 64 == 0) {
+        // tile: enough workgroups to fill the chip (about 256), as large as allows
+        auto f = run_router2<32, 32>;
+        if (H > 64) f = (size_t)((BT + 63) / 64) * ((H + 127) / 128) >= 256 ? run_router2<64, 128> : run_router2<32, 64>;
+        else if (H > 32) f = run_router2<32, 64>;
+        return f((const uint16_t*)X, (const uint16_t*)Wr, BT, T, d, H, z, xnorm, stream);
+    }
     dim3 grid((BT + kRouterTokens - 1) / kRouterTokens, (H + kRouterHeads - 1) / kRouterHeads);
     if (dtype == kBF16)
         hipLaunchKernelGGL(router_kernel<uint16_t>, grid, dim3(256), 0, stream, (const uint16_t*)X,

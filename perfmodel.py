@@ -148,7 +148,7 @@ def paper_mosa_heads_for_budget(layers, h, hp, T, baseline_heads, dense_heads, s
 # Kernel-name patterns of each stage (MoSA heads only: dense heads reuse the
 # same kernels, so workloads with dense heads are not attributed here).
 STAGE_KERNELS = {
-    "router": (r"router_kernel",),
+    "router": (r"router_kernel", r"RouterPolicy2"),
     "select": (r"select_\w*kernel",),
     "qkv": (r"(?<!Wgrad)QkvPolicy",),
     "qkv_attn": (r"QkvAttnPolicy",),
