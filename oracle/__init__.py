@@ -36,6 +36,18 @@ _p = ctypes.c_void_p
 _i = ctypes.c_int
 
 
+class Options(ctypes.Structure):
+    """Layer variants (``orc_options`` in mosa_oracle.c): forced first token,
+    fixed sparse stride, rotary encoding at positions I, local window of the
+    dense heads."""
+    _fields_ = [("first_token", ctypes.c_int32), ("fixed_stride", ctypes.c_int32),
+                ("rope", ctypes.c_int32), ("window", ctypes.c_int32), ("rope_base", ctypes.c_double)]
+
+
+def options(first_token=False, fixed_stride=0, rope=False, rope_base=10000.0, window=0):
+    return Options(int(bool(first_token)), int(fixed_stride), int(bool(rope)), int(window), float(rope_base))
+
+
 def _declare(L):
     L.orc_fsum.argtypes = [_p, ctypes.c_int64, _p]
     L.orc_router_keys.argtypes = [_i, _i, _i, _i, _i, _p, _p, _p]
@@ -43,11 +55,16 @@ def _declare(L):
     L.orc_head_attend.argtypes = [_i, _i, _i, _i, _i, _p, _p, _p, _p, _p, _p, _p, _p]
     L.orc_forward.argtypes = [_i] * 9 + [_p] * 18
     L.orc_backward.argtypes = [_i] * 9 + [_p] * 21
+    L.orc_forward_ex.argtypes = [_i] * 9 + [_p] * 18 + [ctypes.POINTER(Options)]
+    L.orc_backward_ex.argtypes = [_i] * 9 + [_p] * 21 + [ctypes.POINTER(Options)]
+    L.orc_select_ex.argtypes = [_i, _i, _i, _i, _i, _p, _p]
+    L.orc_rope.argtypes = [_i, _i, ctypes.c_double, _p, _i, _p]
     L.orc_max_threads.argtypes = []
     L.orc_set_threads.argtypes = [_i]
     L.orc_set_threads.restype = None
     for name in ("orc_fsum", "orc_router_keys", "orc_select", "orc_head_attend",
-                 "orc_forward", "orc_backward", "orc_max_threads"):
+                 "orc_forward", "orc_backward", "orc_max_threads", "orc_forward_ex", "orc_backward_ex",
+                 "orc_select_ex", "orc_rope"):
         getattr(L, name).restype = ctypes.c_int
 
 
@@ -101,13 +118,25 @@ def router_keys(X, Wr):
     return keys
 
 
-def select(keys, k):
-    """Expert-choice TopK per (b,h) row of keys [B,H,T]: I [B,H,k] ascending."""
+def select(keys, k, first_token=False):
+    """Expert-choice TopK per (b,h) row of keys [B,H,T]: I [B,H,k] ascending
+    (first_token: token 0 plus the best k - 1 of t >= 1)."""
     keys = np.ascontiguousarray(keys, dtype=np.float64)
     B, H, T = keys.shape
     I = np.empty((B, H, k), dtype=np.int32)
-    _check(lib().orc_select(B, H, T, k, _ptr(keys), _ptr(I)), "select")
+    _check(lib().orc_select_ex(B, H, T, k, int(bool(first_token)), _ptr(keys), _ptr(I)), "select")
     return I
+
+
+def rope(v, positions, base=10000.0, sign=1):
+    """Rotary encoding of the rows of v [n, dh] at the given positions (sign -1:
+    the inverse rotation); returns a new float64 array."""
+    out = np.array(v, dtype=np.float64, copy=True, order="C")
+    p = np.ascontiguousarray(positions, dtype=np.int32)
+    n, dh = out.shape
+    assert p.shape == (n,)
+    _check(lib().orc_rope(n, dh, float(base), _ptr(p), int(sign), _ptr(out)), "rope")
+    return out
 
 
 def head_attend(Xb, Wq, Wk, Wv, Wo, I, r=None, causal=True, Y=None):
@@ -129,7 +158,7 @@ def head_attend(Xb, Wq, Wk, Wv, Wo, I, r=None, causal=True, Y=None):
 
 def _unpack(inp):
     X = _c(inp["X"])
-    H = inp["Wr"].shape[0] if inp.get("Wr") is not None else 0
+    H = inp["Wq"].shape[0] if inp.get("Wq") is not None else 0
     Hd = inp["Wq_d"].shape[0] if inp.get("Wq_d") is not None else 0
     ws = [_c(inp.get(n)) for n in ("Wr", "Wq", "Wk", "Wv", "Wo", "Wq_d", "Wk_d", "Wv_d", "Wo_d")]
     if H > 0:
@@ -139,10 +168,11 @@ def _unpack(inp):
     return X, H, Hd, dh, ws
 
 
-def forward(inp, k, causal=True, intermediates=False):
+def forward(inp, k, causal=True, intermediates=False, opts=None):
     """Layer forward.  ``inp`` holds X [B,T,d] and the weights (see workloads.py).
     Returns dict with Y [B,T,d], I [B,H,k], r [B,H,k], keys [B,H,T] and, if
-    ``intermediates``, Q, K, V, A [B,H,k,dh] of the MoSA heads (float64)."""
+    ``intermediates``, Q, K, V (after the rotary encoding, if any), A
+    [B,H,k,dh] of the MoSA heads (float64).  ``opts``: ``options(...)``."""
     X, H, Hd, dh, ws = _unpack(inp)
     B, T, d = X.shape
     kk = k if H > 0 else 0
@@ -151,9 +181,10 @@ def forward(inp, k, causal=True, intermediates=False):
     r = np.empty((B, H, kk), dtype=np.float64)
     keys = np.empty((B, H, T), dtype=np.float64)
     qkva = [np.empty((B, H, kk, dh), dtype=np.float64) if intermediates else None for _ in range(4)]
-    st = lib().orc_forward(_dtype_code(X), B, T, d, H, dh, kk, int(causal), Hd, _ptr(X),
-                           *[_ptr(w) for w in ws], _ptr(Y), _ptr(I), _ptr(r), _ptr(keys),
-                           *[_ptr(a) for a in qkva])
+    o = options() if opts is None else opts
+    st = lib().orc_forward_ex(_dtype_code(X), B, T, d, H, dh, kk, int(causal), Hd, _ptr(X),
+                              *[_ptr(w) for w in ws], _ptr(Y), _ptr(I), _ptr(r), _ptr(keys),
+                              *[_ptr(a) for a in qkva], ctypes.byref(o))
     _check(st, "forward")
     out = {"Y": Y, "I": I, "r": r, "keys": keys}
     if intermediates:
@@ -161,7 +192,7 @@ def forward(inp, k, causal=True, intermediates=False):
     return out
 
 
-def backward(inp, dY, k, causal=True):
+def backward(inp, dY, k, causal=True, opts=None):
     """Layer backward (I held fixed).  Returns dict of float64 gradients:
     dX, dWr, dWq, dWk, dWv, dWo and, with dense heads, dWq_d, dWk_d, dWv_d, dWo_d."""
     X, H, Hd, dh, ws = _unpack(inp)
@@ -177,8 +208,9 @@ def backward(inp, dY, k, causal=True):
         g.update(dWq_d=np.empty((Hd, d, dh)), dWk_d=np.empty((Hd, d, dh)),
                  dWv_d=np.empty((Hd, d, dh)), dWo_d=np.empty((Hd, dh, d)))
     names = ("dWr", "dWq", "dWk", "dWv", "dWo", "dWq_d", "dWk_d", "dWv_d", "dWo_d")
-    st = lib().orc_backward(_dtype_code(X), B, T, d, H, dh, kk, int(causal), Hd, _ptr(X),
-                            *[_ptr(w) for w in ws], _ptr(dY), _ptr(g["dX"]),
-                            *[_ptr(g.get(n)) for n in names])
+    o = options() if opts is None else opts
+    st = lib().orc_backward_ex(_dtype_code(X), B, T, d, H, dh, kk, int(causal), Hd, _ptr(X),
+                               *[_ptr(w) for w in ws], _ptr(dY), _ptr(g["dX"]),
+                               *[_ptr(g.get(n)) for n in names], ctypes.byref(o))
     _check(st, "backward")
     return g

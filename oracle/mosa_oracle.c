@@ -28,6 +28,21 @@
  *            + sum over dense causal heads (Eq. 2; hybrid layer,
  *              "Hybridization" paragraph), i.e. heads with I = 0..T-1, r = 1.
  *
+ * Variants of the layer (orc_options; all off by default):
+ *   first_token  - every MoSA head always takes token 0 and chooses the other
+ *                  k - 1 among t >= 1 by router score; token 0 is scaled by
+ *                  its own r like any other (Section 3.2, IsoFLOP setting)
+ *   fixed_stride - fixed sparse attention as a special case of MoSA:
+ *                  I = 0, rho, 2 rho, ... and r = 1, no router (Section 3.1,
+ *                  "Fixed Sparse Attention")
+ *   rope         - rotary position encoding of q and k after the projections,
+ *                  at the original positions I (Section 2.2, "Positional
+ *                  encodings"); the first dh/2 dimensions are rotated in
+ *                  adjacent pairs (2j, 2j+1) by angle p base^(-2j/(dh/2)), the
+ *                  other half is left unchanged
+ *   window       - the dense heads are local (sliding-window) causal heads:
+ *                  query t sees keys t - window + 1 .. t (Section 3.4)
+ *
  * Backward: the chain rule through the same expressions with I held fixed
  * (TopK is piecewise constant; the router receives its gradient through r,
  * Section 2.2 last paragraph), sigma'(s) = r (1 - r).
@@ -56,6 +71,17 @@
  * "exact key" statement above holds for ORC_F32 and ORC_BF16 only. */
 enum { ORC_F32 = 0, ORC_BF16 = 1, ORC_F64 = 2 };
 enum { ORC_OK = 0, ORC_EINVAL = -1, ORC_ENOMEM = -2, ORC_EEXPANSION = -3 };
+
+/* Layer variants (see the header comment); NULL means all off. */
+typedef struct orc_options {
+    int32_t first_token;
+    int32_t fixed_stride;
+    int32_t rope;
+    int32_t window;
+    double rope_base;
+} orc_options;
+
+static const orc_options orc_defaults = {0, 0, 0, 0, 10000.0};
 
 /* ------------------------------------------------------------------------ */
 /* Input widening                                                            */
@@ -188,28 +214,57 @@ static int ascending_i32(const void* pa, const void* pb) {
     return (a > b) - (a < b);
 }
 
-/* The k tokens that come first under (key desc, t asc), written ascending. */
-static int select_row(int T, int k, const double* key, int32_t* I) {
+/* The k tokens that come first under (key desc, t asc), written ascending.
+ * first: token 0 is taken first and the other k - 1 come from t >= 1. */
+static int select_row(int T, int k, int first, const double* key, int32_t* I) {
     candidate* c = (candidate*)malloc((size_t)T * sizeof(candidate));
     if (!c) return ORC_ENOMEM;
-    for (int t = 0; t < T; ++t) {
-        c[t].key = key[t];
-        c[t].t = t;
+    const int t0 = first ? 1 : 0, n = T - t0;
+    for (int t = t0; t < T; ++t) {
+        c[t - t0].key = key[t];
+        c[t - t0].t = t;
     }
-    qsort(c, (size_t)T, sizeof(candidate), candidate_order);
-    for (int i = 0; i < k; ++i) I[i] = c[i].t;
+    qsort(c, (size_t)n, sizeof(candidate), candidate_order);
+    if (first) I[0] = 0;
+    for (int i = t0; i < k; ++i) I[i] = c[i - t0].t;
     qsort(I, (size_t)k, sizeof(int32_t), ascending_i32);
     free(c);
     return ORC_OK;
 }
 
-int orc_select(int B, int H, int T, int k, const double* keys, int32_t* I) {
+int orc_select_ex(int B, int H, int T, int k, int first_token, const double* keys, int32_t* I) {
     if (B < 1 || H < 1 || T < 1 || k < 1 || k > T || !keys || !I) return ORC_EINVAL;
     int err = 0;
 #pragma omp parallel for schedule(dynamic) reduction(| : err)
     for (int bh = 0; bh < B * H; ++bh)
-        err |= select_row(T, k, keys + (size_t)bh * T, I + (size_t)bh * k) ? 1 : 0;
+        err |= select_row(T, k, first_token != 0, keys + (size_t)bh * T, I + (size_t)bh * k) ? 1 : 0;
     return err ? ORC_ENOMEM : ORC_OK;
+}
+
+int orc_select(int B, int H, int T, int k, const double* keys, int32_t* I) {
+    return orc_select_ex(B, H, T, k, 0, keys, I);
+}
+
+/* Rotary encoding of one head vector v [dh] at position p (sign -1: the
+ * inverse rotation, the transpose used by the backward pass).  The first
+ * R = dh / 2 dimensions are rotated in pairs (2j, 2j+1), j < R / 2, by the
+ * angle p theta_j with theta_j = base^(-2j/R); the rest stay as they are. */
+static void rope_rotate(int dh, double base, double p, int sign, double* v) {
+    const int R = dh / 2;
+    for (int j = 0; j < R / 2; ++j) {
+        const double theta = pow(base, -2.0 * j / R);
+        const double a = sign * p * theta, c = cos(a), sn = sin(a);
+        const double x = v[2 * j], y = v[2 * j + 1];
+        v[2 * j] = x * c - y * sn;
+        v[2 * j + 1] = x * sn + y * c;
+    }
+}
+
+/* Exported for the oracle's own tests: rotate n vectors of dh at positions p. */
+int orc_rope(int n, int dh, double base, const int32_t* p, int sign, double* v) {
+    if (n < 0 || dh < 4 || dh % 4 || !(base > 1.0) || (sign != 1 && sign != -1) || !p || !v) return ORC_EINVAL;
+    for (int i = 0; i < n; ++i) rope_rotate(dh, base, (double)p[i], sign, v + (size_t)i * dh);
+    return ORC_OK;
 }
 
 /* ------------------------------------------------------------------------ */
@@ -253,14 +308,23 @@ static void project(int n, int d, int dh, const double* Xs, const double* W, dou
         }
 }
 
-static int may_attend(int causal, const int32_t* I, int i, int j) {
-    return !causal || I[i] >= I[j];
+/* Per-head attention options: the causal flag, the local window (dense
+ * heads; 0 = none) and the rotary encoding (rope_base > 0) at positions I. */
+typedef struct {
+    int causal, window;
+    double rope_base;
+} head_opts;
+
+static int may_attend(const head_opts* o, const int32_t* I, int i, int j) {
+    if (o->causal && I[i] < I[j]) return 0;
+    if (o->window > 0 && I[i] - I[j] >= o->window) return 0;
+    return 1;
 }
 
 /* Forward of one head on the n tokens I (any order, no repeats).
  * Xb: [T, d] rows of one batch element; W*: [d, dh]; Wo: [dh, d].
  * Writes Xo[i, :] = r_i * A_i W^O for i < n.  r == NULL means r = 1. */
-static void head_forward(int d, int dh, int n, int causal, const double* Xb, const double* Wq,
+static void head_forward(int d, int dh, int n, const head_opts* o, const double* Xb, const double* Wq,
                          const double* Wk, const double* Wv, const double* Wo, const int32_t* I,
                          const double* r, head_state* s, double* Xo) {
     /* gather */
@@ -270,13 +334,19 @@ static void head_forward(int d, int dh, int n, int causal, const double* Xb, con
     project(n, d, dh, s->Xs, Wq, s->Q);
     project(n, d, dh, s->Xs, Wk, s->K);
     project(n, d, dh, s->Xs, Wv, s->V);
+    /* rotary encoding of q and k at the original positions I */
+    if (o->rope_base > 0.0)
+        for (int i = 0; i < n; ++i) {
+            rope_rotate(dh, o->rope_base, (double)I[i], 1, s->Q + (size_t)i * dh);
+            rope_rotate(dh, o->rope_base, (double)I[i], 1, s->K + (size_t)i * dh);
+        }
     /* attention, Eq. 1: P = softmax((Q K^T + M) / sqrt(h')), computed max-subtracted */
     const double scale = 1.0 / sqrt((double)dh);
     for (int i = 0; i < n; ++i) {
         double* Pi = s->P + (size_t)i * n;
         double mx = -INFINITY;
         for (int j = 0; j < n; ++j) {
-            if (!may_attend(causal, I, i, j)) continue;
+            if (!may_attend(o, I, i, j)) continue;
             double dot = 0.0;
             for (int e = 0; e < dh; ++e) dot += s->Q[(size_t)i * dh + e] * s->K[(size_t)j * dh + e];
             Pi[j] = dot * scale;
@@ -284,7 +354,7 @@ static void head_forward(int d, int dh, int n, int causal, const double* Xb, con
         }
         double den = 0.0;
         for (int j = 0; j < n; ++j) {
-            if (!may_attend(causal, I, i, j)) { Pi[j] = 0.0; continue; }
+            if (!may_attend(o, I, i, j)) { Pi[j] = 0.0; continue; }
             Pi[j] = exp(Pi[j] - mx);
             den += Pi[j];
         }
@@ -309,10 +379,10 @@ static void head_forward(int d, int dh, int n, int causal, const double* Xb, con
 /* Backward of one head given dXo = dY[I] (n x d).  Accumulates into the
  * per-head weight gradients (caller owns them, no sharing between threads),
  * writes dXs (n x d) and, when r != NULL, the router gradient into dWr. */
-static void head_backward(int d, int dh, int n, const double* Wq, const double* Wk,
-                          const double* Wv, const double* Wo, const double* Wr, const double* r,
-                          const head_state* s, const double* dXo, double* dWq, double* dWk,
-                          double* dWv, double* dWo, double* dWr, double* dXs) {
+static void head_backward(int d, int dh, int n, const head_opts* o, const int32_t* I, const double* Wq,
+                          const double* Wk, const double* Wv, const double* Wo, const double* Wr,
+                          const double* r, const head_state* s, const double* dXo, double* dWq,
+                          double* dWk, double* dWv, double* dWo, double* dWr, double* dXs) {
     const double scale = 1.0 / sqrt((double)dh);
     double* dAt = (double*)calloc((size_t)n * dh, sizeof(double)); /* d(diag(r) A) */
     double* dA = (double*)calloc((size_t)n * dh, sizeof(double));
@@ -375,6 +445,12 @@ static void head_backward(int d, int dh, int n, const double* Wq, const double* 
             for (int i = 0; i < n; ++i) acc += dP[(size_t)i * n + j] * s->Q[(size_t)i * dh + e];
             dK[(size_t)j * dh + e] = acc * scale;
         }
+    /* through the rotation: d(X^s W^Q) = R(p)^T dQ, likewise for K */
+    if (o->rope_base > 0.0)
+        for (int i = 0; i < n; ++i) {
+            rope_rotate(dh, o->rope_base, (double)I[i], -1, dQ + (size_t)i * dh);
+            rope_rotate(dh, o->rope_base, (double)I[i], -1, dK + (size_t)i * dh);
+        }
     /* projections Q = Xs W^Q etc., router s = Xs W^r */
     for (int c = 0; c < d; ++c) {
         for (int e = 0; e < dh; ++e) {
@@ -421,7 +497,8 @@ int orc_head_attend(int T, int d, int dh, int n, int causal, const double* Xb, c
     if (head_state_alloc(&s, n, d, dh)) return ORC_ENOMEM;
     double* Xo = (double*)malloc((size_t)n * d * sizeof(double));
     if (!Xo) { head_state_free(&s); return ORC_ENOMEM; }
-    head_forward(d, dh, n, causal, Xb, Wq, Wk, Wv, Wo, I, r, &s, Xo);
+    const head_opts o = {causal, 0, 0.0};
+    head_forward(d, dh, n, &o, Xb, Wq, Wk, Wv, Wo, I, r, &s, Xo);
     for (int i = 0; i < n; ++i)
         for (int c = 0; c < d; ++c) Y[(size_t)I[i] * d + c] += Xo[(size_t)i * d + c];
     free(Xo);
@@ -435,7 +512,18 @@ int orc_head_attend(int T, int d, int dh, int n, int causal, const double* Xb, c
 
 typedef struct {
     int dtype, B, T, d, H, dh, k, causal, Hd;
+    orc_options opt;
 } layer_shape;
+
+/* Attention options of the MoSA heads and of the dense heads. */
+static head_opts mosa_opts(const layer_shape* L) {
+    head_opts o = {L->causal, 0, L->opt.rope ? L->opt.rope_base : 0.0};
+    return o;
+}
+static head_opts dense_opts(const layer_shape* L) {
+    head_opts o = {L->causal, L->opt.window, L->opt.rope ? L->opt.rope_base : 0.0};
+    return o;
+}
 
 typedef struct {
     double *Wr, *Wq, *Wk, *Wv, *Wo;     /* MoSA heads */
@@ -454,7 +542,8 @@ static int weights_widen(const layer_shape* L, const void* Wr, const void* Wq, c
     memset(w, 0, sizeof *w);
     size_t proj = (size_t)L->d * L->dh;
     if (L->H > 0) {
-        w->Wr = widen_all(Wr, L->dtype, (size_t)L->H * L->d);
+        /* fixed sparse attention has no router: W^r may be NULL */
+        w->Wr = Wr ? widen_all(Wr, L->dtype, (size_t)L->H * L->d) : (double*)calloc((size_t)L->H * L->d, sizeof(double));
         w->Wq = widen_all(Wq, L->dtype, (size_t)L->H * proj);
         w->Wk = widen_all(Wk, L->dtype, (size_t)L->H * proj);
         w->Wv = widen_all(Wv, L->dtype, (size_t)L->H * proj);
@@ -480,17 +569,32 @@ static int shape_ok(const layer_shape* L, const void* X, const void* Wr, const v
     if (L->dtype != ORC_F32 && L->dtype != ORC_BF16 && L->dtype != ORC_F64) return 0;
     if (L->B < 1 || L->T < 1 || L->d < 1 || L->dh < 1 || L->H < 0 || L->Hd < 0) return 0;
     if (L->H + L->Hd < 1 || !X) return 0;
-    if (L->H > 0 && (L->k < 1 || L->k > L->T || !Wr || !Wq || !Wk || !Wv || !Wo)) return 0;
+    if (L->H > 0 && (L->k < 1 || L->k > L->T || !Wq || !Wk || !Wv || !Wo)) return 0;
+    if (L->H > 0 && !Wr && L->opt.fixed_stride <= 0) return 0;
     if (L->Hd > 0 && (!Wqd || !Wkd || !Wvd || !Wod)) return 0;
+    const orc_options* o = &L->opt;
+    if (o->fixed_stride < 0 || o->window < 0 || (o->rope && !(o->rope_base > 1.0))) return 0;
+    if (o->rope && L->dh % 4) return 0;
+    if (o->fixed_stride > 0 && (o->first_token || (double)(L->k - 1) * o->fixed_stride > L->T - 1)) return 0;
     return 1;
 }
 
 /* Selection for every (b,h): I [B,H,k] ascending, r [B,H,k], keys [B,H,T]. */
 static int layer_select(const layer_shape* L, const void* X, const void* Wr, double* keys,
                         int32_t* I, double* r) {
+    if (L->opt.fixed_stride > 0) {
+        /* I = 0, rho, 2 rho, ...; r = 1; no router (keys reported as 0) */
+        memset(keys, 0, (size_t)L->B * L->H * L->T * sizeof(double));
+        for (size_t bh = 0; bh < (size_t)L->B * L->H; ++bh)
+            for (int i = 0; i < L->k; ++i) {
+                I[bh * L->k + i] = i * L->opt.fixed_stride;
+                r[bh * L->k + i] = 1.0;
+            }
+        return ORC_OK;
+    }
     int e = orc_router_keys(L->dtype, L->B, L->T, L->d, L->H, X, Wr, keys);
     if (e) return e;
-    e = orc_select(L->B, L->H, L->T, L->k, keys, I);
+    e = orc_select_ex(L->B, L->H, L->T, L->k, L->opt.first_token, keys, I);
     if (e) return e;
     for (size_t bh = 0; bh < (size_t)L->B * L->H; ++bh)
         for (int i = 0; i < L->k; ++i) {
@@ -504,12 +608,12 @@ static int layer_select(const layer_shape* L, const void* X, const void* Wr, dou
  * Optional outputs (NULL to skip): I_out [B,H,k], r_out [B,H,k],
  * keys_out [B,H,T], and the per-head intermediates of the MoSA heads
  * Q_out, K_out, V_out, A_out [B,H,k,dh] (A before the router scaling). */
-int orc_forward(int dtype, int B, int T, int d, int H, int dh, int k, int causal, int Hd,
-                const void* X, const void* Wr, const void* Wq, const void* Wk, const void* Wv,
-                const void* Wo, const void* Wqd, const void* Wkd, const void* Wvd,
-                const void* Wod, double* Y, int32_t* I_out, double* r_out, double* keys_out,
-                double* Q_out, double* K_out, double* V_out, double* A_out) {
-    layer_shape L = {dtype, B, T, d, H, dh, k, causal, Hd};
+int orc_forward_ex(int dtype, int B, int T, int d, int H, int dh, int k, int causal, int Hd,
+                   const void* X, const void* Wr, const void* Wq, const void* Wk, const void* Wv,
+                   const void* Wo, const void* Wqd, const void* Wkd, const void* Wvd,
+                   const void* Wod, double* Y, int32_t* I_out, double* r_out, double* keys_out,
+                   double* Q_out, double* K_out, double* V_out, double* A_out, const orc_options* opt) {
+    layer_shape L = {dtype, B, T, d, H, dh, k, causal, Hd, opt ? *opt : orc_defaults};
     if (!shape_ok(&L, X, Wr, Wq, Wk, Wv, Wo, Wqd, Wkd, Wvd, Wod) || !Y) return ORC_EINVAL;
     const size_t proj = (size_t)d * dh;
     int err = ORC_ENOMEM;
@@ -540,7 +644,8 @@ int orc_forward(int dtype, int B, int T, int d, int H, int dh, int k, int causal
         int b = bh / H, h = bh % H;
         head_state s;
         if (head_state_alloc(&s, k, d, dh)) { fail |= 1; continue; }
-        head_forward(d, dh, k, causal, Xd + (size_t)b * T * d, w.Wq + h * proj, w.Wk + h * proj,
+        const head_opts o = mosa_opts(&L);
+        head_forward(d, dh, k, &o, Xd + (size_t)b * T * d, w.Wq + h * proj, w.Wk + h * proj,
                      w.Wv + h * proj, w.Wo + h * proj, I + (size_t)bh * k, r + (size_t)bh * k, &s,
                      XoM + (size_t)bh * k * d);
         size_t qo = (size_t)bh * k * dh;
@@ -556,7 +661,8 @@ int orc_forward(int dtype, int B, int T, int d, int H, int dh, int k, int causal
         int b = bh / Hd, h = bh % Hd;
         head_state s;
         if (head_state_alloc(&s, T, d, dh)) { fail |= 1; continue; }
-        head_forward(d, dh, T, causal, Xd + (size_t)b * T * d, w.Wqd + h * proj, w.Wkd + h * proj,
+        const head_opts o = dense_opts(&L);
+        head_forward(d, dh, T, &o, Xd + (size_t)b * T * d, w.Wqd + h * proj, w.Wkd + h * proj,
                      w.Wvd + h * proj, w.Wod + h * proj, iota, NULL, &s,
                      XoD + (size_t)bh * T * d);
         head_state_free(&s);
@@ -594,13 +700,13 @@ done:
  * Outputs (double, written not accumulated): dX [B,T,d], dWr [H,d],
  * dWq/dWk/dWv [H,d,dh], dWo [H,dh,d], and the dense-head gradients
  * dWqd/dWkd/dWvd [Hd,d,dh], dWod [Hd,dh,d] (NULL allowed when Hd == 0). */
-int orc_backward(int dtype, int B, int T, int d, int H, int dh, int k, int causal, int Hd,
-                 const void* X, const void* Wr, const void* Wq, const void* Wk, const void* Wv,
-                 const void* Wo, const void* Wqd, const void* Wkd, const void* Wvd,
-                 const void* Wod, const void* dY, double* dX, double* dWr, double* dWq,
-                 double* dWk, double* dWv, double* dWo, double* dWqd, double* dWkd, double* dWvd,
-                 double* dWod) {
-    layer_shape L = {dtype, B, T, d, H, dh, k, causal, Hd};
+int orc_backward_ex(int dtype, int B, int T, int d, int H, int dh, int k, int causal, int Hd,
+                    const void* X, const void* Wr, const void* Wq, const void* Wk, const void* Wv,
+                    const void* Wo, const void* Wqd, const void* Wkd, const void* Wvd,
+                    const void* Wod, const void* dY, double* dX, double* dWr, double* dWq,
+                    double* dWk, double* dWv, double* dWo, double* dWqd, double* dWkd, double* dWvd,
+                    double* dWod, const orc_options* opt) {
+    layer_shape L = {dtype, B, T, d, H, dh, k, causal, Hd, opt ? *opt : orc_defaults};
     if (!shape_ok(&L, X, Wr, Wq, Wk, Wv, Wo, Wqd, Wkd, Wvd, Wod) || !dY || !dX) return ORC_EINVAL;
     if (H > 0 && (!dWr || !dWq || !dWk || !dWv || !dWo)) return ORC_EINVAL;
     if (Hd > 0 && (!dWqd || !dWkd || !dWvd || !dWod)) return ORC_EINVAL;
@@ -647,15 +753,18 @@ int orc_backward(int dtype, int B, int T, int d, int H, int dh, int k, int causa
         double* dXo = (double*)malloc((size_t)k * d * sizeof(double));
         double* Xo = (double*)malloc((size_t)k * d * sizeof(double));
         if (!dXo || !Xo || head_state_alloc(&s, k, d, dh)) { fail |= 1; free(dXo); free(Xo); continue; }
+        const head_opts o = mosa_opts(&L);
+        /* fixed sparse attention: r = 1 and no router gradient */
+        const int routed = L.opt.fixed_stride <= 0;
         for (int b = 0; b < B; ++b) {
             size_t bh = (size_t)b * H + h;
             const int32_t* Ib = I + bh * k;
-            head_forward(d, dh, k, causal, Xd + (size_t)b * T * d, w.Wq + h * proj,
+            head_forward(d, dh, k, &o, Xd + (size_t)b * T * d, w.Wq + h * proj,
                          w.Wk + h * proj, w.Wv + h * proj, w.Wo + h * proj, Ib, r + bh * k, &s, Xo);
             for (int i = 0; i < k; ++i)
                 memcpy(dXo + (size_t)i * d, dYd + ((size_t)b * T + Ib[i]) * d, (size_t)d * sizeof(double));
-            head_backward(d, dh, k, w.Wq + h * proj, w.Wk + h * proj, w.Wv + h * proj,
-                          w.Wo + h * proj, w.Wr + (size_t)h * d, r + bh * k, &s, dXo,
+            head_backward(d, dh, k, &o, Ib, w.Wq + h * proj, w.Wk + h * proj, w.Wv + h * proj,
+                          w.Wo + h * proj, w.Wr + (size_t)h * d, routed ? r + bh * k : NULL, &s, dXo,
                           dWq + h * proj, dWk + h * proj, dWv + h * proj, dWo + h * proj,
                           dWr + (size_t)h * d, dXsM + bh * k * d);
         }
@@ -668,12 +777,13 @@ int orc_backward(int dtype, int B, int T, int d, int H, int dh, int k, int causa
         double* dXo = (double*)malloc((size_t)T * d * sizeof(double));
         double* Xo = (double*)malloc((size_t)T * d * sizeof(double));
         if (!dXo || !Xo || head_state_alloc(&s, T, d, dh)) { fail |= 1; free(dXo); free(Xo); continue; }
+        const head_opts o = dense_opts(&L);
         for (int b = 0; b < B; ++b) {
             size_t bh = (size_t)b * Hd + h;
-            head_forward(d, dh, T, causal, Xd + (size_t)b * T * d, w.Wqd + h * proj,
+            head_forward(d, dh, T, &o, Xd + (size_t)b * T * d, w.Wqd + h * proj,
                          w.Wkd + h * proj, w.Wvd + h * proj, w.Wod + h * proj, iota, NULL, &s, Xo);
             memcpy(dXo, dYd + (size_t)b * T * d, (size_t)T * d * sizeof(double));
-            head_backward(d, dh, T, w.Wqd + h * proj, w.Wkd + h * proj, w.Wvd + h * proj,
+            head_backward(d, dh, T, &o, iota, w.Wqd + h * proj, w.Wkd + h * proj, w.Wvd + h * proj,
                           w.Wod + h * proj, NULL, NULL, &s, dXo, dWqd + h * proj, dWkd + h * proj,
                           dWvd + h * proj, dWod + h * proj, NULL, dXsD + bh * T * d);
         }
@@ -704,6 +814,25 @@ done:
     free(keys); free(I); free(r); free(dXsM); free(dXsD); free(iota); free(Xd); free(dYd);
     weights_free(&w);
     return err;
+}
+
+int orc_forward(int dtype, int B, int T, int d, int H, int dh, int k, int causal, int Hd,
+                const void* X, const void* Wr, const void* Wq, const void* Wk, const void* Wv,
+                const void* Wo, const void* Wqd, const void* Wkd, const void* Wvd,
+                const void* Wod, double* Y, int32_t* I_out, double* r_out, double* keys_out,
+                double* Q_out, double* K_out, double* V_out, double* A_out) {
+    return orc_forward_ex(dtype, B, T, d, H, dh, k, causal, Hd, X, Wr, Wq, Wk, Wv, Wo, Wqd, Wkd, Wvd, Wod, Y,
+                          I_out, r_out, keys_out, Q_out, K_out, V_out, A_out, NULL);
+}
+
+int orc_backward(int dtype, int B, int T, int d, int H, int dh, int k, int causal, int Hd,
+                 const void* X, const void* Wr, const void* Wq, const void* Wk, const void* Wv,
+                 const void* Wo, const void* Wqd, const void* Wkd, const void* Wvd,
+                 const void* Wod, const void* dY, double* dX, double* dWr, double* dWq,
+                 double* dWk, double* dWv, double* dWo, double* dWqd, double* dWkd, double* dWvd,
+                 double* dWod) {
+    return orc_backward_ex(dtype, B, T, d, H, dh, k, causal, Hd, X, Wr, Wq, Wk, Wv, Wo, Wqd, Wkd, Wvd, Wod, dY,
+                           dX, dWr, dWq, dWk, dWv, dWo, dWqd, dWkd, dWvd, dWod, NULL);
 }
 
 int orc_max_threads(void) {
