@@ -121,9 +121,10 @@ def cpu_baseline(w, inp, with_backward, target_s):
         sub = dict(inp)
         sub["X"] = np.ascontiguousarray(inp["X"][:nb])
         t0 = time.perf_counter()
-        oracle.forward(sub, w.k, causal=w.causal)
+        oracle.forward(sub, w.k, causal=w.causal, opts=oracle.options(**w.variants()))
         if with_backward:
-            oracle.backward(sub, np.ascontiguousarray(inp["dY"][:nb]), w.k, causal=w.causal)
+            oracle.backward(sub, np.ascontiguousarray(inp["dY"][:nb]), w.k, causal=w.causal,
+                            opts=oracle.options(**w.variants()))
         return time.perf_counter() - t0
 
     t1 = run(1)
@@ -164,7 +165,8 @@ def main():
         return torch.from_numpy(a).cuda()
 
     d = {n: dev(v) for n, v in inp.items()}
-    shape = mosa.make_shape(w.batch, w.seq_len, w.d_model, w.heads, w.d_head, w.k, w.causal, w.dense_heads, w.dtype)
+    shape = mosa.make_shape(w.batch, w.seq_len, w.d_model, w.heads, w.d_head, w.k, w.causal, w.dense_heads, w.dtype,
+                            **w.variants())
     weights = {n: d.get(n) for n in mosa.WEIGHT_NAMES}
     saved, scratch = mosa.alloc_workspace(shape)
     Y = torch.empty_like(d["X"])

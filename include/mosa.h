@@ -60,7 +60,29 @@ typedef enum { MOSA_F32 = 0, MOSA_BF16 = 1 } mosa_dtype;
 /* Shape of one layer call.  Limits: batch >= 1; 1 <= seq_len <= 16384;
  * d_model a multiple of 64; d_head 32 or 64; heads >= 0 and dense_heads >= 0
  * with heads + dense_heads >= 1; 1 <= k <= seq_len when heads > 0
- * (k = seq_len selects every token); causal 0 or 1. */
+ * (k = seq_len selects every token); causal 0 or 1.
+ *
+ * Variants of the layer (0 = off; a zero-initialised tail gives the plain
+ * layer):
+ *   first_token   1: every MoSA head always keeps token 0 and chooses the
+ *                 other k - 1 among t >= 1 by router score; token 0 is scaled
+ *                 by its own r (Section 3.2, IsoFLOP setting).
+ *   fixed_stride  rho > 0: fixed sparse attention as a special case of MoSA
+ *                 (Section 3.1): I = 0, rho, ..., (k - 1) rho for every head
+ *                 and batch element, r = 1, no router.  Needs
+ *                 (k - 1) rho <= seq_len - 1 and first_token == 0; W^r may be
+ *                 NULL in mosa_forward / mosa_backward and dW^r NULL in
+ *                 mosa_backward (when given it is written with zeros).
+ *   rope          1: rotary position encoding of q and k after the
+ *                 projections, at the tokens' ORIGINAL positions I
+ *                 (Section 2.2, "Positional encodings"); dense heads use
+ *                 positions 0..T-1.  The first d_head/2 dimensions are rotated
+ *                 in adjacent pairs (2j, 2j+1) by the angle
+ *                 p * rope_base^(-2j/(d_head/2)); the other half is unchanged.
+ *   rope_base     the base of those angles (> 1; used when rope == 1).
+ *   window        w > 0: the dense heads are local (sliding-window) causal
+ *                 heads, query t seeing keys t - w + 1 .. t (Section 3.4);
+ *                 needs causal == 1. */
 typedef struct mosa_shape {
     int32_t batch;       /* B */
     int32_t seq_len;     /* T */
@@ -71,7 +93,16 @@ typedef struct mosa_shape {
     int32_t causal;      /* 1: M_ij = 0 iff I_i >= I_j; 0: no mask */
     int32_t dense_heads; /* Hd, dense heads (all T tokens, r = 1) */
     int32_t dtype;       /* mosa_dtype */
+    int32_t first_token; /* variants, see above */
+    int32_t fixed_stride;
+    int32_t rope;
+    float rope_base;
+    int32_t window;
 } mosa_shape;
+
+/* The paper's adaptive k for short inputs (Section 3.5): max(floor(T / rho), 2),
+ * clamped to T; rho >= 1. Returns 0 for invalid arguments. */
+int mosa_adaptive_k(int seq_len, int rho);
 
 /* Layer parameters, theta_h = (W^Q, W^K, W^V, W^O, W^r) per head (Section 2.2),
  * in the paper's X W orientation:
@@ -112,9 +143,10 @@ typedef struct mosa_grads {
  *     router value: r_i (softmax(Q K^T / sqrt(dh) + M) V)_i);
  *   lse [B,H,k] fp32 (natural-log sum of exp of the scaled scores);
  *   the same for the dense heads with k = T: QKVd [B,Hd,T,3,dh], Ad [B,Hd,T,dh],
- *   lsed [B,Hd,T]. */
+ *   lsed [B,Hd,T];
+ *   rope [T, dh/4] float2 (cos, sin) table of the rotary encoding (rope == 1). */
 typedef struct mosa_saved_layout {
-    size_t I, r, slot, QKV, A, lse, QKVd, Ad, lsed;
+    size_t I, r, slot, QKV, A, lse, QKVd, Ad, lsed, rope;
     size_t total;
 } mosa_saved_layout;
 

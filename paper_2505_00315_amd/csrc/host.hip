@@ -19,7 +19,7 @@ struct Layout {
     // forward scratch
     size_t z, xnorm, unc_tok, unc_key, unc_sel, Xo, ybase;
     // backward scratch
-    size_t dA, D, dz, dz16, dQKV, dXs, dAd, Dd, dQKVd, wpart, dxbase;
+    size_t dA, D, dz, dz16, dQKV, dXs, dAd, Dd, dQKVd, wpart, dxbase, dwr;
     size_t scratch_total;
 };
 
@@ -51,8 +51,20 @@ int validate_shape(const mosa_shape* s) {
     if (rows > 2.0e9) return MOSA_ERR_UNSUPPORTED;
     // row counts of one head (B * k or B * T) are divided with a float reciprocal
     if ((double)s->batch * s->seq_len >= 16777216.0) return MOSA_ERR_UNSUPPORTED;
+    // variants
+    if (s->first_token != 0 && s->first_token != 1) return MOSA_ERR_INVALID_ARG;
+    if (s->rope != 0 && s->rope != 1) return MOSA_ERR_INVALID_ARG;
+    if (s->fixed_stride < 0 || s->window < 0) return MOSA_ERR_INVALID_ARG;
+    if (s->rope && !(s->rope_base > 1.0f)) return MOSA_ERR_INVALID_ARG;
+    if (s->window > 0 && !s->causal) return MOSA_ERR_INVALID_ARG;
+    if (s->window > 0 && s->dense_heads > 0) return MOSA_ERR_UNSUPPORTED;  // local heads: not built yet
+    if (s->heads > 0 && s->fixed_stride > 0 &&
+        (s->first_token || (long long)(s->k - 1) * s->fixed_stride > s->seq_len - 1))
+        return MOSA_ERR_INVALID_ARG;
     return MOSA_OK;
 }
+
+bool routed(const mosa_shape* s) { return s->heads > 0 && s->fixed_stride == 0; }
 
 Layout make_layout(const mosa_shape* s) {
     const size_t B = s->batch, T = s->seq_len, d = s->d_model, H = s->heads, Hd = s->dense_heads, dh = s->d_head;
@@ -69,6 +81,7 @@ Layout make_layout(const mosa_shape* s) {
     L.saved.QKVd = sv.take(B * Hd * T * 3 * dh * es);
     L.saved.Ad = sv.take(B * Hd * T * dh * es);
     L.saved.lsed = sv.take(B * Hd * T * 4);
+    L.saved.rope = sv.take(s->rope ? T * (dh / 4) * 8 : 0);  // (cos, sin) table
     L.saved.total = sv.total();
 
     // forward and backward scratch share the same buffer (used at different times)
@@ -91,6 +104,7 @@ Layout make_layout(const mosa_shape* s) {
     L.Dd = bw.take(B * Hd * T * 4);
     L.dQKVd = bw.take(B * Hd * T * 3 * dh * es);
     L.dxbase = bw.take(Hd > 0 ? B * T * d * 4 : 0);  // dense heads' part of dX (fp32)
+    L.dwr = bw.take(H > 0 && s->fixed_stride > 0 ? H * d * es : 0);  // dW^r sink without a router
     {
         const int dt = s->dtype == MOSA_BF16 ? kBF16 : kF32;
         const size_t pm = wgrad_partial_bytes(dt, (int)B, (int)d, (int)H, (int)dh, (int)k, 1);
@@ -106,9 +120,11 @@ inline bool aligned(const void* p, size_t a) { return ((uintptr_t)p % a) == 0; }
 int check_weights(const mosa_shape* s, const mosa_weights* w) {
     if (!w) return MOSA_ERR_INVALID_ARG;
     if (s->heads > 0) {
-        const void* need[5] = {w->Wr, w->Wq, w->Wk, w->Wv, w->Wo};
+        const void* need[4] = {w->Wq, w->Wk, w->Wv, w->Wo};
         for (const void* p : need)
             if (!p || !aligned(p, 16)) return MOSA_ERR_INVALID_ARG;
+        // fixed sparse attention has no router: W^r may be NULL
+        if ((routed(s) && !w->Wr) || (w->Wr && !aligned(w->Wr, 16))) return MOSA_ERR_INVALID_ARG;
     }
     if (s->dense_heads > 0) {
         const void* need[4] = {w->Wq_d, w->Wk_d, w->Wv_d, w->Wo_d};
@@ -201,18 +217,28 @@ int mosa_forward_timed(const mosa_shape* s, const void* X, const mosa_weights* w
     float* lsed = at<float>(saved, L.saved.lsed);
     void* Xo = at<char>(scratch, L.Xo);
 
+    float2* rope = s->rope ? at<float2>(saved, L.saved.rope) : nullptr;
+    if (rope) {
+        e |= launch_rope_table(T, dh, s->rope_base, rope, stream);
+        e |= sm.mark("rope_table");
+    }
     if (H > 0) {
-        float* z = at<float>(scratch, L.z);
-        float* xnorm = at<float>(scratch, L.xnorm);
-        e |= launch_router(dt, X, w->Wr, B, T, d, H, z, xnorm, stream);
-        e |= sm.mark("router");
-        e |= launch_select(dt, z, xnorm, X, w->Wr, B, T, d, H, k, I, r, slot, at<int32_t>(scratch, L.unc_tok),
-                           at<double>(scratch, L.unc_key), at<int32_t>(scratch, L.unc_sel), stream);
+        if (routed(s)) {
+            float* z = at<float>(scratch, L.z);
+            float* xnorm = at<float>(scratch, L.xnorm);
+            e |= launch_router(dt, X, w->Wr, B, T, d, H, z, xnorm, stream);
+            e |= sm.mark("router");
+            e |= launch_select(dt, z, xnorm, X, w->Wr, B, T, d, H, k, s->first_token, I, r, slot,
+                               at<int32_t>(scratch, L.unc_tok), at<double>(scratch, L.unc_key),
+                               at<int32_t>(scratch, L.unc_sel), stream);
+        } else {
+            e |= launch_fixed_select(B, T, H, k, s->fixed_stride, I, r, slot, stream);
+        }
         e |= sm.mark("select");
-        const int fused = launch_qkv_attn(dt, X, I, w->Wq, w->Wk, w->Wv, B, T, d, H, dh, k, QKV, r, causal, A, lse,
-                                          stream);
+        const int fused = launch_qkv_attn(dt, X, I, w->Wq, w->Wk, w->Wv, B, T, d, H, dh, k, QKV, rope, r, causal, A,
+                                          lse, stream);
         if (fused == 1) {
-            e |= launch_qkv(dt, X, I, w->Wq, w->Wk, w->Wv, B, T, d, H, dh, k, QKV, stream);
+            e |= launch_qkv(dt, X, I, w->Wq, w->Wk, w->Wv, B, T, d, H, dh, k, QKV, rope, stream);
             e |= sm.mark("qkv");
             e |= launch_attn_fwd(dt, QKV, r, B * H, k, dh, causal, A, lse, stream);
             e |= sm.mark("attn");
@@ -224,7 +250,7 @@ int mosa_forward_timed(const mosa_shape* s, const void* X, const mosa_weights* w
         e |= sm.mark("out_proj");
     }
     if (Hd > 0) {
-        e |= launch_qkv(dt, X, nullptr, w->Wq_d, w->Wk_d, w->Wv_d, B, T, d, Hd, dh, T, QKVd, stream);
+        e |= launch_qkv(dt, X, nullptr, w->Wq_d, w->Wk_d, w->Wv_d, B, T, d, Hd, dh, T, QKVd, rope, stream);
         e |= sm.mark("qkv_dense");
         e |= launch_attn_fwd(dt, QKVd, nullptr, B * Hd, T, dh, causal, Ad, lsed, stream);
         e |= sm.mark("attn_dense");
@@ -255,9 +281,10 @@ int mosa_backward_timed(const mosa_shape* s, const void* X, const mosa_weights* 
     if (!X || !dY || !dX || !g || !aligned(X, 16) || !aligned(dY, 16) || !aligned(dX, 16)) return MOSA_ERR_INVALID_ARG;
     if (!saved || !scratch || !aligned(saved, kAlign) || !aligned(scratch, kAlign)) return MOSA_ERR_INVALID_ARG;
     if (s->heads > 0) {
-        const void* need[5] = {g->dWr, g->dWq, g->dWk, g->dWv, g->dWo};
+        const void* need[4] = {g->dWq, g->dWk, g->dWv, g->dWo};
         for (const void* p : need)
             if (!p || !aligned(p, 16)) return MOSA_ERR_INVALID_ARG;
+        if ((routed(s) && !g->dWr) || (g->dWr && !aligned(g->dWr, 16))) return MOSA_ERR_INVALID_ARG;
     }
     if (s->dense_heads > 0) {
         const void* need[4] = {g->dWq_d, g->dWk_d, g->dWv_d, g->dWo_d};
@@ -292,6 +319,13 @@ int mosa_backward_timed(const mosa_shape* s, const void* X, const mosa_weights* 
     float* Dd = at<float>(scratch, L.Dd);
     void* dQKVd = at<char>(scratch, L.dQKVd);
     float* wpart = at<float>(scratch, L.wpart);
+    const float2* rope = s->rope ? at<float2>(saved, L.saved.rope) : nullptr;
+    // Without a router (fixed sparse attention) r = 1, so dz = dr r (1 - r) = 0
+    // and every router term vanishes; W^Q stands in for the unread-in-effect
+    // W^r rows (multiplied by dz = 0) and dW^r (all zeros) goes to a sink
+    // when the caller passes none.
+    const void* Wr = w->Wr ? w->Wr : w->Wq;
+    void* dWr = g->dWr ? g->dWr : at<char>(scratch, L.dwr);
 
     if (H > 0) {
         e |= launch_dattn_out(dt, dY, I, r, w->Wo, A, B, T, d, H, dh, k, dA, D, dz, dz16, stream);
@@ -300,16 +334,20 @@ int mosa_backward_timed(const mosa_shape* s, const void* X, const mosa_weights* 
         e |= sm.mark("attn_bwd_kv");
         e |= launch_attn_bwd(dt, QKV, dA, lse, D, B * H, k, dh, causal, dQKV, 1, stream);
         e |= sm.mark("attn_bwd_q");
+        if (rope) {
+            e |= launch_rope_grad(dt, dQKV, I, rope, B * H * k, k, dh, stream);
+            e |= sm.mark("rope_grad");
+        }
         // untimed: the weight gradients and the dX rows in one grouped launch
         const int grouped = ev ? 1
-                               : launch_bwd_proj(dt, X, dY, I, A, dQKV, dz16, dz, w->Wq, w->Wk, w->Wv, w->Wr, B, T, d,
-                                                 H, dh, k, g->dWq, g->dWk, g->dWv, g->dWr, g->dWo, dXs, stream);
+                               : launch_bwd_proj(dt, X, dY, I, A, dQKV, dz16, dz, w->Wq, w->Wk, w->Wv, Wr, B, T, d,
+                                                 H, dh, k, g->dWq, g->dWk, g->dWv, dWr, g->dWo, dXs, stream);
         if (grouped < 0) e |= 1;
         if (grouped == 1) {
-            e |= launch_wgrad(dt, X, dY, I, A, dQKV, dz16, B, T, d, H, dh, k, g->dWq, g->dWk, g->dWv, g->dWr,
+            e |= launch_wgrad(dt, X, dY, I, A, dQKV, dz16, B, T, d, H, dh, k, g->dWq, g->dWk, g->dWv, dWr,
                               g->dWo, wpart, 2, stream);
             e |= sm.mark("wgrad");
-            e |= launch_dx_proj(dt, dQKV, dz, w->Wq, w->Wk, w->Wv, w->Wr, B, d, H, dh, k, dXs, stream);
+            e |= launch_dx_proj(dt, dQKV, dz, w->Wq, w->Wk, w->Wv, Wr, B, d, H, dh, k, dXs, stream);
             e |= sm.mark("dx_proj");
         }
     }
@@ -321,6 +359,10 @@ int mosa_backward_timed(const mosa_shape* s, const void* X, const mosa_weights* 
         e |= sm.mark("attn_bwd_kv_dense");
         e |= launch_attn_bwd(dt, QKVd, dAd, lsed, Dd, B * Hd, T, dh, causal, dQKVd, 1, stream);
         e |= sm.mark("attn_bwd_q_dense");
+        if (rope) {
+            e |= launch_rope_grad(dt, dQKVd, nullptr, rope, B * Hd * T, T, dh, stream);
+            e |= sm.mark("rope_grad_dense");
+        }
         e |= launch_wgrad(dt, X, dY, nullptr, Ad, dQKVd, nullptr, B, T, d, Hd, dh, T, g->dWq_d, g->dWk_d,
                           g->dWv_d, nullptr, g->dWo_d, wpart, 0, stream);
         e |= sm.mark("wgrad_qkv_dense");
@@ -332,6 +374,12 @@ int mosa_backward_timed(const mosa_shape* s, const void* X, const mosa_weights* 
                            at<float>(scratch, L.dxbase), stream);
     e |= sm.mark("dx_combine");
     return e ? MOSA_ERR_HIP : MOSA_OK;
+}
+
+int mosa_adaptive_k(int seq_len, int rho) {
+    if (seq_len < 1 || rho < 1) return 0;
+    const int k = seq_len / rho > 2 ? seq_len / rho : 2;
+    return k < seq_len ? k : seq_len;
 }
 
 int mosa_backward(const mosa_shape* s, const void* X, const mosa_weights* w, const void* dY, const void* saved,

@@ -19,14 +19,28 @@ int launch_router(int dtype, const void* X, const void* Wr, int B, int T, int d,
 // Certified expert-choice top-k per (b,h): I ascending, r = sigmoid(z) at I,
 // slot[b,h,t] = position of t in I or -1.  unc_tok / unc_key / unc_sel are
 // per-row scratch of T entries each.
+// first_token: token 0 is always kept, the other k - 1 chosen among t >= 1.
 int launch_select(int dtype, const float* z, const float* xnorm, const void* X, const void* Wr, int B,
-                  int T, int d, int H, int k, int32_t* I, float* r, int16_t* slot, int32_t* unc_tok,
-                  double* unc_key, int32_t* unc_sel, hipStream_t stream);
+                  int T, int d, int H, int k, int first_token, int32_t* I, float* r, int16_t* slot,
+                  int32_t* unc_tok, double* unc_key, int32_t* unc_sel, hipStream_t stream);
+
+// Fixed sparse attention (no router): I[b,h,i] = i * stride, r = 1, and the slot map.
+int launch_fixed_select(int B, int T, int H, int k, int stride, int32_t* I, float* r, int16_t* slot,
+                        hipStream_t stream);
+
+// Rotary encoding: tab [T, dh/4] (cos, sin) pairs; the inverse rotation of the
+// dQ and dK parts of `rows` packed dQ | dK | dV rows (row = (b,h,i), position
+// I[row], or i = row % n when I == nullptr), in place.
+int launch_rope_table(int T, int dh, float base, float2* tab, hipStream_t stream);
+int launch_rope_grad(int dtype, void* dQKV, const int32_t* I, const float2* tab, int rows, int n, int dh,
+                     hipStream_t stream);
 
 // QKV[b,h,i,:] = X[b, I[b,h,i], :] . [Wq | Wk | Wv][h]  (packed rows of 3*dh)
-// for i < n (I == nullptr: identity, i.e. a dense head with n = T).
+// for i < n (I == nullptr: identity, i.e. a dense head with n = T); with a
+// rotary table, q and k rotated at position I[b,h,i] (or i).
 int launch_qkv(int dtype, const void* X, const int32_t* I, const void* Wq, const void* Wk,
-               const void* Wv, int B, int T, int d, int H, int dh, int n, void* QKV, hipStream_t stream);
+               const void* Wv, int B, int T, int d, int H, int dh, int n, void* QKV, const float2* rope,
+               hipStream_t stream);
 
 // A = diag(r) softmax(Q K^T / sqrt(dh) + causal mask in slot order) V per
 // (b,h) (r == nullptr: r = 1); lse = log-sum-exp of the scaled scores
@@ -35,8 +49,8 @@ int launch_qkv(int dtype, const void* X, const int32_t* I, const void* Wq, const
 // n = 16, 32, 64 or 128 rows (the outputs of launch_qkv and launch_attn_fwd);
 // returns 1 without launching when the shape does not qualify.
 int launch_qkv_attn(int dtype, const void* X, const int32_t* I, const void* Wq, const void* Wk, const void* Wv,
-                    int B, int T, int d, int H, int dh, int n, void* QKV, const float* r, int causal, void* A,
-                    float* lse, hipStream_t stream);
+                    int B, int T, int d, int H, int dh, int n, void* QKV, const float2* rope, const float* r,
+                    int causal, void* A, float* lse, hipStream_t stream);
 int launch_attn_fwd(int dtype, const void* QKV, const float* r, int BH, int n, int dh, int causal, void* A,
                     float* lse, hipStream_t stream);
 

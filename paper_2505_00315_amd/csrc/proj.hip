@@ -14,6 +14,7 @@
 #include "gemm.h"
 #include "gemm2.h"
 #include "kernels.h"
+#include "rope.h"
 
 namespace mosa {
 
@@ -32,6 +33,7 @@ struct QkvPolicy {
         const ST* W2;
         ST* out;  // [B, H, n, 3*DH]
         int T, d, H, n, M, mtiles;
+        const float2* rope;  // rotary table [T, DH/4] or nullptr
     };
     struct ARef {
         const ST* p;
@@ -82,8 +84,17 @@ struct QkvPolicy {
             const int b = m / a.n, i = m % a.n;
             float x[8];
             cs_load8(Cs, ldc, ml, c, x);
+            rope_cols(a, h, b, i, c, x);
             vec8_store<ST>(a.out + (((size_t)b * a.H + h) * a.n + i) * NT + c, vec8_from_f32<ST>(x));
         }
+    }
+    // columns c .. c + 7 of row (b, h, i): the rotary encoding of q and k
+    __device__ static void rope_cols(const Args& a, int h, int b, int i, int c, float (&x)[8]) {
+        if (!a.rope) return;
+        const int cq = c < DH ? c : c - DH;  // column within q or k
+        if (c >= 2 * DH || cq >= DH / 2) return;
+        const int pos = a.I ? a.I[((size_t)b * a.H + h) * a.n + i] : i;
+        rope8<DH>(x, cq, a.rope, pos, 1.f);
     }
 };
 
@@ -158,6 +169,16 @@ struct QkvAttnPolicy : QkvPolicy2<DH> {
             const int ml = v / VPR, u = v % VPR, m = m0 + ml;
             float x[8];
             cs_load8(Cs, ldc, ml, 8 * u, x);
+            if (a.rope && u < 2 * U) {
+                // rotated q stays in the C tile for the attention below
+                const int mm = min(m, a.M - 1);
+                QkvPolicy<ST, DH>::rope_cols(a, h, mm / a.n, mm % a.n, 8 * u, x);
+                if (u < U) {  // the C tile is this workgroup's LDS; each vector has one owner
+                    float* cq = const_cast<float*>(Cs) + ml * ldc + 8 * u;
+                    *reinterpret_cast<float4*>(cq) = make_float4(x[0], x[1], x[2], x[3]);
+                    *reinterpret_cast<float4*>(cq + 4) = make_float4(x[4], x[5], x[6], x[7]);
+                }
+            }
             const uint4 y = vec8_from_f32<ST>(x).v;
             if (m < a.M) {
                 const int b = m / a.n, i = m % a.n;
@@ -196,9 +217,9 @@ struct QkvAttnPolicy : QkvPolicy2<DH> {
 
 template <typename ST, int DH>
 int run(const ST* X, const int32_t* I, const ST* Wq, const ST* Wk, const ST* Wv, int B, int T, int d, int H, int n,
-        ST* out, hipStream_t stream) {
+        ST* out, const float2* rope, hipStream_t stream) {
     using P = QkvPolicy<ST, DH>;
-    typename P::Args a{X, I, Wq, Wk, Wv, out, T, d, H, n, B * n, (B * n + P::MT - 1) / P::MT};
+    typename P::Args a{X, I, Wq, Wk, Wv, out, T, d, H, n, B * n, (B * n + P::MT - 1) / P::MT, rope};
     if constexpr (sizeof(ST) == 2) {
         if (d % QkvPolicy2<DH>::KC == 0) return launch_gemm2<QkvPolicy2<DH>>(a, QkvPolicy2<DH>::mtiles(B * n) * H, stream);
     }
@@ -208,8 +229,8 @@ int run(const ST* X, const int32_t* I, const ST* Wq, const ST* Wk, const ST* Wv,
 }  // namespace
 
 int launch_qkv_attn(int dtype, const void* X, const int32_t* I, const void* Wq, const void* Wk, const void* Wv,
-                    int B, int T, int d, int H, int dh, int n, void* QKV, const float* r, int causal, void* A,
-                    float* lse, hipStream_t stream) {
+                    int B, int T, int d, int H, int dh, int n, void* QKV, const float2* rope, const float* r,
+                    int causal, void* A, float* lse, hipStream_t stream) {
     if (dtype != kBF16 || n < 16 || n % 16 || 128 % n || (dh != 64 && dh != 32)) return 1;
     const float scale = 1.0f / sqrtf((float)dh);
     auto go = [&](auto tag) {
@@ -219,7 +240,7 @@ int launch_qkv_attn(int dtype, const void* X, const int32_t* I, const void* Wq, 
         typename P::Args a{};
         static_cast<typename QkvPolicy<uint16_t, DH>::Args&>(a) = {
             (const uint16_t*)X, I, (const uint16_t*)Wq, (const uint16_t*)Wk, (const uint16_t*)Wv, (uint16_t*)QKV,
-            T, d, H, n, B * n, 0};
+            T, d, H, n, B * n, 0, rope};
         a.r = r;
         a.A = (uint16_t*)A;
         a.lse = lse;
@@ -231,15 +252,15 @@ int launch_qkv_attn(int dtype, const void* X, const int32_t* I, const void* Wq, 
 }
 
 int launch_qkv(int dtype, const void* X, const int32_t* I, const void* Wq, const void* Wk, const void* Wv, int B,
-               int T, int d, int H, int dh, int n, void* QKV, hipStream_t stream) {
+               int T, int d, int H, int dh, int n, void* QKV, const float2* rope, hipStream_t stream) {
     if (dtype == kBF16) {
         auto f = dh == 64 ? run<uint16_t, 64> : run<uint16_t, 32>;
         return f((const uint16_t*)X, I, (const uint16_t*)Wq, (const uint16_t*)Wk, (const uint16_t*)Wv, B, T, d, H, n,
-                 (uint16_t*)QKV, stream);
+                 (uint16_t*)QKV, rope, stream);
     }
     auto f = dh == 64 ? run<float, 64> : run<float, 32>;
     return f((const float*)X, I, (const float*)Wq, (const float*)Wk, (const float*)Wv, B, T, d, H, n, (float*)QKV,
-             stream);
+             rope, stream);
 }
 
 }  // namespace mosa

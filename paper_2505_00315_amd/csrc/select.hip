@@ -100,7 +100,7 @@ __device__ __forceinline__ uint32_t block_exclusive_scan_u32(uint32_t v, uint32_
 template <typename ST, int NW, int EPT>
 __global__ __launch_bounds__(64 * NW) void select_rows_kernel(
     const float* __restrict__ z, const float* __restrict__ xnorm, const ST* __restrict__ X,
-    const ST* __restrict__ Wr, int T, int d, int H, int k, int32_t* __restrict__ I, float* __restrict__ r,
+    const ST* __restrict__ Wr, int T, int d, int H, int k, int first, int32_t* __restrict__ I, float* __restrict__ r,
     int16_t* __restrict__ slot, int32_t* __restrict__ unc_tok, double* __restrict__ unc_key,
     int32_t* __restrict__ unc_sel) {
     constexpr int NT = 64 * NW;
@@ -157,6 +157,9 @@ __global__ __launch_bounds__(64 * NW) void select_rows_kernel(
         lo[e] = ok ? order_key(f32_down((double)zv[e] - beta)) : 0u;  // 0: below every real key
         hi[e] = ok ? order_key(f32_up((double)zv[e] + beta)) : 0u;
     }
+    // forced first token: token 0 above every real key, so it is certainly in
+    // and the other k - 1 are the best of t >= 1 (r_0 still from its logit)
+    if (first && tid == 0) lo[0] = hi[0] = 0xffffffffu;
 
     // k-th largest lo (A) and (k+1)-th largest hi (B): 8 bits per pass.
     const bool all = k >= T;
@@ -392,12 +395,12 @@ __global__ __launch_bounds__(64 * NW) void select_rows_kernel(
 
 template <typename ST>
 int launch_select_t(const float* z, const float* xnorm, const ST* X, const ST* Wr, int B, int T, int d, int H,
-                    int k, int32_t* I, float* r, int16_t* slot, int32_t* unc_tok, double* unc_key,
+                    int k, int first, int32_t* I, float* r, int16_t* slot, int32_t* unc_tok, double* unc_key,
                     int32_t* unc_sel, hipStream_t stream) {
     const dim3 grid(B * H);
 #define MOSA_SELECT_ROWS(NW, E)                                                                                \
     hipLaunchKernelGGL((select_rows_kernel<ST, NW, E>), grid, dim3(64 * NW), 0, stream, z, xnorm, X, Wr, T, d, H, \
-                       k, I, r, slot, unc_tok, unc_key, unc_sel)
+                       k, first, I, r, slot, unc_tok, unc_key, unc_sel)
     if (T <= 256) MOSA_SELECT_ROWS(4, 1);
     else if (T <= 512) MOSA_SELECT_ROWS(4, 2);
     else if (T <= 1024) MOSA_SELECT_ROWS(8, 2);
@@ -409,15 +412,37 @@ int launch_select_t(const float* z, const float* xnorm, const ST* X, const ST* W
     return hipGetLastError() == hipSuccess ? 0 : -1;
 }
 
+// Fixed sparse attention (paper Section 3.1, as a special case of MoSA):
+// I = 0, stride, 2 stride, ..., r = 1; one workgroup per (b, h) row.
+__global__ __launch_bounds__(256) void fixed_select_kernel(int T, int k, int stride, int32_t* __restrict__ I,
+                                                           float* __restrict__ r, int16_t* __restrict__ slot) {
+    const size_t row = blockIdx.x;
+    for (int i = threadIdx.x; i < k; i += 256) {
+        I[row * k + i] = i * stride;
+        r[row * k + i] = 1.0f;
+    }
+    for (int t = threadIdx.x; t < T; t += 256)
+        slot[row * T + t] = (t % stride == 0 && t / stride < k) ? (int16_t)(t / stride) : (int16_t)-1;
+}
+
 }  // namespace
 
+int launch_fixed_select(int B, int T, int H, int k, int stride, int32_t* I, float* r, int16_t* slot,
+                        hipStream_t stream) {
+    if (B * H == 0) return 0;
+    if (stride < 1 || (long long)(k - 1) * stride > T - 1) return -1;
+    hipLaunchKernelGGL(fixed_select_kernel, dim3(B * H), dim3(256), 0, stream, T, k, stride, I, r, slot);
+    return hipGetLastError() == hipSuccess ? 0 : -1;
+}
+
 int launch_select(int dtype, const float* z, const float* xnorm, const void* X, const void* Wr, int B, int T,
-                  int d, int H, int k, int32_t* I, float* r, int16_t* slot, int32_t* unc_tok, double* unc_key,
-                  int32_t* unc_sel, hipStream_t stream) {
+                  int d, int H, int k, int first_token, int32_t* I, float* r, int16_t* slot, int32_t* unc_tok,
+                  double* unc_key, int32_t* unc_sel, hipStream_t stream) {
     if (dtype == kBF16)
-        return launch_select_t<uint16_t>(z, xnorm, (const uint16_t*)X, (const uint16_t*)Wr, B, T, d, H, k, I, r,
-                                         slot, unc_tok, unc_key, unc_sel, stream);
-    return launch_select_t<float>(z, xnorm, (const float*)X, (const float*)Wr, B, T, d, H, k, I, r, slot, unc_tok,
+        return launch_select_t<uint16_t>(z, xnorm, (const uint16_t*)X, (const uint16_t*)Wr, B, T, d, H, k,
+                                         first_token, I, r, slot, unc_tok, unc_key, unc_sel, stream);
+    return launch_select_t<float>(z, xnorm, (const float*)X, (const float*)Wr, B, T, d, H, k, first_token, I, r,
+                                  slot, unc_tok,
                                   unc_key, unc_sel, stream);
 }
 

@@ -21,17 +21,18 @@ MOSA_F32 = 0
 MOSA_BF16 = 1
 
 SYMBOLS = ("mosa_workspace_size", "mosa_saved_offsets", "mosa_forward", "mosa_backward",
-           "mosa_forward_timed", "mosa_backward_timed", "mosa_status_string")
+           "mosa_forward_timed", "mosa_backward_timed", "mosa_status_string", "mosa_adaptive_k")
 MAX_STAGES = 32
 
 WEIGHT_NAMES = ("Wr", "Wq", "Wk", "Wv", "Wo", "Wq_d", "Wk_d", "Wv_d", "Wo_d")
 GRAD_NAMES = tuple("d" + n for n in WEIGHT_NAMES)
-SAVED_NAMES = ("I", "r", "slot", "QKV", "A", "lse", "QKVd", "Ad", "lsed")
+SAVED_NAMES = ("I", "r", "slot", "QKV", "A", "lse", "QKVd", "Ad", "lsed", "rope")
 
 
 class Shape(ctypes.Structure):
     _fields_ = [(n, ctypes.c_int32) for n in
-                ("batch", "seq_len", "d_model", "heads", "d_head", "k", "causal", "dense_heads", "dtype")]
+                ("batch", "seq_len", "d_model", "heads", "d_head", "k", "causal", "dense_heads", "dtype",
+                 "first_token", "fixed_stride", "rope")] + [("rope_base", ctypes.c_float), ("window", ctypes.c_int32)]
 
 
 class Weights(ctypes.Structure):
@@ -80,6 +81,8 @@ def lib():
         L.mosa_backward_timed.argtypes = L.mosa_backward.argtypes + [P(StageEvents)]
         L.mosa_status_string.argtypes = [ctypes.c_int]
         L.mosa_status_string.restype = ctypes.c_char_p
+        L.mosa_adaptive_k.argtypes = [ctypes.c_int, ctypes.c_int]
+        L.mosa_adaptive_k.restype = ctypes.c_int
         for n in ("mosa_workspace_size", "mosa_saved_offsets", "mosa_forward", "mosa_backward",
                   "mosa_forward_timed", "mosa_backward_timed"):
             getattr(L, n).restype = ctypes.c_int
@@ -96,10 +99,20 @@ def _check(status, what):
         raise MosaError(status, what)
 
 
-def make_shape(batch, seq_len, d_model, heads, d_head, k, causal=True, dense_heads=0, dtype="bf16"):
+def make_shape(batch, seq_len, d_model, heads, d_head, k, causal=True, dense_heads=0, dtype="bf16",
+               first_token=False, fixed_stride=0, rope=False, rope_base=10000.0, window=0):
     code = {"bf16": MOSA_BF16, "f32": MOSA_F32, torch.bfloat16: MOSA_BF16, torch.float32: MOSA_F32}[dtype]
     return Shape(batch, seq_len, d_model, heads, d_head, k if heads > 0 else 0, int(bool(causal)),
-                 dense_heads, code)
+                 dense_heads, code, int(bool(first_token)), int(fixed_stride), int(bool(rope)),
+                 float(rope_base), int(window))
+
+
+def adaptive_k(seq_len, rho):
+    """The paper's k for short inputs, max(floor(T / rho), 2) (Section 3.5)."""
+    k = lib().mosa_adaptive_k(int(seq_len), int(rho))
+    if k <= 0:
+        raise ValueError(f"adaptive_k: invalid seq_len={seq_len} or rho={rho}")
+    return k
 
 
 def torch_dtype(shape: Shape):

@@ -41,9 +41,14 @@ def stage_work(w, with_backward=True):
     def add(name, nbytes, flops):
         out[name] = StageWork(name, float(nbytes), float(flops))
 
-    if H:
+    if w.rope:
+        add("rope_table", T * (dh // 4) * 8, 0.0)
+    if H and w.fixed_stride:
+        add("select", rows * 8 + B * H * T * 2, 0.0)  # I, r and the slot map written
+    elif H:
         add("router", X + H * d * es + B * H * T * 4 + B * T * 4, 2.0 * B * T * H * d)
         add("select", B * H * T * 4 + B * T * 4 + H * d * es + rows * 8 + B * H * T * 2, 0.0)
+    if H:
         add("qkv", X + 3 * H * d * dh * es + 3 * rows * dh * es + rows * 4, 2.0 * rows * d * 3 * dh)
         add("attn", 4 * rows * dh * es + rows * 4, 4.0 * dh * _pairs(k, w.causal) * B * H)
         # the two in one launch (groups of k | 128 rows): Q|K|V written once
@@ -61,6 +66,8 @@ def stage_work(w, with_backward=True):
         add("bwd_out", X + H * dh * d * es + 2 * rows * dh * es + rows * 16, 2.0 * rows * d * dh)
         add("attn_bwd_kv", 6 * rows * dh * es + rows * 8, 8.0 * dh * _pairs(k, w.causal) * B * H)
         add("attn_bwd_q", 5 * rows * dh * es + rows * 8, 6.0 * dh * _pairs(k, w.causal) * B * H)
+        if w.rope:  # dQ and dK halves read and written, I read
+            add("rope_grad", 2 * rows * dh * es + rows * 4, 0.0)
         # dW^{Q,K,V,r} and dW^O (one grouped launch): X and dY read, the
         # selected rows' dQ|dK|dV and r A, I, the gradients written once
         add("wgrad", 2 * X + 4 * rows * dh * es + rows * 4 + 4 * H * d * dh * es + H * d * es,
@@ -70,6 +77,8 @@ def stage_work(w, with_backward=True):
         add("bwd_out_dense", X + Hd * dh * d * es + 2 * R * dh * es + R * 4, 2.0 * R * d * dh)
         add("attn_bwd_kv_dense", 6 * R * dh * es + R * 8, 8.0 * dh * _pairs(T, w.causal) * B * Hd)
         add("attn_bwd_q_dense", 5 * R * dh * es + R * 8, 6.0 * dh * _pairs(T, w.causal) * B * Hd)
+        if w.rope:
+            add("rope_grad_dense", 2 * R * dh * es, 0.0)
         add("wgrad_qkv_dense", X + 3 * R * dh * es + 3 * Hd * d * dh * es, 2.0 * R * d * 3 * dh)
         add("wgrad_o_dense", X + R * dh * es + Hd * dh * d * es, 2.0 * R * dh * d)
     add("dx_scatter",
@@ -150,6 +159,8 @@ def paper_mosa_heads_for_budget(layers, h, hp, T, baseline_heads, dense_heads, s
 STAGE_KERNELS = {
     "router": (r"router_kernel", r"RouterPolicy2"),
     "select": (r"select_\w*kernel",),
+    "rope_table": (r"rope_table_kernel",),
+    "rope_grad": (r"rope_grad_kernel",),
     "qkv": (r"(?<!Wgrad)QkvPolicy",),
     "qkv_attn": (r"QkvAttnPolicy",),
     "attn": (r"attn_fwd",),

@@ -29,7 +29,7 @@ def rel_err(got, ref):
 
 def shape_of(w: wl.Workload):
     return mosa.make_shape(w.batch, w.seq_len, w.d_model, w.heads, w.d_head, w.k, w.causal, w.dense_heads,
-                           w.dtype)
+                           w.dtype, **w.variants())
 
 
 def device_inputs(inp):

@@ -54,6 +54,12 @@ def test_workspace_size_and_layout():
     (dict(d_head=48), mosa.MOSA_ERR_UNSUPPORTED),
     (dict(d_model=96), mosa.MOSA_ERR_UNSUPPORTED),
     (dict(seq_len=20000, k=10), mosa.MOSA_ERR_UNSUPPORTED),
+    # variants
+    (dict(fixed_stride=64, k=17), mosa.MOSA_ERR_INVALID_ARG),    # 16 * 64 > T - 1
+    (dict(fixed_stride=8, first_token=True), mosa.MOSA_ERR_INVALID_ARG),
+    (dict(rope=True, rope_base=1.0), mosa.MOSA_ERR_INVALID_ARG),
+    (dict(window=8, causal=False, dense_heads=1), mosa.MOSA_ERR_INVALID_ARG),
+    (dict(fixed_stride=-1), mosa.MOSA_ERR_INVALID_ARG),
 ])
 def test_invalid_shapes_rejected(kw, status):
     base = dict(batch=2, seq_len=1024, d_model=128, heads=4, d_head=32, k=16, causal=True, dense_heads=0,
@@ -108,3 +114,24 @@ def test_backward_rejects_before_any_device_work():
                          1 << 40, ctypes.c_void_p(0x2000), 0, ctypes.byref(g), ctypes.c_void_p(0x20000), 1 << 40,
                          None)
     assert st == mosa.MOSA_ERR_INVALID_ARG  # dY missing
+
+
+def test_variant_fields_and_rope_table_offset():
+    s = mosa.make_shape(2, 1024, 128, 4, 64, 64, True, 1, "bf16", first_token=True, rope=True, rope_base=500.0)
+    assert (s.first_token, s.rope, s.rope_base) == (1, 1, 500.0)
+    off = mosa.saved_offsets(s)
+    assert off["rope"] % 256 == 0 and off["total"] >= off["rope"] + 1024 * (64 // 4) * 8
+    s2 = mosa.make_shape(2, 1024, 128, 4, 64, 64, True, 1, "bf16")
+    assert mosa.saved_offsets(s2)["total"] < off["total"]
+    fixed = mosa.make_shape(2, 1024, 128, 4, 64, 16, True, 0, "bf16", fixed_stride=64)
+    mosa.workspace_size(fixed)  # 15 * 64 <= 1023
+
+
+def test_adaptive_k():
+    # Section 3.5: k = max(floor(T / rho), 2), at most T
+    assert mosa.adaptive_k(1024, 64) == 16
+    assert mosa.adaptive_k(1024, 8) == 128
+    assert mosa.adaptive_k(10, 8) == 2
+    assert mosa.adaptive_k(1, 8) == 1
+    with pytest.raises(ValueError):
+        mosa.adaptive_k(0, 8)

@@ -30,9 +30,21 @@ class Workload:
     dtype: str = "bf16"  # storage type: "bf16" or "f32"
     backward: bool = False
     seed: int = 0
+    # variants of the layer (all off by default): forced first token
+    # (Section 3.2), fixed sparse stride (Section 3.1), rotary encoding at the
+    # original positions (Section 2.2), local window of the dense heads (Section 3.4)
+    first_token: bool = False
+    fixed_stride: int = 0
+    rope: bool = False
+    rope_base: float = 10000.0
+    window: int = 0
 
     def as_dict(self):
         return asdict(self)
+
+    def variants(self):
+        return dict(first_token=self.first_token, fixed_stride=self.fixed_stride, rope=self.rope,
+                    rope_base=self.rope_base, window=self.window)
 
     @property
     def tokens(self):
@@ -48,6 +60,12 @@ WORKLOADS = {
     "hybrid_d1024": Workload("hybrid_d1024", 8, 1024, 1024, 256, 64, 16, dense_heads=4,
                              backward=True, seed=3),
     "long_t8192": Workload("long_t8192", 1, 8192, 1024, 64, 64, 512, seed=4),
+    # the fwd_d512 shape in the paper's IsoFLOP setting (rotary encoding at the
+    # original positions, token 0 always kept), and as fixed sparse attention
+    # with stride 8 (I = 0, 8, ..., 1016; r = 1)
+    "fwd_d512_rope_first": Workload("fwd_d512_rope_first", 8, 1024, 512, 32, 64, 128, seed=1,
+                                    first_token=True, rope=True),
+    "fixed_d512": Workload("fixed_d512", 8, 1024, 512, 32, 64, 128, seed=1, fixed_stride=8),
 }
 
 
@@ -105,7 +123,7 @@ def make_inputs(w: Workload, seed=None, with_grad=None):
 
 
 def small(name="small", batch=2, seq_len=96, d_model=64, heads=3, d_head=32, k=20,
-          dense_heads=0, causal=True, dtype="bf16", backward=True, seed=11):
-    """A small workload for fast checks."""
+          dense_heads=0, causal=True, dtype="bf16", backward=True, seed=11, **variants):
+    """A small workload for fast checks (``variants``: the Workload variant fields)."""
     return Workload(name, batch, seq_len, d_model, heads, d_head, k, dense_heads, causal, dtype,
-                    backward, seed)
+                    backward, seed, **variants)
