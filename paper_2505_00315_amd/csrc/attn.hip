@@ -119,7 +119,7 @@ __global__ __launch_bounds__(256) void attn_fwd_kernel(const ST* __restrict__ QK
 // current one is processed.  Causal blocks are launched heaviest first.
 template <typename ST, int DH>
 __global__ __launch_bounds__(256) void attn_fwd_tiled_kernel(const ST* __restrict__ QKV, int BH, int n, int causal,
-                                                             float scale, const float* __restrict__ rw,
+                                                             int lb, float scale, const float* __restrict__ rw,
                                                              ST* __restrict__ A, float* __restrict__ lse) {
     constexpr int QB = 64, KB = 64, RS = 3 * DH;
     constexpr int PAD = 16 / (int)sizeof(ST);
@@ -151,8 +151,10 @@ __global__ __launch_bounds__(256) void attn_fwd_tiled_kernel(const ST* __restric
 #pragma unroll
     for (int db = 0; db < DH / 16; ++db) o[db] = zero4();
 
+    // causal with a local window (lb = window - 1 keys back): the block's keys
+    // start at q0 - lb
     const int kv_end = causal ? min(n, q0 + QB) : n;
-    const int ntiles = (kv_end + KB - 1) / KB;
+    const int ntiles = (kv_end + KB - 1) / KB, t0 = causal ? max(0, q0 - lb) / KB : 0;
     Vec8<ST> kreg[PER], vreg[PER];
     // rows past n are clamped to row n-1 (finite values whose scores are masked)
     auto load_tile = [&](int j0) {
@@ -174,8 +176,8 @@ __global__ __launch_bounds__(256) void attn_fwd_tiled_kernel(const ST* __restric
         }
     };
 
-    load_tile(0);
-    for (int t = 0; t < ntiles; ++t) {
+    load_tile(t0 * KB);
+    for (int t = t0; t < ntiles; ++t) {
         const int j0 = t * KB;
         __syncthreads();  // every wave is done with the previous tile
         store_tile();
@@ -197,21 +199,23 @@ __global__ __launch_bounds__(256) void attn_fwd_tiled_kernel(const ST* __restric
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
                 const int key = j0 + sb * 16 + 4 * g + i;
-                const bool ok = key < n && (!causal || key <= q);
+                const bool ok = key < n && (!causal || (key <= q && q - key <= lb));
                 s[sb][i] = ok ? s[sb][i] * scale : -__builtin_inff();
                 mloc = fmaxf(mloc, s[sb][i]);
             }
         mloc = fmaxf(mloc, __shfl_xor(mloc, 16, 64));
         mloc = fmaxf(mloc, __shfl_xor(mloc, 32, 64));
-        // tile 0 always holds key 0, allowed for every query: m_new is finite
+        // With a window a query may have no allowed key in this tile yet
+        // (m_new = -inf): it then adds nothing.  Its own key comes later.
         const float m_new = fmaxf(m_run, mloc);
-        const float alpha = expf(m_run - m_new);
+        const float m_use = m_new == -__builtin_inff() ? 0.f : m_new;
+        const float alpha = expf(m_run - m_use);
         float p[4][4], lsum = 0.f;
 #pragma unroll
         for (int sb = 0; sb < 4; ++sb)
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
-                p[sb][i] = expf(s[sb][i] - m_new);
+                p[sb][i] = expf(s[sb][i] - m_use);
                 lsum += p[sb][i];
             }
         lsum += __shfl_xor(lsum, 16, 64);
@@ -304,11 +308,12 @@ __global__ __launch_bounds__(512) void attn_fwd_lds_kernel(const uint16_t* __res
 }
 
 template <typename ST>
-int launch_attn_fwd_t(const ST* QKV, const float* r, int BH, int n, int dh, int causal, ST* A, float* lse,
-                     hipStream_t stream) {
+int launch_attn_fwd_t(const ST* QKV, const float* r, int BH, int n, int dh, int causal, int window, ST* A,
+                      float* lse, hipStream_t stream) {
     const float scale = 1.0f / sqrtf((float)dh);
+    const int lb = window > 0 ? window - 1 : n;  // keys a query may look back
     if constexpr (sizeof(ST) == 2) {
-        if (n > 32 && n <= kAttnLdsMaxN) {
+        if (n > 32 && n <= kAttnLdsMaxN && window == 0) {
             if (dh == 64)
                 hipLaunchKernelGGL((attn_fwd_lds_kernel<64>), dim3(BH), dim3(512), 0, stream, QKV, BH, n, causal, scale,
                                    r, A, lse);
@@ -318,14 +323,14 @@ int launch_attn_fwd_t(const ST* QKV, const float* r, int BH, int n, int dh, int 
             return hipGetLastError() == hipSuccess ? 0 : -1;
         }
     }
-    if (n > 32) {
+    if (n > 32 || window > 0) {
         const dim3 grid(BH * ((n + 63) / 64)), block(256);
         if (dh == 64)
-            hipLaunchKernelGGL((attn_fwd_tiled_kernel<ST, 64>), grid, block, 0, stream, QKV, BH, n, causal, scale, r, A,
-                               lse);
+            hipLaunchKernelGGL((attn_fwd_tiled_kernel<ST, 64>), grid, block, 0, stream, QKV, BH, n, causal, lb, scale,
+                               r, A, lse);
         else
-            hipLaunchKernelGGL((attn_fwd_tiled_kernel<ST, 32>), grid, block, 0, stream, QKV, BH, n, causal, scale, r, A,
-                               lse);
+            hipLaunchKernelGGL((attn_fwd_tiled_kernel<ST, 32>), grid, block, 0, stream, QKV, BH, n, causal, lb, scale,
+                               r, A, lse);
         return hipGetLastError() == hipSuccess ? 0 : -1;
     }
     const int tasks = BH * ((n + 15) / 16);
@@ -339,11 +344,12 @@ int launch_attn_fwd_t(const ST* QKV, const float* r, int BH, int n, int dh, int 
 
 }  // namespace
 
-int launch_attn_fwd(int dtype, const void* QKV, const float* r, int BH, int n, int dh, int causal, void* A, float* lse,
-                    hipStream_t stream) {
+int launch_attn_fwd(int dtype, const void* QKV, const float* r, int BH, int n, int dh, int causal, int window,
+                    void* A, float* lse, hipStream_t stream) {
     if (dtype == kBF16)
-        return launch_attn_fwd_t<uint16_t>((const uint16_t*)QKV, r, BH, n, dh, causal, (uint16_t*)A, lse, stream);
-    return launch_attn_fwd_t<float>((const float*)QKV, r, BH, n, dh, causal, (float*)A, lse, stream);
+        return launch_attn_fwd_t<uint16_t>((const uint16_t*)QKV, r, BH, n, dh, causal, window, (uint16_t*)A, lse,
+                                           stream);
+    return launch_attn_fwd_t<float>((const float*)QKV, r, BH, n, dh, causal, window, (float*)A, lse, stream);
 }
 
 }  // namespace mosa

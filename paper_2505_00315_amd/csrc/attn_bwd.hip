@@ -25,7 +25,7 @@ namespace {
 template <typename ST, int DH>
 __global__ __launch_bounds__(256) void attn_bwd_kv_kernel(const ST* __restrict__ QKV, const ST* __restrict__ dA,
                                                           const float* __restrict__ lse, const float* __restrict__ D,
-                                                          int BH, int n, int causal, float scale,
+                                                          int BH, int n, int causal, int lb, float scale,
                                                           ST* __restrict__ dQKV) {
     constexpr int RS = 3 * DH;  // row stride of the packed Q | K | V (and dQ | dK | dV) rows
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
@@ -51,7 +51,9 @@ __global__ __launch_bounds__(256) void attn_bwd_kv_kernel(const ST* __restrict__
 #pragma unroll
     for (int db = 0; db < DH / 16; ++db) dKt[db] = dVt[db] = zero4();
 
-    for (int i0 = causal ? j0 : 0; i0 < n; i0 += 16) {
+    // causal with a window: queries up to lb past the block's last key see it
+    const int i_end = causal ? min(n, j0 + 16 + lb) : n;
+    for (int i0 = causal ? j0 : 0; i0 < i_end; i0 += 16) {
         const int qa = i0 + c16;  // query this lane feeds as MFMA A row
         f32x4 s = zero4(), dp = zero4();
 #pragma unroll
@@ -66,7 +68,7 @@ __global__ __launch_bounds__(256) void attn_bwd_kv_kernel(const ST* __restrict__
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
             const int q = i0 + 4 * g + i;
-            const bool ok = q < n && key < n && (!causal || key <= q);
+            const bool ok = q < n && key < n && (!causal || (key <= q && q - key <= lb));
             const float l = q < n ? lse[base + q] : 0.f;
             const float dd = q < n ? D[base + q] : 0.f;
             p[i] = ok ? expf(s[i] * scale - l) : 0.f;
@@ -103,7 +105,7 @@ __global__ __launch_bounds__(256) void attn_bwd_kv_kernel(const ST* __restrict__
 template <typename ST, int DH>
 __global__ __launch_bounds__(256) void attn_bwd_q_kernel(const ST* __restrict__ QKV, const ST* __restrict__ dA,
                                                          const float* __restrict__ lse, const float* __restrict__ D,
-                                                         int BH, int n, int causal, float scale,
+                                                         int BH, int n, int causal, int lb, float scale,
                                                          ST* __restrict__ dQKV) {
     constexpr int RS = 3 * DH;
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
@@ -132,7 +134,7 @@ __global__ __launch_bounds__(256) void attn_bwd_q_kernel(const ST* __restrict__ 
     for (int db = 0; db < DH / 16; ++db) dQt[db] = zero4();
 
     const int kv_end = causal ? min(n, i0 + 16) : n;
-    for (int j0 = 0; j0 < kv_end; j0 += 16) {
+    for (int j0 = causal ? max(0, i0 - lb) / 16 * 16 : 0; j0 < kv_end; j0 += 16) {
         const int kr = j0 + c16;
         f32x4 s = zero4(), dp = zero4();
 #pragma unroll
@@ -147,7 +149,7 @@ __global__ __launch_bounds__(256) void attn_bwd_q_kernel(const ST* __restrict__ 
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
             const int j = j0 + 4 * g + i;
-            const bool ok = q < n && j < n && (!causal || j <= q);
+            const bool ok = q < n && j < n && (!causal || (j <= q && q - j <= lb));
             const float p = ok ? expf(s[i] * scale - lq) : 0.f;
             ds[i] = p * (dp[i] - dq);
         }
@@ -192,7 +194,7 @@ template <typename ST, int DH>
 __global__ __launch_bounds__(256) void attn_bwd_kv_tiled_kernel(const ST* __restrict__ QKV, const ST* __restrict__ dA,
                                                                 const float* __restrict__ lse,
                                                                 const float* __restrict__ D, int BH, int n, int causal,
-                                                                float scale, ST* __restrict__ dQKV) {
+                                                                int lb, float scale, ST* __restrict__ dQKV) {
     using TL = BwdTile<ST, DH>;
     constexpr int TB = TL::TB, RS = TL::RS, LDR = TL::LDR, LDT = TL::LDT, VPR = TL::VPR, PER = TL::PER;
     __shared__ __attribute__((aligned(16))) ST Qs[TB * LDR];
@@ -224,7 +226,9 @@ __global__ __launch_bounds__(256) void attn_bwd_kv_tiled_kernel(const ST* __rest
 #pragma unroll
     for (int db = 0; db < DH / 16; ++db) dKt[db] = dVt[db] = zero4();
 
-    const int it0 = causal ? kb : 0;
+    // causal: query tiles from the block's own; with a window only those
+    // within lb of its last key
+    const int it0 = causal ? kb : 0, it_end = causal ? min(nkb, (k0 + TB - 1 + lb) / TB + 1) : nkb;
     Vec8<ST> qreg[PER], areg[PER];
     float lreg = 0.f, dreg = 0.f;
     // query rows past n are clamped to row n-1 (their scores are masked)
@@ -259,12 +263,12 @@ __global__ __launch_bounds__(256) void attn_bwd_kv_tiled_kernel(const ST* __rest
     };
 
     load_tile(it0 * TB);
-    for (int it = it0; it < nkb; ++it) {
+    for (int it = it0; it < it_end; ++it) {
         const int i0 = it * TB;
         __syncthreads();
         store_tile();
         __syncthreads();
-        load_tile(min(it + 1, nkb - 1) * TB);
+        load_tile(min(it + 1, it_end - 1) * TB);
         // S and dP for 4 sub-blocks of 16 queries: lane = key c16, rows = queries 4g + i
         float p[4][4], ds[4][4];
 #pragma unroll
@@ -278,7 +282,7 @@ __global__ __launch_bounds__(256) void attn_bwd_kv_tiled_kernel(const ST* __rest
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
                 const int ql = sb * 16 + 4 * g + i, q = i0 + ql;
-                const bool ok = q < n && key < n && (!causal || key <= q);
+                const bool ok = q < n && key < n && (!causal || (key <= q && q - key <= lb));
                 p[sb][i] = ok ? expf(s[i] * scale - ls[ql]) : 0.f;
                 ds[sb][i] = p[sb][i] * (dp[i] - Dsh[ql]);
             }
@@ -335,7 +339,7 @@ template <typename ST, int DH>
 __global__ __launch_bounds__(256) void attn_bwd_q_tiled_kernel(const ST* __restrict__ QKV, const ST* __restrict__ dA,
                                                                const float* __restrict__ lse,
                                                                const float* __restrict__ D, int BH, int n, int causal,
-                                                               float scale, ST* __restrict__ dQKV) {
+                                                               int lb, float scale, ST* __restrict__ dQKV) {
     using TL = BwdTile<ST, DH>;
     constexpr int TB = TL::TB, RS = TL::RS, LDR = TL::LDR, LDT = TL::LDT, VPR = TL::VPR, PER = TL::PER;
     __shared__ __attribute__((aligned(16))) ST Ks[TB * LDR];
@@ -368,7 +372,7 @@ __global__ __launch_bounds__(256) void attn_bwd_q_tiled_kernel(const ST* __restr
     for (int db = 0; db < DH / 16; ++db) dQt[db] = zero4();
 
     const int kv_end = causal ? min(n, q0 + TB) : n;
-    const int ntiles = (kv_end + TB - 1) / TB;
+    const int ntiles = (kv_end + TB - 1) / TB, t0 = causal ? max(0, q0 - lb) / TB : 0;
     Vec8<ST> kreg[PER], vreg[PER];
     auto load_tile = [&](int j0) {
 #pragma unroll
@@ -390,8 +394,8 @@ __global__ __launch_bounds__(256) void attn_bwd_q_tiled_kernel(const ST* __restr
         }
     };
 
-    load_tile(0);
-    for (int t = 0; t < ntiles; ++t) {
+    load_tile(t0 * TB);
+    for (int t = t0; t < ntiles; ++t) {
         const int j0 = t * TB;
         __syncthreads();
         store_tile();
@@ -410,7 +414,7 @@ __global__ __launch_bounds__(256) void attn_bwd_q_tiled_kernel(const ST* __restr
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
                 const int j = j0 + sb * 16 + 4 * g + i;
-                const bool ok = j < n && q < n && (!causal || j <= q);
+                const bool ok = j < n && q < n && (!causal || (j <= q && q - j <= lb));
                 const float pp = ok ? expf(s[i] * scale - lq) : 0.f;
                 ds[sb][i] = pp * (dp[i] - dq);
             }
@@ -663,10 +667,11 @@ __global__ __launch_bounds__(512) void attn_bwd_lds_kernel(const uint16_t* __res
 
 template <typename ST>
 int launch_t(const ST* QKV, const ST* dA, const float* lse, const float* D, int BH, int n, int dh, int causal,
-             ST* dQKV, int pass, hipStream_t stream) {
+             int window, ST* dQKV, int pass, hipStream_t stream) {
     const float scale = 1.0f / sqrtf((float)dh);
+    const int lb = window > 0 ? window - 1 : n;  // keys a query may look back
     if constexpr (sizeof(ST) == 2) {
-      if (n > 32 && n <= kAttnBwdLdsMaxN) {
+      if (n > 32 && n <= kAttnBwdLdsMaxN && window == 0) {
         // both passes in one launch: the second call has nothing left to do
         if (pass != 0) return 0;
         auto kern = dh == 64 ? attn_bwd_lds_kernel<64> : attn_bwd_lds_kernel<32>;
@@ -681,10 +686,10 @@ int launch_t(const ST* QKV, const ST* dA, const float* lse, const float* D, int 
         hipLaunchKernelGGL(kern, dim3(BH), dim3(512), lds, stream, QKV, dA, lse, D, BH, n, causal, scale, dQKV);
         return hipGetLastError() == hipSuccess ? 0 : -1;
       }
-      if (n > 32) {
+      if (n > 32 || window > 0) {
         const dim3 grid(BH * ((n + 63) / 64)), block(256);
 #define MOSA_ATTN_BWD_T(KERN, DHV) \
-    hipLaunchKernelGGL((KERN<ST, DHV>), grid, block, 0, stream, QKV, dA, lse, D, BH, n, causal, scale, dQKV)
+    hipLaunchKernelGGL((KERN<ST, DHV>), grid, block, 0, stream, QKV, dA, lse, D, BH, n, causal, lb, scale, dQKV)
         if (pass == 0) {
             if (dh == 64) MOSA_ATTN_BWD_T(attn_bwd_kv_tiled_kernel, 64);
             else MOSA_ATTN_BWD_T(attn_bwd_kv_tiled_kernel, 32);
@@ -699,7 +704,7 @@ int launch_t(const ST* QKV, const ST* dA, const float* lse, const float* D, int 
     const int tasks = BH * ((n + 15) / 16);
     dim3 grid((tasks + 3) / 4), block(256);
 #define MOSA_ATTN_BWD(KERN, DHV) \
-    hipLaunchKernelGGL((KERN<ST, DHV>), grid, block, 0, stream, QKV, dA, lse, D, BH, n, causal, scale, dQKV)
+    hipLaunchKernelGGL((KERN<ST, DHV>), grid, block, 0, stream, QKV, dA, lse, D, BH, n, causal, lb, scale, dQKV)
     if (pass == 0) {
         if (dh == 64) MOSA_ATTN_BWD(attn_bwd_kv_kernel, 64);
         else MOSA_ATTN_BWD(attn_bwd_kv_kernel, 32);
@@ -714,12 +719,12 @@ int launch_t(const ST* QKV, const ST* dA, const float* lse, const float* D, int 
 }  // namespace
 
 int launch_attn_bwd(int dtype, const void* QKV, const void* dA, const float* lse, const float* D, int BH, int n,
-                    int dh, int causal, void* dQKV, int pass, hipStream_t stream) {
+                    int dh, int causal, int window, void* dQKV, int pass, hipStream_t stream) {
     if (dtype == kBF16)
-        return launch_t<uint16_t>((const uint16_t*)QKV, (const uint16_t*)dA, lse, D, BH, n, dh, causal,
+        return launch_t<uint16_t>((const uint16_t*)QKV, (const uint16_t*)dA, lse, D, BH, n, dh, causal, window,
                                   (uint16_t*)dQKV, pass, stream);
-    return launch_t<float>((const float*)QKV, (const float*)dA, lse, D, BH, n, dh, causal, (float*)dQKV, pass,
-                           stream);
+    return launch_t<float>((const float*)QKV, (const float*)dA, lse, D, BH, n, dh, causal, window, (float*)dQKV,
+                           pass, stream);
 }
 
 }  // namespace mosa

@@ -57,7 +57,6 @@ int validate_shape(const mosa_shape* s) {
     if (s->fixed_stride < 0 || s->window < 0) return MOSA_ERR_INVALID_ARG;
     if (s->rope && !(s->rope_base > 1.0f)) return MOSA_ERR_INVALID_ARG;
     if (s->window > 0 && !s->causal) return MOSA_ERR_INVALID_ARG;
-    if (s->window > 0 && s->dense_heads > 0) return MOSA_ERR_UNSUPPORTED;  // local heads: not built yet
     if (s->heads > 0 && s->fixed_stride > 0 &&
         (s->first_token || (long long)(s->k - 1) * s->fixed_stride > s->seq_len - 1))
         return MOSA_ERR_INVALID_ARG;
@@ -240,7 +239,7 @@ int mosa_forward_timed(const mosa_shape* s, const void* X, const mosa_weights* w
         if (fused == 1) {
             e |= launch_qkv(dt, X, I, w->Wq, w->Wk, w->Wv, B, T, d, H, dh, k, QKV, rope, stream);
             e |= sm.mark("qkv");
-            e |= launch_attn_fwd(dt, QKV, r, B * H, k, dh, causal, A, lse, stream);
+            e |= launch_attn_fwd(dt, QKV, r, B * H, k, dh, causal, 0, A, lse, stream);
             e |= sm.mark("attn");
         } else {
             e |= fused;
@@ -252,7 +251,7 @@ int mosa_forward_timed(const mosa_shape* s, const void* X, const mosa_weights* w
     if (Hd > 0) {
         e |= launch_qkv(dt, X, nullptr, w->Wq_d, w->Wk_d, w->Wv_d, B, T, d, Hd, dh, T, QKVd, rope, stream);
         e |= sm.mark("qkv_dense");
-        e |= launch_attn_fwd(dt, QKVd, nullptr, B * Hd, T, dh, causal, Ad, lsed, stream);
+        e |= launch_attn_fwd(dt, QKVd, nullptr, B * Hd, T, dh, causal, s->window, Ad, lsed, stream);
         e |= sm.mark("attn_dense");
     }
     e |= launch_out_combine(dt, Ad, w->Wo_d, slot, Xo, B, T, d, H, dh, k, Hd, Y, accumulate,
@@ -330,9 +329,9 @@ int mosa_backward_timed(const mosa_shape* s, const void* X, const mosa_weights* 
     if (H > 0) {
         e |= launch_dattn_out(dt, dY, I, r, w->Wo, A, B, T, d, H, dh, k, dA, D, dz, dz16, stream);
         e |= sm.mark("bwd_out");
-        e |= launch_attn_bwd(dt, QKV, dA, lse, D, B * H, k, dh, causal, dQKV, 0, stream);
+        e |= launch_attn_bwd(dt, QKV, dA, lse, D, B * H, k, dh, causal, 0, dQKV, 0, stream);
         e |= sm.mark("attn_bwd_kv");
-        e |= launch_attn_bwd(dt, QKV, dA, lse, D, B * H, k, dh, causal, dQKV, 1, stream);
+        e |= launch_attn_bwd(dt, QKV, dA, lse, D, B * H, k, dh, causal, 0, dQKV, 1, stream);
         e |= sm.mark("attn_bwd_q");
         if (rope) {
             e |= launch_rope_grad(dt, dQKV, I, rope, B * H * k, k, dh, stream);
@@ -355,9 +354,9 @@ int mosa_backward_timed(const mosa_shape* s, const void* X, const mosa_weights* 
         e |= launch_dattn_out(dt, dY, nullptr, nullptr, w->Wo_d, Ad, B, T, d, Hd, dh, T, dAd, Dd, nullptr, nullptr,
                               stream);
         e |= sm.mark("bwd_out_dense");
-        e |= launch_attn_bwd(dt, QKVd, dAd, lsed, Dd, B * Hd, T, dh, causal, dQKVd, 0, stream);
+        e |= launch_attn_bwd(dt, QKVd, dAd, lsed, Dd, B * Hd, T, dh, causal, s->window, dQKVd, 0, stream);
         e |= sm.mark("attn_bwd_kv_dense");
-        e |= launch_attn_bwd(dt, QKVd, dAd, lsed, Dd, B * Hd, T, dh, causal, dQKVd, 1, stream);
+        e |= launch_attn_bwd(dt, QKVd, dAd, lsed, Dd, B * Hd, T, dh, causal, s->window, dQKVd, 1, stream);
         e |= sm.mark("attn_bwd_q_dense");
         if (rope) {
             e |= launch_rope_grad(dt, dQKVd, nullptr, rope, B * Hd * T, T, dh, stream);

@@ -51,7 +51,8 @@ int launch_qkv(int dtype, const void* X, const int32_t* I, const void* Wq, const
 int launch_qkv_attn(int dtype, const void* X, const int32_t* I, const void* Wq, const void* Wk, const void* Wv,
                     int B, int T, int d, int H, int dh, int n, void* QKV, const float2* rope, const float* r,
                     int causal, void* A, float* lse, hipStream_t stream);
-int launch_attn_fwd(int dtype, const void* QKV, const float* r, int BH, int n, int dh, int causal, void* A,
+// window > 0 (causal only): query t sees keys t - window + 1 .. t (local heads).
+int launch_attn_fwd(int dtype, const void* QKV, const float* r, int BH, int n, int dh, int causal, int window, void* A,
                     float* lse, hipStream_t stream);
 
 // Xo[b,h,i,:] = A[b,h,i,:] Wo[h]  (A already scaled by r).
@@ -73,7 +74,7 @@ int launch_dattn_out(int dtype, const void* dY, const int32_t* I, const float* r
 
 // Attention backward into packed dQKV rows; pass 0 writes dK, dV, pass 1 writes dQ.
 int launch_attn_bwd(int dtype, const void* QKV, const void* dA, const float* lse, const float* D, int BH,
-                    int n, int dh, int causal, void* dQKV, int pass, hipStream_t stream);
+                    int n, int dh, int causal, int window, void* dQKV, int pass, hipStream_t stream);
 
 // Weight gradients; which 0: dWq, dWk, dWv (+ dWr when non-null), which 1: dWo,
 // which 2: both (in one launch where the gathered-row engine applies).

@@ -21,8 +21,14 @@ class StageWork:
     flops: float
 
 
-def _pairs(n, causal):
-    return n * (n + 1) / 2 if causal else n * n
+def _pairs(n, causal, window=0):
+    """(query, key) pairs attention computes: all, the causal triangle, or the
+    causal band of a local window (query t sees keys t - window + 1 .. t)."""
+    if not causal:
+        return n * n
+    if window and window < n:
+        return window * (window + 1) / 2 + (n - window) * window
+    return n * (n + 1) / 2
 
 
 def stage_work(w, with_backward=True):
@@ -56,7 +62,8 @@ def stage_work(w, with_backward=True):
         add("qkv_attn", out["qkv"].bytes + rows * dh * es + rows * 8, out["qkv"].flops + out["attn"].flops)
     if Hd:
         add("qkv_dense", X + 3 * Hd * d * dh * es + 3 * B * Hd * T * dh * es, 2.0 * B * Hd * T * d * 3 * dh)
-        add("attn_dense", 4 * B * Hd * T * dh * es + B * Hd * T * 4, 4.0 * dh * _pairs(T, w.causal) * B * Hd)
+        add("attn_dense", 4 * B * Hd * T * dh * es + B * Hd * T * 4,
+            4.0 * dh * _pairs(T, w.causal, w.window) * B * Hd)
     add("out_scatter",
         rows * dh * es + rows * 8 + H * dh * d * es + B * Hd * T * dh * es + Hd * dh * d * es + X,
         2.0 * rows * dh * d + 2.0 * B * Hd * T * dh * d)
@@ -75,8 +82,8 @@ def stage_work(w, with_backward=True):
     if Hd:
         R = B * Hd * T
         add("bwd_out_dense", X + Hd * dh * d * es + 2 * R * dh * es + R * 4, 2.0 * R * d * dh)
-        add("attn_bwd_kv_dense", 6 * R * dh * es + R * 8, 8.0 * dh * _pairs(T, w.causal) * B * Hd)
-        add("attn_bwd_q_dense", 5 * R * dh * es + R * 8, 6.0 * dh * _pairs(T, w.causal) * B * Hd)
+        add("attn_bwd_kv_dense", 6 * R * dh * es + R * 8, 8.0 * dh * _pairs(T, w.causal, w.window) * B * Hd)
+        add("attn_bwd_q_dense", 5 * R * dh * es + R * 8, 6.0 * dh * _pairs(T, w.causal, w.window) * B * Hd)
         if w.rope:
             add("rope_grad_dense", 2 * R * dh * es, 0.0)
         add("wgrad_qkv_dense", X + 3 * R * dh * es + 3 * Hd * d * dh * es, 2.0 * R * d * 3 * dh)

@@ -66,6 +66,11 @@ WORKLOADS = {
     "fwd_d512_rope_first": Workload("fwd_d512_rope_first", 8, 1024, 512, 32, 64, 128, seed=1,
                                     first_token=True, rope=True),
     "fixed_d512": Workload("fixed_d512", 8, 1024, 512, 32, 64, 128, seed=1, fixed_stride=8),
+    # the long-sequence hybrid of Section 3.4: 60 MoSA heads with k = 64 beside
+    # 4 local (sliding-window) heads, d_model 1024, T = 8192 (window 512: the
+    # paper does not state it)
+    "long_local_t8192": Workload("long_local_t8192", 1, 8192, 1024, 60, 64, 64, dense_heads=4,
+                                 backward=True, seed=4, window=512),
 }
 
 
