@@ -73,6 +73,8 @@ def stage_work(w, with_backward=True):
         add("bwd_out", X + H * dh * d * es + 2 * rows * dh * es + rows * 16, 2.0 * rows * d * dh)
         add("attn_bwd_kv", 6 * rows * dh * es + rows * 8, 8.0 * dh * _pairs(k, w.causal) * B * H)
         add("attn_bwd_q", 5 * rows * dh * es + rows * 8, 6.0 * dh * _pairs(k, w.causal) * B * H)
+        # both passes: Q, K, V, dA read, dQ | dK | dV written, lse and D read
+        add("attn_bwd", 7 * rows * dh * es + rows * 8, 14.0 * dh * _pairs(k, w.causal) * B * H)
         if w.rope:  # dQ and dK halves read and written, I read
             add("rope_grad", 2 * rows * dh * es + rows * 4, 0.0)
         # dW^{Q,K,V,r} and dW^O (one grouped launch): X and dY read, the
@@ -84,6 +86,7 @@ def stage_work(w, with_backward=True):
         add("bwd_out_dense", X + Hd * dh * d * es + 2 * R * dh * es + R * 4, 2.0 * R * d * dh)
         add("attn_bwd_kv_dense", 6 * R * dh * es + R * 8, 8.0 * dh * _pairs(T, w.causal, w.window) * B * Hd)
         add("attn_bwd_q_dense", 5 * R * dh * es + R * 8, 6.0 * dh * _pairs(T, w.causal, w.window) * B * Hd)
+        add("attn_bwd_dense", 7 * R * dh * es + R * 8, 14.0 * dh * _pairs(T, w.causal, w.window) * B * Hd)
         if w.rope:
             add("rope_grad_dense", 2 * R * dh * es, 0.0)
         add("wgrad_qkv_dense", X + 3 * R * dh * es + 3 * Hd * d * dh * es, 2.0 * R * d * 3 * dh)
@@ -95,8 +98,11 @@ def stage_work(w, with_backward=True):
     return out
 
 
-# Stages made of two kernels (the library records one event per kernel).
-GROUPS = {"out_scatter": ("out_proj", "out_combine"), "dx_scatter": ("dx_proj", "dx_combine")}
+# Stages made of two kernels (the library records one event per kernel); the
+# attention backward's two passes are one stage (one launch does both when
+# the group fits one workgroup).
+GROUPS = {"out_scatter": ("out_proj", "out_combine"), "dx_scatter": ("dx_proj", "dx_combine"),
+          "attn_bwd": ("attn_bwd_kv", "attn_bwd_q"), "attn_bwd_dense": ("attn_bwd_kv_dense", "attn_bwd_q_dense")}
 
 
 def group_stage_times(kernel_ms):
@@ -173,8 +179,7 @@ STAGE_KERNELS = {
     "attn": (r"attn_fwd",),
     "out_scatter": (r"OutProj\w*Policy", r"OutCombinePolicy", r"OutDensePolicy", r"combine_rows_kernel<[^>]*, 0>"),
     "bwd_out": (r"BwdOutPolicy",),
-    "attn_bwd_kv": (r"attn_bwd_kv",),
-    "attn_bwd_q": (r"attn_bwd_q",),
+    "attn_bwd": (r"attn_bwd_kv", r"attn_bwd_q", r"attn_bwd_lds"),
     "wgrad": (r"WgradQkvPolicy<[^>]*, true, true>", r"WgradQkvPolicy2", r"WgradOPolicy<[^>]*, true>",
               r"WgradOPolicy2", r"wgrad_qkv_reduce", r"wgrad_o_reduce"),
     "dx_scatter": (r"DxProj\w*Policy", r"DxCombinePolicy", r"DxDensePolicy", r"combine_rows_kernel<[^>]*, 1>"),
@@ -210,17 +215,20 @@ def traffic_summary(fetch_dir, write_dir, copy_bytes):
     for rows, key, scale in ((fetch, "fetch", f_scale), (write, "write", w_scale)):
         for stage, pats in STAGE_KERNELS.items():
             # grouped launches (several stages' work in one kernel) are left out;
-            # a stage's launches = its dispatches / the distinct kernels it runs
+            # a stage's traffic per launch = the sum over its kernels of each
+            # kernel's average per dispatch (kernels may run in different steps)
             hit = [r for r in rows[:-1] if not re.search(GROUPED_KERNEL, r["Kernel_Name"])
                    and any(re.search(p, r["Kernel_Name"]) for p in pats)]
             if not hit:
                 continue
-            launches = len(hit) / len({r["Kernel_Name"] for r in hit})
-            kib = sum(float(r["Counter_Value"]) for r in hit)
+            per = {}
+            for r in hit:
+                per.setdefault(r["Kernel_Name"], []).append(float(r["Counter_Value"]))
+            kib = sum(sum(v) / len(v) for v in per.values())
             if kib:
                 d = out.setdefault(stage, {})
-                d[key + "_kib"] = kib / launches
-                d[key + "_bytes"] = kib / launches * 1024.0 * scale
+                d[key + "_kib"] = kib
+                d[key + "_bytes"] = kib * 1024.0 * scale
     for d in out.values():
         d["hbm_bytes_per_launch"] = d.get("fetch_bytes", 0.0) + d.get("write_bytes", 0.0)
     return out, f_scale, w_scale
