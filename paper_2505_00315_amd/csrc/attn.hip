@@ -296,7 +296,9 @@ __global__ __launch_bounds__(512) void attn_fwd_lds_kernel(const uint16_t* __res
             lds_load16(Vp + row + 8 * (pos ^ vt_swz<U>(key)), base + TILE + 1024 * NW * j);
         }
     }
-    const int nqb = (n + 15) / 16, qb = wave, q = 16 * qb + c16;
+    // causal work of query block b is b + 1; waves w and w + 4 share a SIMD,
+    // so with 8 blocks they take blocks s and 7 - s
+    const int nqb = (n + 15) / 16, qb = nqb == 8 && causal && wave >= 4 ? 11 - wave : wave, q = 16 * qb + c16;
     Frag8<ST> qf[DH / 32];
 #pragma unroll
     for (int st = 0; st < DH / 32; ++st) qf[st] = frag8_load<ST>(Qp + (size_t)min(q, n - 1) * RS + st * 32 + 8 * g);

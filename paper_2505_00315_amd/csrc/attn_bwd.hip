@@ -229,6 +229,7 @@ __global__ __launch_bounds__(256) void attn_bwd_kv_tiled_kernel(const ST* __rest
     // causal: query tiles from the block's own; with a window only those
     // within lb of its last key
     const int it0 = causal ? kb : 0, it_end = causal ? min(nkb, (k0 + TB - 1 + lb) / TB + 1) : nkb;
+    const float c2 = scale * 1.44269504088896341f;  // P = 2^(s c2 - lse log2 e)
     Vec8<ST> qreg[PER], areg[PER];
     float lreg = 0.f, dreg = 0.f;
     // query rows past n are clamped to row n-1 (their scores are masked)
@@ -241,7 +242,7 @@ __global__ __launch_bounds__(256) void attn_bwd_kv_tiled_kernel(const ST* __rest
             areg[p] = vec8_load<ST>(dAp + row * DH + dc);
         }
         const size_t rq = (size_t)min(i0 + lane, n - 1);
-        lreg = lse[base + rq];
+        lreg = lse[base + rq] * 1.44269504088896341f;  // log2 e
         dreg = D[base + rq];
     };
     auto store_tile = [&]() {
@@ -283,7 +284,7 @@ __global__ __launch_bounds__(256) void attn_bwd_kv_tiled_kernel(const ST* __rest
             for (int i = 0; i < 4; ++i) {
                 const int ql = sb * 16 + 4 * g + i, q = i0 + ql;
                 const bool ok = q < n && key < n && (!causal || (key <= q && q - key <= lb));
-                p[sb][i] = ok ? expf(s[i] * scale - ls[ql]) : 0.f;
+                p[sb][i] = ok ? __builtin_amdgcn_exp2f(fmaf(s[i], c2, -ls[ql])) : 0.f;
                 ds[sb][i] = p[sb][i] * (dp[i] - Dsh[ql]);
             }
         }
@@ -366,7 +367,8 @@ __global__ __launch_bounds__(256) void attn_bwd_q_tiled_kernel(const ST* __restr
         qf[st] = frag8_load<ST>(Qp + qrow * RS + st * 32 + 8 * g);
         af[st] = frag8_load<ST>(dAp + qrow * DH + st * 32 + 8 * g);
     }
-    const float lq = lse[base + qrow], dq = D[base + qrow];
+    const float lq = lse[base + qrow] * 1.44269504088896341f, dq = D[base + qrow];  // lse in log2 units
+    const float c2 = scale * 1.44269504088896341f;  // P = 2^(s c2 - lq)
     f32x4 dQt[DH / 16];
 #pragma unroll
     for (int db = 0; db < DH / 16; ++db) dQt[db] = zero4();
@@ -415,7 +417,7 @@ __global__ __launch_bounds__(256) void attn_bwd_q_tiled_kernel(const ST* __restr
             for (int i = 0; i < 4; ++i) {
                 const int j = j0 + sb * 16 + 4 * g + i;
                 const bool ok = j < n && q < n && (!causal || (j <= q && q - j <= lb));
-                const float pp = ok ? expf(s[i] * scale - lq) : 0.f;
+                const float pp = ok ? __builtin_amdgcn_exp2f(fmaf(s[i], c2, -lq)) : 0.f;
                 ds[sb][i] = pp * (dp[i] - dq);
             }
         }
@@ -516,7 +518,7 @@ __global__ __launch_bounds__(512) void attn_bwd_lds_kernel(const uint16_t* __res
     }
     if (tid < NMAX) {
         const size_t r = base + min(tid, n - 1);
-        lse_s[tid] = lse[r];
+        lse_s[tid] = lse[r] * 1.44269504088896341f;  // log2 e: P = 2^(s c - lse log2 e)
         D_s[tid] = D[r];
     }
     wait_vmcnt<0>();
@@ -550,9 +552,15 @@ __global__ __launch_bounds__(512) void attn_bwd_lds_kernel(const uint16_t* __res
     auto ds_unit = [](int q, int key8) { return q * 16 + ((key8 >> 3) ^ (q & 15)); };  // dS tile, 16-byte unit
 
     const int nb = (n + 15) / 16;
-    // Phase 1: key block kb = wave.
-    if (wave < nb) {
-        const int kb = wave, key = 16 * kb + c16;
+    // With 8 blocks the causal work of block b is 8 - b (phase 1) or b + 1
+    // (phase 2); waves w and w + 4 share a SIMD, so they take blocks s and
+    // 7 - s: every SIMD gets the same work.
+    const int blk = nb == 8 && causal && wave >= 4 ? 11 - wave : wave;
+    const float c2 = scale * 1.44269504088896341f;
+    // Phase 1: key block kb.
+    if (blk < nb) {
+        const int kb = blk, key = 16 * kb + c16;
+        const int qmin = key >= n ? n : (causal ? key : 0);  // first query that sees this key
         Frag8<ST> kf[DH / 32], vf[DH / 32];
 #pragma unroll
         for (int st = 0; st < DH / 32; ++st) {
@@ -579,8 +587,8 @@ __global__ __launch_bounds__(512) void attn_bwd_lds_kernel(const uint16_t* __res
 #pragma unroll
                 for (int i = 0; i < 4; ++i) {
                     const int q = 16 * qb + 4 * g + i;
-                    const bool ok = qb < nb && q < n && key < n && (!causal || key <= q);
-                    const float pv = ok ? expf(s[i] * scale - lse_s[q & (NMAX - 1)]) : 0.f;
+                    const bool ok = qb < nb && q >= qmin && q < n;
+                    const float pv = ok ? __builtin_amdgcn_exp2f(fmaf(s[i], c2, -lse_s[q & (NMAX - 1)])) : 0.f;
                     const float dsv = pv * (dp[i] - D_s[q & (NMAX - 1)]);
                     p[hq][i] = pv;
                     ds[hq][i] = dsv;
@@ -627,9 +635,9 @@ __global__ __launch_bounds__(512) void attn_bwd_lds_kernel(const uint16_t* __res
         }
     }
     __syncthreads();  // the dS tile is complete
-    // Phase 2: query block qb = wave: dQ^T += K^T dS^T over 32 keys per MFMA.
-    if (wave < nb) {
-        const int qb = wave, q = 16 * qb + c16;
+    // Phase 2: query block qb = blk: dQ^T += K^T dS^T over 32 keys per MFMA.
+    if (blk < nb) {
+        const int qb = blk, q = 16 * qb + c16;
         f32x4 dQt[DH / 16];
 #pragma unroll
         for (int db = 0; db < DH / 16; ++db) dQt[db] = zero4();
