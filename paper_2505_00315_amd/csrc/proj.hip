@@ -74,8 +74,10 @@ struct QkvPolicy {
         epilogue_rows<MT>(a, h, m0, Cs, ldc, tid);
     }
     // rows m0 .. m0 + ROWS - 1 of the C tile to their packed Q | K | V rows
+    // (tab_s: the rotary rows of the tile staged by rope_stage, or nullptr)
     template <int ROWS>
-    __device__ static void epilogue_rows(const Args& a, int h, int m0, const float* Cs, int ldc, int tid) {
+    __device__ static void epilogue_rows(const Args& a, int h, int m0, const float* Cs, int ldc, int tid,
+                                         const float2* tab_s = nullptr) {
         constexpr int VPR = NT / 8;  // vectors per row
         for (int v = tid; v < ROWS * VPR; v += 256) {
             const int ml = v / VPR, c = (v % VPR) * 8;
@@ -84,7 +86,8 @@ struct QkvPolicy {
             const int b = m / a.n, i = m % a.n;
             float x[8];
             cs_load8(Cs, ldc, ml, c, x);
-            rope_cols(a, h, b, i, c, x);
+            if (tab_s) rope_cols_at(tab_s, ml, c, x);
+            else rope_cols(a, h, b, i, c, x);
             vec8_store<ST>(a.out + (((size_t)b * a.H + h) * a.n + i) * NT + c, vec8_from_f32<ST>(x));
         }
     }
@@ -96,6 +99,31 @@ struct QkvPolicy {
         const int pos = a.I ? a.I[((size_t)b * a.H + h) * a.n + i] : i;
         rope8<DH>(x, cq, a.rope, pos, 1.f);
     }
+    // the same from a staged table row (row ml of the tile)
+    __device__ static void rope_cols_at(const float2* tab_s, int ml, int c, float (&x)[8]) {
+        const int cq = c < DH ? c : c - DH;
+        if (c >= 2 * DH || cq >= DH / 2) return;
+        rope8<DH>(x, cq, tab_s, ml, 1.f);
+    }
+    // The (cos, sin) rows of the tile's ROWS rows (positions I, or i for dense
+    // heads; rows past M take the last row's) into LDS, all loads issued
+    // before any is used; ends with a barrier.
+    template <int ROWS>
+    __device__ static void rope_stage(const Args& a, int h, int m0, int tid, float2* tab_s) {
+        constexpr int Q4 = DH / 8, PER = ROWS * Q4 / 256;  // float4 units per row / per thread
+        static_assert(ROWS * Q4 % 256 == 0, "table tile");
+        float4 t[PER];
+#pragma unroll
+        for (int j = 0; j < PER; ++j) {
+            const int e = tid + 256 * j, ml = e / Q4, q4 = e % Q4, m = min(m0 + ml, a.M - 1);
+            const int b = m / a.n, i = m % a.n;
+            const int pos = a.I ? a.I[((size_t)b * a.H + h) * a.n + i] : i;
+            t[j] = reinterpret_cast<const float4*>(a.rope + (size_t)pos * (DH / 4))[q4];
+        }
+#pragma unroll
+        for (int j = 0; j < PER; ++j) reinterpret_cast<float4*>(tab_s)[tid + 256 * j] = t[j];
+        __syncthreads();
+    }
 };
 
 // bf16 storage: the multi-stage engine with direct-to-LDS loads (gemm2.h).
@@ -105,7 +133,8 @@ template <int DH>
 struct QkvPolicy2 {
     using ST = uint16_t;
     static constexpr int MT = 128, NT = 3 * DH, KC = DH == 64 ? 32 : 64, WM = 2, WN = 2, STAGES = 4;
-    static constexpr size_t EPI_LDS = 0;
+    static constexpr size_t TAB_LDS = (size_t)MT * (DH / 4) * 8;  // staged rotary rows
+    static constexpr size_t EPI_LDS = TAB_LDS;
     static constexpr bool A_KCONTIG = true, B_KCONTIG = false;
     using Args = typename QkvPolicy<ST, DH>::Args;
     struct ARef {
@@ -133,8 +162,13 @@ struct QkvPolicy2 {
         return W + ((size_t)h * a.d + k) * DH + (n8 % DH);
     }
     __device__ static void epilogue(const Args& a, int h, int m0, int, const float* Cs, int ldc, int tid,
-                                    unsigned char*) {
-        QkvPolicy<ST, DH>::template epilogue_rows<MT>(a, h, m0, Cs, ldc, tid);
+                                    unsigned char* extra) {
+        float2* tab_s = nullptr;
+        if (a.rope) {
+            tab_s = reinterpret_cast<float2*>(extra);
+            QkvPolicy<ST, DH>::template rope_stage<MT>(a, h, m0, tid, tab_s);
+        }
+        QkvPolicy<ST, DH>::template epilogue_rows<MT>(a, h, m0, Cs, ldc, tid, tab_s);
     }
 };
 
@@ -151,7 +185,8 @@ struct QkvAttnPolicy : QkvPolicy2<DH> {
     static constexpr int MT = Base::MT, U = DH / 8, KROWS = MT, VROWS = MT + 16;
     // bf16 K tile, then the V tile with 16 zero rows after it (the last
     // group's odd key block reads 16 rows past its end, at weight zero)
-    static constexpr size_t EPI_LDS = (size_t)(KROWS + VROWS) * DH * 2;
+    static constexpr size_t KV_LDS = (size_t)(KROWS + VROWS) * DH * 2;
+    static constexpr size_t EPI_LDS = KV_LDS + Base::TAB_LDS;  // then the staged rotary rows
     static_assert(MT == 128 && Base::WM * Base::WN == 4, "two query blocks per wave");
     struct Args : QkvPolicy<ST, DH>::Args {
         const float* r;  // [B, H, n] router weights of the selected rows
@@ -165,14 +200,15 @@ struct QkvAttnPolicy : QkvPolicy2<DH> {
         constexpr int VPR = 3 * U;  // 16-byte vectors per packed row
         unsigned char* Ks = extra;
         unsigned char* Vs = extra + (size_t)KROWS * DH * 2;
+        float2* tab_s = reinterpret_cast<float2*>(extra + KV_LDS);
+        if (a.rope) QkvPolicy<ST, DH>::template rope_stage<MT>(a, h, m0, tid, tab_s);
         for (int v = tid; v < MT * VPR; v += 256) {
             const int ml = v / VPR, u = v % VPR, m = m0 + ml;
             float x[8];
             cs_load8(Cs, ldc, ml, 8 * u, x);
             if (a.rope && u < 2 * U) {
                 // rotated q stays in the C tile for the attention below
-                const int mm = min(m, a.M - 1);
-                QkvPolicy<ST, DH>::rope_cols(a, h, mm / a.n, mm % a.n, 8 * u, x);
+                QkvPolicy<ST, DH>::rope_cols_at(tab_s, ml, 8 * u, x);
                 if (u < U) {  // the C tile is this workgroup's LDS; each vector has one owner
                     float* cq = const_cast<float*>(Cs) + ml * ldc + 8 * u;
                     *reinterpret_cast<float4*>(cq) = make_float4(x[0], x[1], x[2], x[3]);
