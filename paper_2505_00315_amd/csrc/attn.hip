@@ -117,7 +117,7 @@ __global__ __launch_bounds__(256) void attn_fwd_kernel(const ST* __restrict__ QK
 // (A operand of O^T += V^T P^T, K = 32 keys per MFMA, P^T straight from the
 // S^T registers).  The next tile's global loads are in flight while the
 // current one is processed.  Causal blocks are launched heaviest first.
-template <typename ST, int DH>
+template <typename ST, int DH, bool WIN>
 __global__ __launch_bounds__(256) void attn_fwd_tiled_kernel(const ST* __restrict__ QKV, int BH, int n, int causal,
                                                              int lb, float scale, const float* __restrict__ rw,
                                                              ST* __restrict__ A, float* __restrict__ lse) {
@@ -154,7 +154,7 @@ __global__ __launch_bounds__(256) void attn_fwd_tiled_kernel(const ST* __restric
     // causal with a local window (lb = window - 1 keys back): the block's keys
     // start at q0 - lb
     const int kv_end = causal ? min(n, q0 + QB) : n;
-    const int ntiles = (kv_end + KB - 1) / KB, t0 = causal ? max(0, q0 - lb) / KB : 0;
+    const int ntiles = (kv_end + KB - 1) / KB, t0 = WIN && causal ? max(0, q0 - lb) / KB : 0;
     Vec8<ST> kreg[PER], vreg[PER];
     // rows past n are clamped to row n-1 (finite values whose scores are masked)
     auto load_tile = [&](int j0) {
@@ -199,7 +199,7 @@ __global__ __launch_bounds__(256) void attn_fwd_tiled_kernel(const ST* __restric
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
                 const int key = j0 + sb * 16 + 4 * g + i;
-                const bool ok = key < n && (!causal || (key <= q && q - key <= lb));
+                const bool ok = key < n && (!causal || (key <= q && (!WIN || q - key <= lb)));
                 s[sb][i] = ok ? s[sb][i] * scale : -__builtin_inff();
                 mloc = fmaxf(mloc, s[sb][i]);
             }
@@ -208,7 +208,7 @@ __global__ __launch_bounds__(256) void attn_fwd_tiled_kernel(const ST* __restric
         // With a window a query may have no allowed key in this tile yet
         // (m_new = -inf): it then adds nothing.  Its own key comes later.
         const float m_new = fmaxf(m_run, mloc);
-        const float m_use = m_new == -__builtin_inff() ? 0.f : m_new;
+        const float m_use = WIN && m_new == -__builtin_inff() ? 0.f : m_new;
         const float alpha = expf(m_run - m_use);
         float p[4][4], lsum = 0.f;
 #pragma unroll
@@ -327,12 +327,9 @@ int launch_attn_fwd_t(const ST* QKV, const float* r, int BH, int n, int dh, int 
     }
     if (n > 32 || window > 0) {
         const dim3 grid(BH * ((n + 63) / 64)), block(256);
-        if (dh == 64)
-            hipLaunchKernelGGL((attn_fwd_tiled_kernel<ST, 64>), grid, block, 0, stream, QKV, BH, n, causal, lb, scale,
-                               r, A, lse);
-        else
-            hipLaunchKernelGGL((attn_fwd_tiled_kernel<ST, 32>), grid, block, 0, stream, QKV, BH, n, causal, lb, scale,
-                               r, A, lse);
+        auto kern = window > 0 ? (dh == 64 ? attn_fwd_tiled_kernel<ST, 64, true> : attn_fwd_tiled_kernel<ST, 32, true>)
+                               : (dh == 64 ? attn_fwd_tiled_kernel<ST, 64, false> : attn_fwd_tiled_kernel<ST, 32, false>);
+        hipLaunchKernelGGL(kern, grid, block, 0, stream, QKV, BH, n, causal, lb, scale, r, A, lse);
         return hipGetLastError() == hipSuccess ? 0 : -1;
     }
     const int tasks = BH * ((n + 15) / 16);

@@ -22,7 +22,7 @@ namespace mosa {
 
 namespace {
 
-template <typename ST, int DH>
+template <typename ST, int DH, bool WIN>
 __global__ __launch_bounds__(256) void attn_bwd_kv_kernel(const ST* __restrict__ QKV, const ST* __restrict__ dA,
                                                           const float* __restrict__ lse, const float* __restrict__ D,
                                                           int BH, int n, int causal, int lb, float scale,
@@ -52,7 +52,7 @@ __global__ __launch_bounds__(256) void attn_bwd_kv_kernel(const ST* __restrict__
     for (int db = 0; db < DH / 16; ++db) dKt[db] = dVt[db] = zero4();
 
     // causal with a window: queries up to lb past the block's last key see it
-    const int i_end = causal ? min(n, j0 + 16 + lb) : n;
+    const int i_end = WIN && causal ? min(n, j0 + 16 + lb) : n;
     for (int i0 = causal ? j0 : 0; i0 < i_end; i0 += 16) {
         const int qa = i0 + c16;  // query this lane feeds as MFMA A row
         f32x4 s = zero4(), dp = zero4();
@@ -68,7 +68,7 @@ __global__ __launch_bounds__(256) void attn_bwd_kv_kernel(const ST* __restrict__
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
             const int q = i0 + 4 * g + i;
-            const bool ok = q < n && key < n && (!causal || (key <= q && q - key <= lb));
+            const bool ok = q < n && key < n && (!causal || (key <= q && (!WIN || q - key <= lb)));
             const float l = q < n ? lse[base + q] : 0.f;
             const float dd = q < n ? D[base + q] : 0.f;
             p[i] = ok ? expf(s[i] * scale - l) : 0.f;
@@ -102,7 +102,7 @@ __global__ __launch_bounds__(256) void attn_bwd_kv_kernel(const ST* __restrict__
     }
 }
 
-template <typename ST, int DH>
+template <typename ST, int DH, bool WIN>
 __global__ __launch_bounds__(256) void attn_bwd_q_kernel(const ST* __restrict__ QKV, const ST* __restrict__ dA,
                                                          const float* __restrict__ lse, const float* __restrict__ D,
                                                          int BH, int n, int causal, int lb, float scale,
@@ -134,7 +134,7 @@ __global__ __launch_bounds__(256) void attn_bwd_q_kernel(const ST* __restrict__ 
     for (int db = 0; db < DH / 16; ++db) dQt[db] = zero4();
 
     const int kv_end = causal ? min(n, i0 + 16) : n;
-    for (int j0 = causal ? max(0, i0 - lb) / 16 * 16 : 0; j0 < kv_end; j0 += 16) {
+    for (int j0 = WIN && causal ? max(0, i0 - lb) / 16 * 16 : 0; j0 < kv_end; j0 += 16) {
         const int kr = j0 + c16;
         f32x4 s = zero4(), dp = zero4();
 #pragma unroll
@@ -149,7 +149,7 @@ __global__ __launch_bounds__(256) void attn_bwd_q_kernel(const ST* __restrict__ 
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
             const int j = j0 + 4 * g + i;
-            const bool ok = q < n && j < n && (!causal || (j <= q && q - j <= lb));
+            const bool ok = q < n && j < n && (!causal || (j <= q && (!WIN || q - j <= lb)));
             const float p = ok ? expf(s[i] * scale - lq) : 0.f;
             ds[i] = p * (dp[i] - dq);
         }
@@ -190,7 +190,7 @@ struct BwdTile {
     static_assert(PER >= 1 && TB * VPR % 256 == 0, "tile shape");
 };
 
-template <typename ST, int DH>
+template <typename ST, int DH, bool WIN>
 __global__ __launch_bounds__(256) void attn_bwd_kv_tiled_kernel(const ST* __restrict__ QKV, const ST* __restrict__ dA,
                                                                 const float* __restrict__ lse,
                                                                 const float* __restrict__ D, int BH, int n, int causal,
@@ -228,7 +228,7 @@ __global__ __launch_bounds__(256) void attn_bwd_kv_tiled_kernel(const ST* __rest
 
     // causal: query tiles from the block's own; with a window only those
     // within lb of its last key
-    const int it0 = causal ? kb : 0, it_end = causal ? min(nkb, (k0 + TB - 1 + lb) / TB + 1) : nkb;
+    const int it0 = causal ? kb : 0, it_end = WIN && causal ? min(nkb, (k0 + TB - 1 + lb) / TB + 1) : nkb;
     const float c2 = scale * 1.44269504088896341f;  // P = 2^(s c2 - lse log2 e)
     Vec8<ST> qreg[PER], areg[PER];
     float lreg = 0.f, dreg = 0.f;
@@ -283,7 +283,7 @@ __global__ __launch_bounds__(256) void attn_bwd_kv_tiled_kernel(const ST* __rest
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
                 const int ql = sb * 16 + 4 * g + i, q = i0 + ql;
-                const bool ok = q < n && key < n && (!causal || (key <= q && q - key <= lb));
+                const bool ok = q < n && key < n && (!causal || (key <= q && (!WIN || q - key <= lb)));
                 p[sb][i] = ok ? __builtin_amdgcn_exp2f(fmaf(s[i], c2, -ls[ql])) : 0.f;
                 ds[sb][i] = p[sb][i] * (dp[i] - Dsh[ql]);
             }
@@ -336,7 +336,7 @@ __global__ __launch_bounds__(256) void attn_bwd_kv_tiled_kernel(const ST* __rest
     }
 }
 
-template <typename ST, int DH>
+template <typename ST, int DH, bool WIN>
 __global__ __launch_bounds__(256) void attn_bwd_q_tiled_kernel(const ST* __restrict__ QKV, const ST* __restrict__ dA,
                                                                const float* __restrict__ lse,
                                                                const float* __restrict__ D, int BH, int n, int causal,
@@ -374,7 +374,7 @@ __global__ __launch_bounds__(256) void attn_bwd_q_tiled_kernel(const ST* __restr
     for (int db = 0; db < DH / 16; ++db) dQt[db] = zero4();
 
     const int kv_end = causal ? min(n, q0 + TB) : n;
-    const int ntiles = (kv_end + TB - 1) / TB, t0 = causal ? max(0, q0 - lb) / TB : 0;
+    const int ntiles = (kv_end + TB - 1) / TB, t0 = WIN && causal ? max(0, q0 - lb) / TB : 0;
     Vec8<ST> kreg[PER], vreg[PER];
     auto load_tile = [&](int j0) {
 #pragma unroll
@@ -416,7 +416,7 @@ __global__ __launch_bounds__(256) void attn_bwd_q_tiled_kernel(const ST* __restr
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
                 const int j = j0 + sb * 16 + 4 * g + i;
-                const bool ok = j < n && q < n && (!causal || (j <= q && q - j <= lb));
+                const bool ok = j < n && q < n && (!causal || (j <= q && (!WIN || q - j <= lb)));
                 const float pp = ok ? __builtin_amdgcn_exp2f(fmaf(s[i], c2, -lq)) : 0.f;
                 ds[sb][i] = pp * (dp[i] - dq);
             }
@@ -696,8 +696,11 @@ int launch_t(const ST* QKV, const ST* dA, const float* lse, const float* D, int 
       }
       if (n > 32 || window > 0) {
         const dim3 grid(BH * ((n + 63) / 64)), block(256);
-#define MOSA_ATTN_BWD_T(KERN, DHV) \
-    hipLaunchKernelGGL((KERN<ST, DHV>), grid, block, 0, stream, QKV, dA, lse, D, BH, n, causal, lb, scale, dQKV)
+#define MOSA_ATTN_BWD_T(KERN, DHV)                                                                   \
+    do {                                                                                              \
+        auto kern = window > 0 ? KERN<ST, DHV, true> : KERN<ST, DHV, false>;                          \
+        hipLaunchKernelGGL(kern, grid, block, 0, stream, QKV, dA, lse, D, BH, n, causal, lb, scale, dQKV); \
+    } while (0)
         if (pass == 0) {
             if (dh == 64) MOSA_ATTN_BWD_T(attn_bwd_kv_tiled_kernel, 64);
             else MOSA_ATTN_BWD_T(attn_bwd_kv_tiled_kernel, 32);
@@ -711,8 +714,11 @@ int launch_t(const ST* QKV, const ST* dA, const float* lse, const float* D, int 
     }
     const int tasks = BH * ((n + 15) / 16);
     dim3 grid((tasks + 3) / 4), block(256);
-#define MOSA_ATTN_BWD(KERN, DHV) \
-    hipLaunchKernelGGL((KERN<ST, DHV>), grid, block, 0, stream, QKV, dA, lse, D, BH, n, causal, lb, scale, dQKV)
+#define MOSA_ATTN_BWD(KERN, DHV)                                                                     \
+    do {                                                                                              \
+        auto kern = window > 0 ? KERN<ST, DHV, true> : KERN<ST, DHV, false>;                          \
+        hipLaunchKernelGGL(kern, grid, block, 0, stream, QKV, dA, lse, D, BH, n, causal, lb, scale, dQKV); \
+    } while (0)
     if (pass == 0) {
         if (dh == 64) MOSA_ATTN_BWD(attn_bwd_kv_kernel, 64);
         else MOSA_ATTN_BWD(attn_bwd_kv_kernel, 32);

@@ -340,6 +340,89 @@ struct WgradOPolicy2 {
     }
 };
 
+// Dense heads (bf16) on the same engine: R = B T rows split into S ranges of
+// up to 4096 rows (the row table), one fp32 partial tile per range, summed in
+// range order by the reduce kernels.  "batch" = h S + s.  Row r of range s:
+// x = r' = s KS + r (the row of X or dY), y = (b Hd + h) T + t (the head's
+// row), y = -1 past the range.
+__device__ __forceinline__ int2 wgrad_dense_k_row(const FastDiv& Td, int R, int KS, int T, int H, int batch, int S,
+                                                  int k, int K) {
+    const int h = batch / S, s = batch % S, r = min(s * KS + min(k, K - 1), R - 1);
+    int b, t;
+    fast_divmod(Td, r, b, t);
+    return make_int2(r, k < K ? (b * H + h) * T + t : -1);
+}
+
+template <int DH>
+struct WgradQkvDensePolicy2 : WgradQkvPolicy2<DH> {
+    using ST = uint16_t;
+    static constexpr int MT = DH == 64 ? 192 : 128;  // [dQ | dK | dV] (DH 32: zero rows past 96)
+    using Args = typename WgradQkvPolicy2<DH>::Args;  // I unused, cps = rows per range
+    __device__ static void tile(const Args& a, int logical, int& batch, int& m0, int& n0) {
+        batch = logical / a.mtiles;  // h S + s
+        m0 = 0;
+        n0 = (logical % a.mtiles) * WgradQkvPolicy2<DH>::NT;
+    }
+    __device__ static int k_size(const Args& a, int batch) { return min(a.cps, a.R - (batch % a.S) * a.cps); }
+    __device__ static int2 k_row(const Args& a, int batch, int k, int K) {
+        return wgrad_dense_k_row(a.nd, a.R, a.cps, a.T, a.H, batch, a.S, k, K);
+    }
+    __device__ static void a_mlane(const Args& a, int, int m8, const ST*& base, uint32_t& stride) {
+        if (m8 < 3 * DH) {
+            base = a.dQKV + m8;
+            stride = 3 * DH;
+        } else {
+            base = g2_zero;
+            stride = 0;
+        }
+    }
+    __device__ static void b_mlane(const Args& a, int, int n8, const ST*& base, uint32_t& stride) {
+        base = a.X + n8;
+        stride = a.d;
+    }
+    // fp32 partial: part[s][h][c][3 DH], columns m .. m + 7 of row c = n
+    __device__ static void store8(const Args& a, int batch, int m, int n, const float (&x)[8]) {
+        if (m >= 3 * DH) return;
+        const int h = batch / a.S, s = batch % a.S;
+        float* p = a.part + (((size_t)s * a.H + h) * a.d + n) * (3 * DH) + m;
+        reinterpret_cast<float4*>(p)[0] = make_float4(x[0], x[1], x[2], x[3]);
+        reinterpret_cast<float4*>(p)[1] = make_float4(x[4], x[5], x[6], x[7]);
+    }
+};
+
+template <int DH>
+struct WgradODensePolicy2 : WgradOPolicy2<DH> {
+    using ST = uint16_t;
+    using Args = typename WgradOPolicy2<DH>::Args;  // I unused, cps = rows per range
+    __device__ static void tile(const Args& a, int logical, int& batch, int& m0, int& n0) {
+        batch = logical / a.ntiles;  // h S + s
+        m0 = (logical % a.ntiles) * WgradOPolicy2<DH>::MT;
+        n0 = 0;
+    }
+    __device__ static int k_size(const Args& a, int batch) { return min(a.cps, a.R - (batch % a.S) * a.cps); }
+    __device__ static int2 k_row(const Args& a, int batch, int k, int K) {
+        return wgrad_dense_k_row(a.nd, a.R, a.cps, a.T, a.H, batch, a.S, k, K);
+    }
+    // fp32 partial: part[s][h][e][c], columns c = m .. m + 7 of row e = n
+    __device__ static void store8(const Args& a, int batch, int m, int n, const float (&x)[8]) {
+        const int h = batch / a.S, s = batch % a.S;
+        float* p = a.part + (((size_t)s * a.H + h) * DH + n) * a.d + m;
+        reinterpret_cast<float4*>(p)[0] = make_float4(x[0], x[1], x[2], x[3]);
+        reinterpret_cast<float4*>(p)[1] = make_float4(x[4], x[5], x[6], x[7]);
+    }
+};
+
+// Row ranges of the dense-head split: enough workgroups for the chip (about
+// 512 for `tiles` output tiles per range), each range at most 4096 rows.
+inline int dense_ranges(int R, int tiles, int kc, int& rows) {
+    int S = std::max(1, (512 + tiles - 1) / tiles);
+    S = std::max(S, (R + 4095) / 4096);
+    rows = (R + S - 1) / S;
+    rows = (rows + kc - 1) / kc * kc;
+    if (rows > 4096) return 0;
+    return (R + rows - 1) / rows;
+}
+
 // Rows of the k-row table for a gathered range of R rows (0: not usable).
 template <class P2>
 int wgrad2_table_rows(int R, int d) {
@@ -368,6 +451,23 @@ int run_qkv_t(const ST* X, const int32_t* I, const ST* dQKV, const ST* dz16, int
         if (const int rows = wgrad2_table_rows<P2>(R, d)) {
             typename P::Args a{X, I, dQKV, dz16, dWq, dWk, dWv, dWr, part, T, d, H, n, R, d / 64, 1, 0, make_fastdiv(n)};
             return launch_gemm2<P2>(a, H * (d / 64), stream, rows);
+        }
+    }
+    if constexpr (sizeof(ST) == 2 && !ROUTER && !GATHER) {
+        using P2 = WgradQkvDensePolicy2<DH>;
+        int rows;
+        const int S = dense_ranges(R, H * (d / 64), P2::KC, rows);
+        if (S > 0 && d % 64 == 0) {
+            typename P2::Args a{X, I, dQKV, dz16, dWq, dWk, dWv, dWr, part, T, d, H, n, R, d / 64, S, rows,
+                                make_fastdiv(n)};
+            int e = launch_gemm2<P2>(a, S * H * (d / 64), stream, rows);
+            if (e == 0) {
+                const int total = H * d * (3 * DH / 8);
+                hipLaunchKernelGGL((wgrad_qkv_reduce_kernel<ST, DH, false>), dim3((total + 255) / 256), dim3(256), 0,
+                                   stream, part, S, H, d, dWq, dWk, dWv, dWr);
+                e = hipGetLastError() == hipSuccess ? 0 : -1;
+            }
+            return e;
         }
     }
     int cps;
@@ -401,6 +501,22 @@ int run_o_t(const ST* dY, const int32_t* I, const ST* A, int B, int T, int d, in
         if (const int rows = wgrad2_table_rows<P2>(R, d)) {
             typename P::Args a{dY, I, A, dWo, part, T, d, H, n, R, d / 64, 1, 0, make_fastdiv(n)};
             return launch_gemm2<P2>(a, H * (d / 64), stream, rows);
+        }
+    }
+    if constexpr (sizeof(ST) == 2 && !GATHER) {
+        using P2 = WgradODensePolicy2<DH>;
+        int rows;
+        const int S = dense_ranges(R, H * (d / 64), P2::KC, rows);
+        if (S > 0 && d % 64 == 0) {
+            typename P2::Args a{dY, I, A, dWo, part, T, d, H, n, R, d / 64, S, rows, make_fastdiv(n)};
+            int e = launch_gemm2<P2>(a, S * H * (d / 64), stream, rows);
+            if (e == 0) {
+                const size_t n8 = (size_t)H * DH * d / 8;
+                hipLaunchKernelGGL((wgrad_o_reduce_kernel<ST>), dim3((unsigned)((n8 + 255) / 256)), dim3(256), 0,
+                                   stream, part, S, n8, dWo);
+                e = hipGetLastError() == hipSuccess ? 0 : -1;
+            }
+            return e;
         }
     }
     int cps;
@@ -478,8 +594,17 @@ size_t partial_bytes(int B, int d, int H, int n, bool router) {
     const int sq = choose_splits(H * mtiles, (R + PQ::KC - 1) / PQ::KC, cps);
     const int so = choose_splits(H * ntiles, (R + PO::KC - 1) / PO::KC, cps);
     const size_t nq = 3 * DH + (router ? 16 : 0);
-    const size_t bq = sq > 1 ? (size_t)sq * H * d * nq * 4 : 0;
-    const size_t bo = so > 1 ? (size_t)so * H * DH * d * 4 : 0;
+    size_t bq = sq > 1 ? (size_t)sq * H * d * nq * 4 : 0;
+    size_t bo = so > 1 ? (size_t)so * H * DH * d * 4 : 0;
+    if constexpr (sizeof(ST) == 2) {
+        if (!router && d % 64 == 0) {  // dense heads on the multi-stage engine: one partial per row range
+            int rows;
+            const int sd = dense_ranges(R, H * (d / 64), WgradQkvDensePolicy2<DH>::KC, rows);
+            const int so2 = dense_ranges(R, H * (d / 64), WgradODensePolicy2<DH>::KC, rows);
+            bq = std::max(bq, (size_t)sd * H * d * 3 * DH * 4);
+            bo = std::max(bo, (size_t)so2 * H * DH * d * 4);
+        }
+    }
     return bq > bo ? bq : bo;
 }
 
