@@ -16,6 +16,7 @@
 #include "common.h"
 #include "gemm2.h"
 #include "kernels.h"
+#include "rope.h"
 #include "tiles.h"
 
 namespace mosa {
@@ -26,7 +27,8 @@ template <typename ST, int DH, bool WIN>
 __global__ __launch_bounds__(256) void attn_bwd_kv_kernel(const ST* __restrict__ QKV, const ST* __restrict__ dA,
                                                           const float* __restrict__ lse, const float* __restrict__ D,
                                                           int BH, int n, int causal, int lb, float scale,
-                                                          ST* __restrict__ dQKV) {
+                                                          ST* __restrict__ dQKV, const int32_t* __restrict__ rI,
+                                                          const float2* __restrict__ rtab) {
     constexpr int RS = 3 * DH;  // row stride of the packed Q | K | V (and dQ | dK | dV) rows
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int g = lane >> 4, c16 = lane & 15;
@@ -92,13 +94,17 @@ __global__ __launch_bounds__(256) void attn_bwd_kv_kernel(const ST* __restrict__
     }
     if (key < n) {
         // lane: key column c16, d_head rows db*16 + 4g + i
+        const int pos = rtab ? (rI ? rI[base + key] : key) : 0;
 #pragma unroll
-        for (int db = 0; db < DH / 16; ++db)
+        for (int db = 0; db < DH / 16; ++db) {
+            float x[4] = {dKt[db][0] * scale, dKt[db][1] * scale, dKt[db][2] * scale, dKt[db][3] * scale};
+            if (rtab) rope4_back<DH>(x, db * 16 + 4 * g, rtab, pos);
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
                 st1<ST>(dQKV + (base + key) * RS + 2 * DH + db * 16 + 4 * g + i, dVt[db][i]);
-                st1<ST>(dQKV + (base + key) * RS + DH + db * 16 + 4 * g + i, dKt[db][i] * scale);
+                st1<ST>(dQKV + (base + key) * RS + DH + db * 16 + 4 * g + i, x[i]);
             }
+        }
     }
 }
 
@@ -106,7 +112,8 @@ template <typename ST, int DH, bool WIN>
 __global__ __launch_bounds__(256) void attn_bwd_q_kernel(const ST* __restrict__ QKV, const ST* __restrict__ dA,
                                                          const float* __restrict__ lse, const float* __restrict__ D,
                                                          int BH, int n, int causal, int lb, float scale,
-                                                         ST* __restrict__ dQKV) {
+                                                         ST* __restrict__ dQKV, const int32_t* __restrict__ rI,
+                                                         const float2* __restrict__ rtab) {
     constexpr int RS = 3 * DH;
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int g = lane >> 4, c16 = lane & 15;
@@ -167,10 +174,14 @@ __global__ __launch_bounds__(256) void attn_bwd_q_kernel(const ST* __restrict__ 
         mfma_drain();  // the loop may exit right here
     }
     if (q < n) {
+        const int pos = rtab ? (rI ? rI[base + q] : q) : 0;
 #pragma unroll
-        for (int db = 0; db < DH / 16; ++db)
+        for (int db = 0; db < DH / 16; ++db) {
+            float x[4] = {dQt[db][0] * scale, dQt[db][1] * scale, dQt[db][2] * scale, dQt[db][3] * scale};
+            if (rtab) rope4_back<DH>(x, db * 16 + 4 * g, rtab, pos);
 #pragma unroll
-            for (int i = 0; i < 4; ++i) st1<ST>(dQKV + (base + q) * RS + db * 16 + 4 * g + i, dQt[db][i] * scale);
+            for (int i = 0; i < 4; ++i) st1<ST>(dQKV + (base + q) * RS + db * 16 + 4 * g + i, x[i]);
+        }
     }
 }
 
@@ -194,7 +205,9 @@ template <typename ST, int DH, bool WIN>
 __global__ __launch_bounds__(256) void attn_bwd_kv_tiled_kernel(const ST* __restrict__ QKV, const ST* __restrict__ dA,
                                                                 const float* __restrict__ lse,
                                                                 const float* __restrict__ D, int BH, int n, int causal,
-                                                                int lb, float scale, ST* __restrict__ dQKV) {
+                                                                int lb, float scale, ST* __restrict__ dQKV,
+                                                                const int32_t* __restrict__ rI,
+                                                                const float2* __restrict__ rtab) {
     using TL = BwdTile<ST, DH>;
     constexpr int TB = TL::TB, RS = TL::RS, LDR = TL::LDR, LDT = TL::LDT, VPR = TL::VPR, PER = TL::PER;
     __shared__ __attribute__((aligned(16))) ST Qs[TB * LDR];
@@ -330,7 +343,14 @@ __global__ __launch_bounds__(256) void attn_bwd_kv_tiled_kernel(const ST* __rest
         const int r = e / VPR, dc = (e % VPR) * 8;
         if (wk0 + r < n) {
             ST* out = dQKV + (base + wk0 + r) * RS;
-            vec8_store<ST>(out + DH + dc, vec8_load<ST>(Ks_out + r * LDR + dc));
+            Vec8<ST> kv = vec8_load<ST>(Ks_out + r * LDR + dc);
+            if (rtab && dc < DH / 2) {  // back through the rotation
+                float x[8];
+                vec8_to_f32<ST>(kv, x);
+                rope8<DH>(x, dc, rtab, rI ? rI[base + wk0 + r] : wk0 + r, -1.f);
+                kv = vec8_from_f32<ST>(x);
+            }
+            vec8_store<ST>(out + DH + dc, kv);
             vec8_store<ST>(out + 2 * DH + dc, vec8_load<ST>(Vs_out + r * LDR + dc));
         }
     }
@@ -340,7 +360,9 @@ template <typename ST, int DH, bool WIN>
 __global__ __launch_bounds__(256) void attn_bwd_q_tiled_kernel(const ST* __restrict__ QKV, const ST* __restrict__ dA,
                                                                const float* __restrict__ lse,
                                                                const float* __restrict__ D, int BH, int n, int causal,
-                                                               int lb, float scale, ST* __restrict__ dQKV) {
+                                                               int lb, float scale, ST* __restrict__ dQKV,
+                                                               const int32_t* __restrict__ rI,
+                                                               const float2* __restrict__ rtab) {
     using TL = BwdTile<ST, DH>;
     constexpr int TB = TL::TB, RS = TL::RS, LDR = TL::LDR, LDT = TL::LDT, VPR = TL::VPR, PER = TL::PER;
     __shared__ __attribute__((aligned(16))) ST Ks[TB * LDR];
@@ -450,7 +472,16 @@ __global__ __launch_bounds__(256) void attn_bwd_q_tiled_kernel(const ST* __restr
 #pragma unroll
     for (int e = lane; e < 16 * VPR; e += 64) {
         const int r = e / VPR, dc = (e % VPR) * 8;
-        if (wq0 + r < n) vec8_store<ST>(dQKV + (base + wq0 + r) * RS + dc, vec8_load<ST>(Qs_out + r * LDR + dc));
+        if (wq0 + r < n) {
+            Vec8<ST> qv = vec8_load<ST>(Qs_out + r * LDR + dc);
+            if (rtab && dc < DH / 2) {  // back through the rotation
+                float x[8];
+                vec8_to_f32<ST>(qv, x);
+                rope8<DH>(x, dc, rtab, rI ? rI[base + wq0 + r] : wq0 + r, -1.f);
+                qv = vec8_from_f32<ST>(x);
+            }
+            vec8_store<ST>(dQKV + (base + wq0 + r) * RS + dc, qv);
+        }
     }
 }
 
@@ -480,7 +511,8 @@ __global__ __launch_bounds__(512) void attn_bwd_lds_kernel(const uint16_t* __res
                                                            const uint16_t* __restrict__ dA,
                                                            const float* __restrict__ lse, const float* __restrict__ D,
                                                            int BH, int n, int causal, float scale,
-                                                           uint16_t* __restrict__ dQKV) {
+                                                           uint16_t* __restrict__ dQKV, const int32_t* __restrict__ rI,
+                                                           const float2* __restrict__ rtab) {
     using ST = uint16_t;
     using L = AttnBwdLds<DH>;
     constexpr int RS = 3 * DH, NMAX = L::NMAX, LPR = L::LPR, NW = L::NW, TILE = L::TILE;
@@ -623,12 +655,14 @@ __global__ __launch_bounds__(512) void attn_bwd_lds_kernel(const uint16_t* __res
         mfma_drain();
         if (key < n) {
             ST* out = dQKV + (base + key) * RS;
+            const int pos = rtab ? (rI ? rI[base + key] : key) : 0;
 #pragma unroll
             for (int db = 0; db < DH / 16; ++db) {
                 // lane: key c16, d = 16 db + 4 g + i
+                float x[4] = {dKt[db][0] * scale, dKt[db][1] * scale, dKt[db][2] * scale, dKt[db][3] * scale};
+                if (rtab) rope4_back<DH>(x, 16 * db + 4 * g, rtab, pos);
                 *reinterpret_cast<uint2*>(out + DH + 16 * db + 4 * g) =
-                    make_uint2(pack_bf16x2(dKt[db][0] * scale, dKt[db][1] * scale),
-                               pack_bf16x2(dKt[db][2] * scale, dKt[db][3] * scale));
+                    make_uint2(pack_bf16x2(x[0], x[1]), pack_bf16x2(x[2], x[3]));
                 *reinterpret_cast<uint2*>(out + 2 * DH + 16 * db + 4 * g) =
                     make_uint2(pack_bf16x2(dVt[db][0], dVt[db][1]), pack_bf16x2(dVt[db][2], dVt[db][3]));
             }
@@ -664,18 +698,21 @@ __global__ __launch_bounds__(512) void attn_bwd_lds_kernel(const uint16_t* __res
         mfma_drain();
         if (q < n) {
             ST* out = dQKV + (base + q) * RS;
+            const int pos = rtab ? (rI ? rI[base + q] : q) : 0;
 #pragma unroll
-            for (int db = 0; db < DH / 16; ++db)
+            for (int db = 0; db < DH / 16; ++db) {
+                float x[4] = {dQt[db][0] * scale, dQt[db][1] * scale, dQt[db][2] * scale, dQt[db][3] * scale};
+                if (rtab) rope4_back<DH>(x, 16 * db + 4 * g, rtab, pos);
                 *reinterpret_cast<uint2*>(out + 16 * db + 4 * g) =
-                    make_uint2(pack_bf16x2(dQt[db][0] * scale, dQt[db][1] * scale),
-                               pack_bf16x2(dQt[db][2] * scale, dQt[db][3] * scale));
+                    make_uint2(pack_bf16x2(x[0], x[1]), pack_bf16x2(x[2], x[3]));
+            }
         }
     }
 }
 
 template <typename ST>
 int launch_t(const ST* QKV, const ST* dA, const float* lse, const float* D, int BH, int n, int dh, int causal,
-             int window, ST* dQKV, int pass, hipStream_t stream) {
+             int window, ST* dQKV, const int32_t* rI, const float2* rtab, int pass, hipStream_t stream) {
     const float scale = 1.0f / sqrtf((float)dh);
     const int lb = window > 0 ? window - 1 : n;  // keys a query may look back
     if constexpr (sizeof(ST) == 2) {
@@ -691,7 +728,8 @@ int launch_t(const ST* QKV, const ST* dA, const float* lse, const float* D, int 
                 return -1;
             attr[dh == 64] = true;
         }
-        hipLaunchKernelGGL(kern, dim3(BH), dim3(512), lds, stream, QKV, dA, lse, D, BH, n, causal, scale, dQKV);
+        hipLaunchKernelGGL(kern, dim3(BH), dim3(512), lds, stream, QKV, dA, lse, D, BH, n, causal, scale, dQKV, rI,
+                           rtab);
         return hipGetLastError() == hipSuccess ? 0 : -1;
       }
       if (n > 32 || window > 0) {
@@ -699,7 +737,7 @@ int launch_t(const ST* QKV, const ST* dA, const float* lse, const float* D, int 
 #define MOSA_ATTN_BWD_T(KERN, DHV)                                                                   \
     do {                                                                                              \
         auto kern = window > 0 ? KERN<ST, DHV, true> : KERN<ST, DHV, false>;                          \
-        hipLaunchKernelGGL(kern, grid, block, 0, stream, QKV, dA, lse, D, BH, n, causal, lb, scale, dQKV); \
+        hipLaunchKernelGGL(kern, grid, block, 0, stream, QKV, dA, lse, D, BH, n, causal, lb, scale, dQKV, rI, rtab); \
     } while (0)
         if (pass == 0) {
             if (dh == 64) MOSA_ATTN_BWD_T(attn_bwd_kv_tiled_kernel, 64);
@@ -717,7 +755,7 @@ int launch_t(const ST* QKV, const ST* dA, const float* lse, const float* D, int 
 #define MOSA_ATTN_BWD(KERN, DHV)                                                                     \
     do {                                                                                              \
         auto kern = window > 0 ? KERN<ST, DHV, true> : KERN<ST, DHV, false>;                          \
-        hipLaunchKernelGGL(kern, grid, block, 0, stream, QKV, dA, lse, D, BH, n, causal, lb, scale, dQKV); \
+        hipLaunchKernelGGL(kern, grid, block, 0, stream, QKV, dA, lse, D, BH, n, causal, lb, scale, dQKV, rI, rtab); \
     } while (0)
     if (pass == 0) {
         if (dh == 64) MOSA_ATTN_BWD(attn_bwd_kv_kernel, 64);
@@ -733,12 +771,13 @@ int launch_t(const ST* QKV, const ST* dA, const float* lse, const float* D, int 
 }  // namespace
 
 int launch_attn_bwd(int dtype, const void* QKV, const void* dA, const float* lse, const float* D, int BH, int n,
-                    int dh, int causal, int window, void* dQKV, int pass, hipStream_t stream) {
+                    int dh, int causal, int window, void* dQKV, const int32_t* rope_I, const float2* rope,
+                    int pass, hipStream_t stream) {
     if (dtype == kBF16)
         return launch_t<uint16_t>((const uint16_t*)QKV, (const uint16_t*)dA, lse, D, BH, n, dh, causal, window,
-                                  (uint16_t*)dQKV, pass, stream);
+                                  (uint16_t*)dQKV, rope_I, rope, pass, stream);
     return launch_t<float>((const float*)QKV, (const float*)dA, lse, D, BH, n, dh, causal, window, (float*)dQKV,
-                           pass, stream);
+                           rope_I, rope, pass, stream);
 }
 
 }  // namespace mosa

@@ -329,14 +329,12 @@ int mosa_backward_timed(const mosa_shape* s, const void* X, const mosa_weights* 
     if (H > 0) {
         e |= launch_dattn_out(dt, dY, I, r, w->Wo, A, B, T, d, H, dh, k, dA, D, dz, dz16, stream);
         e |= sm.mark("bwd_out");
-        e |= launch_attn_bwd(dt, QKV, dA, lse, D, B * H, k, dh, causal, 0, dQKV, 0, stream);
+        // with the rotary encoding, dQ and dK leave these kernels turned back
+        // through the rotation (the gradients of the unrotated q and k)
+        e |= launch_attn_bwd(dt, QKV, dA, lse, D, B * H, k, dh, causal, 0, dQKV, I, rope, 0, stream);
         e |= sm.mark("attn_bwd_kv");
-        e |= launch_attn_bwd(dt, QKV, dA, lse, D, B * H, k, dh, causal, 0, dQKV, 1, stream);
+        e |= launch_attn_bwd(dt, QKV, dA, lse, D, B * H, k, dh, causal, 0, dQKV, I, rope, 1, stream);
         e |= sm.mark("attn_bwd_q");
-        if (rope) {
-            e |= launch_rope_grad(dt, dQKV, I, rope, B * H * k, k, dh, stream);
-            e |= sm.mark("rope_grad");
-        }
         // untimed: the weight gradients and the dX rows in one grouped launch
         const int grouped = ev ? 1
                                : launch_bwd_proj(dt, X, dY, I, A, dQKV, dz16, dz, w->Wq, w->Wk, w->Wv, Wr, B, T, d,
@@ -354,14 +352,12 @@ int mosa_backward_timed(const mosa_shape* s, const void* X, const mosa_weights* 
         e |= launch_dattn_out(dt, dY, nullptr, nullptr, w->Wo_d, Ad, B, T, d, Hd, dh, T, dAd, Dd, nullptr, nullptr,
                               stream);
         e |= sm.mark("bwd_out_dense");
-        e |= launch_attn_bwd(dt, QKVd, dAd, lsed, Dd, B * Hd, T, dh, causal, s->window, dQKVd, 0, stream);
+        e |= launch_attn_bwd(dt, QKVd, dAd, lsed, Dd, B * Hd, T, dh, causal, s->window, dQKVd, nullptr, rope, 0,
+                             stream);
         e |= sm.mark("attn_bwd_kv_dense");
-        e |= launch_attn_bwd(dt, QKVd, dAd, lsed, Dd, B * Hd, T, dh, causal, s->window, dQKVd, 1, stream);
+        e |= launch_attn_bwd(dt, QKVd, dAd, lsed, Dd, B * Hd, T, dh, causal, s->window, dQKVd, nullptr, rope, 1,
+                             stream);
         e |= sm.mark("attn_bwd_q_dense");
-        if (rope) {
-            e |= launch_rope_grad(dt, dQKVd, nullptr, rope, B * Hd * T, T, dh, stream);
-            e |= sm.mark("rope_grad_dense");
-        }
         e |= launch_wgrad(dt, X, dY, nullptr, Ad, dQKVd, nullptr, B, T, d, Hd, dh, T, g->dWq_d, g->dWk_d,
                           g->dWv_d, nullptr, g->dWo_d, wpart, 0, stream);
         e |= sm.mark("wgrad_qkv_dense");

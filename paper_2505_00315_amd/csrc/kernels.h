@@ -28,12 +28,8 @@ int launch_select(int dtype, const float* z, const float* xnorm, const void* X, 
 int launch_fixed_select(int B, int T, int H, int k, int stride, int32_t* I, float* r, int16_t* slot,
                         hipStream_t stream);
 
-// Rotary encoding: tab [T, dh/4] (cos, sin) pairs; the inverse rotation of the
-// dQ and dK parts of `rows` packed dQ | dK | dV rows (row = (b,h,i), position
-// I[row], or i = row % n when I == nullptr), in place.
+// Rotary encoding: tab [T, dh/4] (cos, sin) pairs of positions 0..T-1.
 int launch_rope_table(int T, int dh, float base, float2* tab, hipStream_t stream);
-int launch_rope_grad(int dtype, void* dQKV, const int32_t* I, const float2* tab, int rows, int n, int dh,
-                     hipStream_t stream);
 
 // QKV[b,h,i,:] = X[b, I[b,h,i], :] . [Wq | Wk | Wv][h]  (packed rows of 3*dh)
 // for i < n (I == nullptr: identity, i.e. a dense head with n = T); with a
@@ -74,7 +70,8 @@ int launch_dattn_out(int dtype, const void* dY, const int32_t* I, const float* r
 
 // Attention backward into packed dQKV rows; pass 0 writes dK, dV, pass 1 writes dQ.
 int launch_attn_bwd(int dtype, const void* QKV, const void* dA, const float* lse, const float* D, int BH,
-                    int n, int dh, int causal, int window, void* dQKV, int pass, hipStream_t stream);
+                    int n, int dh, int causal, int window, void* dQKV, const int32_t* rope_I,
+                    const float2* rope, int pass, hipStream_t stream);
 
 // Weight gradients; which 0: dWq, dWk, dWv (+ dWr when non-null), which 1: dWo,
 // which 2: both (in one launch where the gathered-row engine applies).

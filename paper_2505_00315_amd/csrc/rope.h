@@ -26,4 +26,18 @@ __device__ __forceinline__ void rope8(float (&x)[8], int c0, const float2* __res
     }
 }
 
+// 4 consecutive columns d0 .. d0 + 3 (d0 % 4 == 0) of a dQ or dK row at
+// position pos: the two pairs turned back by R(p)^T if they lie in the
+// rotated half (the gradient with respect to the unrotated q or k).
+template <int DH>
+__device__ __forceinline__ void rope4_back(float (&x)[4], int d0, const float2* __restrict__ tab, int pos) {
+    if (d0 >= DH / 2) return;
+    const float4 t = *reinterpret_cast<const float4*>(tab + (size_t)pos * (DH / 4) + d0 / 2);
+    const float u0 = x[0], v0 = x[1], u1 = x[2], v1 = x[3];
+    x[0] = u0 * t.x + v0 * t.y;
+    x[1] = v0 * t.x - u0 * t.y;
+    x[2] = u1 * t.z + v1 * t.w;
+    x[3] = v1 * t.z - u1 * t.w;
+}
+
 }  // namespace mosa

@@ -75,8 +75,6 @@ def stage_work(w, with_backward=True):
         add("attn_bwd_q", 5 * rows * dh * es + rows * 8, 6.0 * dh * _pairs(k, w.causal) * B * H)
         # both passes: Q, K, V, dA read, dQ | dK | dV written, lse and D read
         add("attn_bwd", 7 * rows * dh * es + rows * 8, 14.0 * dh * _pairs(k, w.causal) * B * H)
-        if w.rope:  # dQ and dK halves read and written, I read
-            add("rope_grad", 2 * rows * dh * es + rows * 4, 0.0)
         # dW^{Q,K,V,r} and dW^O (one grouped launch): X and dY read, the
         # selected rows' dQ|dK|dV and r A, I, the gradients written once
         add("wgrad", 2 * X + 4 * rows * dh * es + rows * 4 + 4 * H * d * dh * es + H * d * es,
@@ -87,8 +85,6 @@ def stage_work(w, with_backward=True):
         add("attn_bwd_kv_dense", 6 * R * dh * es + R * 8, 8.0 * dh * _pairs(T, w.causal, w.window) * B * Hd)
         add("attn_bwd_q_dense", 5 * R * dh * es + R * 8, 6.0 * dh * _pairs(T, w.causal, w.window) * B * Hd)
         add("attn_bwd_dense", 7 * R * dh * es + R * 8, 14.0 * dh * _pairs(T, w.causal, w.window) * B * Hd)
-        if w.rope:
-            add("rope_grad_dense", 2 * R * dh * es, 0.0)
         add("wgrad_qkv_dense", X + 3 * R * dh * es + 3 * Hd * d * dh * es, 2.0 * R * d * 3 * dh)
         add("wgrad_o_dense", X + R * dh * es + Hd * dh * d * es, 2.0 * R * dh * d)
     add("dx_scatter",
@@ -173,7 +169,6 @@ STAGE_KERNELS = {
     "router": (r"router_kernel", r"RouterPolicy2"),
     "select": (r"select_\w*kernel",),
     "rope_table": (r"rope_table_kernel",),
-    "rope_grad": (r"rope_grad_kernel",),
     "qkv": (r"(?<!Wgrad)QkvPolicy",),
     "qkv_attn": (r"QkvAttnPolicy",),
     "attn": (r"attn_fwd",),
