@@ -146,7 +146,8 @@ __global__ __launch_bounds__(256) void attn_fwd_tiled_kernel(const ST* __restric
 #pragma unroll
     for (int st = 0; st < DH / 32; ++st) qf[st] = frag8_load<ST>(Qp + (size_t)min(q, n - 1) * RS + st * 32 + 8 * g);
 
-    float m_run = -__builtin_inff(), l_run = 0.f;
+    float m_run = -__builtin_inff(), l_run = 0.f;  // running max in log2 units
+    const float c2 = scale * 1.44269504088896341f;
     f32x4 o[DH / 16];
 #pragma unroll
     for (int db = 0; db < DH / 16; ++db) o[db] = zero4();
@@ -166,13 +167,21 @@ __global__ __launch_bounds__(256) void attn_fwd_tiled_kernel(const ST* __restric
             vreg[p] = vec8_load<ST>(Vp + row * RS + dc);
         }
     };
+    // bf16: V rows stay row-major (16-byte units permuted per key row by
+    // vt_swz) and are read transposed (ds_read_b64_tr_b16), as in attn_lds.h
+    unsigned char* const Vs = reinterpret_cast<unsigned char*>(Vt);
+    static_assert(sizeof(ST) != 2 || DH * LDT * 2 >= KB * DH * 2, "V tile fits");
     auto store_tile = [&]() {
 #pragma unroll
         for (int p = 0; p < PER; ++p) {
             const int v = tid + 256 * p, key = v / VPR, dc = (v % VPR) * 8;
             vec8_store<ST>(Ks + key * LDR + dc, kreg[p]);
+            if constexpr (sizeof(ST) == 2) {
+                *reinterpret_cast<uint4*>(Vs + (key * VPR + ((dc >> 3) ^ vt_swz<VPR>(key))) * 16) = vreg[p].v;
+            } else {
 #pragma unroll
-            for (int j = 0; j < 8; ++j) Vt[(dc + j) * LDT + key] = vec8_elem<ST>(vreg[p], j);
+                for (int j = 0; j < 8; ++j) Vt[(dc + j) * LDT + key] = vec8_elem<ST>(vreg[p], j);
+            }
         }
     };
 
@@ -200,7 +209,8 @@ __global__ __launch_bounds__(256) void attn_fwd_tiled_kernel(const ST* __restric
             for (int i = 0; i < 4; ++i) {
                 const int key = j0 + sb * 16 + 4 * g + i;
                 const bool ok = key < n && (!causal || (key <= q && (!WIN || q - key <= lb)));
-                s[sb][i] = ok ? s[sb][i] * scale : -__builtin_inff();
+                // scores in log2 units: s scale log2(e), so that p = 2^(s - m)
+                s[sb][i] = ok ? s[sb][i] * c2 : -__builtin_inff();
                 mloc = fmaxf(mloc, s[sb][i]);
             }
         mloc = fmaxf(mloc, __shfl_xor(mloc, 16, 64));
@@ -209,13 +219,13 @@ __global__ __launch_bounds__(256) void attn_fwd_tiled_kernel(const ST* __restric
         // (m_new = -inf): it then adds nothing.  Its own key comes later.
         const float m_new = fmaxf(m_run, mloc);
         const float m_use = WIN && m_new == -__builtin_inff() ? 0.f : m_new;
-        const float alpha = expf(m_run - m_use);
+        const float alpha = __builtin_amdgcn_exp2f(m_run - m_use);
         float p[4][4], lsum = 0.f;
 #pragma unroll
         for (int sb = 0; sb < 4; ++sb)
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
-                p[sb][i] = expf(s[sb][i] - m_use);
+                p[sb][i] = __builtin_amdgcn_exp2f(s[sb][i] - m_use);
                 lsum += p[sb][i];
             }
         lsum += __shfl_xor(lsum, 16, 64);
@@ -231,10 +241,31 @@ __global__ __launch_bounds__(256) void attn_fwd_tiled_kernel(const ST* __restric
             const float pv[8] = {p[2 * u][0], p[2 * u][1], p[2 * u][2], p[2 * u][3],
                                  p[2 * u + 1][0], p[2 * u + 1][1], p[2 * u + 1][2], p[2 * u + 1][3]};
             const Frag8<ST> pf = frag8_from<ST>(pv);
+            if constexpr (sizeof(ST) == 2) {
+                // lane reads d columns 16 db + 4 (c16 % 4) .. + 3 at keys k0 and k0 + 16
+                u32x4 vt[DH / 16];
+                const int k0 = 32 * u + 4 * g + (c16 >> 2), k1 = k0 + 16;
 #pragma unroll
-            for (int db = 0; db < DH / 16; ++db) {
-                const ST* vrow = Vt + (db * 16 + c16) * LDT + 32 * u + 4 * g;
-                mma8(o[db], frag8_from_quads<ST>(quad_load<ST>(vrow), quad_load<ST>(vrow + 16)), pf);
+                for (int db = 0; db < DH / 16; ++db) {
+                    const int mcol = 16 * db + 4 * (c16 & 3), un = mcol >> 3, half = (mcol >> 2) & 1;
+                    const u32x2 lo = lds_read_tr16(Vs + (k0 * VPR + (un ^ vt_swz<VPR>(k0))) * 16 + 8 * half);
+                    const u32x2 hi = lds_read_tr16(Vs + (k1 * VPR + (un ^ vt_swz<VPR>(k1))) * 16 + 8 * half);
+                    vt[db] = u32x4{lo.x, lo.y, hi.x, hi.y};
+                }
+                lds_wait();
+#pragma unroll
+                for (int db = 0; db < DH / 16; ++db) {
+                    lds_ready(vt[db]);
+                    Frag8<ST> vf;
+                    vf.v = __builtin_bit_cast(bf16x8, vt[db]);
+                    mma8(o[db], vf, pf);
+                }
+            } else {
+#pragma unroll
+                for (int db = 0; db < DH / 16; ++db) {
+                    const ST* vrow = Vt + (db * 16 + c16) * LDT + 32 * u + 4 * g;
+                    mma8(o[db], frag8_from_quads<ST>(quad_load<ST>(vrow), quad_load<ST>(vrow + 16)), pf);
+                }
             }
         }
         mfma_drain();  // the loop may exit right here
@@ -252,7 +283,7 @@ __global__ __launch_bounds__(256) void attn_fwd_tiled_kernel(const ST* __restric
             if constexpr (sizeof(ST) == 2) Os[c16 * LDR + db * 16 + 4 * g + i] = f32_to_bf16(x);
             else Os[c16 * LDR + db * 16 + 4 * g + i] = x;
         }
-    if (g == 0 && q < n) lse[(size_t)bh * n + q] = m_run + logf(l_run);
+    if (g == 0 && q < n) lse[(size_t)bh * n + q] = m_run * 0.69314718055994531f + logf(l_run);  // ln 2
     __syncthreads();
 #pragma unroll
     for (int e = lane; e < 16 * VPR; e += 64) {
