@@ -187,15 +187,14 @@ __global__ __launch_bounds__(256) void attn_bwd_q_kernel(const ST* __restrict__ 
 
 // Tiled passes for n > 32 (bf16 storage): a workgroup owns 64 keys (kv
 // pass) or 64 queries (q pass) of one (b,h), 16 per wave, and walks the other
-// side in tiles of 64 rows staged once in LDS for all four waves, row-major
-// for the score MFMAs and transposed for the MFMAs that contract over rows
-// (32 rows per MFMA, P and dS straight from registers).  The next tile's
+// side in tiles of 64 rows staged once in LDS for all four waves, row-major;
+// the MFMAs that contract over rows (32 rows per MFMA, P and dS straight from
+// registers) read their operands transposed with ds_read_b64_tr_b16.  The next tile's
 // global loads overlap the current tile's MFMAs.
 template <typename ST, int DH>
 struct BwdTile {
     static constexpr int TB = 64, RS = 3 * DH;
     static constexpr int LDR = DH + 16 / (int)sizeof(ST);  // row-major rows
-    static constexpr int LDT = TB + 4;                      // transposed rows
     static constexpr int VPR = DH / 8;
     static constexpr int PER = TB * VPR / 256;
     static_assert(PER >= 1 && TB * VPR % 256 == 0, "tile shape");
@@ -209,11 +208,10 @@ __global__ __launch_bounds__(256) void attn_bwd_kv_tiled_kernel(const ST* __rest
                                                                 const int32_t* __restrict__ rI,
                                                                 const float2* __restrict__ rtab) {
     using TL = BwdTile<ST, DH>;
-    constexpr int TB = TL::TB, RS = TL::RS, LDR = TL::LDR, LDT = TL::LDT, VPR = TL::VPR, PER = TL::PER;
+    constexpr int TB = TL::TB, RS = TL::RS, LDR = TL::LDR, VPR = TL::VPR, PER = TL::PER;
+    static_assert(sizeof(ST) == 2, "bf16: transposed operands by ds_read_b64_tr_b16");
     __shared__ __attribute__((aligned(16))) ST Qs[TB * LDR];
     __shared__ __attribute__((aligned(16))) ST dAs[TB * LDR];
-    __shared__ __attribute__((aligned(16))) ST QT[DH * LDT];
-    __shared__ __attribute__((aligned(16))) ST dAT[DH * LDT];
     __shared__ float ls[TB], Dsh[TB];
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -264,11 +262,6 @@ __global__ __launch_bounds__(256) void attn_bwd_kv_tiled_kernel(const ST* __rest
             const int v = tid + 256 * p, r = v / VPR, dc = (v % VPR) * 8;
             vec8_store<ST>(Qs + r * LDR + dc, qreg[p]);
             vec8_store<ST>(dAs + r * LDR + dc, areg[p]);
-#pragma unroll
-            for (int j = 0; j < 8; ++j) {
-                QT[(dc + j) * LDT + r] = vec8_elem<ST>(qreg[p], j);
-                dAT[(dc + j) * LDT + r] = vec8_elem<ST>(areg[p], j);
-            }
         }
         if (tid < TB) {
             ls[tid] = lreg;
@@ -309,12 +302,31 @@ __global__ __launch_bounds__(256) void attn_bwd_kv_tiled_kernel(const ST* __rest
             const float dv[8] = {ds[2 * u][0], ds[2 * u][1], ds[2 * u][2], ds[2 * u][3],
                                  ds[2 * u + 1][0], ds[2 * u + 1][1], ds[2 * u + 1][2], ds[2 * u + 1][3]};
             const Frag8<ST> pf = frag8_from<ST>(pv), dsf = frag8_from<ST>(dv);
+            // dA^T and Q^T over the queries of those slots, read transposed
+            // from the row-major tiles: lane d columns 16 db + 4 (c16 % 4) ..
+            // + 3 at query rows r0 and r0 + 16
+            const int r0 = 32 * u + 4 * g + (c16 >> 2);
+            u32x4 at[DH / 16], qt[DH / 16];
 #pragma unroll
             for (int db = 0; db < DH / 16; ++db) {
-                const ST* ar = dAT + (db * 16 + c16) * LDT + 32 * u + 4 * g;
-                const ST* qr = QT + (db * 16 + c16) * LDT + 32 * u + 4 * g;
-                mma8(dVt[db], frag8_from_quads<ST>(quad_load<ST>(ar), quad_load<ST>(ar + 16)), pf);
-                mma8(dKt[db], frag8_from_quads<ST>(quad_load<ST>(qr), quad_load<ST>(qr + 16)), dsf);
+                const int mcol = 16 * db + 4 * (c16 & 3);
+                const unsigned char* a0 = reinterpret_cast<const unsigned char*>(dAs + r0 * LDR + mcol);
+                const unsigned char* q0p = reinterpret_cast<const unsigned char*>(Qs + r0 * LDR + mcol);
+                const u32x2 alo = lds_read_tr16(a0), ahi = lds_read_tr16(a0 + 32 * LDR);
+                const u32x2 qlo = lds_read_tr16(q0p), qhi = lds_read_tr16(q0p + 32 * LDR);
+                at[db] = u32x4{alo.x, alo.y, ahi.x, ahi.y};
+                qt[db] = u32x4{qlo.x, qlo.y, qhi.x, qhi.y};
+            }
+            lds_wait();
+#pragma unroll
+            for (int db = 0; db < DH / 16; ++db) {
+                lds_ready(at[db]);
+                lds_ready(qt[db]);
+                Frag8<ST> fa, fq;
+                fa.v = __builtin_bit_cast(bf16x8, at[db]);
+                fq.v = __builtin_bit_cast(bf16x8, qt[db]);
+                mma8(dVt[db], fa, pf);
+                mma8(dKt[db], fq, dsf);
             }
         }
         mfma_drain();  // the loop may exit right here
@@ -364,10 +376,10 @@ __global__ __launch_bounds__(256) void attn_bwd_q_tiled_kernel(const ST* __restr
                                                                const int32_t* __restrict__ rI,
                                                                const float2* __restrict__ rtab) {
     using TL = BwdTile<ST, DH>;
-    constexpr int TB = TL::TB, RS = TL::RS, LDR = TL::LDR, LDT = TL::LDT, VPR = TL::VPR, PER = TL::PER;
+    constexpr int TB = TL::TB, RS = TL::RS, LDR = TL::LDR, VPR = TL::VPR, PER = TL::PER;
+    static_assert(sizeof(ST) == 2, "bf16: transposed operands by ds_read_b64_tr_b16");
     __shared__ __attribute__((aligned(16))) ST Ks[TB * LDR];
     __shared__ __attribute__((aligned(16))) ST Vs[TB * LDR];
-    __shared__ __attribute__((aligned(16))) ST KT[DH * LDT];
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int g = lane >> 4, c16 = lane & 15;
@@ -413,8 +425,6 @@ __global__ __launch_bounds__(256) void attn_bwd_q_tiled_kernel(const ST* __restr
             const int v = tid + 256 * p, r = v / VPR, dc = (v % VPR) * 8;
             vec8_store<ST>(Ks + r * LDR + dc, kreg[p]);
             vec8_store<ST>(Vs + r * LDR + dc, vreg[p]);
-#pragma unroll
-            for (int j = 0; j < 8; ++j) KT[(dc + j) * LDT + r] = vec8_elem<ST>(kreg[p], j);
         }
     };
 
@@ -449,10 +459,23 @@ __global__ __launch_bounds__(256) void attn_bwd_q_tiled_kernel(const ST* __restr
             const float dv[8] = {ds[2 * u][0], ds[2 * u][1], ds[2 * u][2], ds[2 * u][3],
                                  ds[2 * u + 1][0], ds[2 * u + 1][1], ds[2 * u + 1][2], ds[2 * u + 1][3]};
             const Frag8<ST> dsf = frag8_from<ST>(dv);
+            // K^T over the keys of those slots, read transposed from the row-major tile
+            const int r0 = 32 * u + 4 * g + (c16 >> 2);
+            u32x4 kt[DH / 16];
 #pragma unroll
             for (int db = 0; db < DH / 16; ++db) {
-                const ST* kr = KT + (db * 16 + c16) * LDT + 32 * u + 4 * g;
-                mma8(dQt[db], frag8_from_quads<ST>(quad_load<ST>(kr), quad_load<ST>(kr + 16)), dsf);
+                const unsigned char* k0p =
+                    reinterpret_cast<const unsigned char*>(Ks + r0 * LDR + 16 * db + 4 * (c16 & 3));
+                const u32x2 lo = lds_read_tr16(k0p), hi = lds_read_tr16(k0p + 32 * LDR);
+                kt[db] = u32x4{lo.x, lo.y, hi.x, hi.y};
+            }
+            lds_wait();
+#pragma unroll
+            for (int db = 0; db < DH / 16; ++db) {
+                lds_ready(kt[db]);
+                Frag8<ST> fk;
+                fk.v = __builtin_bit_cast(bf16x8, kt[db]);
+                mma8(dQt[db], fk, dsf);
             }
         }
         mfma_drain();  // the loop may exit right here
