@@ -141,6 +141,52 @@ def cpu_baseline(w, inp, with_backward, target_s):
                       f"fp64 CPU oracle, {t:.1f} s"}
 
 
+def time_comparator(w, steps, warmup, with_bwd):
+    """Whole steps of the comparator workload on the same GPU and stream
+    (inputs resident, no instrumentation inside the timed region)."""
+    import numpy as np
+    import torch
+
+    from paper_2505_00315_amd import mosa
+
+    inp = wl.make_inputs(w, with_grad=with_bwd)
+
+    def dev(a):
+        if a is None:
+            return None
+        if a.dtype == np.uint16:
+            return torch.from_numpy(a.view(np.int16).copy()).view(torch.bfloat16).cuda()
+        return torch.from_numpy(a).cuda()
+
+    d = {n: dev(v) for n, v in inp.items()}
+    shape = mosa.make_shape(w.batch, w.seq_len, w.d_model, w.heads, w.d_head, w.k, w.causal, w.dense_heads, w.dtype,
+                            **w.variants())
+    weights = {n: d.get(n) for n in mosa.WEIGHT_NAMES}
+    saved, scratch = mosa.alloc_workspace(shape)
+    Y, dX = torch.empty_like(d["X"]), torch.empty_like(d["X"])
+    grads = {"d" + n: torch.empty_like(d[n]) for n in mosa.WEIGHT_NAMES if d.get(n) is not None and d[n].numel()}
+    stream = torch.cuda.current_stream()
+
+    def step():
+        mosa.forward(shape, d["X"], weights, Y=Y, saved=saved, scratch=scratch, stream=stream)
+        if with_bwd:
+            mosa.backward(shape, d["X"], weights, d["dY"], saved, grads, dX=dX, scratch=scratch, stream=stream)
+
+    for _ in range(warmup):
+        step()
+    torch.cuda.synchronize()
+    start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    start.record(stream)
+    for _ in range(steps):
+        step()
+    stop.record(stream)
+    torch.cuda.synchronize()
+    ms = start.elapsed_time(stop) / steps
+    return {"workload": w.name, "dense_heads": w.dense_heads, "mosa_heads": w.heads, "seq_len": w.seq_len,
+            "pass": "forward+backward" if with_bwd else "forward", "ms_per_step": ms,
+            "tokens_per_s": w.batch * w.seq_len / (ms / 1e3)}
+
+
 def main():
     args = parse_args()
     if args.gpus != 1:
@@ -269,6 +315,14 @@ def main():
         "stages": stages,
         "roofline": roof,
     }
+    comp = wl.COMPARATORS.get(w.name)
+    if comp:
+        cw = wl.WORKLOADS[comp]
+        line["comparator"] = time_comparator(cw, args.steps, args.warmup, with_bwd)
+        # the paper's FLOP formula (Appendix A) for the two layers, one sequence
+        line["comparator"]["paper_gflops"] = {
+            w.name: round(w.heads * pm.paper_flops_mosa_head(w.d_model, w.d_head, w.seq_len, w.k) / 1e9, 2),
+            cw.name: round(cw.dense_heads * pm.paper_flops_dense_head(cw.d_model, cw.d_head, cw.seq_len) / 1e9, 2)}
     if args.calibrate_copy > 0:
         nel = args.calibrate_copy * (1 << 20) // 4
         src_t = torch.ones(nel, dtype=torch.float32, device="cuda")

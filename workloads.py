@@ -71,7 +71,14 @@ WORKLOADS = {
     # paper does not state it)
     "long_local_t8192": Workload("long_local_t8192", 1, 8192, 1024, 60, 64, 64, dense_heads=4,
                                  backward=True, seed=4, window=512),
+    # the dense causal layer that the long-sequence MoSA layer is compared
+    # with: by the paper's FLOP formula (Appendix A) 64 MoSA heads with
+    # k = 512 cost about as much as one dense head at T = 8192
+    "long_dense1_t8192": Workload("long_dense1_t8192", 1, 8192, 1024, 0, 64, 0, dense_heads=1, seed=4),
 }
+
+# Workloads timed together with a comparator of equal FLOPs on the same GPU.
+COMPARATORS = {"long_t8192": "long_dense1_t8192"}
 
 
 def f32_to_bf16_bits(a):
