@@ -111,24 +111,26 @@ __global__ __launch_bounds__(256) void attn_fwd_kernel(const ST* __restrict__ QK
     }
 }
 
-// Tiled variant for n > 32: a workgroup owns 64 query rows of one (b,h)
-// (16 per wave) and walks the keys in tiles of 64 staged in LDS once for all
-// four waves: K row-major (A operand of S^T = K Q^T) and V transposed
+// Tiled variant for n > 32 (and every local-window head): a workgroup owns
+// 16 NWV query rows of one (b,h), 16 per wave (128 rows for bf16 with
+// 64-wide heads, else 64), and walks the keys in tiles of 64 staged in LDS
+// once for all its waves: K row-major (A operand of S^T = K Q^T) and V
 // (A operand of O^T += V^T P^T, K = 32 keys per MFMA, P^T straight from the
-// S^T registers).  The next tile's global loads are in flight while the
-// current one is processed.  Causal blocks are launched heaviest first.
-template <typename ST, int DH, bool WIN>
-__global__ __launch_bounds__(256) void attn_fwd_tiled_kernel(const ST* __restrict__ QKV, int BH, int n, int causal,
+// S^T registers; bf16 keeps V row-major and reads it transposed).  Online
+// softmax in log2 units.  The next tile's global loads are in flight while
+// the current one is processed.  Causal blocks are launched heaviest first.
+template <typename ST, int DH, bool WIN, int NWV>
+__global__ __launch_bounds__(64 * NWV) void attn_fwd_tiled_kernel(const ST* __restrict__ QKV, int BH, int n, int causal,
                                                              int lb, float scale, const float* __restrict__ rw,
                                                              ST* __restrict__ A, float* __restrict__ lse) {
-    constexpr int QB = 64, KB = 64, RS = 3 * DH;
+    constexpr int NT = 64 * NWV, QB = 16 * NWV, KB = 64, RS = 3 * DH;
     constexpr int PAD = 16 / (int)sizeof(ST);
     constexpr int LDR = DH + PAD;   // row-major K rows (and the output staging)
     constexpr int LDT = KB + 4;     // transposed V rows (keys), quad reads stay aligned
     constexpr int VPR = DH / 8;     // Vec8 per row
-    constexpr int PER = KB * VPR / 256;
-    static_assert(PER >= 1 && KB * VPR % 256 == 0, "tile shape");
-    __shared__ __attribute__((aligned(16))) ST Ks[KB * LDR];
+    constexpr int PER = KB * VPR / NT;
+    static_assert(PER >= 1 && KB * VPR % NT == 0, "tile shape");
+    __shared__ __attribute__((aligned(16))) ST Ks[(KB > QB ? KB : QB) * LDR];  // K tile, then the output rows
     __shared__ __attribute__((aligned(16))) ST Vt[DH * LDT];
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -161,7 +163,7 @@ __global__ __launch_bounds__(256) void attn_fwd_tiled_kernel(const ST* __restric
     auto load_tile = [&](int j0) {
 #pragma unroll
         for (int p = 0; p < PER; ++p) {
-            const int v = tid + 256 * p, key = v / VPR, dc = (v % VPR) * 8;
+            const int v = tid + NT * p, key = v / VPR, dc = (v % VPR) * 8;
             const size_t row = (size_t)min(j0 + key, n - 1);
             kreg[p] = vec8_load<ST>(Kp + row * RS + dc);
             vreg[p] = vec8_load<ST>(Vp + row * RS + dc);
@@ -174,7 +176,7 @@ __global__ __launch_bounds__(256) void attn_fwd_tiled_kernel(const ST* __restric
     auto store_tile = [&]() {
 #pragma unroll
         for (int p = 0; p < PER; ++p) {
-            const int v = tid + 256 * p, key = v / VPR, dc = (v % VPR) * 8;
+            const int v = tid + NT * p, key = v / VPR, dc = (v % VPR) * 8;
             vec8_store<ST>(Ks + key * LDR + dc, kreg[p]);
             if constexpr (sizeof(ST) == 2) {
                 *reinterpret_cast<uint4*>(Vs + (key * VPR + ((dc >> 3) ^ vt_swz<VPR>(key))) * 16) = vreg[p].v;
@@ -357,9 +359,14 @@ int launch_attn_fwd_t(const ST* QKV, const float* r, int BH, int n, int dh, int 
         }
     }
     if (n > 32 || window > 0) {
-        const dim3 grid(BH * ((n + 63) / 64)), block(256);
-        auto kern = window > 0 ? (dh == 64 ? attn_fwd_tiled_kernel<ST, 64, true> : attn_fwd_tiled_kernel<ST, 32, true>)
-                               : (dh == 64 ? attn_fwd_tiled_kernel<ST, 64, false> : attn_fwd_tiled_kernel<ST, 32, false>);
+        // bf16 with 64-wide heads: 128 queries (8 waves) per workgroup share each K/V tile
+        constexpr int W64 = sizeof(ST) == 2 ? 8 : 4;
+        auto kern = window > 0 ? (dh == 64 ? attn_fwd_tiled_kernel<ST, 64, true, W64>
+                                           : attn_fwd_tiled_kernel<ST, 32, true, 4>)
+                               : (dh == 64 ? attn_fwd_tiled_kernel<ST, 64, false, W64>
+                                           : attn_fwd_tiled_kernel<ST, 32, false, 4>);
+        const int qbw = 16 * (dh == 64 ? W64 : 4);
+        const dim3 grid(BH * ((n + qbw - 1) / qbw)), block(4 * qbw);
         hipLaunchKernelGGL(kern, grid, block, 0, stream, QKV, BH, n, causal, lb, scale, r, A, lse);
         return hipGetLastError() == hipSuccess ? 0 : -1;
     }
