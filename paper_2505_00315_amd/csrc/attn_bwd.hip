@@ -196,29 +196,30 @@ struct BwdTile {
     static constexpr int TB = 64, RS = 3 * DH;
     static constexpr int LDR = DH + 16 / (int)sizeof(ST);  // row-major rows
     static constexpr int VPR = DH / 8;
-    static constexpr int PER = TB * VPR / 256;
-    static_assert(PER >= 1 && TB * VPR % 256 == 0, "tile shape");
 };
 
-template <typename ST, int DH, bool WIN>
-__global__ __launch_bounds__(256) void attn_bwd_kv_tiled_kernel(const ST* __restrict__ QKV, const ST* __restrict__ dA,
+template <typename ST, int DH, bool WIN, int NWV>
+__global__ __launch_bounds__(64 * NWV) void attn_bwd_kv_tiled_kernel(const ST* __restrict__ QKV, const ST* __restrict__ dA,
                                                                 const float* __restrict__ lse,
                                                                 const float* __restrict__ D, int BH, int n, int causal,
                                                                 int lb, float scale, ST* __restrict__ dQKV,
                                                                 const int32_t* __restrict__ rI,
                                                                 const float2* __restrict__ rtab) {
     using TL = BwdTile<ST, DH>;
-    constexpr int TB = TL::TB, RS = TL::RS, LDR = TL::LDR, VPR = TL::VPR, PER = TL::PER;
+    // OB keys owned by the workgroup (16 per wave), query tiles of TB rows
+    constexpr int TB = TL::TB, RS = TL::RS, LDR = TL::LDR, VPR = TL::VPR, NT = 64 * NWV, OB = 16 * NWV;
+    constexpr int PER = TB * VPR / NT, SR = OB > TB ? OB : TB;
+    static_assert(PER >= 1 && TB * VPR % NT == 0, "tile shape");
     static_assert(sizeof(ST) == 2, "bf16: transposed operands by ds_read_b64_tr_b16");
-    __shared__ __attribute__((aligned(16))) ST Qs[TB * LDR];
-    __shared__ __attribute__((aligned(16))) ST dAs[TB * LDR];
+    __shared__ __attribute__((aligned(16))) ST Qs[SR * LDR];   // query tile, then the dK rows
+    __shared__ __attribute__((aligned(16))) ST dAs[SR * LDR];  // dA tile, then the dV rows
     __shared__ float ls[TB], Dsh[TB];
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int g = lane >> 4, c16 = lane & 15;
-    const int nkb = (n + TB - 1) / TB;
+    const int nkb = (n + OB - 1) / OB, nqt = (n + TB - 1) / TB;
     const int bh = blockIdx.x / nkb, kb = blockIdx.x % nkb;  // causal: low kb has the most query tiles
-    const int k0 = kb * TB, wk0 = k0 + 16 * wave;
+    const int k0 = kb * OB, wk0 = k0 + 16 * wave;
     const size_t base = (size_t)bh * n;
     const ST* Qp = QKV + base * RS;
     const ST* Kp = Qp + DH;
@@ -239,7 +240,7 @@ __global__ __launch_bounds__(256) void attn_bwd_kv_tiled_kernel(const ST* __rest
 
     // causal: query tiles from the block's own; with a window only those
     // within lb of its last key
-    const int it0 = causal ? kb : 0, it_end = WIN && causal ? min(nkb, (k0 + TB - 1 + lb) / TB + 1) : nkb;
+    const int it0 = causal ? k0 / TB : 0, it_end = WIN && causal ? min(nqt, (k0 + OB - 1 + lb) / TB + 1) : nqt;
     const float c2 = scale * 1.44269504088896341f;  // P = 2^(s c2 - lse log2 e)
     Vec8<ST> qreg[PER], areg[PER];
     float lreg = 0.f, dreg = 0.f;
@@ -247,7 +248,7 @@ __global__ __launch_bounds__(256) void attn_bwd_kv_tiled_kernel(const ST* __rest
     auto load_tile = [&](int i0) {
 #pragma unroll
         for (int p = 0; p < PER; ++p) {
-            const int v = tid + 256 * p, r = v / VPR, dc = (v % VPR) * 8;
+            const int v = tid + NT * p, r = v / VPR, dc = (v % VPR) * 8;
             const size_t row = (size_t)min(i0 + r, n - 1);
             qreg[p] = vec8_load<ST>(Qp + row * RS + dc);
             areg[p] = vec8_load<ST>(dAp + row * DH + dc);
@@ -259,7 +260,7 @@ __global__ __launch_bounds__(256) void attn_bwd_kv_tiled_kernel(const ST* __rest
     auto store_tile = [&]() {
 #pragma unroll
         for (int p = 0; p < PER; ++p) {
-            const int v = tid + 256 * p, r = v / VPR, dc = (v % VPR) * 8;
+            const int v = tid + NT * p, r = v / VPR, dc = (v % VPR) * 8;
             vec8_store<ST>(Qs + r * LDR + dc, qreg[p]);
             vec8_store<ST>(dAs + r * LDR + dc, areg[p]);
         }
@@ -368,25 +369,28 @@ __global__ __launch_bounds__(256) void attn_bwd_kv_tiled_kernel(const ST* __rest
     }
 }
 
-template <typename ST, int DH, bool WIN>
-__global__ __launch_bounds__(256) void attn_bwd_q_tiled_kernel(const ST* __restrict__ QKV, const ST* __restrict__ dA,
+template <typename ST, int DH, bool WIN, int NWV>
+__global__ __launch_bounds__(64 * NWV) void attn_bwd_q_tiled_kernel(const ST* __restrict__ QKV, const ST* __restrict__ dA,
                                                                const float* __restrict__ lse,
                                                                const float* __restrict__ D, int BH, int n, int causal,
                                                                int lb, float scale, ST* __restrict__ dQKV,
                                                                const int32_t* __restrict__ rI,
                                                                const float2* __restrict__ rtab) {
     using TL = BwdTile<ST, DH>;
-    constexpr int TB = TL::TB, RS = TL::RS, LDR = TL::LDR, VPR = TL::VPR, PER = TL::PER;
+    // OB queries owned by the workgroup (16 per wave), key tiles of TB rows
+    constexpr int TB = TL::TB, RS = TL::RS, LDR = TL::LDR, VPR = TL::VPR, NT = 64 * NWV, OB = 16 * NWV;
+    constexpr int PER = TB * VPR / NT, SR = OB > TB ? OB : TB;
+    static_assert(PER >= 1 && TB * VPR % NT == 0, "tile shape");
     static_assert(sizeof(ST) == 2, "bf16: transposed operands by ds_read_b64_tr_b16");
-    __shared__ __attribute__((aligned(16))) ST Ks[TB * LDR];
+    __shared__ __attribute__((aligned(16))) ST Ks[SR * LDR];  // key tile, then the dQ rows
     __shared__ __attribute__((aligned(16))) ST Vs[TB * LDR];
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int g = lane >> 4, c16 = lane & 15;
-    const int nqb = (n + TB - 1) / TB;
+    const int nqb = (n + OB - 1) / OB;
     const int bh = blockIdx.x / nqb;
     const int qb = causal ? nqb - 1 - blockIdx.x % nqb : blockIdx.x % nqb;
-    const int q0 = qb * TB, wq0 = q0 + 16 * wave;
+    const int q0 = qb * OB, wq0 = q0 + 16 * wave;
     const size_t base = (size_t)bh * n;
     const ST* Qp = QKV + base * RS;
     const ST* Kp = Qp + DH;
@@ -407,13 +411,13 @@ __global__ __launch_bounds__(256) void attn_bwd_q_tiled_kernel(const ST* __restr
 #pragma unroll
     for (int db = 0; db < DH / 16; ++db) dQt[db] = zero4();
 
-    const int kv_end = causal ? min(n, q0 + TB) : n;
+    const int kv_end = causal ? min(n, q0 + OB) : n;
     const int ntiles = (kv_end + TB - 1) / TB, t0 = WIN && causal ? max(0, q0 - lb) / TB : 0;
     Vec8<ST> kreg[PER], vreg[PER];
     auto load_tile = [&](int j0) {
 #pragma unroll
         for (int p = 0; p < PER; ++p) {
-            const int v = tid + 256 * p, r = v / VPR, dc = (v % VPR) * 8;
+            const int v = tid + NT * p, r = v / VPR, dc = (v % VPR) * 8;
             const size_t row = (size_t)min(j0 + r, n - 1);
             kreg[p] = vec8_load<ST>(Kp + row * RS + dc);
             vreg[p] = vec8_load<ST>(Vp + row * RS + dc);
@@ -422,7 +426,7 @@ __global__ __launch_bounds__(256) void attn_bwd_q_tiled_kernel(const ST* __restr
     auto store_tile = [&]() {
 #pragma unroll
         for (int p = 0; p < PER; ++p) {
-            const int v = tid + 256 * p, r = v / VPR, dc = (v % VPR) * 8;
+            const int v = tid + NT * p, r = v / VPR, dc = (v % VPR) * 8;
             vec8_store<ST>(Ks + r * LDR + dc, kreg[p]);
             vec8_store<ST>(Vs + r * LDR + dc, vreg[p]);
         }
@@ -756,10 +760,12 @@ int launch_t(const ST* QKV, const ST* dA, const float* lse, const float* D, int 
         return hipGetLastError() == hipSuccess ? 0 : -1;
       }
       if (n > 32 || window > 0) {
-        const dim3 grid(BH * ((n + 63) / 64)), block(256);
-#define MOSA_ATTN_BWD_T(KERN, DHV)                                                                   \
-    do {                                                                                              \
-        auto kern = window > 0 ? KERN<ST, DHV, true> : KERN<ST, DHV, false>;                          \
+        // 64-wide heads: 128 owned rows on 8 waves per workgroup; 32-wide: 64 on 4
+#define MOSA_ATTN_BWD_T(KERN, DHV)                                                                     \
+    do {                                                                                                \
+        constexpr int NWV = DHV == 64 ? 8 : 4;                                                          \
+        auto kern = window > 0 ? KERN<ST, DHV, true, NWV> : KERN<ST, DHV, false, NWV>;                  \
+        const dim3 grid(BH * ((n + 16 * NWV - 1) / (16 * NWV))), block(64 * NWV);                       \
         hipLaunchKernelGGL(kern, grid, block, 0, stream, QKV, dA, lse, D, BH, n, causal, lb, scale, dQKV, rI, rtab); \
     } while (0)
         if (pass == 0) {
