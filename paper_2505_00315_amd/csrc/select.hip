@@ -403,6 +403,9 @@ int launch_select_t(const float* z, const float* xnorm, const ST* X, const ST* W
                        k, first, I, r, slot, unc_tok, unc_key, unc_sel)
     if (T <= 256) MOSA_SELECT_ROWS(4, 1);
     else if (T <= 512) MOSA_SELECT_ROWS(4, 2);
+    // many rows: the chip is full with smaller workgroups, and 4 waves pass
+    // the per-row barriers faster than 8
+    else if (T <= 1024 && B * H >= 1024) MOSA_SELECT_ROWS(4, 4);
     else if (T <= 1024) MOSA_SELECT_ROWS(8, 2);
     else if (T <= 2048) MOSA_SELECT_ROWS(4, 8);
     else if (T <= 8192) MOSA_SELECT_ROWS(16, 8);

@@ -69,6 +69,8 @@ def test_tiny_f32_workload(orc):
     dict(batch=3, seq_len=96, k=16, heads=3, d_model=64),
     dict(seq_len=160, k=32, d_head=32, causal=False),
     dict(batch=1, seq_len=128, k=64, d_head=64, d_model=128),
+    # 1024 routed rows of T <= 1024: the selection's many-row launch shape
+    dict(batch=4, seq_len=700, heads=256, k=37, d_head=32, d_model=64),
 ])
 def test_small_shapes(orc, kw):
     check_forward(orc, wl.small(**kw))
