@@ -93,3 +93,13 @@ def test_workload_fwdbwd_full(orc):
 
 def test_workload_hybrid_full(orc):
     check_backward(orc, wl.WORKLOADS["hybrid_d1024"])
+
+
+def test_workload_default_full(orc):
+    """The benchmark's default workload (B=8, T=1024, d=512, 32 heads, k=128),
+    forward and backward at full size through the same entry points."""
+    check_backward(orc, wl.WORKLOADS["fwd_d512"])
+
+
+def test_workload_long_full(orc):
+    check_backward(orc, wl.WORKLOADS["long_t8192"])

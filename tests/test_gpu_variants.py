@@ -155,3 +155,10 @@ def test_local_window(orc, kw):
     check_forward(orc, w)
     # window 1: P = 1 on the diagonal, dS = P (dP - D) = 0, so dW^Q = dW^K = 0
     check_backward(orc, w, zero=("dWq_d", "dWk_d") if w.window == 1 else ())
+
+
+def test_workload_long_local_full(orc):
+    """60 MoSA heads (k = 64) beside 4 local heads (window 512) at T = 8192,
+    forward at full size."""
+    w = wl.WORKLOADS["long_local_t8192"]
+    check_forward(orc, w, wl.make_inputs(w, with_grad=False))
