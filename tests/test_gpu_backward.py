@@ -103,3 +103,10 @@ def test_workload_default_full(orc):
 
 def test_workload_long_full(orc):
     check_backward(orc, wl.WORKLOADS["long_t8192"])
+
+
+@pytest.mark.parametrize("name", ["pm_tiny_mosa", "pm_large_mosa", "pm_tiny_dense"])
+def test_workload_perplexity_matched_full(orc, name):
+    """The attention layers of the perplexity-matched pairs (4 dense + MoSA
+    heads, and the dense baseline), forward and backward at full size."""
+    check_backward(orc, wl.WORKLOADS[name])
