@@ -183,3 +183,11 @@ def test_workload_hybrid_sampled(orc):
 def test_workload_long(orc):
     w = wl.WORKLOADS["long_t8192"]
     check_forward(orc, w, wl.make_inputs(w))
+
+
+@pytest.mark.parametrize("name", ["iso_tiny_rho2", "iso_tiny_rho64"])
+def test_workload_isoflop_sampled(orc, name):
+    """The FLOP-matched Tiny hybrids at the two ends of the sparsity range
+    (13 MoSA heads with k = 512; 505 heads with k = 16), batch element 0."""
+    w = wl.WORKLOADS[name]
+    check_forward(orc, w, wl.make_inputs(w, with_grad=False), batches=[0])
