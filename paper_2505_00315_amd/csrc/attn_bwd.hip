@@ -199,12 +199,11 @@ struct BwdTile {
 };
 
 template <typename ST, int DH, bool WIN, int NWV>
-__global__ __launch_bounds__(64 * NWV) void attn_bwd_kv_tiled_kernel(const ST* __restrict__ QKV, const ST* __restrict__ dA,
-                                                                const float* __restrict__ lse,
-                                                                const float* __restrict__ D, int BH, int n, int causal,
-                                                                int lb, float scale, ST* __restrict__ dQKV,
-                                                                const int32_t* __restrict__ rI,
-                                                                const float2* __restrict__ rtab) {
+__device__ __forceinline__ void attn_bwd_kv_tiled_body(int blk, const ST* __restrict__ QKV, const ST* __restrict__ dA,
+                                                       const float* __restrict__ lse, const float* __restrict__ D,
+                                                       int BH, int n, int causal, int lb, float scale,
+                                                       ST* __restrict__ dQKV, const int32_t* __restrict__ rI,
+                                                       const float2* __restrict__ rtab) {
     using TL = BwdTile<ST, DH>;
     // OB keys owned by the workgroup (16 per wave), query tiles of TB rows
     constexpr int TB = TL::TB, RS = TL::RS, LDR = TL::LDR, VPR = TL::VPR, NT = 64 * NWV, OB = 16 * NWV;
@@ -218,7 +217,10 @@ __global__ __launch_bounds__(64 * NWV) void attn_bwd_kv_tiled_kernel(const ST* _
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int g = lane >> 4, c16 = lane & 15;
     const int nkb = (n + OB - 1) / OB, nqt = (n + TB - 1) / TB;
-    const int bh = blockIdx.x / nkb, kb = blockIdx.x % nkb;  // causal: low kb has the most query tiles
+    // block order: the owned key blocks with the most query tiles (causal: low
+    // kb) first, over all (b, h)
+    const int bh = blk % BH, kb = blk / BH;
+    (void)nkb;
     const int k0 = kb * OB, wk0 = k0 + 16 * wave;
     const size_t base = (size_t)bh * n;
     const ST* Qp = QKV + base * RS;
@@ -370,12 +372,11 @@ __global__ __launch_bounds__(64 * NWV) void attn_bwd_kv_tiled_kernel(const ST* _
 }
 
 template <typename ST, int DH, bool WIN, int NWV>
-__global__ __launch_bounds__(64 * NWV) void attn_bwd_q_tiled_kernel(const ST* __restrict__ QKV, const ST* __restrict__ dA,
-                                                               const float* __restrict__ lse,
-                                                               const float* __restrict__ D, int BH, int n, int causal,
-                                                               int lb, float scale, ST* __restrict__ dQKV,
-                                                               const int32_t* __restrict__ rI,
-                                                               const float2* __restrict__ rtab) {
+__device__ __forceinline__ void attn_bwd_q_tiled_body(int blk, const ST* __restrict__ QKV, const ST* __restrict__ dA,
+                                                      const float* __restrict__ lse, const float* __restrict__ D,
+                                                      int BH, int n, int causal, int lb, float scale,
+                                                      ST* __restrict__ dQKV, const int32_t* __restrict__ rI,
+                                                      const float2* __restrict__ rtab) {
     using TL = BwdTile<ST, DH>;
     // OB queries owned by the workgroup (16 per wave), key tiles of TB rows
     constexpr int TB = TL::TB, RS = TL::RS, LDR = TL::LDR, VPR = TL::VPR, NT = 64 * NWV, OB = 16 * NWV;
@@ -388,8 +389,10 @@ __global__ __launch_bounds__(64 * NWV) void attn_bwd_q_tiled_kernel(const ST* __
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int g = lane >> 4, c16 = lane & 15;
     const int nqb = (n + OB - 1) / OB;
-    const int bh = blockIdx.x / nqb;
-    const int qb = causal ? nqb - 1 - blockIdx.x % nqb : blockIdx.x % nqb;
+    // block order: the owned query blocks with the most key tiles (causal:
+    // high qb) first, over all (b, h)
+    const int bh = blk % BH;
+    const int qb = causal ? nqb - 1 - blk / BH : blk / BH;
     const int q0 = qb * OB, wq0 = q0 + 16 * wave;
     const size_t base = (size_t)bh * n;
     const ST* Qp = QKV + base * RS;
@@ -511,6 +514,31 @@ __global__ __launch_bounds__(64 * NWV) void attn_bwd_q_tiled_kernel(const ST* __
         }
     }
 }
+
+#define MOSA_BWD_TILED_PARAMS                                                                                    \
+    const ST *__restrict__ QKV, const ST *__restrict__ dA, const float *__restrict__ lse,                          \
+        const float *__restrict__ D, int BH, int n, int causal, int lb, float scale, ST *__restrict__ dQKV,       \
+        const int32_t *__restrict__ rI, const float2 *__restrict__ rtab
+#define MOSA_BWD_TILED_ARGS QKV, dA, lse, D, BH, n, causal, lb, scale, dQKV, rI, rtab
+
+template <typename ST, int DH, bool WIN, int NWV>
+__global__ __launch_bounds__(64 * NWV) void attn_bwd_kv_tiled_kernel(MOSA_BWD_TILED_PARAMS) {
+    attn_bwd_kv_tiled_body<ST, DH, WIN, NWV>(blockIdx.x, MOSA_BWD_TILED_ARGS);
+}
+template <typename ST, int DH, bool WIN, int NWV>
+__global__ __launch_bounds__(64 * NWV) void attn_bwd_q_tiled_kernel(MOSA_BWD_TILED_PARAMS) {
+    attn_bwd_q_tiled_body<ST, DH, WIN, NWV>(blockIdx.x, MOSA_BWD_TILED_ARGS);
+}
+// Both passes in one launch (they are independent): even blocks take the dK,
+// dV pass, odd blocks the dQ pass, each in its longest-first order, so the
+// short blocks of one pass fill the CUs beside the long blocks of the other.
+template <typename ST, int DH, bool WIN, int NWV>
+__global__ __launch_bounds__(64 * NWV) void attn_bwd_tiled_both_kernel(MOSA_BWD_TILED_PARAMS) {
+    if (blockIdx.x & 1) attn_bwd_q_tiled_body<ST, DH, WIN, NWV>(blockIdx.x >> 1, MOSA_BWD_TILED_ARGS);
+    else attn_bwd_kv_tiled_body<ST, DH, WIN, NWV>(blockIdx.x >> 1, MOSA_BWD_TILED_ARGS);
+}
+#undef MOSA_BWD_TILED_PARAMS
+#undef MOSA_BWD_TILED_ARGS
 
 // bf16, n <= 128: both passes in one workgroup of 8 waves per (b, h).  Q, K,
 // V and dA of all n rows go into LDS once (direct global->LDS loads, rows
@@ -744,8 +772,8 @@ int launch_t(const ST* QKV, const ST* dA, const float* lse, const float* D, int 
     const int lb = window > 0 ? window - 1 : n;  // keys a query may look back
     if constexpr (sizeof(ST) == 2) {
       if (n > 32 && n <= kAttnBwdLdsMaxN && window == 0) {
-        // both passes in one launch: the second call has nothing left to do
-        if (pass != 0) return 0;
+        // both passes in one launch: the call for the dQ pass has nothing left to do
+        if (pass == 1) return 0;
         auto kern = dh == 64 ? attn_bwd_lds_kernel<64> : attn_bwd_lds_kernel<32>;
         const size_t lds = dh == 64 ? AttnBwdLds<64>::lds : AttnBwdLds<32>::lds;
         static bool attr[2] = {false, false};
@@ -765,10 +793,13 @@ int launch_t(const ST* QKV, const ST* dA, const float* lse, const float* D, int 
     do {                                                                                                \
         constexpr int NWV = DHV == 64 ? 8 : 4;                                                          \
         auto kern = window > 0 ? KERN<ST, DHV, true, NWV> : KERN<ST, DHV, false, NWV>;                  \
-        const dim3 grid(BH * ((n + 16 * NWV - 1) / (16 * NWV))), block(64 * NWV);                       \
+        const dim3 grid((pass == 2 ? 2 : 1) * BH * ((n + 16 * NWV - 1) / (16 * NWV))), block(64 * NWV); \
         hipLaunchKernelGGL(kern, grid, block, 0, stream, QKV, dA, lse, D, BH, n, causal, lb, scale, dQKV, rI, rtab); \
     } while (0)
-        if (pass == 0) {
+        if (pass == 2) {
+            if (dh == 64) MOSA_ATTN_BWD_T(attn_bwd_tiled_both_kernel, 64);
+            else MOSA_ATTN_BWD_T(attn_bwd_tiled_both_kernel, 32);
+        } else if (pass == 0) {
             if (dh == 64) MOSA_ATTN_BWD_T(attn_bwd_kv_tiled_kernel, 64);
             else MOSA_ATTN_BWD_T(attn_bwd_kv_tiled_kernel, 32);
         } else {
@@ -779,6 +810,9 @@ int launch_t(const ST* QKV, const ST* dA, const float* lse, const float* D, int 
         return hipGetLastError() == hipSuccess ? 0 : -1;
       }
     }
+    if (pass == 2)
+        return launch_t<ST>(QKV, dA, lse, D, BH, n, dh, causal, window, dQKV, rI, rtab, 0, stream) |
+               launch_t<ST>(QKV, dA, lse, D, BH, n, dh, causal, window, dQKV, rI, rtab, 1, stream);
     const int tasks = BH * ((n + 15) / 16);
     dim3 grid((tasks + 3) / 4), block(256);
 #define MOSA_ATTN_BWD(KERN, DHV)                                                                     \

@@ -331,10 +331,15 @@ int mosa_backward_timed(const mosa_shape* s, const void* X, const mosa_weights* 
         e |= sm.mark("bwd_out");
         // with the rotary encoding, dQ and dK leave these kernels turned back
         // through the rotation (the gradients of the unrotated q and k)
-        e |= launch_attn_bwd(dt, QKV, dA, lse, D, B * H, k, dh, causal, 0, dQKV, I, rope, 0, stream);
-        e |= sm.mark("attn_bwd_kv");
-        e |= launch_attn_bwd(dt, QKV, dA, lse, D, B * H, k, dh, causal, 0, dQKV, I, rope, 1, stream);
-        e |= sm.mark("attn_bwd_q");
+        // untimed: the two passes in one launch where that applies
+        if (ev) {
+            e |= launch_attn_bwd(dt, QKV, dA, lse, D, B * H, k, dh, causal, 0, dQKV, I, rope, 0, stream);
+            e |= sm.mark("attn_bwd_kv");
+            e |= launch_attn_bwd(dt, QKV, dA, lse, D, B * H, k, dh, causal, 0, dQKV, I, rope, 1, stream);
+            e |= sm.mark("attn_bwd_q");
+        } else {
+            e |= launch_attn_bwd(dt, QKV, dA, lse, D, B * H, k, dh, causal, 0, dQKV, I, rope, 2, stream);
+        }
         // untimed: the weight gradients and the dX rows in one grouped launch
         const int grouped = ev ? 1
                                : launch_bwd_proj(dt, X, dY, I, A, dQKV, dz16, dz, w->Wq, w->Wk, w->Wv, Wr, B, T, d,
@@ -352,12 +357,17 @@ int mosa_backward_timed(const mosa_shape* s, const void* X, const mosa_weights* 
         e |= launch_dattn_out(dt, dY, nullptr, nullptr, w->Wo_d, Ad, B, T, d, Hd, dh, T, dAd, Dd, nullptr, nullptr,
                               stream);
         e |= sm.mark("bwd_out_dense");
-        e |= launch_attn_bwd(dt, QKVd, dAd, lsed, Dd, B * Hd, T, dh, causal, s->window, dQKVd, nullptr, rope, 0,
-                             stream);
-        e |= sm.mark("attn_bwd_kv_dense");
-        e |= launch_attn_bwd(dt, QKVd, dAd, lsed, Dd, B * Hd, T, dh, causal, s->window, dQKVd, nullptr, rope, 1,
-                             stream);
-        e |= sm.mark("attn_bwd_q_dense");
+        if (ev) {
+            e |= launch_attn_bwd(dt, QKVd, dAd, lsed, Dd, B * Hd, T, dh, causal, s->window, dQKVd, nullptr, rope, 0,
+                                 stream);
+            e |= sm.mark("attn_bwd_kv_dense");
+            e |= launch_attn_bwd(dt, QKVd, dAd, lsed, Dd, B * Hd, T, dh, causal, s->window, dQKVd, nullptr, rope, 1,
+                                 stream);
+            e |= sm.mark("attn_bwd_q_dense");
+        } else {
+            e |= launch_attn_bwd(dt, QKVd, dAd, lsed, Dd, B * Hd, T, dh, causal, s->window, dQKVd, nullptr, rope, 2,
+                                 stream);
+        }
         e |= launch_wgrad(dt, X, dY, nullptr, Ad, dQKVd, nullptr, B, T, d, Hd, dh, T, g->dWq_d, g->dWk_d,
                           g->dWv_d, nullptr, g->dWo_d, wpart, 0, stream);
         e |= sm.mark("wgrad_qkv_dense");

@@ -68,7 +68,8 @@ int launch_dattn_out(int dtype, const void* dY, const int32_t* I, const float* r
                      const void* A, int B, int T, int d, int H, int dh, int n, void* dA, float* D, float* dz,
                      void* dz16, hipStream_t stream);
 
-// Attention backward into packed dQKV rows; pass 0 writes dK, dV, pass 1 writes dQ.
+// Attention backward into packed dQKV rows; pass 0 writes dK, dV, pass 1 writes dQ,
+// pass 2 both (one launch where the kernels allow it).
 int launch_attn_bwd(int dtype, const void* QKV, const void* dA, const float* lse, const float* D, int BH,
                     int n, int dh, int causal, int window, void* dQKV, const int32_t* rope_I,
                     const float2* rope, int pass, hipStream_t stream);
