@@ -174,7 +174,7 @@ STAGE_KERNELS = {
     "attn": (r"attn_fwd",),
     "out_scatter": (r"OutProj\w*Policy", r"OutCombinePolicy", r"OutDensePolicy", r"combine_rows_kernel<[^>]*, 0>"),
     "bwd_out": (r"BwdOutPolicy",),
-    "attn_bwd": (r"attn_bwd_kv", r"attn_bwd_q", r"attn_bwd_lds"),
+    "attn_bwd": (r"attn_bwd_kv", r"attn_bwd_q", r"attn_bwd_lds", r"attn_bwd_tiled_both"),
     "wgrad": (r"WgradQkvPolicy<[^>]*, true, true>", r"WgradQkvPolicy2", r"WgradOPolicy<[^>]*, true>",
               r"WgradOPolicy2", r"wgrad_qkv_reduce", r"wgrad_o_reduce"),
     "dx_scatter": (r"DxProj\w*Policy", r"DxCombinePolicy", r"DxDensePolicy", r"combine_rows_kernel<[^>]*, 1>"),
