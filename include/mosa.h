@@ -13,9 +13,12 @@
  *
  * Conventions shared by every entry point
  *   - All tensor pointers are DEVICE pointers, row-major, owned by the
- *     caller.  The library allocates no memory and keeps no global state;
- *     temporary memory comes in through `scratch`, state kept from the
- *     forward for the backward through `saved`.
+ *     caller.  The library allocates no memory and keeps no state between
+ *     calls (kernels that need more than 64 KB of LDS have that limit set
+ *     on the current device before each launch); temporary memory comes in
+ *     through `scratch`, state kept from the forward for the backward
+ *     through `saved`.  Calls from several host threads, on one device or
+ *     several, do not interfere as long as they use different buffers.
  *   - `stream` is a hipStream_t (NULL: the default stream).  Calls only
  *     enqueue work; errors raised while kernels execute surface at the next
  *     synchronisation of that stream.
@@ -144,9 +147,15 @@ typedef struct mosa_grads {
  *   lse [B,H,k] fp32 (natural-log sum of exp of the scaled scores);
  *   the same for the dense heads with k = T: QKVd [B,Hd,T,3,dh], Ad [B,Hd,T,dh],
  *   lsed [B,Hd,T];
- *   rope [T, dh/4] float2 (cos, sin) table of the rotary encoding (rope == 1). */
+ *   rope [T, dh/4] float2 (cos, sin) table of the rotary encoding (rope == 1);
+ *   status [B,H] int32: 0 when the selection of row (b, h) holds exactly k
+ *     certified tokens; 1 when it does not, which happens only if the
+ *     router's logit error bound (an assumption about the MFMA adder, see
+ *     mosa_forward) failed: I and r of that row are then padded with token 0
+ *     and r = 0 or cut at k, and the outputs of the call must not be used.
+ *     Callers that need the guarantee read this array after the forward. */
 typedef struct mosa_saved_layout {
-    size_t I, r, slot, QKV, A, lse, QKVd, Ad, lsed, rope;
+    size_t I, r, slot, QKV, A, lse, QKVd, Ad, lsed, rope, status;
     size_t total;
 } mosa_saved_layout;
 
@@ -167,7 +176,12 @@ int mosa_saved_offsets(const mosa_shape* s, mosa_saved_layout* out);
  *   saved / scratch: caller buffers of at least the mosa_workspace_size
  *   sizes; `saved` must stay unmodified until the matching mosa_backward.
  *   When H > 0, the first B*H*T*4 bytes of `scratch` hold the fp32 router
- *   logits z [B,H,T] after the call (until scratch is reused). */
+ *   logits z [B,H,T] after the call (until scratch is reused).
+ *   The selection is certified against the exact keys with an error bound
+ *   on the fp32 router logits that assumes each 32-term MFMA chunk sum lies
+ *   within (K+1) units in the last place of its largest term of the exact
+ *   chunk sum (doubled for margin); the selection status in `saved` records
+ *   any row where that assumption failed. */
 int mosa_forward(const mosa_shape* s, const void* X, const mosa_weights* w, void* Y,
                  int accumulate, int32_t* I_out, float* r_out, void* saved, size_t saved_bytes,
                  void* scratch, size_t scratch_bytes, void* stream);
@@ -183,12 +197,13 @@ int mosa_backward(const mosa_shape* s, const void* X, const mosa_weights* w, con
 
 /* Stage timing for profiling and benchmarks.  The caller creates up to
  * MOSA_MAX_STAGES hipEvent_t handles and stores them in `events`; the timed
- * variants below do exactly the work of mosa_forward / mosa_backward and in
- * addition record events[0] on `stream` before the first kernel and
- * events[j] after stage j (one kernel per stage), setting names[j] to a
- * static stage name and `count` to the number of events recorded.  The time
- * of stage j is hipEventElapsedTime(events[j-1], events[j]).  A NULL
- * `ev` makes them identical to the untimed calls. */
+ * variants below launch exactly the kernels of mosa_forward / mosa_backward,
+ * in the same order with the same arguments, and in addition record
+ * events[0] on `stream` before the first kernel and events[j] after the j-th
+ * kernel launch, setting names[j] to that kernel's static stage name and
+ * `count` to the number of events recorded.  The time of stage j is
+ * hipEventElapsedTime(events[j-1], events[j]).  A NULL `ev` makes them
+ * identical to the untimed calls. */
 #define MOSA_MAX_STAGES 32
 typedef struct mosa_stage_events {
     void* events[MOSA_MAX_STAGES];

@@ -776,13 +776,7 @@ int launch_t(const ST* QKV, const ST* dA, const float* lse, const float* D, int 
         if (pass == 1) return 0;
         auto kern = dh == 64 ? attn_bwd_lds_kernel<64> : attn_bwd_lds_kernel<32>;
         const size_t lds = dh == 64 ? AttnBwdLds<64>::lds : AttnBwdLds<32>::lds;
-        static bool attr[2] = {false, false};
-        if (!attr[dh == 64]) {
-            if (hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds) !=
-                hipSuccess)
-                return -1;
-            attr[dh == 64] = true;
-        }
+        if (allow_lds((const void*)kern, lds)) return -1;
         hipLaunchKernelGGL(kern, dim3(BH), dim3(512), lds, stream, QKV, dA, lse, D, BH, n, causal, scale, dQKV, rI,
                            rtab);
         return hipGetLastError() == hipSuccess ? 0 : -1;
@@ -833,14 +827,34 @@ int launch_t(const ST* QKV, const ST* dA, const float* lse, const float* D, int 
 
 }  // namespace
 
+// One launch for both passes where a kernel does both (bf16: the LDS kernel
+// for 32 < n <= its limit, the tiled kernels otherwise), else the two passes.
+template <typename ST>
+bool both_in_one(int n, int window) {
+    if constexpr (sizeof(ST) == 2) return n > 32 || window > 0;
+    return false;
+}
+
 int launch_attn_bwd(int dtype, const void* QKV, const void* dA, const float* lse, const float* D, int BH, int n,
                     int dh, int causal, int window, void* dQKV, const int32_t* rope_I, const float2* rope,
-                    int pass, hipStream_t stream) {
-    if (dtype == kBF16)
-        return launch_t<uint16_t>((const uint16_t*)QKV, (const uint16_t*)dA, lse, D, BH, n, dh, causal, window,
-                                  (uint16_t*)dQKV, rope_I, rope, pass, stream);
-    return launch_t<float>((const float*)QKV, (const float*)dA, lse, D, BH, n, dh, causal, window, (float*)dQKV,
-                           rope_I, rope, pass, stream);
+                    int dense, const Marker& mk, hipStream_t stream) {
+    auto run = [&](auto tag, int pass) {
+        using ST = decltype(tag);
+        return launch_t<ST>((const ST*)QKV, (const ST*)dA, lse, D, BH, n, dh, causal, window, (ST*)dQKV, rope_I,
+                            rope, pass, stream);
+    };
+    auto go = [&](auto tag) {
+        using ST = decltype(tag);
+        if (both_in_one<ST>(n, window)) {
+            const int e = run(tag, 2);
+            return e | mk(dense ? "attn_bwd_dense" : "attn_bwd");
+        }
+        int e = run(tag, 0);
+        e |= mk(dense ? "attn_bwd_kv_dense" : "attn_bwd_kv");
+        e |= run(tag, 1);
+        return e | mk(dense ? "attn_bwd_q_dense" : "attn_bwd_q");
+    };
+    return dtype == kBF16 ? go(uint16_t{}) : go(float{});
 }
 
 }  // namespace mosa

@@ -173,6 +173,14 @@ __device__ __forceinline__ void mma4(f32x4& acc, const Frag4<float>& a, const Fr
 
 __device__ __forceinline__ f32x4 zero4() { return f32x4{0.f, 0.f, 0.f, 0.f}; }
 
+// Allows a kernel more than the default 64 KB of dynamic LDS on the current
+// device.  Called before every such launch (the attribute is cheap to set),
+// so the library keeps no record of which kernels were raised where.
+inline int allow_lds(const void* kern, size_t bytes) {
+    if (bytes <= 64 * 1024) return 0;
+    return hipFuncSetAttribute(kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)bytes) == hipSuccess ? 0 : -1;
+}
+
 // Explicit wait states between the last MFMA of a loop and the first VALU
 // read of its accumulators after the loop: the compiler's hazard insertion
 // has been seen to miss the path that leaves a loop (or skips a block) right

@@ -253,7 +253,7 @@ int run_proj(const ST* dQKV, const float* dz, const ST* Wq, const ST* Wk, const 
 
 template <typename ST, int DH>
 int run_combine(const ST* dQKVd, const ST* Wq, const ST* Wk, const ST* Wv, const int16_t* slot, const ST* dXs, int B,
-                int T, int d, int H, int k, int Hd, ST* dX, int accumulate, float* base, hipStream_t stream) {
+                int T, int d, int H, int k, int Hd, ST* dX, int accumulate, float* base, const Marker& mk, hipStream_t stream) {
     using P = DxCombinePolicy<ST, DH>;
     typename P::Args a{dQKVd, Wq, Wk, Wv, slot, dXs, dX, T, d, H, k, Hd, accumulate, (T + P::MT - 1) / P::MT,
                        (d + P::NT - 1) / P::NT};
@@ -277,11 +277,12 @@ int run_combine(const ST* dQKVd, const ST* Wq, const ST* Wk, const ST* Wv, const
                 ad.base = base;
                 e = launch_gemm<ST, PD>(ad, B * a.mtiles * a.ntiles, stream);
             }
-            if (e) return e;
+            if (e | mk("dx_dense")) return -1;
         }
-        return launch_combine_rows<ST, 1>(slot, dXs, Hd > 0 ? base : nullptr, dX, B, T, d, H, k, accumulate, stream);
+        return launch_combine_rows<ST, 1>(slot, dXs, Hd > 0 ? base : nullptr, dX, B, T, d, H, k, accumulate, stream) |
+               mk("dx_combine");
     }
-    return launch_gemm<ST, P>(a, B * a.mtiles * a.ntiles, stream);
+    return launch_gemm<ST, P>(a, B * a.mtiles * a.ntiles, stream) | mk("dx_combine");
 }
 
 }  // namespace
@@ -301,15 +302,15 @@ int launch_dx_proj(int dtype, const void* dQKV, const float* dz, const void* Wq,
 
 int launch_dx_combine(int dtype, const void* dQKVd, const void* Wq_d, const void* Wk_d, const void* Wv_d,
                       const int16_t* slot, const void* dXs, int B, int T, int d, int H, int dh, int k, int Hd,
-                      void* dX, int accumulate, float* base, hipStream_t stream) {
+                      void* dX, int accumulate, float* base, const Marker& mk, hipStream_t stream) {
     if (dtype == kBF16) {
         auto f = dh == 64 ? run_combine<uint16_t, 64> : run_combine<uint16_t, 32>;
         return f((const uint16_t*)dQKVd, (const uint16_t*)Wq_d, (const uint16_t*)Wk_d, (const uint16_t*)Wv_d, slot,
-                 (const uint16_t*)dXs, B, T, d, H, k, Hd, (uint16_t*)dX, accumulate, base, stream);
+                 (const uint16_t*)dXs, B, T, d, H, k, Hd, (uint16_t*)dX, accumulate, base, mk, stream);
     }
     auto f = dh == 64 ? run_combine<float, 64> : run_combine<float, 32>;
     return f((const float*)dQKVd, (const float*)Wq_d, (const float*)Wk_d, (const float*)Wv_d, slot,
-             (const float*)dXs, B, T, d, H, k, Hd, (float*)dX, accumulate, base, stream);
+             (const float*)dXs, B, T, d, H, k, Hd, (float*)dX, accumulate, base, mk, stream);
 }
 
 }  // namespace mosa

@@ -522,15 +522,7 @@ int launch_gemm2(const typename P::Args& args, int nblocks, hipStream_t stream, 
     const size_t lds = Gemm2Shape<P>::lds_bytes(ktab_rows);
     if (lds > 160 * 1024) return -1;
     auto kern = gemm2_kernel<P>;
-    if (lds > 64 * 1024) {
-        static size_t set = 0;
-        if (lds > set) {
-            if (hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds) !=
-                hipSuccess)
-                return -1;
-            set = lds;
-        }
-    }
+    if (allow_lds((const void*)kern, lds)) return -1;
     hipLaunchKernelGGL(kern, dim3(nblocks), dim3(256), lds, stream, args);
     return hipGetLastError() == hipSuccess ? 0 : -1;
 }
@@ -549,15 +541,7 @@ int launch_gemm2_dual(const typename P1::Args& a1, int n1, int rows1, const type
     for (int x = 0; x < 8; ++x)  // xcd_dual_id's assumption
         if (nb / 8 + (x < nb % 8 ? 1 : 0) < n1 / 8 + (x < n1 % 8 ? 1 : 0)) return -1;
     auto kern = gemm2_dual_kernel<P1, P2>;
-    if (lds > 64 * 1024) {
-        static size_t set = 0;
-        if (lds > set) {
-            if (hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds) !=
-                hipSuccess)
-                return -1;
-            set = lds;
-        }
-    }
+    if (allow_lds((const void*)kern, lds)) return -1;
     hipLaunchKernelGGL(kern, dim3(nb), dim3(256), lds, stream, a1, a2, n1);
     return hipGetLastError() == hipSuccess ? 0 : -1;
 }

@@ -85,15 +85,7 @@ int launch_group3(const typename J0::Args& a0, int n0, size_t lds0, const typena
     if (lds2 > lds) lds = lds2;
     if (lds > 160 * 1024) return 1;
     auto kern = group3_kernel<J0, J1, J2>;
-    if (lds > 64 * 1024) {
-        static size_t set = 0;
-        if (lds > set) {
-            if (hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds) !=
-                hipSuccess)
-                return -1;
-            set = lds;
-        }
-    }
+    if (allow_lds((const void*)kern, lds)) return -1;
     hipLaunchKernelGGL(kern, dim3(nb), dim3(256), lds, stream, a0, a1, a2, n0, n1);
     return hipGetLastError() == hipSuccess ? 0 : -1;
 }

@@ -81,6 +81,7 @@ Layout make_layout(const mosa_shape* s) {
     L.saved.Ad = sv.take(B * Hd * T * dh * es);
     L.saved.lsed = sv.take(B * Hd * T * 4);
     L.saved.rope = sv.take(s->rope ? T * (dh / 4) * 8 : 0);  // (cos, sin) table
+    L.saved.status = sv.take(B * H * 4);                      // selection status per (b, h)
     L.saved.total = sv.total();
 
     // forward and backward scratch share the same buffer (used at different times)
@@ -142,7 +143,8 @@ const T* at(const void* base, size_t off) {
     return reinterpret_cast<const T*>(static_cast<const char*>(base) + off);
 }
 
-// Records a caller-created hipEvent_t after a stage (profiling variants only).
+// Records a caller-created hipEvent_t after every kernel launch (timed
+// variants only); a call without events records nothing.
 struct StageMarks {
     mosa_stage_events* ev;
     hipStream_t stream;
@@ -152,6 +154,8 @@ struct StageMarks {
         ev->names[ev->count] = name;
         return hipEventRecord(static_cast<hipEvent_t>(ev->events[ev->count++]), stream) != hipSuccess;
     }
+    static int hook(void* ctx, const char* name) { return static_cast<StageMarks*>(ctx)->mark(name); }
+    Marker marker() { return Marker{&StageMarks::hook, this}; }
 };
 
 }  // namespace
@@ -214,6 +218,7 @@ int mosa_forward_timed(const mosa_shape* s, const void* X, const mosa_weights* w
     void* QKVd = at<char>(saved, L.saved.QKVd);
     void* Ad = at<char>(saved, L.saved.Ad);
     float* lsed = at<float>(saved, L.saved.lsed);
+    int32_t* status = at<int32_t>(saved, L.saved.status);
     void* Xo = at<char>(scratch, L.Xo);
 
     float2* rope = s->rope ? at<float2>(saved, L.saved.rope) : nullptr;
@@ -229,9 +234,9 @@ int mosa_forward_timed(const mosa_shape* s, const void* X, const mosa_weights* w
             e |= sm.mark("router");
             e |= launch_select(dt, z, xnorm, X, w->Wr, B, T, d, H, k, s->first_token, I, r, slot,
                                at<int32_t>(scratch, L.unc_tok), at<double>(scratch, L.unc_key),
-                               at<int32_t>(scratch, L.unc_sel), stream);
+                               at<int32_t>(scratch, L.unc_sel), status, stream);
         } else {
-            e |= launch_fixed_select(B, T, H, k, s->fixed_stride, I, r, slot, stream);
+            e |= launch_fixed_select(B, T, H, k, s->fixed_stride, I, r, slot, status, stream);
         }
         e |= sm.mark("select");
         const int fused = launch_qkv_attn(dt, X, I, w->Wq, w->Wk, w->Wv, B, T, d, H, dh, k, QKV, rope, r, causal, A,
@@ -255,8 +260,7 @@ int mosa_forward_timed(const mosa_shape* s, const void* X, const mosa_weights* w
         e |= sm.mark("attn_dense");
     }
     e |= launch_out_combine(dt, Ad, w->Wo_d, slot, Xo, B, T, d, H, dh, k, Hd, Y, accumulate,
-                            at<float>(scratch, L.ybase), stream);
-    e |= sm.mark("out_combine");
+                            at<float>(scratch, L.ybase), sm.marker(), stream);
     if (H > 0 && I_out)
         e |= hipMemcpyAsync(I_out, I, (size_t)B * H * k * 4, hipMemcpyDeviceToDevice, stream) != hipSuccess;
     if (H > 0 && r_out)
@@ -326,29 +330,21 @@ int mosa_backward_timed(const mosa_shape* s, const void* X, const mosa_weights* 
     const void* Wr = w->Wr ? w->Wr : w->Wq;
     void* dWr = g->dWr ? g->dWr : at<char>(scratch, L.dwr);
 
+    const Marker mk = sm.marker();
     if (H > 0) {
         e |= launch_dattn_out(dt, dY, I, r, w->Wo, A, B, T, d, H, dh, k, dA, D, dz, dz16, stream);
         e |= sm.mark("bwd_out");
         // with the rotary encoding, dQ and dK leave these kernels turned back
         // through the rotation (the gradients of the unrotated q and k)
-        // untimed: the two passes in one launch where that applies
-        if (ev) {
-            e |= launch_attn_bwd(dt, QKV, dA, lse, D, B * H, k, dh, causal, 0, dQKV, I, rope, 0, stream);
-            e |= sm.mark("attn_bwd_kv");
-            e |= launch_attn_bwd(dt, QKV, dA, lse, D, B * H, k, dh, causal, 0, dQKV, I, rope, 1, stream);
-            e |= sm.mark("attn_bwd_q");
-        } else {
-            e |= launch_attn_bwd(dt, QKV, dA, lse, D, B * H, k, dh, causal, 0, dQKV, I, rope, 2, stream);
-        }
-        // untimed: the weight gradients and the dX rows in one grouped launch
-        const int grouped = ev ? 1
-                               : launch_bwd_proj(dt, X, dY, I, A, dQKV, dz16, dz, w->Wq, w->Wk, w->Wv, Wr, B, T, d,
-                                                 H, dh, k, g->dWq, g->dWk, g->dWv, dWr, g->dWo, dXs, stream);
+        e |= launch_attn_bwd(dt, QKV, dA, lse, D, B * H, k, dh, causal, 0, dQKV, I, rope, 0, mk, stream);
+        // the weight gradients and the dX rows in one grouped launch where it applies
+        const int grouped = launch_bwd_proj(dt, X, dY, I, A, dQKV, dz16, dz, w->Wq, w->Wk, w->Wv, Wr, B, T, d, H, dh,
+                                            k, g->dWq, g->dWk, g->dWv, dWr, g->dWo, dXs, stream);
         if (grouped < 0) e |= 1;
+        if (grouped == 0) e |= sm.mark("bwd_proj");
         if (grouped == 1) {
-            e |= launch_wgrad(dt, X, dY, I, A, dQKV, dz16, B, T, d, H, dh, k, g->dWq, g->dWk, g->dWv, dWr,
-                              g->dWo, wpart, 2, stream);
-            e |= sm.mark("wgrad");
+            e |= launch_wgrad(dt, X, dY, I, A, dQKV, dz16, B, T, d, H, dh, k, g->dWq, g->dWk, g->dWv, dWr, g->dWo,
+                              wpart, 2, mk, stream);
             e |= launch_dx_proj(dt, dQKV, dz, w->Wq, w->Wk, w->Wv, Wr, B, d, H, dh, k, dXs, stream);
             e |= sm.mark("dx_proj");
         }
@@ -357,27 +353,15 @@ int mosa_backward_timed(const mosa_shape* s, const void* X, const mosa_weights* 
         e |= launch_dattn_out(dt, dY, nullptr, nullptr, w->Wo_d, Ad, B, T, d, Hd, dh, T, dAd, Dd, nullptr, nullptr,
                               stream);
         e |= sm.mark("bwd_out_dense");
-        if (ev) {
-            e |= launch_attn_bwd(dt, QKVd, dAd, lsed, Dd, B * Hd, T, dh, causal, s->window, dQKVd, nullptr, rope, 0,
-                                 stream);
-            e |= sm.mark("attn_bwd_kv_dense");
-            e |= launch_attn_bwd(dt, QKVd, dAd, lsed, Dd, B * Hd, T, dh, causal, s->window, dQKVd, nullptr, rope, 1,
-                                 stream);
-            e |= sm.mark("attn_bwd_q_dense");
-        } else {
-            e |= launch_attn_bwd(dt, QKVd, dAd, lsed, Dd, B * Hd, T, dh, causal, s->window, dQKVd, nullptr, rope, 2,
-                                 stream);
-        }
+        e |= launch_attn_bwd(dt, QKVd, dAd, lsed, Dd, B * Hd, T, dh, causal, s->window, dQKVd, nullptr, rope, 1, mk,
+                             stream);
         e |= launch_wgrad(dt, X, dY, nullptr, Ad, dQKVd, nullptr, B, T, d, Hd, dh, T, g->dWq_d, g->dWk_d,
-                          g->dWv_d, nullptr, g->dWo_d, wpart, 0, stream);
-        e |= sm.mark("wgrad_qkv_dense");
+                          g->dWv_d, nullptr, g->dWo_d, wpart, 0, mk, stream);
         e |= launch_wgrad(dt, X, dY, nullptr, Ad, dQKVd, nullptr, B, T, d, Hd, dh, T, g->dWq_d, g->dWk_d,
-                          g->dWv_d, nullptr, g->dWo_d, wpart, 1, stream);
-        e |= sm.mark("wgrad_o_dense");
+                          g->dWv_d, nullptr, g->dWo_d, wpart, 1, mk, stream);
     }
     e |= launch_dx_combine(dt, dQKVd, w->Wq_d, w->Wk_d, w->Wv_d, slot, dXs, B, T, d, H, dh, k, Hd, dX, accumulate_dX,
-                           at<float>(scratch, L.dxbase), stream);
-    e |= sm.mark("dx_combine");
+                           at<float>(scratch, L.dxbase), mk, stream);
     return e ? MOSA_ERR_HIP : MOSA_OK;
 }
 

@@ -265,15 +265,7 @@ int launch_rowgemm(const typename P::Args& args, int nblocks, hipStream_t stream
     if (nblocks <= 0) return 0;
     constexpr size_t lds = RowGemmShape<P>::lds_bytes();
     auto kern = rowgemm_kernel<P>;
-    if (lds > 64 * 1024) {
-        static bool set = false;
-        if (!set) {
-            if (hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds) !=
-                hipSuccess)
-                return -1;
-            set = true;
-        }
-    }
+    if (allow_lds((const void*)kern, lds)) return -1;
     hipLaunchKernelGGL(kern, dim3(nblocks), dim3(256), lds, stream, args);
     return hipGetLastError() == hipSuccess ? 0 : -1;
 }

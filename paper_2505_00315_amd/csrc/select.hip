@@ -102,7 +102,7 @@ __global__ __launch_bounds__(64 * NW) void select_rows_kernel(
     const float* __restrict__ z, const float* __restrict__ xnorm, const ST* __restrict__ X,
     const ST* __restrict__ Wr, int T, int d, int H, int k, int first, int32_t* __restrict__ I, float* __restrict__ r,
     int16_t* __restrict__ slot, int32_t* __restrict__ unc_tok, double* __restrict__ unc_key,
-    int32_t* __restrict__ unc_sel) {
+    int32_t* __restrict__ unc_sel, int32_t* __restrict__ status) {
     constexpr int NT = 64 * NW;
     static_assert(NT >= 256, "one thread per histogram bin");
     __shared__ uint32_t s_hist[256];   // packed counts: A in bits 0..15, B in 16..31
@@ -385,8 +385,10 @@ __global__ __launch_bounds__(64 * NW) void select_rows_kernel(
         if (t < T) slot[rowT + t] = sl;
         pos0 += stripe;
     }
-    // Only reachable if the logit error bound were violated: keep every slot
-    // defined (token 0, r = 0) so that downstream kernels stay in bounds.
+    // Exactly k tokens unless the logit error bound was violated.  Then the
+    // row is flagged for the caller, and every slot is kept defined (token 0,
+    // r = 0) so that the kernels downstream stay in bounds.
+    if (tid == 0) status[row] = pos0 == k ? 0 : 1;
     for (int pos = pos0 + tid; pos < k; pos += NT) {
         I[(size_t)row * k + pos] = 0;
         r[(size_t)row * k + pos] = 0.f;
@@ -396,11 +398,11 @@ __global__ __launch_bounds__(64 * NW) void select_rows_kernel(
 template <typename ST>
 int launch_select_t(const float* z, const float* xnorm, const ST* X, const ST* Wr, int B, int T, int d, int H,
                     int k, int first, int32_t* I, float* r, int16_t* slot, int32_t* unc_tok, double* unc_key,
-                    int32_t* unc_sel, hipStream_t stream) {
+                    int32_t* unc_sel, int32_t* status, hipStream_t stream) {
     const dim3 grid(B * H);
 #define MOSA_SELECT_ROWS(NW, E)                                                                                \
     hipLaunchKernelGGL((select_rows_kernel<ST, NW, E>), grid, dim3(64 * NW), 0, stream, z, xnorm, X, Wr, T, d, H, \
-                       k, first, I, r, slot, unc_tok, unc_key, unc_sel)
+                       k, first, I, r, slot, unc_tok, unc_key, unc_sel, status)
     if (T <= 256) MOSA_SELECT_ROWS(4, 1);
     else if (T <= 512) MOSA_SELECT_ROWS(4, 2);
     // many rows: the chip is full with smaller workgroups, and 4 waves pass
@@ -418,8 +420,10 @@ int launch_select_t(const float* z, const float* xnorm, const ST* X, const ST* W
 // Fixed sparse attention (paper Section 3.1, as a special case of MoSA):
 // I = 0, stride, 2 stride, ..., r = 1; one workgroup per (b, h) row.
 __global__ __launch_bounds__(256) void fixed_select_kernel(int T, int k, int stride, int32_t* __restrict__ I,
-                                                           float* __restrict__ r, int16_t* __restrict__ slot) {
+                                                           float* __restrict__ r, int16_t* __restrict__ slot,
+                                                           int32_t* __restrict__ status) {
     const size_t row = blockIdx.x;
+    if (threadIdx.x == 0) status[row] = 0;
     for (int i = threadIdx.x; i < k; i += 256) {
         I[row * k + i] = i * stride;
         r[row * k + i] = 1.0f;
@@ -431,22 +435,21 @@ __global__ __launch_bounds__(256) void fixed_select_kernel(int T, int k, int str
 }  // namespace
 
 int launch_fixed_select(int B, int T, int H, int k, int stride, int32_t* I, float* r, int16_t* slot,
-                        hipStream_t stream) {
+                        int32_t* status, hipStream_t stream) {
     if (B * H == 0) return 0;
     if (stride < 1 || (long long)(k - 1) * stride > T - 1) return -1;
-    hipLaunchKernelGGL(fixed_select_kernel, dim3(B * H), dim3(256), 0, stream, T, k, stride, I, r, slot);
+    hipLaunchKernelGGL(fixed_select_kernel, dim3(B * H), dim3(256), 0, stream, T, k, stride, I, r, slot, status);
     return hipGetLastError() == hipSuccess ? 0 : -1;
 }
 
 int launch_select(int dtype, const float* z, const float* xnorm, const void* X, const void* Wr, int B, int T,
                   int d, int H, int k, int first_token, int32_t* I, float* r, int16_t* slot, int32_t* unc_tok,
-                  double* unc_key, int32_t* unc_sel, hipStream_t stream) {
+                  double* unc_key, int32_t* unc_sel, int32_t* status, hipStream_t stream) {
     if (dtype == kBF16)
         return launch_select_t<uint16_t>(z, xnorm, (const uint16_t*)X, (const uint16_t*)Wr, B, T, d, H, k,
-                                         first_token, I, r, slot, unc_tok, unc_key, unc_sel, stream);
+                                         first_token, I, r, slot, unc_tok, unc_key, unc_sel, status, stream);
     return launch_select_t<float>(z, xnorm, (const float*)X, (const float*)Wr, B, T, d, H, k, first_token, I, r,
-                                  slot, unc_tok,
-                                  unc_key, unc_sel, stream);
+                                  slot, unc_tok, unc_key, unc_sel, status, stream);
 }
 
 }  // namespace mosa

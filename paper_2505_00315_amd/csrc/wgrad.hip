@@ -441,16 +441,25 @@ int choose_splits(int base_tiles, int nchunks, int& cps) {
     return nchunks > 0 ? (nchunks + cps - 1) / cps : 1;
 }
 
+// Stage names of the weight-gradient kernels (MoSA heads / dense heads).
+inline const char* wname(bool dense, int which, bool reduce) {
+    static const char* const names[2][2][2] = {
+        {{"wgrad_qkv", "wgrad_qkv_reduce"}, {"wgrad_o", "wgrad_o_reduce"}},
+        {{"wgrad_qkv_dense", "wgrad_qkv_dense_reduce"}, {"wgrad_o_dense", "wgrad_o_dense_reduce"}}};
+    return names[dense][which][reduce];
+}
+
 template <typename ST, int DH, bool ROUTER, bool GATHER>
 int run_qkv_t(const ST* X, const int32_t* I, const ST* dQKV, const ST* dz16, int B, int T, int d, int H, int n,
-              ST* dWq, ST* dWk, ST* dWv, ST* dWr, float* part, hipStream_t stream) {
+              ST* dWq, ST* dWk, ST* dWv, ST* dWr, float* part, const Marker& mk, hipStream_t stream) {
     using P = WgradQkvPolicy<ST, DH, ROUTER, GATHER>;
+    const bool dense = !GATHER;
     const int mtiles = (d + P::MT - 1) / P::MT, R = B * n;
     if constexpr (sizeof(ST) == 2 && ROUTER && GATHER) {
         using P2 = WgradQkvPolicy2<DH>;
         if (const int rows = wgrad2_table_rows<P2>(R, d)) {
             typename P::Args a{X, I, dQKV, dz16, dWq, dWk, dWv, dWr, part, T, d, H, n, R, d / 64, 1, 0, make_fastdiv(n)};
-            return launch_gemm2<P2>(a, H * (d / 64), stream, rows);
+            return launch_gemm2<P2>(a, H * (d / 64), stream, rows) | mk(wname(dense, 0, false));
         }
     }
     if constexpr (sizeof(ST) == 2 && !ROUTER && !GATHER) {
@@ -461,11 +470,13 @@ int run_qkv_t(const ST* X, const int32_t* I, const ST* dQKV, const ST* dz16, int
             typename P2::Args a{X, I, dQKV, dz16, dWq, dWk, dWv, dWr, part, T, d, H, n, R, d / 64, S, rows,
                                 make_fastdiv(n)};
             int e = launch_gemm2<P2>(a, S * H * (d / 64), stream, rows);
+            e |= mk(wname(dense, 0, false));
             if (e == 0) {
                 const int total = H * d * (3 * DH / 8);
                 hipLaunchKernelGGL((wgrad_qkv_reduce_kernel<ST, DH, false>), dim3((total + 255) / 256), dim3(256), 0,
                                    stream, part, S, H, d, dWq, dWk, dWv, dWr);
                 e = hipGetLastError() == hipSuccess ? 0 : -1;
+                e |= mk(wname(dense, 0, true));
             }
             return e;
         }
@@ -474,33 +485,36 @@ int run_qkv_t(const ST* X, const int32_t* I, const ST* dQKV, const ST* dz16, int
     const int S = choose_splits(H * mtiles, (R + P::KC - 1) / P::KC, cps);
     typename P::Args a{X, I, dQKV, dz16, dWq, dWk, dWv, dWr, part, T, d, H, n, R, mtiles, S, cps, make_fastdiv(n)};
     int e = launch_gemm<ST, P>(a, S * H * mtiles, stream);
+    e |= mk(wname(dense, 0, false));
     if (S > 1 && e == 0) {
         const int total = H * d * (3 * DH / 8 + (ROUTER ? 1 : 0));
         hipLaunchKernelGGL((wgrad_qkv_reduce_kernel<ST, DH, ROUTER>), dim3((total + 255) / 256), dim3(256), 0, stream,
                            part, S, H, d, dWq, dWk, dWv, dWr);
         e = hipGetLastError() == hipSuccess ? 0 : -1;
+        e |= mk(wname(dense, 0, true));
     }
     return e;
 }
 
 template <typename ST, int DH>
 int run_qkv(const ST* X, const int32_t* I, const ST* dQKV, const ST* dz16, int B, int T, int d, int H, int n, ST* dWq,
-            ST* dWk, ST* dWv, ST* dWr, float* part, hipStream_t stream) {
+            ST* dWk, ST* dWv, ST* dWr, float* part, const Marker& mk, hipStream_t stream) {
     if (I)  // MoSA heads: gathered rows and the router column
-        return run_qkv_t<ST, DH, true, true>(X, I, dQKV, dz16, B, T, d, H, n, dWq, dWk, dWv, dWr, part, stream);
-    return run_qkv_t<ST, DH, false, false>(X, I, dQKV, dz16, B, T, d, H, n, dWq, dWk, dWv, dWr, part, stream);
+        return run_qkv_t<ST, DH, true, true>(X, I, dQKV, dz16, B, T, d, H, n, dWq, dWk, dWv, dWr, part, mk, stream);
+    return run_qkv_t<ST, DH, false, false>(X, I, dQKV, dz16, B, T, d, H, n, dWq, dWk, dWv, dWr, part, mk, stream);
 }
 
 template <typename ST, int DH, bool GATHER>
 int run_o_t(const ST* dY, const int32_t* I, const ST* A, int B, int T, int d, int H, int n, ST* dWo, float* part,
-            hipStream_t stream) {
+            const Marker& mk, hipStream_t stream) {
     using P = WgradOPolicy<ST, DH, GATHER>;
+    const bool dense = !GATHER;
     const int ntiles = (d + P::NT - 1) / P::NT, R = B * n;
     if constexpr (sizeof(ST) == 2 && GATHER) {
         using P2 = WgradOPolicy2<DH>;
         if (const int rows = wgrad2_table_rows<P2>(R, d)) {
             typename P::Args a{dY, I, A, dWo, part, T, d, H, n, R, d / 64, 1, 0, make_fastdiv(n)};
-            return launch_gemm2<P2>(a, H * (d / 64), stream, rows);
+            return launch_gemm2<P2>(a, H * (d / 64), stream, rows) | mk(wname(dense, 1, false));
         }
     }
     if constexpr (sizeof(ST) == 2 && !GATHER) {
@@ -510,11 +524,13 @@ int run_o_t(const ST* dY, const int32_t* I, const ST* A, int B, int T, int d, in
         if (S > 0 && d % 64 == 0) {
             typename P2::Args a{dY, I, A, dWo, part, T, d, H, n, R, d / 64, S, rows, make_fastdiv(n)};
             int e = launch_gemm2<P2>(a, S * H * (d / 64), stream, rows);
+            e |= mk(wname(dense, 1, false));
             if (e == 0) {
                 const size_t n8 = (size_t)H * DH * d / 8;
                 hipLaunchKernelGGL((wgrad_o_reduce_kernel<ST>), dim3((unsigned)((n8 + 255) / 256)), dim3(256), 0,
                                    stream, part, S, n8, dWo);
                 e = hipGetLastError() == hipSuccess ? 0 : -1;
+                e |= mk(wname(dense, 1, true));
             }
             return e;
         }
@@ -523,20 +539,22 @@ int run_o_t(const ST* dY, const int32_t* I, const ST* A, int B, int T, int d, in
     const int S = choose_splits(H * ntiles, (R + P::KC - 1) / P::KC, cps);
     typename P::Args a{dY, I, A, dWo, part, T, d, H, n, R, ntiles, S, cps, make_fastdiv(n)};
     int e = launch_gemm<ST, P>(a, S * H * ntiles, stream);
+    e |= mk(wname(dense, 1, false));
     if (S > 1 && e == 0) {
         const size_t n8 = (size_t)H * DH * d / 8;
         hipLaunchKernelGGL((wgrad_o_reduce_kernel<ST>), dim3((unsigned)((n8 + 255) / 256)), dim3(256), 0, stream, part,
                            S, n8, dWo);
         e = hipGetLastError() == hipSuccess ? 0 : -1;
+        e |= mk(wname(dense, 1, true));
     }
     return e;
 }
 
 template <typename ST, int DH>
 int run_o(const ST* dY, const int32_t* I, const ST* A, int B, int T, int d, int H, int n, ST* dWo, float* part,
-          hipStream_t stream) {
-    if (I) return run_o_t<ST, DH, true>(dY, I, A, B, T, d, H, n, dWo, part, stream);
-    return run_o_t<ST, DH, false>(dY, I, A, B, T, d, H, n, dWo, part, stream);
+          const Marker& mk, hipStream_t stream) {
+    if (I) return run_o_t<ST, DH, true>(dY, I, A, B, T, d, H, n, dWo, part, mk, stream);
+    return run_o_t<ST, DH, false>(dY, I, A, B, T, d, H, n, dWo, part, mk, stream);
 }
 
 // dW^{Q,K,V,r} and dW^O of the MoSA heads in one launch of the gathered-row
@@ -612,7 +630,7 @@ size_t partial_bytes(int B, int d, int H, int n, bool router) {
 
 int launch_wgrad(int dtype, const void* X, const void* dY, const int32_t* I, const void* A, const void* dQKV,
                  const void* dz16, int B, int T, int d, int H, int dh, int n, void* dWq, void* dWk, void* dWv,
-                 void* dWr, void* dWo, float* part, int which, hipStream_t stream) {
+                 void* dWr, void* dWo, float* part, int which, const Marker& mk, hipStream_t stream) {
     if (H == 0) return 0;
     if (which == 2) {
         // both: one launch on the gathered-row engine where it applies
@@ -621,31 +639,31 @@ int launch_wgrad(int dtype, const void* X, const void* dY, const int32_t* I, con
             auto both = dh == 64 ? run_both<64> : run_both<32>;
             const int e = both((const ST*)X, (const ST*)dY, I, (const ST*)A, (const ST*)dQKV, (const ST*)dz16, B, T, d,
                                H, n, (ST*)dWq, (ST*)dWk, (ST*)dWv, (ST*)dWr, (ST*)dWo, stream);
-            if (e != 1) return e;
+            if (e != 1) return e | mk("wgrad");
         }
         const int e0 = launch_wgrad(dtype, X, dY, I, A, dQKV, dz16, B, T, d, H, dh, n, dWq, dWk, dWv, dWr, dWo, part,
-                                    0, stream);
+                                    0, mk, stream);
         return e0 | launch_wgrad(dtype, X, dY, I, A, dQKV, dz16, B, T, d, H, dh, n, dWq, dWk, dWv, dWr, dWo, part, 1,
-                                 stream);
+                                 mk, stream);
     }
     if (dtype == kBF16) {
         using ST = uint16_t;
         if (which == 0) {
             auto f = dh == 64 ? run_qkv<ST, 64> : run_qkv<ST, 32>;
             return f((const ST*)X, I, (const ST*)dQKV, (const ST*)dz16, B, T, d, H, n, (ST*)dWq, (ST*)dWk, (ST*)dWv,
-                     (ST*)dWr, part, stream);
+                     (ST*)dWr, part, mk, stream);
         }
         auto f = dh == 64 ? run_o<ST, 64> : run_o<ST, 32>;
-        return f((const ST*)dY, I, (const ST*)A, B, T, d, H, n, (ST*)dWo, part, stream);
+        return f((const ST*)dY, I, (const ST*)A, B, T, d, H, n, (ST*)dWo, part, mk, stream);
     }
     using ST = float;
     if (which == 0) {
         auto f = dh == 64 ? run_qkv<ST, 64> : run_qkv<ST, 32>;
         return f((const ST*)X, I, (const ST*)dQKV, (const ST*)dz16, B, T, d, H, n, (ST*)dWq, (ST*)dWk, (ST*)dWv,
-                 (ST*)dWr, part, stream);
+                 (ST*)dWr, part, mk, stream);
     }
     auto f = dh == 64 ? run_o<ST, 64> : run_o<ST, 32>;
-    return f((const ST*)dY, I, (const ST*)A, B, T, d, H, n, (ST*)dWo, part, stream);
+    return f((const ST*)dY, I, (const ST*)A, B, T, d, H, n, (ST*)dWo, part, mk, stream);
 }
 
 int launch_bwd_proj(int dtype, const void* X, const void* dY, const int32_t* I, const void* A, const void* dQKV,

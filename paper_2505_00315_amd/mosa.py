@@ -26,7 +26,7 @@ MAX_STAGES = 32
 
 WEIGHT_NAMES = ("Wr", "Wq", "Wk", "Wv", "Wo", "Wq_d", "Wk_d", "Wv_d", "Wo_d")
 GRAD_NAMES = tuple("d" + n for n in WEIGHT_NAMES)
-SAVED_NAMES = ("I", "r", "slot", "QKV", "A", "lse", "QKVd", "Ad", "lsed", "rope")
+SAVED_NAMES = ("I", "r", "slot", "QKV", "A", "lse", "QKVd", "Ad", "lsed", "rope", "status")
 
 
 class Shape(ctypes.Structure):
@@ -151,15 +151,71 @@ def _weights(w):
     return Weights(*[_ptr(w.get(n)) for n in WEIGHT_NAMES])
 
 
+def _weight_numel(shape: Shape):
+    """Element counts of the parameters (Wr [H,d]; Wq/Wk/Wv [H,d,dh]; Wo [H,dh,d];
+    dense heads the same with Hd)."""
+    H, Hd, d, dh = shape.heads, shape.dense_heads, shape.d_model, shape.d_head
+    return {"Wr": H * d, "Wq": H * d * dh, "Wk": H * d * dh, "Wv": H * d * dh, "Wo": H * dh * d,
+            "Wq_d": Hd * d * dh, "Wk_d": Hd * d * dh, "Wv_d": Hd * d * dh, "Wo_d": Hd * dh * d}
+
+
+def _check_tensor(t, what, dtype, numel, device):
+    """A tensor handed to the library must have the storage type, element
+    count and device the shape implies and be contiguous: the kernels index
+    it by the shape alone, so anything else would read or write out of bounds."""
+    if t is None:
+        raise ValueError(f"{what}: missing")
+    if t.dtype != dtype:
+        raise TypeError(f"{what}: dtype {t.dtype}, expected {dtype}")
+    if not t.is_contiguous():
+        raise ValueError(f"{what}: not contiguous")
+    if t.numel() != numel:
+        raise ValueError(f"{what}: {t.numel()} elements, expected {numel}")
+    if t.device != device:
+        raise ValueError(f"{what}: on {t.device}, expected {device}")
+
+
+def _check_params(shape: Shape, params, names, device, optional=()):
+    st = torch_dtype(shape)
+    for n, numel in zip(names, _weight_numel(shape).values()):
+        t = params.get(n)
+        if numel == 0 or (t is None and n in optional):
+            continue
+        _check_tensor(t, n, st, numel, device)
+
+
+def _check_buffers(shape: Shape, saved, scratch, device):
+    need_saved, need_scratch = workspace_size(shape)
+    for t, what, need in ((saved, "saved", need_saved), (scratch, "scratch", need_scratch)):
+        if t is None or t.dtype != torch.uint8 or not t.is_contiguous() or t.device != device:
+            raise ValueError(f"{what}: a contiguous uint8 tensor on {device} is required")
+        if t.numel() < need:
+            raise ValueError(f"{what}: {t.numel()} bytes, at least {need} required")
+
+
 def forward(shape: Shape, X, w, Y=None, accumulate=False, saved=None, scratch=None, I_out=None, r_out=None,
             stream=None, events=None):
     """Run mosa_forward (mosa_forward_timed when ``events`` is a StageEvents).
     ``w`` maps weight names (see WEIGHT_NAMES) to device tensors.
     Returns (Y, saved, scratch)."""
+    st = torch_dtype(shape)
+    dev = X.device
+    act = shape.batch * shape.seq_len * shape.d_model
+    _check_tensor(X, "X", st, act, dev)
+    if dev.type != "cuda":
+        raise ValueError("X: the layer runs on the GPU only")
+    _check_params(shape, w, WEIGHT_NAMES, dev, optional=("Wr",) if shape.fixed_stride else ())
     if Y is None:
         Y = torch.empty_like(X)
+    _check_tensor(Y, "Y", st, act, dev)
     if saved is None or scratch is None:
-        saved, scratch = alloc_workspace(shape, X.device)
+        saved, scratch = alloc_workspace(shape, dev)
+    _check_buffers(shape, saved, scratch, dev)
+    sel = shape.batch * shape.heads * shape.k
+    if I_out is not None:
+        _check_tensor(I_out, "I_out", torch.int32, sel, dev)
+    if r_out is not None:
+        _check_tensor(r_out, "r_out", torch.float32, sel, dev)
     args = [ctypes.byref(shape), _ptr(X), ctypes.byref(_weights(w)), _ptr(Y), int(accumulate), _ptr(I_out),
             _ptr(r_out), _ptr(saved), saved.numel(), _ptr(scratch), scratch.numel(), _stream(stream)]
     if events is None:
@@ -174,10 +230,21 @@ def backward(shape: Shape, X, w, dY, saved, grads, dX=None, accumulate_dX=False,
     """Run mosa_backward (mosa_backward_timed when ``events`` is given).
     ``grads`` maps gradient names (see GRAD_NAMES) to device tensors that are
     written.  Returns dX."""
+    st = torch_dtype(shape)
+    dev = X.device
+    act = shape.batch * shape.seq_len * shape.d_model
+    _check_tensor(X, "X", st, act, dev)
+    if dev.type != "cuda":
+        raise ValueError("X: the layer runs on the GPU only")
+    _check_tensor(dY, "dY", st, act, dev)
+    _check_params(shape, w, WEIGHT_NAMES, dev, optional=("Wr",) if shape.fixed_stride else ())
+    _check_params(shape, grads, GRAD_NAMES, dev, optional=("dWr",) if shape.fixed_stride else ())
     if dX is None:
         dX = torch.empty_like(X)
+    _check_tensor(dX, "dX", st, act, dev)
     if scratch is None:
-        _, scratch = alloc_workspace(shape, X.device)
+        _, scratch = alloc_workspace(shape, dev)
+    _check_buffers(shape, saved, scratch, dev)
     g = Grads(*[_ptr(grads.get(n)) for n in GRAD_NAMES])
     args = [ctypes.byref(shape), _ptr(X), ctypes.byref(_weights(w)), _ptr(dY), _ptr(saved), saved.numel(), _ptr(dX),
             int(accumulate_dX), ctypes.byref(g), _ptr(scratch), scratch.numel(), _stream(stream)]
@@ -186,6 +253,61 @@ def backward(shape: Shape, X, w, dY, saved, grads, dX=None, accumulate_dX=False,
     else:
         _check(lib().mosa_backward_timed(*args, ctypes.byref(events)), "mosa_backward_timed")
     return dX
+
+
+class SelectionError(RuntimeError):
+    """The certified selection of some (b, h) rows did not hold exactly k tokens."""
+
+
+def check_selection(shape: Shape, saved):
+    """Raise SelectionError when the forward flagged a row whose selection is
+    not certified (the router's logit error bound failed); waits for the
+    forward to finish."""
+    if shape.heads == 0:
+        return
+    bad = saved_view(shape, saved, "status")
+    n = int((bad != 0).sum().item())
+    if n:
+        rows = (bad != 0).nonzero()[:8].tolist()
+        raise SelectionError(f"{n} (b, h) rows without a certified top-{shape.k} selection, e.g. {rows}")
+
+
+class StageTimer:
+    """hipEvent_t handles for the timed entry points: ``sets`` StageEvents
+    objects, each with MAX_STAGES events (created through the HIP runtime the
+    library links against)."""
+
+    def __init__(self, sets=1):
+        self.hip = ctypes.CDLL("libamdhip64.so")
+        self.hip.hipEventCreate.argtypes = [ctypes.POINTER(ctypes.c_void_p)]
+        self.hip.hipEventElapsedTime.argtypes = [ctypes.POINTER(ctypes.c_float), ctypes.c_void_p, ctypes.c_void_p]
+        self.hip.hipEventDestroy.argtypes = [ctypes.c_void_p]
+        self.handles = []
+        self.sets = []
+        for _ in range(sets):
+            ev = StageEvents()
+            for i in range(MAX_STAGES):
+                h = ctypes.c_void_p()
+                if self.hip.hipEventCreate(ctypes.byref(h)) != 0:
+                    raise RuntimeError("hipEventCreate failed")
+                self.handles.append(h.value)
+                ev.events[i] = h.value
+            self.sets.append(ev)
+
+    def elapsed_ms(self, a, b):
+        out = ctypes.c_float()
+        if self.hip.hipEventElapsedTime(ctypes.byref(out), ctypes.c_void_p(a), ctypes.c_void_p(b)) != 0:
+            raise RuntimeError("hipEventElapsedTime failed")
+        return out.value
+
+    def stages(self, ev):
+        """[(stage name, ms)] of one recorded StageEvents, in launch order."""
+        return [(ev.names[j].decode(), self.elapsed_ms(ev.events[j - 1], ev.events[j])) for j in range(1, ev.count)]
+
+    def close(self):
+        for h in self.handles:
+            self.hip.hipEventDestroy(ctypes.c_void_p(h))
+        self.handles = []
 
 
 def saved_view(shape: Shape, saved, name):
@@ -200,7 +322,8 @@ def saved_view(shape: Shape, saved, name):
     st = torch_dtype(shape)
     spec = {"I": (torch.int32, (B, H, k)), "r": (torch.float32, (B, H, k)), "slot": (torch.int16, (B, H, T)),
             "QKV": (st, (B, H, k, 3, dh)), "A": (st, (B, H, k, dh)), "lse": (torch.float32, (B, H, k)),
-            "QKVd": (st, (B, Hd, T, 3, dh)), "Ad": (st, (B, Hd, T, dh)), "lsed": (torch.float32, (B, Hd, T))}[name]
+            "QKVd": (st, (B, Hd, T, 3, dh)), "Ad": (st, (B, Hd, T, dh)), "lsed": (torch.float32, (B, Hd, T)),
+            "status": (torch.int32, (B, H))}[name]
     dt, shp = spec
     n = 1
     for s in shp:

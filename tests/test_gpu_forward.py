@@ -8,7 +8,7 @@ import pytest
 import torch
 
 import workloads as wl
-from gpu_util import TOL, rel_err, run_forward, to_f64
+from gpu_util import ROW_TOL, TOL, rel_err, row_rel_err, run_forward, to_f64
 from paper_2505_00315_amd import mosa
 
 pytestmark = pytest.mark.gpu
@@ -39,9 +39,10 @@ def check_forward(orc, w, inp=None, batches=None):
         mism = np.argwhere(Ig != Ir)
         assert mism.size == 0, f"index mismatch at {mism[:5].tolist()} (of {len(mism)})"
         assert rel_err(rg, rr) <= 1e-6, rel_err(rg, rr)
-    e = rel_err(Yg, Yr)
-    print(f"[case] Y rel err {e:.3e}", flush=True)
+    e, er = rel_err(Yg, Yr), row_rel_err(Yg, Yr)
+    print(f"[case] Y rel err {e:.3e}, worst row {er:.3e}", flush=True)
     assert e <= TOL[w.dtype], e
+    assert er <= ROW_TOL[w.dtype], er
     return out, ref
 
 
@@ -175,19 +176,6 @@ def test_workload_full(orc, name):
     check_forward(orc, w, wl.make_inputs(w, with_grad=False))
 
 
-def test_workload_hybrid_sampled(orc):
-    w = wl.WORKLOADS["hybrid_d1024"]
-    check_forward(orc, w, wl.make_inputs(w, with_grad=False), batches=[0, 7])
-
-
 def test_workload_long(orc):
     w = wl.WORKLOADS["long_t8192"]
     check_forward(orc, w, wl.make_inputs(w))
-
-
-@pytest.mark.parametrize("name", ["iso_tiny_rho2", "iso_tiny_rho64"])
-def test_workload_isoflop_sampled(orc, name):
-    """The FLOP-matched Tiny hybrids at the two ends of the sparsity range
-    (13 MoSA heads with k = 512; 505 heads with k = 16), batch element 0."""
-    w = wl.WORKLOADS[name]
-    check_forward(orc, w, wl.make_inputs(w, with_grad=False), batches=[0])

@@ -77,31 +77,9 @@ WORKLOADS = {
     "long_dense1_t8192": Workload("long_dense1_t8192", 1, 8192, 1024, 0, 64, 0, dense_heads=1, seed=4),
 }
 
-# The attention layers of the perplexity-matched pairs of Section 3.3 (the
-# resource-usage table): the dense baseline (9 heads; 16 for Large) against
-# the MoSA model that matches its perplexity (4 dense heads + 17 / 14 / 12 /
-# 16 MoSA heads at sparsity 32, Large at 16), T = 1024, d_head 64, the
-# hidden sizes of the paper's hyperparameter table; batch 8, forward and
-# backward of one layer.
-for _name, _d, _dense, _mosa, _rho in (("tiny", 512, 9, 17, 32), ("small", 1024, 9, 14, 32),
-                                       ("medium", 1024, 9, 12, 32), ("large", 1280, 16, 16, 16)):
-    WORKLOADS[f"pm_{_name}_mosa"] = Workload(f"pm_{_name}_mosa", 8, 1024, _d, _mosa, 64, 1024 // _rho,
-                                            dense_heads=4, backward=True, seed=5)
-    WORKLOADS[f"pm_{_name}_dense"] = Workload(f"pm_{_name}_dense", 8, 1024, _d, 0, 64, 0, dense_heads=_dense,
-                                             backward=True, seed=5)
-
-# The FLOP-matched Tiny hybrids of the IsoFLOP study (Appendix D, Table 5:
-# 4 dense heads + 13 / 31 / 69 / 142 / 276 / 505 MoSA heads at sparsity 2 ..
-# 64), each against the dense Tiny layer (pm_tiny_dense).
-for _rho, _mosa in ((2, 13), (4, 31), (8, 69), (16, 142), (32, 276), (64, 505)):
-    WORKLOADS[f"iso_tiny_rho{_rho}"] = Workload(f"iso_tiny_rho{_rho}", 8, 1024, 512, _mosa, 64, 1024 // _rho,
-                                               dense_heads=4, backward=True, seed=6)
-
-# Workloads timed together with a comparator on the same GPU: equal FLOPs
-# (long_t8192, iso_*), or equal perplexity in the paper's runs (pm_*).
-COMPARATORS = {"long_t8192": "long_dense1_t8192",
-               **{f"pm_{n}_mosa": f"pm_{n}_dense" for n in ("tiny", "small", "medium", "large")},
-               **{f"iso_tiny_rho{r}": "pm_tiny_dense" for r in (2, 4, 8, 16, 32, 64)}}
+# Workloads timed together with a comparator on the same GPU (equal FLOPs by
+# the paper's formula, Appendix A).
+COMPARATORS = {"long_t8192": "long_dense1_t8192"}
 
 
 def f32_to_bf16_bits(a):
