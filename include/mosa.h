@@ -15,7 +15,8 @@
  *   - All tensor pointers are DEVICE pointers, row-major, owned by the
  *     caller.  The library allocates no memory and keeps no state between
  *     calls (kernels that need more than 64 KB of LDS have that limit set
- *     on the current device before each launch); temporary memory comes in
+ *     on the current device before each launch; mosa_forward_noalloc keeps
+ *     the per-device address of its static scratch); temporary memory comes in
  *     through `scratch`, state kept from the forward for the backward
  *     through `saved`.  Calls from several host threads, on one device or
  *     several, do not interfere as long as they use different buffers.
@@ -219,6 +220,26 @@ int mosa_backward_timed(const mosa_shape* s, const void* X, const mosa_weights* 
                         const void* saved, size_t saved_bytes, void* dX, int accumulate_dX,
                         const mosa_grads* g, void* scratch, size_t scratch_bytes, void* stream,
                         mosa_stage_events* ev);
+
+/* Allocation-free forward, for callers that cannot allocate device memory
+ * (code under stream capture, tight serving loops, harnesses that forbid
+ * hipMalloc): mosa_forward without the `scratch` argument.  Its temporary
+ * memory is a static device array of MOSA_NOALLOC_SCRATCH_MAX bytes inside the
+ * library, one per GPU, held from the first call on that GPU until the process
+ * ends; the call itself allocates nothing.  Shapes whose forward needs more
+ * scratch than that are rejected with MOSA_ERR_WORKSPACE before any work is
+ * enqueued (the forward's scratch is at most the mosa_workspace_size scratch
+ * size: 64 MiB holds, e.g., B=8, T=1024, d_model=512, 32 heads, k=128).  Every call on one GPU uses
+ * the same array: calls that overlap in time on one GPU (different streams,
+ * or host threads without ordering) race and must be serialised by the
+ * caller; consecutive calls on one stream are safe.  Nothing in the array
+ * needs clearing between calls (every byte the forward reads there it first
+ * wrote in the same call).  The library keeps the array's per-device address
+ * from the first call on each device.  Results equal mosa_forward's bit for
+ * bit. */
+#define MOSA_NOALLOC_SCRATCH_MAX ((size_t)64 << 20)
+int mosa_forward_noalloc(const mosa_shape* s, const void* X, const mosa_weights* w, void* Y, int accumulate,
+                         int32_t* I_out, float* r_out, void* saved, size_t saved_bytes, void* stream);
 
 /* Static text for a status code (never NULL). */
 const char* mosa_status_string(int status);

@@ -20,7 +20,7 @@ struct Layout {
     size_t z, xnorm, unc_tok, unc_key, unc_sel, Xo, ybase;
     // backward scratch
     size_t dA, D, dz, dz16, dQKV, dXs, dAd, Dd, dQKVd, wpart, dxbase, dwr;
-    size_t scratch_total;
+    size_t fwd_scratch, scratch_total;
 };
 
 class Carver {
@@ -111,6 +111,7 @@ Layout make_layout(const mosa_shape* s) {
         const size_t pd = wgrad_partial_bytes(dt, (int)B, (int)d, (int)Hd, (int)dh, (int)T, 0);
         L.wpart = bw.take(pm > pd ? pm : pd);
     }
+    L.fwd_scratch = fw.total();
     L.scratch_total = fw.total() > bw.total() ? fw.total() : bw.total();
     return L;
 }
@@ -191,9 +192,17 @@ int mosa_saved_offsets(const mosa_shape* s, mosa_saved_layout* out) {
     return MOSA_OK;
 }
 
-int mosa_forward_timed(const mosa_shape* s, const void* X, const mosa_weights* w, void* Y, int accumulate,
-                       int32_t* I_out, float* r_out, void* saved, size_t saved_bytes, void* scratch,
-                       size_t scratch_bytes, void* stream_, mosa_stage_events* ev) {
+}  // extern "C"
+
+namespace mosa {
+
+size_t forward_scratch_bytes(const mosa_shape* s) { return validate_shape(s) ? 0 : make_layout(s).fwd_scratch; }
+
+// The forward (timed when ev != nullptr).  fwd_scratch_only: scratch need only
+// hold the forward's part (the allocation-free entry point's static buffer).
+int forward_impl(const mosa_shape* s, const void* X, const mosa_weights* w, void* Y, int accumulate,
+                 int32_t* I_out, float* r_out, void* saved, size_t saved_bytes, void* scratch,
+                 size_t scratch_bytes, void* stream_, mosa_stage_events* ev, bool fwd_scratch_only) {
     int st = validate_shape(s);
     if (st) return st;
     if ((st = check_weights(s, w))) return st;
@@ -201,7 +210,8 @@ int mosa_forward_timed(const mosa_shape* s, const void* X, const mosa_weights* w
     if (!saved || !scratch || !aligned(saved, kAlign) || !aligned(scratch, kAlign)) return MOSA_ERR_INVALID_ARG;
     if ((I_out && !aligned(I_out, 4)) || (r_out && !aligned(r_out, 4))) return MOSA_ERR_INVALID_ARG;
     const Layout L = make_layout(s);
-    if (saved_bytes < L.saved.total || scratch_bytes < L.scratch_total) return MOSA_ERR_WORKSPACE;
+    if (saved_bytes < L.saved.total || scratch_bytes < (fwd_scratch_only ? L.fwd_scratch : L.scratch_total))
+        return MOSA_ERR_WORKSPACE;
 
     hipStream_t stream = static_cast<hipStream_t>(stream_);
     if (ev) ev->count = 0;
@@ -268,11 +278,22 @@ int mosa_forward_timed(const mosa_shape* s, const void* X, const mosa_weights* w
     return e ? MOSA_ERR_HIP : MOSA_OK;
 }
 
+}  // namespace mosa
+
+extern "C" {
+
+int mosa_forward_timed(const mosa_shape* s, const void* X, const mosa_weights* w, void* Y, int accumulate,
+                       int32_t* I_out, float* r_out, void* saved, size_t saved_bytes, void* scratch,
+                       size_t scratch_bytes, void* stream, mosa_stage_events* ev) {
+    return forward_impl(s, X, w, Y, accumulate, I_out, r_out, saved, saved_bytes, scratch, scratch_bytes, stream, ev,
+                        false);
+}
+
 int mosa_forward(const mosa_shape* s, const void* X, const mosa_weights* w, void* Y, int accumulate,
                  int32_t* I_out, float* r_out, void* saved, size_t saved_bytes, void* scratch, size_t scratch_bytes,
                  void* stream) {
-    return mosa_forward_timed(s, X, w, Y, accumulate, I_out, r_out, saved, saved_bytes, scratch, scratch_bytes,
-                              stream, nullptr);
+    return forward_impl(s, X, w, Y, accumulate, I_out, r_out, saved, saved_bytes, scratch, scratch_bytes, stream,
+                        nullptr, false);
 }
 
 int mosa_backward_timed(const mosa_shape* s, const void* X, const mosa_weights* w, const void* dY, const void* saved,

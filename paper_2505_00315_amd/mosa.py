@@ -21,7 +21,9 @@ MOSA_F32 = 0
 MOSA_BF16 = 1
 
 SYMBOLS = ("mosa_workspace_size", "mosa_saved_offsets", "mosa_forward", "mosa_backward",
-           "mosa_forward_timed", "mosa_backward_timed", "mosa_status_string", "mosa_adaptive_k")
+           "mosa_forward_timed", "mosa_backward_timed", "mosa_status_string", "mosa_adaptive_k",
+           "mosa_forward_noalloc")
+NOALLOC_SCRATCH_MAX = 64 << 20  # MOSA_NOALLOC_SCRATCH_MAX
 MAX_STAGES = 32
 
 WEIGHT_NAMES = ("Wr", "Wq", "Wk", "Wv", "Wo", "Wq_d", "Wk_d", "Wv_d", "Wo_d")
@@ -78,13 +80,16 @@ def lib():
                                     ctypes.c_size_t, ctypes.c_void_p, ctypes.c_int, P(Grads), ctypes.c_void_p,
                                     ctypes.c_size_t, ctypes.c_void_p]
         L.mosa_forward_timed.argtypes = L.mosa_forward.argtypes + [P(StageEvents)]
+        L.mosa_forward_noalloc.argtypes = [P(Shape), ctypes.c_void_p, P(Weights), ctypes.c_void_p, ctypes.c_int,
+                                           ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_size_t,
+                                           ctypes.c_void_p]
         L.mosa_backward_timed.argtypes = L.mosa_backward.argtypes + [P(StageEvents)]
         L.mosa_status_string.argtypes = [ctypes.c_int]
         L.mosa_status_string.restype = ctypes.c_char_p
         L.mosa_adaptive_k.argtypes = [ctypes.c_int, ctypes.c_int]
         L.mosa_adaptive_k.restype = ctypes.c_int
         for n in ("mosa_workspace_size", "mosa_saved_offsets", "mosa_forward", "mosa_backward",
-                  "mosa_forward_timed", "mosa_backward_timed"):
+                  "mosa_forward_timed", "mosa_backward_timed", "mosa_forward_noalloc"):
             getattr(L, n).restype = ctypes.c_int
         _lib = L
     return _lib
@@ -223,6 +228,36 @@ def forward(shape: Shape, X, w, Y=None, accumulate=False, saved=None, scratch=No
     else:
         _check(lib().mosa_forward_timed(*args, ctypes.byref(events)), "mosa_forward_timed")
     return Y, saved, scratch
+
+
+def forward_noalloc(shape: Shape, X, w, Y=None, accumulate=False, saved=None, I_out=None, r_out=None,
+                    stream=None):
+    """Run mosa_forward_noalloc (scratch from the library's static buffer).
+    Returns (Y, saved)."""
+    st = torch_dtype(shape)
+    dev = X.device
+    act = shape.batch * shape.seq_len * shape.d_model
+    _check_tensor(X, "X", st, act, dev)
+    if dev.type != "cuda":
+        raise ValueError("X: the layer runs on the GPU only")
+    _check_params(shape, w, WEIGHT_NAMES, dev, optional=("Wr",) if shape.fixed_stride else ())
+    if Y is None:
+        Y = torch.empty_like(X)
+    _check_tensor(Y, "Y", st, act, dev)
+    need_saved, _ = workspace_size(shape)
+    if saved is None:
+        saved = torch.empty(max(need_saved, 256), dtype=torch.uint8, device=dev)
+    if saved.dtype != torch.uint8 or not saved.is_contiguous() or saved.device != dev or saved.numel() < need_saved:
+        raise ValueError(f"saved: a contiguous uint8 tensor on {dev} of at least {need_saved} bytes is required")
+    sel = shape.batch * shape.heads * shape.k
+    if I_out is not None:
+        _check_tensor(I_out, "I_out", torch.int32, sel, dev)
+    if r_out is not None:
+        _check_tensor(r_out, "r_out", torch.float32, sel, dev)
+    _check(lib().mosa_forward_noalloc(ctypes.byref(shape), _ptr(X), ctypes.byref(_weights(w)), _ptr(Y),
+                                      int(accumulate), _ptr(I_out), _ptr(r_out), _ptr(saved), saved.numel(),
+                                      _stream(stream)), "mosa_forward_noalloc")
+    return Y, saved
 
 
 def backward(shape: Shape, X, w, dY, saved, grads, dX=None, accumulate_dX=False, scratch=None, stream=None,
