@@ -173,6 +173,23 @@ __device__ __forceinline__ void mma4(f32x4& acc, const Frag4<float>& a, const Fr
 
 __device__ __forceinline__ f32x4 zero4() { return f32x4{0.f, 0.f, 0.f, 0.f}; }
 
+// Max / sum over the four rows of 16 lanes (lanes c, c + 16, c + 32, c + 48)
+// with the gfx950 row-swap moves (no LDS traffic): v_permlane16_swap gives
+// every lane the values of both rows of its row pair, v_permlane32_swap those
+// of both halves.  Every lane gets the same result, (x0 op x1) op (x2 op x3).
+__device__ __forceinline__ float rows4_max(float x) {
+    const auto a = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+    x = fmaxf(__uint_as_float(a[0]), __uint_as_float(a[1]));
+    const auto b = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+    return fmaxf(__uint_as_float(b[0]), __uint_as_float(b[1]));
+}
+__device__ __forceinline__ float rows4_sum(float x) {
+    const auto a = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+    x = __uint_as_float(a[0]) + __uint_as_float(a[1]);
+    const auto b = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+    return __uint_as_float(b[0]) + __uint_as_float(b[1]);
+}
+
 // Allows a kernel more than the default 64 KB of dynamic LDS on the current
 // device.  Called before every such launch (the attribute is cheap to set),
 // so the library keeps no record of which kernels were raised where.

@@ -17,7 +17,7 @@ inline size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
 struct Layout {
     mosa_saved_layout saved;
     // forward scratch
-    size_t z, xnorm, unc_tok, unc_key, unc_sel, Xo, ybase;
+    size_t z, xnorm, unc_tok, unc_key, unc_sel, Xo, ybase, apart;
     // backward scratch
     size_t dA, D, dz, dz16, dQKV, dXs, dAd, Dd, dQKVd, wpart, dxbase, dwr;
     size_t fwd_scratch, scratch_total;
@@ -93,6 +93,12 @@ Layout make_layout(const mosa_shape* s) {
     L.unc_sel = fw.take(B * H * T * 4);
     L.Xo = fw.take(B * H * k * d * es);
     L.ybase = fw.take(Hd > 0 ? B * T * d * 4 : 0);  // dense heads' part of Y (fp32)
+    {  // partial results of the attention's key splits (MoSA heads and dense heads run one after the other)
+        const int dt = s->dtype == MOSA_BF16 ? kBF16 : kF32;
+        const size_t pm = H > 0 ? attn_fwd_part_bytes(dt, (int)(B * H), (int)k, (int)dh, s->causal, 0) : 0;
+        const size_t pd = Hd > 0 ? attn_fwd_part_bytes(dt, (int)(B * Hd), (int)T, (int)dh, s->causal, s->window) : 0;
+        L.apart = fw.take(pm > pd ? pm : pd);
+    }
     Carver bw;
     L.dA = bw.take(B * H * k * dh * es);
     L.D = bw.take(B * H * k * 4);
@@ -230,6 +236,7 @@ int forward_impl(const mosa_shape* s, const void* X, const mosa_weights* w, void
     float* lsed = at<float>(saved, L.saved.lsed);
     int32_t* status = at<int32_t>(saved, L.saved.status);
     void* Xo = at<char>(scratch, L.Xo);
+    float* apart = at<float>(scratch, L.apart);
 
     float2* rope = s->rope ? at<float2>(saved, L.saved.rope) : nullptr;
     if (rope) {
@@ -254,8 +261,7 @@ int forward_impl(const mosa_shape* s, const void* X, const mosa_weights* w, void
         if (fused == 1) {
             e |= launch_qkv(dt, X, I, w->Wq, w->Wk, w->Wv, B, T, d, H, dh, k, QKV, rope, stream);
             e |= sm.mark("qkv");
-            e |= launch_attn_fwd(dt, QKV, r, B * H, k, dh, causal, 0, A, lse, stream);
-            e |= sm.mark("attn");
+            e |= launch_attn_fwd(dt, QKV, r, B * H, k, dh, causal, 0, A, lse, apart, 0, sm.marker(), stream);
         } else {
             e |= fused;
             e |= sm.mark("qkv_attn");
@@ -266,8 +272,8 @@ int forward_impl(const mosa_shape* s, const void* X, const mosa_weights* w, void
     if (Hd > 0) {
         e |= launch_qkv(dt, X, nullptr, w->Wq_d, w->Wk_d, w->Wv_d, B, T, d, Hd, dh, T, QKVd, rope, stream);
         e |= sm.mark("qkv_dense");
-        e |= launch_attn_fwd(dt, QKVd, nullptr, B * Hd, T, dh, causal, s->window, Ad, lsed, stream);
-        e |= sm.mark("attn_dense");
+        e |= launch_attn_fwd(dt, QKVd, nullptr, B * Hd, T, dh, causal, s->window, Ad, lsed, apart, 1, sm.marker(),
+                             stream);
     }
     e |= launch_out_combine(dt, Ad, w->Wo_d, slot, Xo, B, T, d, H, dh, k, Hd, Y, accumulate,
                             at<float>(scratch, L.ybase), sm.marker(), stream);

@@ -61,8 +61,13 @@ int launch_qkv_attn(int dtype, const void* X, const int32_t* I, const void* Wq, 
                     int B, int T, int d, int H, int dh, int n, void* QKV, const float2* rope, const float* r,
                     int causal, void* A, float* lse, hipStream_t stream);
 // window > 0 (causal only): query t sees keys t - window + 1 .. t (local heads).
+// part: fp32 scratch of attn_fwd_part_bytes(...) bytes for the partial
+// results of long query blocks cut into key splits (nullptr when that is 0).
+// Marks "attn" (dense heads: "attn_dense"), and "attn_merge" /
+// "attn_dense_merge" after the kernel that combines the splits.
 int launch_attn_fwd(int dtype, const void* QKV, const float* r, int BH, int n, int dh, int causal, int window, void* A,
-                    float* lse, hipStream_t stream);
+                    float* lse, float* part, int dense, const Marker& mk, hipStream_t stream);
+size_t attn_fwd_part_bytes(int dtype, int BH, int n, int dh, int causal, int window);
 
 // Xo[b,h,i,:] = A[b,h,i,:] Wo[h]  (A already scaled by r).
 int launch_out_proj(int dtype, const void* A, const void* Wo, int B, int d, int H, int dh, int k, void* Xo,

@@ -32,7 +32,7 @@ def check_backward(orc, w, inp=None):
     print(f"\n[case] {w}", flush=True)
     inp = wl.make_inputs(w, with_grad=True) if inp is None else inp
     Y, dX, grads, saved = run_fwd_bwd(w, inp)
-    ref = orc.backward(inp, inp["dY"], w.k, causal=w.causal)
+    ref = orc.backward(inp, inp["dY"], w.k, causal=w.causal, opts=orc.options(**w.variants()))
     got = {"dX": to_f64(dX)}
     got.update({n: to_f64(t) for n, t in grads.items() if n in ref})
     errs = {n: rel_err(v, ref[n]) for n, v in got.items()}
@@ -64,6 +64,8 @@ def test_tiny_f32_workload(orc):
     dict(batch=1, seq_len=1000, heads=2, k=500, d_model=192),
     dict(seq_len=256, k=128, d_head=64, d_model=128),
     dict(seq_len=200, k=100, causal=False),
+    dict(batch=2, seq_len=700, heads=0, dense_heads=1, d_head=64, d_model=128, causal=False),
+    dict(batch=2, seq_len=900, heads=0, dense_heads=1, d_head=64, d_model=128, window=600),
 ])
 def test_small_shapes(orc, kw):
     check_backward(orc, wl.small(**kw))
@@ -99,7 +101,7 @@ def test_workload_hybrid_full(orc):
     w = wl.WORKLOADS["hybrid_d1024"]
     inp = wl.make_inputs(w, with_grad=True)
     Y, saved, _ = check_backward(orc, w, inp)
-    ref = orc.forward(inp, w.k, causal=w.causal)
+    ref = orc.forward(inp, w.k, causal=w.causal, opts=orc.options(**w.variants()))
     I = mosa.saved_view(shape_of(w), saved, "I").cpu().numpy()
     mism = np.argwhere(I != ref["I"])
     assert mism.size == 0, f"index mismatch at {mism[:5].tolist()} (of {len(mism)})"

@@ -24,13 +24,13 @@ def check_forward(orc, w, inp=None, batches=None):
     out = run_forward(w, inp)
     Yg = to_f64(out["Y"])
     if batches is None:
-        ref = orc.forward(inp, w.k, causal=w.causal)
+        ref = orc.forward(inp, w.k, causal=w.causal, opts=orc.options(**w.variants()))
         Yr, Ir, rr = ref["Y"], ref["I"], ref["r"]
         Ig, rg = out.get("I"), out.get("r")
     else:  # the layer is independent per batch element: check a sample of them
         sub = dict(inp)
         sub["X"] = np.ascontiguousarray(inp["X"][batches])
-        ref = orc.forward(sub, w.k, causal=w.causal)
+        ref = orc.forward(sub, w.k, causal=w.causal, opts=orc.options(**w.variants()))
         Yr, Ir, rr = ref["Y"], ref["I"], ref["r"]
         Yg = Yg[batches]
         Ig = out["I"][batches] if w.heads else None
@@ -72,6 +72,11 @@ def test_tiny_f32_workload(orc):
     dict(batch=1, seq_len=128, k=64, d_head=64, d_model=128),
     # 1024 routed rows of T <= 1024: the selection's many-row launch shape
     dict(batch=4, seq_len=700, heads=256, k=37, d_head=32, d_model=64),
+    # 64-wide heads past 128 rows: the flash kernel, its key splits merged in
+    # order (non-causal, local window) and its ragged last query block
+    dict(batch=2, seq_len=700, heads=0, dense_heads=1, d_head=64, d_model=128, causal=False),
+    dict(batch=2, seq_len=900, heads=0, dense_heads=1, d_head=64, d_model=128, window=600),
+    dict(batch=1, seq_len=1100, heads=1, k=600, dense_heads=1, d_head=64, d_model=128),
 ])
 def test_small_shapes(orc, kw):
     check_forward(orc, wl.small(**kw))
