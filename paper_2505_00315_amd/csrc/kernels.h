@@ -114,6 +114,16 @@ int launch_bwd_proj(int dtype, const void* X, const void* dY, const int32_t* I, 
                     int B, int T, int d, int H, int dh, int n, void* dWq, void* dWk, void* dWv, void* dWr, void* dWo,
                     void* dXs, hipStream_t stream);
 
+// The same three products for heads with at most 128 selected rows over the
+// batch (B k <= 128; bf16, 64-wide heads): one workgroup per (product, head,
+// range of 64-column tiles of d) with the head's fixed operand in registers and
+// the other streamed through LDS; returns 1, launching nothing, where that does
+// not apply.
+int launch_bwd_head(int dtype, const void* X, const void* dY, const int32_t* I, const void* A, const void* dQKV,
+                    const void* dz16, const float* dz, const void* Wq, const void* Wk, const void* Wv, const void* Wr,
+                    int B, int T, int d, int H, int dh, int k, void* dWq, void* dWk, void* dWv, void* dWr, void* dWo,
+                    void* dXs, hipStream_t stream);
+
 // dXs[b,h,i,:] = dQ Wq^T + dK Wk^T + dV Wv^T + dz Wr  (per selected row).
 int launch_dx_proj(int dtype, const void* dQKV, const float* dz, const void* Wq, const void* Wk,
                    const void* Wv, const void* Wr, int B, int d, int H, int dh, int k, void* dXs,

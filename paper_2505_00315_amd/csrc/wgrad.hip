@@ -671,6 +671,10 @@ int launch_bwd_proj(int dtype, const void* X, const void* dY, const int32_t* I, 
                     int B, int T, int d, int H, int dh, int n, void* dWq, void* dWk, void* dWv, void* dWr, void* dWo,
                     void* dXs, hipStream_t stream) {
     if (dtype != kBF16 || H == 0 || !I) return 1;
+    // few selected rows per head: the per-head streaming kernel
+    const int e = launch_bwd_head(dtype, X, dY, I, A, dQKV, dz16, dz, Wq, Wk, Wv, Wr, B, T, d, H, dh, n, dWq, dWk, dWv,
+                                  dWr, dWo, dXs, stream);
+    if (e != 1) return e;
     using ST = uint16_t;
     auto f = dh == 64 ? run_bwd_proj<64> : run_bwd_proj<32>;
     return f((const ST*)X, (const ST*)dY, I, (const ST*)A, (const ST*)dQKV, (const ST*)dz16, dz, (const ST*)Wq,

@@ -66,6 +66,15 @@ def test_tiny_f32_workload(orc):
     dict(seq_len=200, k=100, causal=False),
     dict(batch=2, seq_len=700, heads=0, dense_heads=1, d_head=64, d_model=128, causal=False),
     dict(batch=2, seq_len=900, heads=0, dense_heads=1, d_head=64, d_model=128, window=600),
+    # 64-wide heads with at most 128 selected rows per head over the batch:
+    # the per-head streaming kernel of the weight gradients and dX rows
+    # (R = B k = 7, 40, 100 rows; one, two and three column tiles), and the
+    # grouped tile kernel just past it (R = 200, 256)
+    dict(batch=1, seq_len=64, heads=2, k=7, d_head=64, d_model=128),
+    dict(batch=2, seq_len=100, heads=3, k=20, d_head=64, d_model=128, dense_heads=1),
+    dict(batch=1, seq_len=300, heads=3, k=100, d_head=64, d_model=192),
+    dict(batch=2, seq_len=300, heads=3, k=100, d_head=64, d_model=192),
+    dict(batch=4, seq_len=128, heads=2, k=64, d_head=64, d_model=64, causal=False),
 ])
 def test_small_shapes(orc, kw):
     check_backward(orc, wl.small(**kw))
