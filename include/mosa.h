@@ -13,16 +13,25 @@
  *
  * Conventions shared by every entry point
  *   - All tensor pointers are DEVICE pointers, row-major, owned by the
- *     caller.  The library allocates no memory and keeps no state between
- *     calls (kernels that need more than 64 KB of LDS have that limit set
+ *     caller.  The library allocates no device memory and keeps no data
+ *     between calls; temporary memory comes in through `scratch`, state kept
+ *     from the forward for the backward through `saved`.  What it does keep
+ *     per device: kernels that need more than 64 KB of LDS have that limit set
  *     on the current device before each launch; mosa_forward_noalloc keeps
- *     the per-device address of its static scratch); temporary memory comes in
- *     through `scratch`, state kept from the forward for the backward
- *     through `saved`.  Calls from several host threads, on one device or
- *     several, do not interfere as long as they use different buffers.
+ *     the address of its static scratch; and the untimed forward and backward
+ *     of a layer with both MoSA and dense heads run the dense heads' kernels
+ *     on an auxiliary stream of the device (non-blocking, default priority,
+ *     created at the first such call and kept until the process ends), forked
+ *     from and joined back into `stream` with events inside the call, so the
+ *     two sets of heads share the CUs.  The enqueue of such calls is
+ *     serialised by a library mutex.  Calls from several host threads, on one
+ *     device or several, do not interfere as long as they use different
+ *     buffers.
  *   - `stream` is a hipStream_t (NULL: the default stream).  Calls only
- *     enqueue work; errors raised while kernels execute surface at the next
- *     synchronisation of that stream.
+ *     enqueue work: everything they enqueue, on the auxiliary stream too, is
+ *     complete when work enqueued on `stream` after the call starts, and
+ *     errors raised while kernels execute surface at the next synchronisation
+ *     of that stream.
  *   - Storage type (`dtype`): MOSA_BF16 or MOSA_F32 for X, dY, every weight,
  *     Y, dX and every weight gradient.  Accumulation is always fp32.
  *     Router logits, r and log-sum-exp values are fp32.
@@ -199,7 +208,8 @@ int mosa_backward(const mosa_shape* s, const void* X, const mosa_weights* w, con
 /* Stage timing for profiling and benchmarks.  The caller creates up to
  * MOSA_MAX_STAGES hipEvent_t handles and stores them in `events`; the timed
  * variants below launch exactly the kernels of mosa_forward / mosa_backward,
- * in the same order with the same arguments, and in addition record
+ * with the same arguments, all on `stream` in one serial order (the dense
+ * heads' kernels are not moved to the auxiliary stream), and in addition record
  * events[0] on `stream` before the first kernel and events[j] after the j-th
  * kernel launch, setting names[j] to that kernel's static stage name and
  * `count` to the number of events recorded.  The time of stage j is

@@ -253,13 +253,14 @@ int run_proj(const ST* dQKV, const float* dz, const ST* Wq, const ST* Wk, const 
 
 template <typename ST, int DH>
 int run_combine(const ST* dQKVd, const ST* Wq, const ST* Wk, const ST* Wv, const int16_t* slot, const ST* dXs, int B,
-                int T, int d, int H, int k, int Hd, ST* dX, int accumulate, float* base, const Marker& mk, hipStream_t stream) {
+                int T, int d, int H, int k, int Hd, ST* dX, int accumulate, float* base, int part, const Marker& mk, hipStream_t stream) {
     using P = DxCombinePolicy<ST, DH>;
     typename P::Args a{dQKVd, Wq, Wk, Wv, slot, dXs, dX, T, d, H, k, Hd, accumulate, (T + P::MT - 1) / P::MT,
                        (d + P::NT - 1) / P::NT};
     if (combine_rows_fits(d, H) && (Hd == 0 || base)) {
         // dense heads first (fp32 into base), then the per-token combination
-        if (Hd > 0) {
+        // (part 1: the first only, part 2: the second only, 0: both)
+        if (Hd > 0 && part != 2) {
             int e;
             if constexpr (sizeof(ST) == 2) {
                 using P2 = DxDensePolicy2<DH>;
@@ -279,9 +280,11 @@ int run_combine(const ST* dQKVd, const ST* Wq, const ST* Wk, const ST* Wv, const
             }
             if (e | mk("dx_dense")) return -1;
         }
+        if (part == 1) return 0;
         return launch_combine_rows<ST, 1>(slot, dXs, Hd > 0 ? base : nullptr, dX, B, T, d, H, k, accumulate, stream) |
                mk("dx_combine");
     }
+    if (part != 0) return 1;  // the one-kernel form cannot be split
     return launch_gemm<ST, P>(a, B * a.mtiles * a.ntiles, stream) | mk("dx_combine");
 }
 
@@ -302,15 +305,15 @@ int launch_dx_proj(int dtype, const void* dQKV, const float* dz, const void* Wq,
 
 int launch_dx_combine(int dtype, const void* dQKVd, const void* Wq_d, const void* Wk_d, const void* Wv_d,
                       const int16_t* slot, const void* dXs, int B, int T, int d, int H, int dh, int k, int Hd,
-                      void* dX, int accumulate, float* base, const Marker& mk, hipStream_t stream) {
+                      void* dX, int accumulate, float* base, int part, const Marker& mk, hipStream_t stream) {
     if (dtype == kBF16) {
         auto f = dh == 64 ? run_combine<uint16_t, 64> : run_combine<uint16_t, 32>;
         return f((const uint16_t*)dQKVd, (const uint16_t*)Wq_d, (const uint16_t*)Wk_d, (const uint16_t*)Wv_d, slot,
-                 (const uint16_t*)dXs, B, T, d, H, k, Hd, (uint16_t*)dX, accumulate, base, mk, stream);
+                 (const uint16_t*)dXs, B, T, d, H, k, Hd, (uint16_t*)dX, accumulate, base, part, mk, stream);
     }
     auto f = dh == 64 ? run_combine<float, 64> : run_combine<float, 32>;
     return f((const float*)dQKVd, (const float*)Wq_d, (const float*)Wk_d, (const float*)Wv_d, slot,
-             (const float*)dXs, B, T, d, H, k, Hd, (float*)dX, accumulate, base, mk, stream);
+             (const float*)dXs, B, T, d, H, k, Hd, (float*)dX, accumulate, base, part, mk, stream);
 }
 
 }  // namespace mosa

@@ -4,6 +4,8 @@
 #include <stddef.h>
 #include <stdint.h>
 
+#include <mutex>
+
 #include "kernels.h"
 #include "mosa.h"
 
@@ -17,9 +19,9 @@ inline size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
 struct Layout {
     mosa_saved_layout saved;
     // forward scratch
-    size_t z, xnorm, unc_tok, unc_key, unc_sel, Xo, ybase, apart;
+    size_t z, xnorm, unc_tok, unc_key, unc_sel, Xo, ybase, apart, apart_d;
     // backward scratch
-    size_t dA, D, dz, dz16, dQKV, dXs, dAd, Dd, dQKVd, wpart, dxbase, dwr;
+    size_t dA, D, dz, dz16, dQKV, dXs, dAd, Dd, dQKVd, wpart, wpart_d, dxbase, dwr;
     size_t fwd_scratch, scratch_total;
 };
 
@@ -93,11 +95,11 @@ Layout make_layout(const mosa_shape* s) {
     L.unc_sel = fw.take(B * H * T * 4);
     L.Xo = fw.take(B * H * k * d * es);
     L.ybase = fw.take(Hd > 0 ? B * T * d * 4 : 0);  // dense heads' part of Y (fp32)
-    {  // partial results of the attention's key splits (MoSA heads and dense heads run one after the other)
+    {  // partial results of the attention's key splits, MoSA and dense heads
+       // apart (the two chains may run at the same time)
         const int dt = s->dtype == MOSA_BF16 ? kBF16 : kF32;
-        const size_t pm = H > 0 ? attn_fwd_part_bytes(dt, (int)(B * H), (int)k, (int)dh, s->causal, 0) : 0;
-        const size_t pd = Hd > 0 ? attn_fwd_part_bytes(dt, (int)(B * Hd), (int)T, (int)dh, s->causal, s->window) : 0;
-        L.apart = fw.take(pm > pd ? pm : pd);
+        L.apart = fw.take(H > 0 ? attn_fwd_part_bytes(dt, (int)(B * H), (int)k, (int)dh, s->causal, 0) : 0);
+        L.apart_d = fw.take(Hd > 0 ? attn_fwd_part_bytes(dt, (int)(B * Hd), (int)T, (int)dh, s->causal, s->window) : 0);
     }
     Carver bw;
     L.dA = bw.take(B * H * k * dh * es);
@@ -113,9 +115,8 @@ Layout make_layout(const mosa_shape* s) {
     L.dwr = bw.take(H > 0 && s->fixed_stride > 0 ? H * d * es : 0);  // dW^r sink without a router
     {
         const int dt = s->dtype == MOSA_BF16 ? kBF16 : kF32;
-        const size_t pm = wgrad_partial_bytes(dt, (int)B, (int)d, (int)H, (int)dh, (int)k, 1);
-        const size_t pd = wgrad_partial_bytes(dt, (int)B, (int)d, (int)Hd, (int)dh, (int)T, 0);
-        L.wpart = bw.take(pm > pd ? pm : pd);
+        L.wpart = bw.take(wgrad_partial_bytes(dt, (int)B, (int)d, (int)H, (int)dh, (int)k, 1));
+        L.wpart_d = bw.take(wgrad_partial_bytes(dt, (int)B, (int)d, (int)Hd, (int)dh, (int)T, 0));
     }
     L.fwd_scratch = fw.total();
     L.scratch_total = fw.total() > bw.total() ? fw.total() : bw.total();
@@ -164,6 +165,45 @@ struct StageMarks {
     static int hook(void* ctx, const char* name) { return static_cast<StageMarks*>(ctx)->mark(name); }
     Marker marker() { return Marker{&StageMarks::hook, this}; }
 };
+
+// The dense heads' chain of kernels is independent of the MoSA heads' until
+// the head-ordered sum, so the untimed calls run it on an auxiliary stream of
+// the device (fork and join through two events), and the two chains share the
+// CUs.  Per device, created at the first call that has both kinds of heads and
+// kept until the process ends; the enqueue of a call is serialised under the
+// mutex, so that one call's fork and join events are not re-recorded by
+// another host thread in between.  Default priority, like every stream here.
+struct AuxStream {
+    hipStream_t s = nullptr;
+    hipEvent_t fork = nullptr, join = nullptr;
+    bool tried = false, ok = false;
+};
+constexpr int kMaxDevices = 64;
+std::mutex g_aux_mu;
+AuxStream g_aux[kMaxDevices];
+
+// The current device's auxiliary stream (g_aux_mu held), or nullptr.
+AuxStream* aux_stream() {
+    int dev = -1;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return nullptr;
+    AuxStream& a = g_aux[dev];
+    if (!a.tried) {
+        a.tried = true;
+        a.ok = hipStreamCreateWithFlags(&a.s, hipStreamNonBlocking) == hipSuccess &&
+               hipEventCreateWithFlags(&a.fork, hipEventDisableTiming) == hipSuccess &&
+               hipEventCreateWithFlags(&a.join, hipEventDisableTiming) == hipSuccess;
+    }
+    return a.ok ? &a : nullptr;
+}
+
+// Fork: work on the returned stream starts after everything enqueued on
+// `main` so far.  Join: `main` waits for everything enqueued on `aux`.
+int aux_fork(AuxStream* ax, hipStream_t main) {
+    return hipEventRecord(ax->fork, main) != hipSuccess || hipStreamWaitEvent(ax->s, ax->fork, 0) != hipSuccess;
+}
+int aux_join(AuxStream* ax, hipStream_t main) {
+    return hipEventRecord(ax->join, ax->s) != hipSuccess || hipStreamWaitEvent(main, ax->join, 0) != hipSuccess;
+}
 
 }  // namespace
 
@@ -243,6 +283,25 @@ int forward_impl(const mosa_shape* s, const void* X, const mosa_weights* w, void
         e |= launch_rope_table(T, dh, s->rope_base, rope, stream);
         e |= sm.mark("rope_table");
     }
+    // the dense heads on the auxiliary stream (untimed calls with both kinds of heads)
+    std::unique_lock<std::mutex> lock(g_aux_mu, std::defer_lock);
+    AuxStream* ax = nullptr;
+    if (!ev && H > 0 && Hd > 0 && combine_split_ok(d, H)) {
+        lock.lock();
+        ax = aux_stream();
+        if (ax && aux_fork(ax, stream)) return MOSA_ERR_HIP;
+    }
+    if (Hd > 0) {
+        hipStream_t ds = ax ? ax->s : stream;
+        e |= launch_qkv(dt, X, nullptr, w->Wq_d, w->Wk_d, w->Wv_d, B, T, d, Hd, dh, T, QKVd, rope, ds);
+        e |= sm.mark("qkv_dense");
+        e |= launch_attn_fwd(dt, QKVd, nullptr, B * Hd, T, dh, causal, s->window, Ad, lsed,
+                             at<float>(scratch, L.apart_d), 1, sm.marker(), ds);
+        if (ax) {
+            e |= launch_out_combine(dt, Ad, w->Wo_d, slot, Xo, B, T, d, H, dh, k, Hd, Y, accumulate,
+                                    at<float>(scratch, L.ybase), 1, sm.marker(), ds);
+        }
+    }
     if (H > 0) {
         if (routed(s)) {
             float* z = at<float>(scratch, L.z);
@@ -269,14 +328,9 @@ int forward_impl(const mosa_shape* s, const void* X, const mosa_weights* w, void
         e |= launch_out_proj(dt, A, w->Wo, B, d, H, dh, k, Xo, stream);
         e |= sm.mark("out_proj");
     }
-    if (Hd > 0) {
-        e |= launch_qkv(dt, X, nullptr, w->Wq_d, w->Wk_d, w->Wv_d, B, T, d, Hd, dh, T, QKVd, rope, stream);
-        e |= sm.mark("qkv_dense");
-        e |= launch_attn_fwd(dt, QKVd, nullptr, B * Hd, T, dh, causal, s->window, Ad, lsed, apart, 1, sm.marker(),
-                             stream);
-    }
+    if (ax) e |= aux_join(ax, stream);
     e |= launch_out_combine(dt, Ad, w->Wo_d, slot, Xo, B, T, d, H, dh, k, Hd, Y, accumulate,
-                            at<float>(scratch, L.ybase), sm.marker(), stream);
+                            at<float>(scratch, L.ybase), ax ? 2 : 0, sm.marker(), stream);
     if (H > 0 && I_out)
         e |= hipMemcpyAsync(I_out, I, (size_t)B * H * k * 4, hipMemcpyDeviceToDevice, stream) != hipSuccess;
     if (H > 0 && r_out)
@@ -358,6 +412,31 @@ int mosa_backward_timed(const mosa_shape* s, const void* X, const mosa_weights* 
     void* dWr = g->dWr ? g->dWr : at<char>(scratch, L.dwr);
 
     const Marker mk = sm.marker();
+    // the dense heads on the auxiliary stream (untimed calls with both kinds of heads)
+    std::unique_lock<std::mutex> lock(g_aux_mu, std::defer_lock);
+    AuxStream* ax = nullptr;
+    if (!ev && H > 0 && Hd > 0 && combine_split_ok(d, H)) {
+        lock.lock();
+        ax = aux_stream();
+        if (ax && aux_fork(ax, stream)) return MOSA_ERR_HIP;
+    }
+    if (Hd > 0) {
+        hipStream_t ds = ax ? ax->s : stream;
+        float* wpd = at<float>(scratch, L.wpart_d);
+        e |= launch_dattn_out(dt, dY, nullptr, nullptr, w->Wo_d, Ad, B, T, d, Hd, dh, T, dAd, Dd, nullptr, nullptr,
+                              ds);
+        e |= sm.mark("bwd_out_dense");
+        e |= launch_attn_bwd(dt, QKVd, dAd, lsed, Dd, B * Hd, T, dh, causal, s->window, dQKVd, nullptr, rope, 1, mk,
+                             ds);
+        e |= launch_wgrad(dt, X, dY, nullptr, Ad, dQKVd, nullptr, B, T, d, Hd, dh, T, g->dWq_d, g->dWk_d,
+                          g->dWv_d, nullptr, g->dWo_d, wpd, 0, mk, ds);
+        e |= launch_wgrad(dt, X, dY, nullptr, Ad, dQKVd, nullptr, B, T, d, Hd, dh, T, g->dWq_d, g->dWk_d,
+                          g->dWv_d, nullptr, g->dWo_d, wpd, 1, mk, ds);
+        if (ax) {
+            e |= launch_dx_combine(dt, dQKVd, w->Wq_d, w->Wk_d, w->Wv_d, slot, dXs, B, T, d, H, dh, k, Hd, dX,
+                                   accumulate_dX, at<float>(scratch, L.dxbase), 1, mk, ds);
+        }
+    }
     if (H > 0) {
         e |= launch_dattn_out(dt, dY, I, r, w->Wo, A, B, T, d, H, dh, k, dA, D, dz, dz16, stream);
         e |= sm.mark("bwd_out");
@@ -376,19 +455,9 @@ int mosa_backward_timed(const mosa_shape* s, const void* X, const mosa_weights* 
             e |= sm.mark("dx_proj");
         }
     }
-    if (Hd > 0) {
-        e |= launch_dattn_out(dt, dY, nullptr, nullptr, w->Wo_d, Ad, B, T, d, Hd, dh, T, dAd, Dd, nullptr, nullptr,
-                              stream);
-        e |= sm.mark("bwd_out_dense");
-        e |= launch_attn_bwd(dt, QKVd, dAd, lsed, Dd, B * Hd, T, dh, causal, s->window, dQKVd, nullptr, rope, 1, mk,
-                             stream);
-        e |= launch_wgrad(dt, X, dY, nullptr, Ad, dQKVd, nullptr, B, T, d, Hd, dh, T, g->dWq_d, g->dWk_d,
-                          g->dWv_d, nullptr, g->dWo_d, wpart, 0, mk, stream);
-        e |= launch_wgrad(dt, X, dY, nullptr, Ad, dQKVd, nullptr, B, T, d, Hd, dh, T, g->dWq_d, g->dWk_d,
-                          g->dWv_d, nullptr, g->dWo_d, wpart, 1, mk, stream);
-    }
+    if (ax) e |= aux_join(ax, stream);
     e |= launch_dx_combine(dt, dQKVd, w->Wq_d, w->Wk_d, w->Wv_d, slot, dXs, B, T, d, H, dh, k, Hd, dX, accumulate_dX,
-                           at<float>(scratch, L.dxbase), mk, stream);
+                           at<float>(scratch, L.dxbase), ax ? 2 : 0, mk, stream);
     return e ? MOSA_ERR_HIP : MOSA_OK;
 }
 

@@ -267,13 +267,14 @@ int run_proj(const ST* A, const ST* Wo, int B, int d, int H, int k, ST* Xo, hipS
 
 template <typename ST, int DH>
 int run_combine(const ST* Ad, const ST* Wod, const int16_t* slot, const ST* Xo, int B, int T, int d, int H, int k,
-                int Hd, ST* Y, int accumulate, float* base, const Marker& mk, hipStream_t stream) {
+                int Hd, ST* Y, int accumulate, float* base, int part, const Marker& mk, hipStream_t stream) {
     using P = OutCombinePolicy<ST, DH>;
     typename P::Args a{Ad, Wod, slot, Xo, Y, T, d, H, k, Hd, accumulate, (T + P::MT - 1) / P::MT,
                        (d + P::NT - 1) / P::NT};
     if (combine_rows_fits(d, H) && (Hd == 0 || base)) {
         // dense heads first (fp32 into base), then the per-token combination
-        if (Hd > 0) {
+        // (part 1: the first only, part 2: the second only, 0: both)
+        if (Hd > 0 && part != 2) {
             int e;
             if constexpr (sizeof(ST) == 2) {
                 using P2 = OutDensePolicy2<DH>;
@@ -289,13 +290,17 @@ int run_combine(const ST* Ad, const ST* Wod, const int16_t* slot, const ST* Xo, 
             }
             if (e | mk("out_dense")) return -1;
         }
+        if (part == 1) return 0;
         return launch_combine_rows<ST, 0>(slot, Xo, Hd > 0 ? base : nullptr, Y, B, T, d, H, k, accumulate, stream) |
                mk("out_combine");
     }
+    if (part != 0) return 1;  // the one-kernel form cannot be split
     return launch_gemm<ST, P>(a, B * a.mtiles * a.ntiles, stream) | mk("out_combine");
 }
 
 }  // namespace
+
+bool combine_split_ok(int d, int H) { return combine_rows_fits(d, H); }
 
 int launch_out_proj(int dtype, const void* A, const void* Wo, int B, int d, int H, int dh, int k, void* Xo,
                     hipStream_t stream) {
@@ -310,15 +315,15 @@ int launch_out_proj(int dtype, const void* A, const void* Wo, int B, int d, int 
 
 int launch_out_combine(int dtype, const void* Ad, const void* Wo_d, const int16_t* slot, const void* Xo, int B,
                        int T, int d, int H, int dh, int k, int Hd, void* Y, int accumulate, float* base,
-                       const Marker& mk, hipStream_t stream) {
+                       int part, const Marker& mk, hipStream_t stream) {
     if (dtype == kBF16) {
         auto f = dh == 64 ? run_combine<uint16_t, 64> : run_combine<uint16_t, 32>;
         return f((const uint16_t*)Ad, (const uint16_t*)Wo_d, slot, (const uint16_t*)Xo, B, T, d, H, k, Hd,
-                 (uint16_t*)Y, accumulate, base, mk, stream);
+                 (uint16_t*)Y, accumulate, base, part, mk, stream);
     }
     auto f = dh == 64 ? run_combine<float, 64> : run_combine<float, 32>;
     return f((const float*)Ad, (const float*)Wo_d, slot, (const float*)Xo, B, T, d, H, k, Hd, (float*)Y, accumulate,
-             base, mk, stream);
+             base, part, mk, stream);
 }
 
 }  // namespace mosa

@@ -215,9 +215,9 @@ def label_dispatches(dispatches, order_info):
 def short_kernel(name):
     """Kernel name without namespaces and argument lists."""
     import re
-    n = name.split("(")[0] if not name.startswith("void ") else name[5:].split("(")[0]
-    n = re.sub(r"mosa::|\(anonymous namespace\)::", "", n)
-    return n.replace("unsigned short", "bf16")
+    n = re.sub(r"mosa::|\(anonymous namespace\)::", "", name)
+    n = n[5:] if n.startswith("void ") else n
+    return n.split("(")[0].replace("unsigned short", "bf16")
 
 
 def per_stage(labelled):
@@ -244,8 +244,9 @@ def copy_scale(other, copy_bytes, counter):
     return copy_bytes / (other[-1][1][counter] * 1024.0)
 
 
-def profile_tables(w, order_info, trace_dir=None, fetch_dir=None, write_dir=None, pmc_dirs=()):
-    """Per-stage rows for the profile summary of workload `w`."""
+def profile_tables(w, order_info, trace_dir=None, fetch_dir=None, write_dir=None, pmc_dirs=(), copy_bytes=256 << 20):
+    """Per-stage rows for the profile summary of workload `w` (copy_bytes: the
+    size of the calibration copy at the end of the FETCH_SIZE / WRITE_SIZE runs)."""
     with_bwd = order_info["pass"] != "forward"
     work = stage_work(w, with_backward=with_bwd)
     rows = {st: {"stage": st} for st in order_info["order"]}
@@ -260,7 +261,7 @@ def profile_tables(w, order_info, trace_dir=None, fetch_dir=None, write_dir=None
         if not d:
             continue
         lab, other = label_dispatches(_by_dispatch(_read_csvs(d, "counter_collection.csv")), order_info)
-        scales[key] = sc = copy_scale(other, order_info["calibrate_copy_bytes"], ctr)
+        scales[key] = sc = copy_scale(other, copy_bytes, ctr)
         for st, e in per_stage(lab).items():
             rows[st][key + "_kib"] = e[ctr]
             rows[st][key + "_bytes"] = e[ctr] * 1024.0 * sc
@@ -360,13 +361,14 @@ def main(argv=None):
     ap.add_argument("--fetch", help="output directory of the FETCH_SIZE run")
     ap.add_argument("--write", help="output directory of the WRITE_SIZE run")
     ap.add_argument("--pmc", action="append", default=[], help="output directories of other counter runs")
+    ap.add_argument("--copy-bytes", type=int, default=256 << 20, help="calibration copy of the counter runs")
     ap.add_argument("--command", action="append", default=[], help="commands that produced the runs")
     ap.add_argument("--markdown", required=True, help="summary file to write")
     ap.add_argument("--traffic", help="counter file to update (lines of this workload replaced)")
     a = ap.parse_args(argv)
     info = json.load(open(a.order))
     w = wl.WORKLOADS[info["workload"]]
-    rows, scales = profile_tables(w, info, a.trace, a.fetch, a.write, a.pmc)
+    rows, scales = profile_tables(w, info, a.trace, a.fetch, a.write, a.pmc, a.copy_bytes)
     with open(a.markdown, "w") as f:
         f.write(profile_markdown(w, info, rows, scales, a.command))
     if a.traffic and a.fetch and a.write:
