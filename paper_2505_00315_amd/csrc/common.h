@@ -256,6 +256,42 @@ __device__ __forceinline__ uint32_t wave_sum_u32(uint32_t x) {
     return __builtin_amdgcn_readlane(wave_inclusive_scan_u32(x), 63);
 }
 
+// The same DPP moves on a double (both 32-bit halves; lanes without a source
+// get 0.0).
+template <int CTRL, int ROWS>
+__device__ __forceinline__ double dpp_f64(double x) {
+    const uint64_t u = (uint64_t)__double_as_longlong(x);
+    const uint32_t lo = __builtin_amdgcn_update_dpp(0u, (uint32_t)u, CTRL, ROWS, 0xf, false);
+    const uint32_t hi = __builtin_amdgcn_update_dpp(0u, (uint32_t)(u >> 32), CTRL, ROWS, 0xf, false);
+    return __longlong_as_double((long long)(((uint64_t)hi << 32) | lo));
+}
+// Sum over the wave of a double, in every lane (register moves only).
+__device__ __forceinline__ double wave_sum_f64(double x) {
+    x += dpp_f64<0x111, 0xf>(x);
+    x += dpp_f64<0x112, 0xf>(x);
+    x += dpp_f64<0x114, 0xf>(x);
+    x += dpp_f64<0x118, 0xf>(x);
+    x += dpp_f64<0x142, 0xa>(x);
+    x += dpp_f64<0x143, 0xc>(x);
+    const uint64_t u = (uint64_t)__double_as_longlong(x);
+    const uint32_t lo = __builtin_amdgcn_readlane((uint32_t)u, 63), hi = __builtin_amdgcn_readlane((uint32_t)(u >> 32), 63);
+    return __longlong_as_double((long long)(((uint64_t)hi << 32) | lo));
+}
+// Maximum over the wave of non-negative floats, in every lane.
+template <int CTRL, int ROWS>
+__device__ __forceinline__ float dpp_f32(float x) {
+    return __uint_as_float(__builtin_amdgcn_update_dpp(0u, __float_as_uint(x), CTRL, ROWS, 0xf, false));
+}
+__device__ __forceinline__ float wave_max_nonneg_f32(float x) {
+    x = fmaxf(x, dpp_f32<0x111, 0xf>(x));
+    x = fmaxf(x, dpp_f32<0x112, 0xf>(x));
+    x = fmaxf(x, dpp_f32<0x114, 0xf>(x));
+    x = fmaxf(x, dpp_f32<0x118, 0xf>(x));
+    x = fmaxf(x, dpp_f32<0x142, 0xa>(x));
+    x = fmaxf(x, dpp_f32<0x143, 0xc>(x));
+    return __uint_as_float(__builtin_amdgcn_readlane(__float_as_uint(x), 63));
+}
+
 // ---------------------------------------------------------------------------
 // Block-wide scans for 256 threads (4 waves).
 // ---------------------------------------------------------------------------

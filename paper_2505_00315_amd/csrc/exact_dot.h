@@ -68,45 +68,48 @@ MOSA_HD inline ProductParts product_parts(uint32_t sx, uint32_t Mx, int Ex, uint
 
 // Round the integer held in `dig` (value = sum dig[j] 2^(32 j) * 2^kLongLsbExp,
 // digits may be any signed values whose sum fits) to the nearest double.
-MOSA_HD inline double long_accumulator_round(const int64_t* dig) {
-    uint32_t w[kLongDigits];
+// The digits are normalised in place (carries propagated, the magnitude's
+// 32-bit words left in the slots), so no local array is needed: on the GPU the
+// digits stay in LDS and the routine uses no private (scratch) memory.
+MOSA_HD inline double long_accumulator_round(int64_t* dig) {
     int64_t carry = 0;
     for (int j = 0; j < kLongDigits; ++j) {
-        int64_t v = dig[j] + carry;
-        w[j] = (uint32_t)((uint64_t)v & 0xffffffffull);
+        const int64_t v = dig[j] + carry;
+        dig[j] = (int64_t)((uint64_t)v & 0xffffffffull);
         carry = v >> 32;  // arithmetic shift: floor division
     }
     const int negative = carry < 0;
     if (negative) {  // two's-complement negation of the 640-bit word
         uint64_t c = 1;
         for (int j = 0; j < kLongDigits; ++j) {
-            uint64_t v = (uint64_t)(uint32_t)~w[j] + c;
-            w[j] = (uint32_t)v;
+            const uint64_t v = (uint64_t)(uint32_t)~(uint32_t)dig[j] + c;
+            dig[j] = (int64_t)(uint32_t)v;
             c = v >> 32;
         }
     }
+    auto w = [dig](int j) { return (uint32_t)dig[j]; };
     int top = -1;
     for (int j = kLongDigits - 1; j >= 0; --j)
-        if (w[j]) { top = j; break; }
+        if (w(j)) { top = j; break; }
     if (top < 0) return 0.0;
     int msb = 31;
-    while (!((w[top] >> msb) & 1u)) --msb;
+    while (!((w(top) >> msb) & 1u)) --msb;
     const int bitpos = 32 * top + msb;  // position of the leading one
 
     // 64-bit window whose bit 63 is the leading one, plus a sticky bit.
     uint64_t win;
     int sticky = 0;
     if (bitpos < 64) {
-        uint64_t all = (uint64_t)w[0] | ((uint64_t)w[1] << 32);
+        uint64_t all = (uint64_t)w(0) | ((uint64_t)w(1) << 32);
         win = all << (63 - bitpos);
     } else {
         const int low = bitpos - 63, wi = low >> 5, sb = low & 31;
-        uint64_t lo64 = (uint64_t)w[wi] | ((wi + 1 < kLongDigits ? (uint64_t)w[wi + 1] : 0ull) << 32);
-        uint64_t hi32 = (wi + 2 < kLongDigits) ? (uint64_t)w[wi + 2] : 0ull;
+        uint64_t lo64 = (uint64_t)w(wi) | ((wi + 1 < kLongDigits ? (uint64_t)w(wi + 1) : 0ull) << 32);
+        uint64_t hi32 = (wi + 2 < kLongDigits) ? (uint64_t)w(wi + 2) : 0ull;
         win = (lo64 >> sb) | (sb ? (hi32 << (64 - sb)) : 0ull);
         if (sb && (lo64 & ((1ull << sb) - 1ull))) sticky = 1;
         for (int j = 0; j < wi; ++j)
-            if (w[j]) sticky = 1;
+            if (w(j)) sticky = 1;
     }
     uint64_t sig = win >> 11;          // 53 bits, leading one at bit 52
     const uint64_t rem = win & 0x7ffull;

@@ -8,12 +8,14 @@
 // fp32 logit z~_t with a proven bound |z~_t - s_t| <= beta_t, so every token
 // has an interval [lo_t, hi_t] that contains its key.  One workgroup of
 // several waves per (b, h) row:
-//   1. radix-select (4 passes of 8 bits over order-preserving uint32 keys held
-//      in registers, LDS histograms) the k-th largest lo, A, and the (k+1)-th
-//      largest hi, B;
+//   1. locate tau, the (k+1)-th largest z~, to within 1024 consecutive
+//      order-preserving uint32 keys (2 radix passes of 11 bits over keys held
+//      in registers; LDS histograms).  With b the largest beta_t of the row,
+//      A = (lower end - b) rounded down is at most the k-th largest lo, and
+//      B = (upper end + b) rounded up at least the (k+1)-th largest hi;
 //   2. hi_t < A  => at least k tokens certainly beat t: t is out;
 //      lo_t > B  => at most k-1 tokens can beat t: t is in;
-//      the rest (typically none or two tokens at the threshold) is uncertain;
+//      the rest (typically the (k+1)-th token alone) is uncertain;
 //   3. the uncertain tokens are re-scored in fp64 (exact products, bounded
 //      summation error), which orders them unless their keys (nearly) tie;
 //      only then is the exact key computed with a long accumulator
@@ -48,6 +50,22 @@ __device__ __forceinline__ uint32_t order_key(float f) {
     return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
 }
 
+constexpr int kBins = 2048;  // radix histogram bins (11-bit digits)
+
+// LDS word of radix bin b: descending position p = kBins - 1 - b, lane
+// p / 32 of the scanning wave, entry j = p % 32 of that lane at word
+// 256 (j / 4) + 4 (p / 32) + j % 4, so that the wave's 16-byte reads of its
+// 32 entries each cover 1 KB without bank conflicts.
+__device__ __forceinline__ int bin_slot(uint32_t b) {
+    const int p = kBins - 1 - (int)b, l = p >> 5, j = p & 31;
+    return 256 * (j >> 2) + 4 * l + (j & 3);
+}
+
+// Inverse of order_key.
+__device__ __forceinline__ float key_float(uint32_t k) {
+    return __uint_as_float((k & 0x80000000u) ? (k & 0x7fffffffu) : ~k);
+}
+
 __device__ __forceinline__ float f32_down(double x) {
     float f = (float)x;
     if ((double)f > x) f = next_down(f);
@@ -72,30 +90,11 @@ __device__ __forceinline__ uint64_t lanes_below() {
 }
 
 // NW waves per row, EPT tokens per thread (token t = e * 64 NW + tid, so loads
-// and stores are coalesced).  Both selections share one packed 32-bit block
-// scan per radix pass; the in-order positions come from per-wave, per-stripe
-// ballot counts; the uncertain tokens (if any) are re-scored one per wave in
-// parallel, their list kept in LDS when short.
+// and stores are coalesced).  One histogram per radix pass, scanned by
+// wave 0; the in-order positions come
+// from per-wave, per-stripe ballot counts; the uncertain tokens (if any) are
+// re-scored one per wave in parallel, their list kept in LDS when short.
 constexpr int kSelectLdsUnc = 64;  // uncertain tokens held in LDS (more: the global scratch arrays)
-
-template <int NW>
-__device__ __forceinline__ uint32_t block_exclusive_scan_u32(uint32_t v, uint32_t* tmp, uint32_t& total) {
-    // inclusive wave scan (DPP), then the wave totals through LDS
-    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-    const uint32_t inc = wave_inclusive_scan_u32(v);
-    if (lane == 63) tmp[w] = inc;
-    __syncthreads();
-    uint32_t base = 0, all = 0;
-#pragma unroll
-    for (int i = 0; i < NW; ++i) {
-        const uint32_t t = tmp[i];
-        base += i < w ? t : 0u;
-        all += t;
-    }
-    __syncthreads();
-    total = all;
-    return base + inc - v;
-}
 
 template <typename ST, int NW, int EPT>
 __global__ __launch_bounds__(64 * NW) void select_rows_kernel(
@@ -104,12 +103,12 @@ __global__ __launch_bounds__(64 * NW) void select_rows_kernel(
     int16_t* __restrict__ slot, int32_t* __restrict__ unc_tok, double* __restrict__ unc_key,
     int32_t* __restrict__ unc_sel, int32_t* __restrict__ status) {
     constexpr int NT = 64 * NW;
-    static_assert(NT >= 256, "one thread per histogram bin");
-    __shared__ uint32_t s_hist[256];   // packed counts: A in bits 0..15, B in 16..31
-    __shared__ uint32_t s_tmp[NW];
+    __shared__ __attribute__((aligned(16))) uint32_t s_hist[2][kBins];  // one per pass
     __shared__ double s_red[NW];
-    __shared__ int s_dig[4];
+    __shared__ int s_dig[2][2];
+    __shared__ float s_xmax[NW];
     __shared__ int s_cnt[NW][EPT];
+    __shared__ int s_cnt2[NW][EPT];
     __shared__ int s_utok[kSelectLdsUnc];
     __shared__ double s_ukey[kSelectLdsUnc];
     __shared__ int s_usel[kSelectLdsUnc];
@@ -136,18 +135,108 @@ __global__ __launch_bounds__(64 * NW) void select_rows_kernel(
         const double v = (double)ld1<ST>(w + c);
         ss += v * v;
     }
+    // The radix select runs on the order keys of z~ itself; lo and hi
+    // (z~ -+ beta_t, rounded outwards) classify the tokens afterwards, once
+    // ||w|| is known, so the loads of w and ||x|| overlap the radix passes.
+    uint32_t key[EPT];
 #pragma unroll
-    for (int o = 32; o >= 1; o >>= 1) ss += __shfl_xor(ss, o, 64);
-    if (lane == 0) s_red[wave] = ss;
+    for (int e = 0; e < EPT; ++e) key[e] = e * NT + tid < T ? order_key(zv[e]) : 0u;
+    // forced first token: token 0 above every real key, so it is certainly in
+    // and the other k - 1 are the best of t >= 1 (r_0 still from its logit)
+    if (first && tid == 0) key[0] = 0xffffffffu;
+    for (int i = tid; i < kBins; i += NT) s_hist[0][i] = 0u;  // the first pass's histogram
     __syncthreads();
-    ss = 0.0;
+    // per-wave ||w||^2 and largest ||x_t|| bound (every xv is a real token's),
+    // published before the first barrier that follows
+    auto publish_norms = [&]() {
+        float xm = xv[0];
 #pragma unroll
-    for (int i = 0; i < NW; ++i) ss += s_red[i];
-    const double wn = sqrt(ss) * (1.0 + 0x1p-30);
+        for (int e = 1; e < EPT; ++e) xm = fmaxf(xm, xv[e]);
+        ss = wave_sum_f64(ss);
+        xm = wave_max_nonneg_f32(xm);
+        if (lane == 0) {
+            s_red[wave] = ss;
+            s_xmax[wave] = xm;
+        }
+    };
+
+    // tau = the (k+1)-th largest z~, located by two radix passes over the
+    // top 22 bits of the keys (11 bits each) to within the 1024 keys
+    // [pref, pref + 1023].  With tlo <= tau <= thi the ends of that range,
+    //   A = down(tlo - bmax) <= the k-th largest lo: the k + 1 tokens with
+    //       z~ >= tau all have lo >= A;
+    //   B = up(thi + bmax) >= the (k+1)-th largest hi: a token with hi > B has
+    //       z~ > tau, and at most k tokens do;
+    // so "lo > B: in" and "hi < A: out" below are sound.  The range widens
+    // the uncertain band by at most 1023 units in the last place of tau.
+    const bool all = k >= T;
+    uint32_t pref = 0u;
+    if (!all) {
+        int rem = k + 1;
+        // Two barriers per pass: the histograms alternate between two
+        // buffers, so the second is cleared while wave 0 scans the first.
+#pragma unroll
+        for (int pass = 0; pass < 2; ++pass) {
+            const int shift = 21 - 11 * pass;
+            const uint32_t himask = pass == 0 ? 0u : 0xffe00000u;
+            uint32_t* hist = s_hist[pass];
+#pragma unroll
+            for (int e = 0; e < EPT; ++e)
+                if (e * NT + tid < T && ((key[e] ^ pref) & himask) == 0u)
+                    atomicAdd(&hist[bin_slot((key[e] >> shift) & (kBins - 1))], 1u);
+            if (pass == 0) publish_norms();
+            __syncthreads();  // this pass's histogram is complete
+            if (wave == 0) {
+                // lane l's 32 bins (descending positions 32 l .. 32 l + 31)
+                // in 8 conflict-free 16-byte reads; the lane whose range holds
+                // the rem-th candidate from the top, then within its range the
+                // bin, each found by a scan and a ballot
+                const uint4* hv = reinterpret_cast<const uint4*>(hist);
+                uint32_t csum = 0u;
+#pragma unroll
+                for (int q = 0; q < 8; ++q) {
+                    const uint4 v = hv[64 * q + lane];
+                    csum += v.x + v.y + v.z + v.w;
+                }
+                const uint32_t incl = wave_inclusive_scan_u32(csum), excl = incl - csum;
+                // (one lane qualifies: rem never exceeds the candidates counted)
+                const uint64_t mL = __ballot(excl < (uint32_t)rem && incl >= (uint32_t)rem);
+                const int L = mL ? __builtin_ctzll(mL) : 0;
+                const uint32_t exL = __builtin_amdgcn_readlane(excl, L);
+                const uint32_t c = lane < 32 ? hist[256 * (lane >> 2) + 4 * L + (lane & 3)] : 0u;
+                const uint32_t ci = wave_inclusive_scan_u32(c) + exL;
+                const uint64_t mj = __ballot(lane < 32 && ci - c < (uint32_t)rem && ci >= (uint32_t)rem);
+                if (mj && lane == __builtin_ctzll(mj)) {
+                    s_dig[pass][0] = kBins - 1 - (32 * L + lane);
+                    s_dig[pass][1] = rem - (int)(ci - c);
+                }
+            }
+            if (pass == 0 && wave == (NW > 1 ? 1 : 0)) {
+                uint4* hz = reinterpret_cast<uint4*>(s_hist[1]);
+                for (int i = lane; i < kBins / 4; i += 64) hz[i] = make_uint4(0u, 0u, 0u, 0u);
+            }
+            __syncthreads();  // digit found, second histogram cleared
+            pref |= (uint32_t)s_dig[pass][0] << shift;
+            rem = s_dig[pass][1];
+        }
+    } else {
+        publish_norms();
+        __syncthreads();
+    }
+
+    double wss = 0.0;
+    float xm = 0.f;
+#pragma unroll
+    for (int i = 0; i < NW; ++i) {
+        wss += s_red[i];
+        xm = fmaxf(xm, s_xmax[i]);
+    }
+    const double wn = sqrt(wss) * (1.0 + 0x1p-30);
     const int nc = d / 32;
     const double coef = (96.0 * 0x1p-23 + 1.01 * (double)nc * 0x1p-24) * (1.0 + 0x1p-10);
     const double absterm = (double)(d + nc) * 0x1p-126 * (1.0 + 0x1p-10);
-
+    // beta grows with ||x||, and so does its fp64 evaluation: bmax >= every beta_t
+    const double bmax = coef * (double)xm * wn + absterm * (1.0 + (double)xm + wn);
     uint32_t lo[EPT], hi[EPT];
 #pragma unroll
     for (int e = 0; e < EPT; ++e) {
@@ -157,56 +246,14 @@ __global__ __launch_bounds__(64 * NW) void select_rows_kernel(
         lo[e] = ok ? order_key(f32_down((double)zv[e] - beta)) : 0u;  // 0: below every real key
         hi[e] = ok ? order_key(f32_up((double)zv[e] + beta)) : 0u;
     }
-    // forced first token: token 0 above every real key, so it is certainly in
-    // and the other k - 1 are the best of t >= 1 (r_0 still from its logit)
     if (first && tid == 0) lo[0] = hi[0] = 0xffffffffu;
-
-    // k-th largest lo (A) and (k+1)-th largest hi (B): 8 bits per pass.
-    const bool all = k >= T;
     uint32_t A = 0u, Bk = 0u;
     if (!all) {
-        uint32_t prefA = 0u, prefB = 0u;
-        int remA = k, remB = k + 1;
-#pragma unroll
-        for (int pass = 0; pass < 4; ++pass) {
-            const int shift = 24 - 8 * pass;
-            const uint32_t himask = pass == 0 ? 0u : (0xffffffffu << (shift + 8));
-            if (tid < 256) s_hist[tid] = 0u;
-            __syncthreads();
-#pragma unroll
-            for (int e = 0; e < EPT; ++e) {
-                if (e * NT + tid < T) {
-                    if (((lo[e] ^ prefA) & himask) == 0u) atomicAdd(&s_hist[(lo[e] >> shift) & 255u], 1u);
-                    if (((hi[e] ^ prefB) & himask) == 0u) atomicAdd(&s_hist[(hi[e] >> shift) & 255u], 1u << 16);
-                }
-            }
-            __syncthreads();
-            // thread i looks at bin 255 - i: the exclusive scan in thread order
-            // counts the candidates in higher bins (both selections packed)
-            const uint32_t cnt = tid < 256 ? s_hist[255 - tid] : 0u;
-            uint32_t tot;
-            const uint32_t above = block_exclusive_scan_u32<NW>(cnt, s_tmp, tot);
-            if (tid < 256) {
-                const int ca = (int)(cnt & 0xffffu), cb = (int)(cnt >> 16);
-                const int aa = (int)(above & 0xffffu), ab = (int)(above >> 16);
-                if (aa < remA && aa + ca >= remA) {
-                    s_dig[0] = 255 - tid;
-                    s_dig[1] = remA - aa;
-                }
-                if (ab < remB && ab + cb >= remB) {
-                    s_dig[2] = 255 - tid;
-                    s_dig[3] = remB - ab;
-                }
-            }
-            __syncthreads();
-            prefA |= (uint32_t)s_dig[0] << shift;
-            remA = s_dig[1];
-            prefB |= (uint32_t)s_dig[2] << shift;
-            remB = s_dig[3];
-            __syncthreads();  // s_dig and s_hist are rewritten by the next pass
-        }
-        A = prefA;
-        Bk = prefB;
+        const float tlo = key_float(pref), thi = key_float(pref | 0x3ffu);
+        // ends that are not finite numbers give no bound (A = 0: nothing is
+        // out, B = max: nothing but a forced token is in)
+        A = isfinite(tlo) ? order_key(f32_down((double)tlo - bmax)) : 0u;
+        Bk = isfinite(thi) ? order_key(f32_up((double)thi + bmax)) : 0xffffffffu;
     }
 
     // Classify; in-order positions of the uncertain tokens from per-wave,
@@ -239,7 +286,6 @@ __global__ __launch_bounds__(64 * NW) void select_rows_kernel(
 #pragma unroll
         for (int i = 0; i < NW; ++i) tot_unc += s_cnt[i][e] >> 16;
     }
-    __syncthreads();  // s_cnt is reused for the selection counts
     int need = k - tot_in;  // 0 <= need <= tot_unc when the bound holds
     if (need < 0) need = 0;
     if (need > tot_unc) need = tot_unc;
@@ -272,8 +318,7 @@ __global__ __launch_bounds__(64 * NW) void select_rows_kernel(
                     for (int j = 0; j < 8; ++j) acc += (double)xv8[j] * (double)wv8[j];
                 }
             }
-#pragma unroll
-            for (int o = 32; o >= 1; o >>= 1) acc += __shfl_xor(acc, o, 64);
+            acc = wave_sum_f64(acc);
             if (lane == 0) ukey[u] = acc;
         }
         if (tid == 0) s_flag = 0;
@@ -361,7 +406,7 @@ __global__ __launch_bounds__(64 * NW) void select_rows_kernel(
 #pragma unroll
     for (int e = 0; e < EPT; ++e) {
         sb[e] = __ballot((selm >> e) & 1u);
-        if (lane == 0) s_cnt[wave][e] = __popcll(sb[e]);
+        if (lane == 0) s_cnt2[wave][e] = __popcll(sb[e]);
     }
     __syncthreads();
     int pos0 = 0;
@@ -370,7 +415,7 @@ __global__ __launch_bounds__(64 * NW) void select_rows_kernel(
         int below = 0, stripe = 0;
 #pragma unroll
         for (int i = 0; i < NW; ++i) {
-            const int c = s_cnt[i][e];
+            const int c = s_cnt2[i][e];
             if (i < wave) below += c;
             stripe += c;
         }
