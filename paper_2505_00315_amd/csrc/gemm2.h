@@ -48,6 +48,10 @@
 //   CHUNK_ADD (k-contiguous A and B): each MFMA from zero, then one add.
 //   EPI_REGS (needs A_INTERLEAVE): no C tile; the engine calls
 //     store8(args, batch, m, n, x[8]) for M indices m .. m + 7 at column n.
+//   a_tile_hook(args, m0, n0, a_tile, tid, state) / a_hook_done(args, m0, n0,
+//     tid, state): called by every thread after the MFMAs of each k chunk with
+//     that chunk's A tile in LDS (k-contiguous layout above), and once after
+//     the last chunk; `state` is one double per thread, zero at the start.
 #pragma once
 
 #include "gemm.h"
@@ -138,6 +142,8 @@ struct G2MinWaves<P, std::void_t<decltype(P::MIN_WAVES)>> : std::integral_consta
 // bound does not depend on the MFMA's internal accumulation).
 template <class P, class = void> struct G2ChunkAdd : std::false_type {};
 template <class P> struct G2ChunkAdd<P, std::void_t<decltype(P::CHUNK_ADD)>> : std::bool_constant<P::CHUNK_ADD> {};
+template <class P, class = void> struct G2AHook : std::false_type {};
+template <class P> struct G2AHook<P, std::void_t<decltype(&P::a_tile_hook)>> : std::true_type {};
 template <class P, class = void> struct G2EpiRegs : std::false_type {};
 template <class P> struct G2EpiRegs<P, std::void_t<decltype(P::EPI_REGS)>> : std::bool_constant<P::EPI_REGS> {};
 
@@ -307,6 +313,7 @@ __device__ __forceinline__ void gemm2_body(const typename P::Args& args, int log
     };
 
     const int wm = wave / S::WN, wn = wave % S::WN;
+    double hook_state = 0.0;
     f32x4 acc[S::FM][S::FN];
 #pragma unroll
     for (int i = 0; i < S::FM; ++i)
@@ -438,6 +445,7 @@ __device__ __forceinline__ void gemm2_body(const typename P::Args& args, int log
                 load_rows(c + STG);
                 __builtin_amdgcn_sched_barrier(0);
                 mfma_buf(u);
+                if constexpr (G2AHook<P>::value) P::a_tile_hook(args, m0, n0, smem + u * S::STAGE_BYTES, tid, hook_state);
                 if (c + 1 == nchunks) {
                     mfma_drain();
                     goto pipeline_done;
@@ -446,6 +454,7 @@ __device__ __forceinline__ void gemm2_body(const typename P::Args& args, int log
         }
     }
 pipeline_done:
+    if constexpr (G2AHook<P>::value) P::a_hook_done(args, m0, n0, tid, hook_state);
     wait_vmcnt<0>();  // the trailing loads write into the buffers the C tile reuses
     if constexpr (S::ER) {
         // lane: M indices 32 p + 8 g .. + 7 of the wave's rows, column c16 of block j

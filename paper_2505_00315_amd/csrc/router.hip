@@ -131,7 +131,8 @@ __global__ __launch_bounds__(256) void router_kernel(const ST* __restrict__ X, c
 // W^r row is fetched once per workgroup rather than once per wave.  Every
 // 32-k MFMA starts from zero and is added to the running sum (CHUNK_ADD): the
 // same summation, and the same error bound, as router_kernel.  The workgroups
-// of the first head tile also write the ||x_t|| bounds of their tokens.
+// of the first head tile also write the ||x_t|| bounds of their tokens,
+// summed from the X tiles in LDS as they pass.
 template <int MT_, int NT_>
 struct RouterPolicy2 {
     using ST = uint16_t;
@@ -162,6 +163,32 @@ struct RouterPolicy2 {
     __device__ static const ST* a_elem(const Args&, int, const ARef& r, int k) { return r.p + k; }
     __device__ static BRef b_row(const Args& a, int, int n) { return {a.Wr + (size_t)min(n, a.H - 1) * a.d}; }
     __device__ static const ST* b_elem(const Args&, int, const BRef& r, int k) { return r.p + k; }
+    // ||x_t||_2 bounds, by the workgroups of the first head tile, from the
+    // X rows of every k chunk while they are in LDS: TPR threads per token,
+    // each summing the squares of UPT 16-byte units (fp64, exact products)
+    static constexpr int TPR = 256 / MT, UPT = (KC / 8) / TPR;
+    static_assert(TPR * MT == 256 && UPT * TPR == KC / 8 && (TPR & (TPR - 1)) == 0, "norm threads");
+    __device__ static void a_tile_hook(const Args&, int, int n0, const unsigned char* ta, int tid, double& ss) {
+        if (n0 != 0) return;
+        const int r = tid / TPR, u0 = (tid % TPR) * UPT;
+#pragma unroll
+        for (int i = 0; i < UPT; ++i) {
+            const int u = u0 + i;
+            const uint4 v = *reinterpret_cast<const uint4*>(ta + (r * (KC / 8) + (u ^ kswz(r, KC / 8))) * 16);
+            float x[8];
+            vec8_to_f32<ST>(Vec8<ST>{v}, x);
+#pragma unroll
+            for (int e = 0; e < 8; ++e) ss += (double)x[e] * (double)x[e];
+        }
+    }
+    __device__ static void a_hook_done(const Args& a, int m0, int n0, int tid, double ss) {
+        if (n0 != 0) return;
+#pragma unroll
+        for (int o = 1; o < TPR; o <<= 1) ss += __shfl_xor(ss, o, 64);
+        const int tok = m0 + tid / TPR;
+        // fp64 rounding of <= d squares and the sqrt: far below 2^-30 relative
+        if (tid % TPR == 0 && tok < a.BT) a.xnorm[tok] = f32_round_up(sqrt(ss) * (1.0 + 0x1p-30));
+    }
     __device__ static void epilogue(const Args& a, int, int m0, int n0, const float* Cs, int ldc, int tid,
                                     unsigned char*) {
         for (int v = tid; v < MT * NT; v += 256) {
@@ -171,21 +198,6 @@ struct RouterPolicy2 {
                 a.z[((size_t)b * a.H + h) * a.T + t] = Cs[ml * ldc + nl];
             }
         }
-        if (n0 != 0) return;
-        // ||x_t||_2 bound: 256 / MT threads per token, fp64 sum of squares
-        constexpr int TPT = 256 / MT;
-        const int ml = tid / TPT, j = tid % TPT, tok = m0 + ml;
-        const ST* xr = a.X + (size_t)min(tok, a.BT - 1) * a.d;
-        double ss = 0.0;
-        for (int c = 8 * j; c < a.d; c += 8 * TPT) {
-            float x[8];
-            vec8_to_f32<ST>(vec8_load<ST>(xr + c), x);
-#pragma unroll
-            for (int e = 0; e < 8; ++e) ss += (double)x[e] * (double)x[e];
-        }
-#pragma unroll
-        for (int o = 1; o < TPT; o <<= 1) ss += __shfl_xor(ss, o, 64);
-        if (j == 0 && tok < a.BT) a.xnorm[tok] = f32_round_up(sqrt(ss) * (1.0 + 0x1p-30));
     }
 };
 
