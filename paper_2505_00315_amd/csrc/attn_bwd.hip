@@ -196,10 +196,20 @@ struct BwdTile {
     static constexpr int TB = 64, RS = 3 * DH;
     static constexpr int LDR = DH + 16 / (int)sizeof(ST);  // row-major rows
     static constexpr int VPR = DH / 8;
+    // LDS of the two passes for NWV waves (16 owned rows per wave); a kernel
+    // that may run either pass takes the larger
+    static constexpr size_t kv_lds(int nwv) {
+        const int sr = 16 * nwv > TB ? 16 * nwv : TB;
+        return 2 * (size_t)sr * LDR * sizeof(ST) + 2 * TB * sizeof(float);
+    }
+    static constexpr size_t q_lds(int nwv) {
+        const int sr = 16 * nwv > TB ? 16 * nwv : TB;
+        return (size_t)(sr + TB) * LDR * sizeof(ST);
+    }
 };
 
 template <typename ST, int DH, bool WIN, int NWV>
-__device__ __forceinline__ void attn_bwd_kv_tiled_body(int blk, const ST* __restrict__ QKV, const ST* __restrict__ dA,
+__device__ __forceinline__ void attn_bwd_kv_tiled_body(unsigned char* smem, int blk, const ST* __restrict__ QKV, const ST* __restrict__ dA,
                                                        const float* __restrict__ lse, const float* __restrict__ D,
                                                        int BH, int n, int causal, int lb, float scale,
                                                        ST* __restrict__ dQKV, const int32_t* __restrict__ rI,
@@ -210,9 +220,10 @@ __device__ __forceinline__ void attn_bwd_kv_tiled_body(int blk, const ST* __rest
     constexpr int PER = TB * VPR / NT, SR = OB > TB ? OB : TB;
     static_assert(PER >= 1 && TB * VPR % NT == 0, "tile shape");
     static_assert(sizeof(ST) == 2, "bf16: transposed operands by ds_read_b64_tr_b16");
-    __shared__ __attribute__((aligned(16))) ST Qs[SR * LDR];   // query tile, then the dK rows
-    __shared__ __attribute__((aligned(16))) ST dAs[SR * LDR];  // dA tile, then the dV rows
-    __shared__ float ls[TB], Dsh[TB];
+    ST* Qs = reinterpret_cast<ST*>(smem);  // query tile, then the dK rows
+    ST* dAs = Qs + SR * LDR;               // dA tile, then the dV rows
+    float* ls = reinterpret_cast<float*>(dAs + SR * LDR);
+    float* Dsh = ls + TB;
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int g = lane >> 4, c16 = lane & 15;
@@ -372,7 +383,7 @@ __device__ __forceinline__ void attn_bwd_kv_tiled_body(int blk, const ST* __rest
 }
 
 template <typename ST, int DH, bool WIN, int NWV>
-__device__ __forceinline__ void attn_bwd_q_tiled_body(int blk, const ST* __restrict__ QKV, const ST* __restrict__ dA,
+__device__ __forceinline__ void attn_bwd_q_tiled_body(unsigned char* smem, int blk, const ST* __restrict__ QKV, const ST* __restrict__ dA,
                                                       const float* __restrict__ lse, const float* __restrict__ D,
                                                       int BH, int n, int causal, int lb, float scale,
                                                       ST* __restrict__ dQKV, const int32_t* __restrict__ rI,
@@ -383,8 +394,8 @@ __device__ __forceinline__ void attn_bwd_q_tiled_body(int blk, const ST* __restr
     constexpr int PER = TB * VPR / NT, SR = OB > TB ? OB : TB;
     static_assert(PER >= 1 && TB * VPR % NT == 0, "tile shape");
     static_assert(sizeof(ST) == 2, "bf16: transposed operands by ds_read_b64_tr_b16");
-    __shared__ __attribute__((aligned(16))) ST Ks[SR * LDR];  // key tile, then the dQ rows
-    __shared__ __attribute__((aligned(16))) ST Vs[TB * LDR];
+    ST* Ks = reinterpret_cast<ST*>(smem);  // key tile, then the dQ rows
+    ST* Vs = Ks + SR * LDR;
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int g = lane >> 4, c16 = lane & 15;
@@ -523,19 +534,25 @@ __device__ __forceinline__ void attn_bwd_q_tiled_body(int blk, const ST* __restr
 
 template <typename ST, int DH, bool WIN, int NWV>
 __global__ __launch_bounds__(64 * NWV) void attn_bwd_kv_tiled_kernel(MOSA_BWD_TILED_PARAMS) {
-    attn_bwd_kv_tiled_body<ST, DH, WIN, NWV>(blockIdx.x, MOSA_BWD_TILED_ARGS);
+    __shared__ __attribute__((aligned(16))) unsigned char smem[BwdTile<ST, DH>::kv_lds(NWV)];
+    attn_bwd_kv_tiled_body<ST, DH, WIN, NWV>(smem, blockIdx.x, MOSA_BWD_TILED_ARGS);
 }
 template <typename ST, int DH, bool WIN, int NWV>
 __global__ __launch_bounds__(64 * NWV) void attn_bwd_q_tiled_kernel(MOSA_BWD_TILED_PARAMS) {
-    attn_bwd_q_tiled_body<ST, DH, WIN, NWV>(blockIdx.x, MOSA_BWD_TILED_ARGS);
+    __shared__ __attribute__((aligned(16))) unsigned char smem[BwdTile<ST, DH>::q_lds(NWV)];
+    attn_bwd_q_tiled_body<ST, DH, WIN, NWV>(smem, blockIdx.x, MOSA_BWD_TILED_ARGS);
 }
 // Both passes in one launch (they are independent): even blocks take the dK,
 // dV pass, odd blocks the dQ pass, each in its longest-first order, so the
 // short blocks of one pass fill the CUs beside the long blocks of the other.
 template <typename ST, int DH, bool WIN, int NWV>
 __global__ __launch_bounds__(64 * NWV) void attn_bwd_tiled_both_kernel(MOSA_BWD_TILED_PARAMS) {
-    if (blockIdx.x & 1) attn_bwd_q_tiled_body<ST, DH, WIN, NWV>(blockIdx.x >> 1, MOSA_BWD_TILED_ARGS);
-    else attn_bwd_kv_tiled_body<ST, DH, WIN, NWV>(blockIdx.x >> 1, MOSA_BWD_TILED_ARGS);
+    using TL = BwdTile<ST, DH>;
+    // one LDS buffer for whichever pass the block runs
+    __shared__ __attribute__((aligned(16))) unsigned char smem[TL::kv_lds(NWV) > TL::q_lds(NWV) ? TL::kv_lds(NWV)
+                                                                                                : TL::q_lds(NWV)];
+    if (blockIdx.x & 1) attn_bwd_q_tiled_body<ST, DH, WIN, NWV>(smem, blockIdx.x >> 1, MOSA_BWD_TILED_ARGS);
+    else attn_bwd_kv_tiled_body<ST, DH, WIN, NWV>(smem, blockIdx.x >> 1, MOSA_BWD_TILED_ARGS);
 }
 #undef MOSA_BWD_TILED_PARAMS
 #undef MOSA_BWD_TILED_ARGS
