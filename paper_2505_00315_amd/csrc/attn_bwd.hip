@@ -185,38 +185,44 @@ __global__ __launch_bounds__(256) void attn_bwd_q_kernel(const ST* __restrict__ 
     }
 }
 
-// Tiled passes for n > 32 (bf16 storage): a workgroup owns 64 keys (kv
-// pass) or 64 queries (q pass) of one (b,h), 16 per wave, and walks the other
-// side in tiles of 64 rows staged once in LDS for all four waves, row-major;
-// the MFMAs that contract over rows (32 rows per MFMA, P and dS straight from
-// registers) read their operands transposed with ds_read_b64_tr_b16.  The next tile's
-// global loads overlap the current tile's MFMAs.
+// Tiled passes for n > 32 (bf16 storage): a workgroup owns OB = 16 CB NWV
+// keys (kv pass) or queries (q pass) of one (b,h), 16 CB per wave, and walks
+// the other side in tiles of 64 rows staged once in LDS for all its waves,
+// row-major; the MFMAs that contract over rows (32 rows per MFMA, P and dS
+// straight from registers) read their operands transposed with
+// ds_read_b64_tr_b16.  Every fragment read from LDS feeds the CB column
+// blocks of the wave, so CB = 2 halves the LDS traffic per MFMA (the passes
+// are bound by it).  The next tile's global loads overlap the current tile's
+// MFMAs.  The result does not depend on CB or NWV: every output element is
+// one lane's fp32 accumulation over the tiles in order.
 template <typename ST, int DH>
 struct BwdTile {
     static constexpr int TB = 64, RS = 3 * DH;
     static constexpr int LDR = DH + 16 / (int)sizeof(ST);  // row-major rows
     static constexpr int VPR = DH / 8;
-    // LDS of the two passes for NWV waves (16 owned rows per wave); a kernel
-    // that may run either pass takes the larger
-    static constexpr size_t kv_lds(int nwv) {
-        const int sr = 16 * nwv > TB ? 16 * nwv : TB;
+    // LDS of the two passes for OB owned rows; a kernel that may run either
+    // pass takes the larger
+    static constexpr size_t kv_lds(int ob) {
+        const int sr = ob > TB ? ob : TB;
         return 2 * (size_t)sr * LDR * sizeof(ST) + 2 * TB * sizeof(float);
     }
-    static constexpr size_t q_lds(int nwv) {
-        const int sr = 16 * nwv > TB ? 16 * nwv : TB;
+    static constexpr size_t q_lds(int ob) {
+        const int sr = ob > TB ? ob : TB;
         return (size_t)(sr + TB) * LDR * sizeof(ST);
     }
+    static constexpr size_t both_lds(int ob) { return kv_lds(ob) > q_lds(ob) ? kv_lds(ob) : q_lds(ob); }
 };
 
-template <typename ST, int DH, bool WIN, int NWV>
-__device__ __forceinline__ void attn_bwd_kv_tiled_body(unsigned char* smem, int blk, const ST* __restrict__ QKV, const ST* __restrict__ dA,
-                                                       const float* __restrict__ lse, const float* __restrict__ D,
-                                                       int BH, int n, int causal, int lb, float scale,
-                                                       ST* __restrict__ dQKV, const int32_t* __restrict__ rI,
+template <typename ST, int DH, bool WIN, int NWV, int CB>
+__device__ __forceinline__ void attn_bwd_kv_tiled_body(unsigned char* smem, int blk, const ST* __restrict__ QKV,
+                                                       const ST* __restrict__ dA, const float* __restrict__ lse,
+                                                       const float* __restrict__ D, int BH, int n, int causal, int lb,
+                                                       float scale, ST* __restrict__ dQKV,
+                                                       const int32_t* __restrict__ rI,
                                                        const float2* __restrict__ rtab) {
     using TL = BwdTile<ST, DH>;
-    // OB keys owned by the workgroup (16 per wave), query tiles of TB rows
-    constexpr int TB = TL::TB, RS = TL::RS, LDR = TL::LDR, VPR = TL::VPR, NT = 64 * NWV, OB = 16 * NWV;
+    // OB keys owned by the workgroup (16 CB per wave), query tiles of TB rows
+    constexpr int TB = TL::TB, RS = TL::RS, LDR = TL::LDR, VPR = TL::VPR, NT = 64 * NWV, OB = 16 * CB * NWV;
     constexpr int PER = TB * VPR / NT, SR = OB > TB ? OB : TB;
     static_assert(PER >= 1 && TB * VPR % NT == 0, "tile shape");
     static_assert(sizeof(ST) == 2, "bf16: transposed operands by ds_read_b64_tr_b16");
@@ -227,29 +233,34 @@ __device__ __forceinline__ void attn_bwd_kv_tiled_body(unsigned char* smem, int 
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int g = lane >> 4, c16 = lane & 15;
-    const int nkb = (n + OB - 1) / OB, nqt = (n + TB - 1) / TB;
-    // block order: the owned key blocks with the most query tiles (causal: low
-    // kb) first, over all (b, h)
+    const int nqt = (n + TB - 1) / TB;
+    // block order: the owned key blocks with the most query tiles (causal:
+    // low kb) first, over all (b, h)
     const int bh = blk % BH, kb = blk / BH;
-    (void)nkb;
-    const int k0 = kb * OB, wk0 = k0 + 16 * wave;
+    const int k0 = kb * OB, wk0 = k0 + 16 * CB * wave;
     const size_t base = (size_t)bh * n;
     const ST* Qp = QKV + base * RS;
     const ST* Kp = Qp + DH;
     const ST* Vp = Qp + 2 * DH;
     const ST* dAp = dA + base * DH;
 
-    const int key = wk0 + c16;  // this lane's key (MFMA column)
-    const size_t krow = (size_t)min(key, n - 1);
-    Frag8<ST> kf[DH / 32], vf[DH / 32];
+    int key[CB];  // this lane's keys (MFMA column of each column block)
+    Frag8<ST> kf[CB][DH / 32], vf[CB][DH / 32];
 #pragma unroll
-    for (int st = 0; st < DH / 32; ++st) {
-        kf[st] = frag8_load<ST>(Kp + krow * RS + st * 32 + 8 * g);
-        vf[st] = frag8_load<ST>(Vp + krow * RS + st * 32 + 8 * g);
+    for (int cb = 0; cb < CB; ++cb) {
+        key[cb] = wk0 + 16 * cb + c16;
+        const size_t krow = (size_t)min(key[cb], n - 1);
+#pragma unroll
+        for (int st = 0; st < DH / 32; ++st) {
+            kf[cb][st] = frag8_load<ST>(Kp + krow * RS + st * 32 + 8 * g);
+            vf[cb][st] = frag8_load<ST>(Vp + krow * RS + st * 32 + 8 * g);
+        }
     }
-    f32x4 dKt[DH / 16], dVt[DH / 16];
+    f32x4 dKt[CB][DH / 16], dVt[CB][DH / 16];
 #pragma unroll
-    for (int db = 0; db < DH / 16; ++db) dKt[db] = dVt[db] = zero4();
+    for (int cb = 0; cb < CB; ++cb)
+#pragma unroll
+        for (int db = 0; db < DH / 16; ++db) dKt[cb][db] = dVt[cb][db] = zero4();
 
     // causal: query tiles from the block's own; with a window only those
     // within lb of its last key
@@ -290,32 +301,48 @@ __device__ __forceinline__ void attn_bwd_kv_tiled_body(unsigned char* smem, int 
         store_tile();
         __syncthreads();
         load_tile(min(it + 1, it_end - 1) * TB);
-        // S and dP for 4 sub-blocks of 16 queries: lane = key c16, rows = queries 4g + i
-        float p[4][4], ds[4][4];
+        // S and dP for 4 sub-blocks of 16 queries: lane = key c16 of each
+        // column block, rows = queries 4g + i
+        float p[CB][4][4], ds[CB][4][4];
 #pragma unroll
         for (int sb = 0; sb < 4; ++sb) {
-            f32x4 s = zero4(), dp = zero4();
+            f32x4 sv[CB], dp[CB];
+#pragma unroll
+            for (int cb = 0; cb < CB; ++cb) sv[cb] = dp[cb] = zero4();
 #pragma unroll
             for (int st = 0; st < DH / 32; ++st) {
-                mma8(s, frag8_load<ST>(Qs + (sb * 16 + c16) * LDR + st * 32 + 8 * g), kf[st]);
-                mma8(dp, frag8_load<ST>(dAs + (sb * 16 + c16) * LDR + st * 32 + 8 * g), vf[st]);
+                const Frag8<ST> qa = frag8_load<ST>(Qs + (sb * 16 + c16) * LDR + st * 32 + 8 * g);
+                const Frag8<ST> aa = frag8_load<ST>(dAs + (sb * 16 + c16) * LDR + st * 32 + 8 * g);
+#pragma unroll
+                for (int cb = 0; cb < CB; ++cb) {
+                    mma8(sv[cb], qa, kf[cb][st]);
+                    mma8(dp[cb], aa, vf[cb][st]);
+                }
             }
 #pragma unroll
-            for (int i = 0; i < 4; ++i) {
-                const int ql = sb * 16 + 4 * g + i, q = i0 + ql;
-                const bool ok = q < n && key < n && (!causal || (key <= q && (!WIN || q - key <= lb)));
-                p[sb][i] = ok ? __builtin_amdgcn_exp2f(fmaf(s[i], c2, -ls[ql])) : 0.f;
-                ds[sb][i] = p[sb][i] * (dp[i] - Dsh[ql]);
-            }
+            for (int cb = 0; cb < CB; ++cb)
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    const int ql = sb * 16 + 4 * g + i, q = i0 + ql, kk = key[cb];
+                    const bool ok = q < n && kk < n && (!causal || (kk <= q && (!WIN || q - kk <= lb)));
+                    p[cb][sb][i] = ok ? __builtin_amdgcn_exp2f(fmaf(sv[cb][i], c2, -ls[ql])) : 0.f;
+                    ds[cb][sb][i] = p[cb][sb][i] * (dp[cb][i] - Dsh[ql]);
+                }
         }
         // dV^T += dA^T P and dK^T += Q^T dS over 32 queries per MFMA
 #pragma unroll
         for (int u = 0; u < 2; ++u) {
-            const float pv[8] = {p[2 * u][0], p[2 * u][1], p[2 * u][2], p[2 * u][3],
-                                 p[2 * u + 1][0], p[2 * u + 1][1], p[2 * u + 1][2], p[2 * u + 1][3]};
-            const float dv[8] = {ds[2 * u][0], ds[2 * u][1], ds[2 * u][2], ds[2 * u][3],
-                                 ds[2 * u + 1][0], ds[2 * u + 1][1], ds[2 * u + 1][2], ds[2 * u + 1][3]};
-            const Frag8<ST> pf = frag8_from<ST>(pv), dsf = frag8_from<ST>(dv);
+            Frag8<ST> pf[CB], dsf[CB];
+#pragma unroll
+            for (int cb = 0; cb < CB; ++cb) {
+                const float pv[8] = {p[cb][2 * u][0], p[cb][2 * u][1], p[cb][2 * u][2], p[cb][2 * u][3],
+                                     p[cb][2 * u + 1][0], p[cb][2 * u + 1][1], p[cb][2 * u + 1][2], p[cb][2 * u + 1][3]};
+                const float dv[8] = {ds[cb][2 * u][0], ds[cb][2 * u][1], ds[cb][2 * u][2], ds[cb][2 * u][3],
+                                     ds[cb][2 * u + 1][0], ds[cb][2 * u + 1][1], ds[cb][2 * u + 1][2],
+                                     ds[cb][2 * u + 1][3]};
+                pf[cb] = frag8_from<ST>(pv);
+                dsf[cb] = frag8_from<ST>(dv);
+            }
             // dA^T and Q^T over the queries of those slots, read transposed
             // from the row-major tiles: lane d columns 16 db + 4 (c16 % 4) ..
             // + 3 at query rows r0 and r0 + 16
@@ -339,33 +366,39 @@ __device__ __forceinline__ void attn_bwd_kv_tiled_body(unsigned char* smem, int 
                 Frag8<ST> fa, fq;
                 fa.v = __builtin_bit_cast(bf16x8, at[db]);
                 fq.v = __builtin_bit_cast(bf16x8, qt[db]);
-                mma8(dVt[db], fa, pf);
-                mma8(dKt[db], fq, dsf);
+#pragma unroll
+                for (int cb = 0; cb < CB; ++cb) {
+                    mma8(dVt[cb][db], fa, pf[cb]);
+                    mma8(dKt[cb][db], fq, dsf[cb]);
+                }
             }
         }
         mfma_drain();  // the loop may exit right here
     }
 
-    // dK, dV rows (lane: key c16, d rows db*16 + 4g + i) through LDS to 16-byte stores
+    // dK, dV rows (lane: key c16 of block cb, d rows db*16 + 4g + i) through
+    // LDS to 16-byte stores
     __syncthreads();
-    ST* Ks_out = Qs + wave * 16 * LDR;
-    ST* Vs_out = dAs + wave * 16 * LDR;
+    ST* Ks_out = Qs + wave * 16 * CB * LDR;
+    ST* Vs_out = dAs + wave * 16 * CB * LDR;
 #pragma unroll
-    for (int db = 0; db < DH / 16; ++db)
+    for (int cb = 0; cb < CB; ++cb)
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            const int e = c16 * LDR + db * 16 + 4 * g + i;
-            if constexpr (sizeof(ST) == 2) {
-                Ks_out[e] = f32_to_bf16(dKt[db][i] * scale);
-                Vs_out[e] = f32_to_bf16(dVt[db][i]);
-            } else {
-                Ks_out[e] = dKt[db][i] * scale;
-                Vs_out[e] = dVt[db][i];
+        for (int db = 0; db < DH / 16; ++db)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const int e = (16 * cb + c16) * LDR + db * 16 + 4 * g + i;
+                if constexpr (sizeof(ST) == 2) {
+                    Ks_out[e] = f32_to_bf16(dKt[cb][db][i] * scale);
+                    Vs_out[e] = f32_to_bf16(dVt[cb][db][i]);
+                } else {
+                    Ks_out[e] = dKt[cb][db][i] * scale;
+                    Vs_out[e] = dVt[cb][db][i];
+                }
             }
-        }
     __syncthreads();
 #pragma unroll
-    for (int e = lane; e < 16 * VPR; e += 64) {
+    for (int e = lane; e < 16 * CB * VPR; e += 64) {
         const int r = e / VPR, dc = (e % VPR) * 8;
         if (wk0 + r < n) {
             ST* out = dQKV + (base + wk0 + r) * RS;
@@ -382,15 +415,16 @@ __device__ __forceinline__ void attn_bwd_kv_tiled_body(unsigned char* smem, int 
     }
 }
 
-template <typename ST, int DH, bool WIN, int NWV>
-__device__ __forceinline__ void attn_bwd_q_tiled_body(unsigned char* smem, int blk, const ST* __restrict__ QKV, const ST* __restrict__ dA,
-                                                      const float* __restrict__ lse, const float* __restrict__ D,
-                                                      int BH, int n, int causal, int lb, float scale,
-                                                      ST* __restrict__ dQKV, const int32_t* __restrict__ rI,
+template <typename ST, int DH, bool WIN, int NWV, int CB>
+__device__ __forceinline__ void attn_bwd_q_tiled_body(unsigned char* smem, int blk, const ST* __restrict__ QKV,
+                                                      const ST* __restrict__ dA, const float* __restrict__ lse,
+                                                      const float* __restrict__ D, int BH, int n, int causal, int lb,
+                                                      float scale, ST* __restrict__ dQKV,
+                                                      const int32_t* __restrict__ rI,
                                                       const float2* __restrict__ rtab) {
     using TL = BwdTile<ST, DH>;
-    // OB queries owned by the workgroup (16 per wave), key tiles of TB rows
-    constexpr int TB = TL::TB, RS = TL::RS, LDR = TL::LDR, VPR = TL::VPR, NT = 64 * NWV, OB = 16 * NWV;
+    // OB queries owned by the workgroup (16 CB per wave), key tiles of TB rows
+    constexpr int TB = TL::TB, RS = TL::RS, LDR = TL::LDR, VPR = TL::VPR, NT = 64 * NWV, OB = 16 * CB * NWV;
     constexpr int PER = TB * VPR / NT, SR = OB > TB ? OB : TB;
     static_assert(PER >= 1 && TB * VPR % NT == 0, "tile shape");
     static_assert(sizeof(ST) == 2, "bf16: transposed operands by ds_read_b64_tr_b16");
@@ -404,26 +438,34 @@ __device__ __forceinline__ void attn_bwd_q_tiled_body(unsigned char* smem, int b
     // high qb) first, over all (b, h)
     const int bh = blk % BH;
     const int qb = causal ? nqb - 1 - blk / BH : blk / BH;
-    const int q0 = qb * OB, wq0 = q0 + 16 * wave;
+    const int q0 = qb * OB, wq0 = q0 + 16 * CB * wave;
     const size_t base = (size_t)bh * n;
     const ST* Qp = QKV + base * RS;
     const ST* Kp = Qp + DH;
     const ST* Vp = Qp + 2 * DH;
     const ST* dAp = dA + base * DH;
 
-    const int q = wq0 + c16;  // this lane's query (MFMA column)
-    const size_t qrow = (size_t)min(q, n - 1);
-    Frag8<ST> qf[DH / 32], af[DH / 32];
+    int q[CB];  // this lane's queries (MFMA column of each column block)
+    Frag8<ST> qf[CB][DH / 32], af[CB][DH / 32];
+    float lq[CB], dq[CB];
 #pragma unroll
-    for (int st = 0; st < DH / 32; ++st) {
-        qf[st] = frag8_load<ST>(Qp + qrow * RS + st * 32 + 8 * g);
-        af[st] = frag8_load<ST>(dAp + qrow * DH + st * 32 + 8 * g);
+    for (int cb = 0; cb < CB; ++cb) {
+        q[cb] = wq0 + 16 * cb + c16;
+        const size_t qrow = (size_t)min(q[cb], n - 1);
+#pragma unroll
+        for (int st = 0; st < DH / 32; ++st) {
+            qf[cb][st] = frag8_load<ST>(Qp + qrow * RS + st * 32 + 8 * g);
+            af[cb][st] = frag8_load<ST>(dAp + qrow * DH + st * 32 + 8 * g);
+        }
+        lq[cb] = lse[base + qrow] * 1.44269504088896341f;  // lse in log2 units
+        dq[cb] = D[base + qrow];
     }
-    const float lq = lse[base + qrow] * 1.44269504088896341f, dq = D[base + qrow];  // lse in log2 units
     const float c2 = scale * 1.44269504088896341f;  // P = 2^(s c2 - lq)
-    f32x4 dQt[DH / 16];
+    f32x4 dQt[CB][DH / 16];
 #pragma unroll
-    for (int db = 0; db < DH / 16; ++db) dQt[db] = zero4();
+    for (int cb = 0; cb < CB; ++cb)
+#pragma unroll
+        for (int db = 0; db < DH / 16; ++db) dQt[cb][db] = zero4();
 
     const int kv_end = causal ? min(n, q0 + OB) : n;
     const int ntiles = (kv_end + TB - 1) / TB, t0 = WIN && causal ? max(0, q0 - lb) / TB : 0;
@@ -453,30 +495,45 @@ __device__ __forceinline__ void attn_bwd_q_tiled_body(unsigned char* smem, int b
         store_tile();
         __syncthreads();
         load_tile(min(t + 1, ntiles - 1) * TB);
-        // S^T and dP^T for 4 sub-blocks of 16 keys: lane = query c16, rows = keys 4g + i
-        float ds[4][4];
+        // S^T and dP^T for 4 sub-blocks of 16 keys: lane = query c16 of each
+        // column block, rows = keys 4g + i
+        float ds[CB][4][4];
 #pragma unroll
         for (int sb = 0; sb < 4; ++sb) {
-            f32x4 s = zero4(), dp = zero4();
+            f32x4 sv[CB], dp[CB];
+#pragma unroll
+            for (int cb = 0; cb < CB; ++cb) sv[cb] = dp[cb] = zero4();
 #pragma unroll
             for (int st = 0; st < DH / 32; ++st) {
-                mma8(s, frag8_load<ST>(Ks + (sb * 16 + c16) * LDR + st * 32 + 8 * g), qf[st]);
-                mma8(dp, frag8_load<ST>(Vs + (sb * 16 + c16) * LDR + st * 32 + 8 * g), af[st]);
+                const Frag8<ST> kk = frag8_load<ST>(Ks + (sb * 16 + c16) * LDR + st * 32 + 8 * g);
+                const Frag8<ST> vv = frag8_load<ST>(Vs + (sb * 16 + c16) * LDR + st * 32 + 8 * g);
+#pragma unroll
+                for (int cb = 0; cb < CB; ++cb) {
+                    mma8(sv[cb], kk, qf[cb][st]);
+                    mma8(dp[cb], vv, af[cb][st]);
+                }
             }
 #pragma unroll
-            for (int i = 0; i < 4; ++i) {
-                const int j = j0 + sb * 16 + 4 * g + i;
-                const bool ok = j < n && q < n && (!causal || (j <= q && (!WIN || q - j <= lb)));
-                const float pp = ok ? __builtin_amdgcn_exp2f(fmaf(s[i], c2, -lq)) : 0.f;
-                ds[sb][i] = pp * (dp[i] - dq);
-            }
+            for (int cb = 0; cb < CB; ++cb)
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    const int j = j0 + sb * 16 + 4 * g + i, qq = q[cb];
+                    const bool ok = j < n && qq < n && (!causal || (j <= qq && (!WIN || qq - j <= lb)));
+                    const float pp = ok ? __builtin_amdgcn_exp2f(fmaf(sv[cb][i], c2, -lq[cb])) : 0.f;
+                    ds[cb][sb][i] = pp * (dp[cb][i] - dq[cb]);
+                }
         }
         // dQ^T += K^T dS^T over 32 keys per MFMA
 #pragma unroll
         for (int u = 0; u < 2; ++u) {
-            const float dv[8] = {ds[2 * u][0], ds[2 * u][1], ds[2 * u][2], ds[2 * u][3],
-                                 ds[2 * u + 1][0], ds[2 * u + 1][1], ds[2 * u + 1][2], ds[2 * u + 1][3]};
-            const Frag8<ST> dsf = frag8_from<ST>(dv);
+            Frag8<ST> dsf[CB];
+#pragma unroll
+            for (int cb = 0; cb < CB; ++cb) {
+                const float dv[8] = {ds[cb][2 * u][0], ds[cb][2 * u][1], ds[cb][2 * u][2], ds[cb][2 * u][3],
+                                     ds[cb][2 * u + 1][0], ds[cb][2 * u + 1][1], ds[cb][2 * u + 1][2],
+                                     ds[cb][2 * u + 1][3]};
+                dsf[cb] = frag8_from<ST>(dv);
+            }
             // K^T over the keys of those slots, read transposed from the row-major tile
             const int r0 = 32 * u + 4 * g + (c16 >> 2);
             u32x4 kt[DH / 16];
@@ -493,25 +550,28 @@ __device__ __forceinline__ void attn_bwd_q_tiled_body(unsigned char* smem, int b
                 lds_ready(kt[db]);
                 Frag8<ST> fk;
                 fk.v = __builtin_bit_cast(bf16x8, kt[db]);
-                mma8(dQt[db], fk, dsf);
+#pragma unroll
+                for (int cb = 0; cb < CB; ++cb) mma8(dQt[cb][db], fk, dsf[cb]);
             }
         }
         mfma_drain();  // the loop may exit right here
     }
 
     __syncthreads();
-    ST* Qs_out = Ks + wave * 16 * LDR;
+    ST* Qs_out = Ks + wave * 16 * CB * LDR;
 #pragma unroll
-    for (int db = 0; db < DH / 16; ++db)
+    for (int cb = 0; cb < CB; ++cb)
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            const int e = c16 * LDR + db * 16 + 4 * g + i;
-            if constexpr (sizeof(ST) == 2) Qs_out[e] = f32_to_bf16(dQt[db][i] * scale);
-            else Qs_out[e] = dQt[db][i] * scale;
-        }
+        for (int db = 0; db < DH / 16; ++db)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const int e = (16 * cb + c16) * LDR + db * 16 + 4 * g + i;
+                if constexpr (sizeof(ST) == 2) Qs_out[e] = f32_to_bf16(dQt[cb][db][i] * scale);
+                else Qs_out[e] = dQt[cb][db][i] * scale;
+            }
     __syncthreads();
 #pragma unroll
-    for (int e = lane; e < 16 * VPR; e += 64) {
+    for (int e = lane; e < 16 * CB * VPR; e += 64) {
         const int r = e / VPR, dc = (e % VPR) * 8;
         if (wq0 + r < n) {
             Vec8<ST> qv = vec8_load<ST>(Qs_out + r * LDR + dc);
@@ -532,27 +592,25 @@ __device__ __forceinline__ void attn_bwd_q_tiled_body(unsigned char* smem, int b
         const int32_t *__restrict__ rI, const float2 *__restrict__ rtab
 #define MOSA_BWD_TILED_ARGS QKV, dA, lse, D, BH, n, causal, lb, scale, dQKV, rI, rtab
 
-template <typename ST, int DH, bool WIN, int NWV>
+template <typename ST, int DH, bool WIN, int NWV, int CB>
 __global__ __launch_bounds__(64 * NWV) void attn_bwd_kv_tiled_kernel(MOSA_BWD_TILED_PARAMS) {
-    __shared__ __attribute__((aligned(16))) unsigned char smem[BwdTile<ST, DH>::kv_lds(NWV)];
-    attn_bwd_kv_tiled_body<ST, DH, WIN, NWV>(smem, blockIdx.x, MOSA_BWD_TILED_ARGS);
+    __shared__ __attribute__((aligned(16))) unsigned char smem[BwdTile<ST, DH>::kv_lds(16 * CB * NWV)];
+    attn_bwd_kv_tiled_body<ST, DH, WIN, NWV, CB>(smem, blockIdx.x, MOSA_BWD_TILED_ARGS);
 }
-template <typename ST, int DH, bool WIN, int NWV>
+template <typename ST, int DH, bool WIN, int NWV, int CB>
 __global__ __launch_bounds__(64 * NWV) void attn_bwd_q_tiled_kernel(MOSA_BWD_TILED_PARAMS) {
-    __shared__ __attribute__((aligned(16))) unsigned char smem[BwdTile<ST, DH>::q_lds(NWV)];
-    attn_bwd_q_tiled_body<ST, DH, WIN, NWV>(smem, blockIdx.x, MOSA_BWD_TILED_ARGS);
+    __shared__ __attribute__((aligned(16))) unsigned char smem[BwdTile<ST, DH>::q_lds(16 * CB * NWV)];
+    attn_bwd_q_tiled_body<ST, DH, WIN, NWV, CB>(smem, blockIdx.x, MOSA_BWD_TILED_ARGS);
 }
 // Both passes in one launch (they are independent): even blocks take the dK,
 // dV pass, odd blocks the dQ pass, each in its longest-first order, so the
 // short blocks of one pass fill the CUs beside the long blocks of the other.
-template <typename ST, int DH, bool WIN, int NWV>
+template <typename ST, int DH, bool WIN, int NWV, int CB>
 __global__ __launch_bounds__(64 * NWV) void attn_bwd_tiled_both_kernel(MOSA_BWD_TILED_PARAMS) {
-    using TL = BwdTile<ST, DH>;
     // one LDS buffer for whichever pass the block runs
-    __shared__ __attribute__((aligned(16))) unsigned char smem[TL::kv_lds(NWV) > TL::q_lds(NWV) ? TL::kv_lds(NWV)
-                                                                                                : TL::q_lds(NWV)];
-    if (blockIdx.x & 1) attn_bwd_q_tiled_body<ST, DH, WIN, NWV>(smem, blockIdx.x >> 1, MOSA_BWD_TILED_ARGS);
-    else attn_bwd_kv_tiled_body<ST, DH, WIN, NWV>(smem, blockIdx.x >> 1, MOSA_BWD_TILED_ARGS);
+    __shared__ __attribute__((aligned(16))) unsigned char smem[BwdTile<ST, DH>::both_lds(16 * CB * NWV)];
+    if (blockIdx.x & 1) attn_bwd_q_tiled_body<ST, DH, WIN, NWV, CB>(smem, blockIdx.x >> 1, MOSA_BWD_TILED_ARGS);
+    else attn_bwd_kv_tiled_body<ST, DH, WIN, NWV, CB>(smem, blockIdx.x >> 1, MOSA_BWD_TILED_ARGS);
 }
 #undef MOSA_BWD_TILED_PARAMS
 #undef MOSA_BWD_TILED_ARGS
@@ -784,7 +842,7 @@ __global__ __launch_bounds__(512) void attn_bwd_lds_kernel(const uint16_t* __res
 
 template <typename ST>
 int launch_t(const ST* QKV, const ST* dA, const float* lse, const float* D, int BH, int n, int dh, int causal,
-             int window, ST* dQKV, const int32_t* rI, const float2* rtab, int pass, hipStream_t stream) {
+             int window, ST* dQKV, const int32_t* rI, const float2* rtab, int pass, int wide, hipStream_t stream) {
     const float scale = 1.0f / sqrtf((float)dh);
     const int lb = window > 0 ? window - 1 : n;  // keys a query may look back
     if constexpr (sizeof(ST) == 2) {
@@ -799,31 +857,33 @@ int launch_t(const ST* QKV, const ST* dA, const float* lse, const float* D, int 
         return hipGetLastError() == hipSuccess ? 0 : -1;
       }
       if (n > 32 || window > 0) {
-        // 64-wide heads: 128 owned rows on 8 waves per workgroup; 32-wide: 64 on 4
-#define MOSA_ATTN_BWD_T(KERN, DHV)                                                                     \
+        // 4 waves per workgroup, 16 owned rows per wave and column block:
+        // 64-wide heads with `wide` two column blocks (128 rows per
+        // workgroup, half the LDS reads per MFMA, one wave per SIMD), else one
+#define MOSA_ATTN_BWD_T(KERN, DHV, CBV)                                                                \
     do {                                                                                                \
-        constexpr int NWV = DHV == 64 ? 8 : 4;                                                          \
-        auto kern = window > 0 ? KERN<ST, DHV, true, NWV> : KERN<ST, DHV, false, NWV>;                  \
-        const dim3 grid((pass == 2 ? 2 : 1) * BH * ((n + 16 * NWV - 1) / (16 * NWV))), block(64 * NWV); \
+        constexpr int NWV = 4, CB = CBV, OB = 16 * CB * NWV;                                            \
+        auto kern = window > 0 ? KERN<ST, DHV, true, NWV, CB> : KERN<ST, DHV, false, NWV, CB>;          \
+        const dim3 grid((pass == 2 ? 2 : 1) * BH * ((n + OB - 1) / OB)), block(64 * NWV);               \
         hipLaunchKernelGGL(kern, grid, block, 0, stream, QKV, dA, lse, D, BH, n, causal, lb, scale, dQKV, rI, rtab); \
     } while (0)
-        if (pass == 2) {
-            if (dh == 64) MOSA_ATTN_BWD_T(attn_bwd_tiled_both_kernel, 64);
-            else MOSA_ATTN_BWD_T(attn_bwd_tiled_both_kernel, 32);
-        } else if (pass == 0) {
-            if (dh == 64) MOSA_ATTN_BWD_T(attn_bwd_kv_tiled_kernel, 64);
-            else MOSA_ATTN_BWD_T(attn_bwd_kv_tiled_kernel, 32);
-        } else {
-            if (dh == 64) MOSA_ATTN_BWD_T(attn_bwd_q_tiled_kernel, 64);
-            else MOSA_ATTN_BWD_T(attn_bwd_q_tiled_kernel, 32);
-        }
+#define MOSA_ATTN_BWD_TD(KERN)                                                                         \
+    do {                                                                                                \
+        if (dh == 64 && wide) MOSA_ATTN_BWD_T(KERN, 64, 2);                                             \
+        else if (dh == 64) MOSA_ATTN_BWD_T(KERN, 64, 1);                                                \
+        else MOSA_ATTN_BWD_T(KERN, 32, 1);                                                              \
+    } while (0)
+        if (pass == 2) MOSA_ATTN_BWD_TD(attn_bwd_tiled_both_kernel);
+        else if (pass == 0) MOSA_ATTN_BWD_TD(attn_bwd_kv_tiled_kernel);
+        else MOSA_ATTN_BWD_TD(attn_bwd_q_tiled_kernel);
+#undef MOSA_ATTN_BWD_TD
 #undef MOSA_ATTN_BWD_T
         return hipGetLastError() == hipSuccess ? 0 : -1;
       }
     }
     if (pass == 2)
-        return launch_t<ST>(QKV, dA, lse, D, BH, n, dh, causal, window, dQKV, rI, rtab, 0, stream) |
-               launch_t<ST>(QKV, dA, lse, D, BH, n, dh, causal, window, dQKV, rI, rtab, 1, stream);
+        return launch_t<ST>(QKV, dA, lse, D, BH, n, dh, causal, window, dQKV, rI, rtab, 0, wide, stream) |
+               launch_t<ST>(QKV, dA, lse, D, BH, n, dh, causal, window, dQKV, rI, rtab, 1, wide, stream);
     const int tasks = BH * ((n + 15) / 16);
     dim3 grid((tasks + 3) / 4), block(256);
 #define MOSA_ATTN_BWD(KERN, DHV)                                                                     \
@@ -858,7 +918,7 @@ int launch_attn_bwd(int dtype, const void* QKV, const void* dA, const float* lse
     auto run = [&](auto tag, int pass) {
         using ST = decltype(tag);
         return launch_t<ST>((const ST*)QKV, (const ST*)dA, lse, D, BH, n, dh, causal, window, (ST*)dQKV, rope_I,
-                            rope, pass, stream);
+                            rope, pass, dense == 2, stream);
     };
     auto go = [&](auto tag) {
         using ST = decltype(tag);
