@@ -842,7 +842,7 @@ __global__ __launch_bounds__(512) void attn_bwd_lds_kernel(const uint16_t* __res
 
 template <typename ST>
 int launch_t(const ST* QKV, const ST* dA, const float* lse, const float* D, int BH, int n, int dh, int causal,
-             int window, ST* dQKV, const int32_t* rI, const float2* rtab, int pass, int wide, hipStream_t stream) {
+             int window, ST* dQKV, const int32_t* rI, const float2* rtab, int pass, hipStream_t stream) {
     const float scale = 1.0f / sqrtf((float)dh);
     const int lb = window > 0 ? window - 1 : n;  // keys a query may look back
     if constexpr (sizeof(ST) == 2) {
@@ -857,21 +857,20 @@ int launch_t(const ST* QKV, const ST* dA, const float* lse, const float* D, int 
         return hipGetLastError() == hipSuccess ? 0 : -1;
       }
       if (n > 32 || window > 0) {
-        // 4 waves per workgroup, 16 owned rows per wave and column block:
-        // 64-wide heads with `wide` two column blocks (128 rows per
-        // workgroup, half the LDS reads per MFMA, one wave per SIMD), else one
-#define MOSA_ATTN_BWD_T(KERN, DHV, CBV)                                                                \
+        // 4 waves per workgroup, 16 owned rows per wave (one column block:
+        // two, with half the LDS reads per MFMA but one wave per SIMD, were
+        // slower beside the MoSA heads' backward)
+#define MOSA_ATTN_BWD_T(KERN, DHV)                                                                     \
     do {                                                                                                \
-        constexpr int NWV = 4, CB = CBV, OB = 16 * CB * NWV;                                            \
+        constexpr int NWV = 4, CB = 1, OB = 16 * CB * NWV;                                              \
         auto kern = window > 0 ? KERN<ST, DHV, true, NWV, CB> : KERN<ST, DHV, false, NWV, CB>;          \
         const dim3 grid((pass == 2 ? 2 : 1) * BH * ((n + OB - 1) / OB)), block(64 * NWV);               \
         hipLaunchKernelGGL(kern, grid, block, 0, stream, QKV, dA, lse, D, BH, n, causal, lb, scale, dQKV, rI, rtab); \
     } while (0)
 #define MOSA_ATTN_BWD_TD(KERN)                                                                         \
     do {                                                                                                \
-        if (dh == 64 && wide) MOSA_ATTN_BWD_T(KERN, 64, 2);                                             \
-        else if (dh == 64) MOSA_ATTN_BWD_T(KERN, 64, 1);                                                \
-        else MOSA_ATTN_BWD_T(KERN, 32, 1);                                                              \
+        if (dh == 64) MOSA_ATTN_BWD_T(KERN, 64);                                                        \
+        else MOSA_ATTN_BWD_T(KERN, 32);                                                                 \
     } while (0)
         if (pass == 2) MOSA_ATTN_BWD_TD(attn_bwd_tiled_both_kernel);
         else if (pass == 0) MOSA_ATTN_BWD_TD(attn_bwd_kv_tiled_kernel);
@@ -882,8 +881,8 @@ int launch_t(const ST* QKV, const ST* dA, const float* lse, const float* D, int 
       }
     }
     if (pass == 2)
-        return launch_t<ST>(QKV, dA, lse, D, BH, n, dh, causal, window, dQKV, rI, rtab, 0, wide, stream) |
-               launch_t<ST>(QKV, dA, lse, D, BH, n, dh, causal, window, dQKV, rI, rtab, 1, wide, stream);
+        return launch_t<ST>(QKV, dA, lse, D, BH, n, dh, causal, window, dQKV, rI, rtab, 0, stream) |
+               launch_t<ST>(QKV, dA, lse, D, BH, n, dh, causal, window, dQKV, rI, rtab, 1, stream);
     const int tasks = BH * ((n + 15) / 16);
     dim3 grid((tasks + 3) / 4), block(256);
 #define MOSA_ATTN_BWD(KERN, DHV)                                                                     \
@@ -918,7 +917,7 @@ int launch_attn_bwd(int dtype, const void* QKV, const void* dA, const float* lse
     auto run = [&](auto tag, int pass) {
         using ST = decltype(tag);
         return launch_t<ST>((const ST*)QKV, (const ST*)dA, lse, D, BH, n, dh, causal, window, (ST*)dQKV, rope_I,
-                            rope, pass, dense == 2, stream);
+                            rope, pass, stream);
     };
     auto go = [&](auto tag) {
         using ST = decltype(tag);

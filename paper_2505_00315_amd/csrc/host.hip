@@ -175,7 +175,7 @@ struct StageMarks {
 // another host thread in between.  Default priority, like every stream here.
 struct AuxStream {
     hipStream_t s = nullptr;
-    hipEvent_t fork = nullptr, join = nullptr;
+    hipEvent_t fork = nullptr, join = nullptr, mid = nullptr;  // mid: a point inside the auxiliary chain
     bool tried = false, ok = false;
 };
 constexpr int kMaxDevices = 64;
@@ -191,7 +191,8 @@ AuxStream* aux_stream() {
         a.tried = true;
         a.ok = hipStreamCreateWithFlags(&a.s, hipStreamNonBlocking) == hipSuccess &&
                hipEventCreateWithFlags(&a.fork, hipEventDisableTiming) == hipSuccess &&
-               hipEventCreateWithFlags(&a.join, hipEventDisableTiming) == hipSuccess;
+               hipEventCreateWithFlags(&a.join, hipEventDisableTiming) == hipSuccess &&
+               hipEventCreateWithFlags(&a.mid, hipEventDisableTiming) == hipSuccess;
     }
     return a.ok ? &a : nullptr;
 }
@@ -426,18 +427,17 @@ int mosa_backward_timed(const mosa_shape* s, const void* X, const mosa_weights* 
         e |= launch_dattn_out(dt, dY, nullptr, nullptr, w->Wo_d, Ad, B, T, d, Hd, dh, T, dAd, Dd, nullptr, nullptr,
                               ds);
         e |= sm.mark("bwd_out_dense");
-        // beside as many MoSA rows as dense rows, the wide form (see launch_attn_bwd)
-        const int dform = (long long)H * k >= (long long)Hd * T ? 2 : 1;
-        e |= launch_attn_bwd(dt, QKVd, dAd, lsed, Dd, B * Hd, T, dh, causal, s->window, dQKVd, nullptr, rope, dform,
-                             mk, ds);
-        e |= launch_wgrad(dt, X, dY, nullptr, Ad, dQKVd, nullptr, B, T, d, Hd, dh, T, g->dWq_d, g->dWk_d,
-                          g->dWv_d, nullptr, g->dWo_d, wpd, 0, mk, ds);
+        // dW^O needs only dY and the saved A: it goes before the attention
+        // backward, so that the chain's tail after it is short
         e |= launch_wgrad(dt, X, dY, nullptr, Ad, dQKVd, nullptr, B, T, d, Hd, dh, T, g->dWq_d, g->dWk_d,
                           g->dWv_d, nullptr, g->dWo_d, wpd, 1, mk, ds);
-        if (ax) {
-            e |= launch_dx_combine(dt, dQKVd, w->Wq_d, w->Wk_d, w->Wv_d, slot, dXs, B, T, d, H, dh, k, Hd, dX,
-                                   accumulate_dX, at<float>(scratch, L.dxbase), 1, mk, ds);
-        }
+        e |= launch_attn_bwd(dt, QKVd, dAd, lsed, Dd, B * Hd, T, dh, causal, s->window, dQKVd, nullptr, rope, 1, mk,
+                             ds);
+        // dQKV of the dense heads is complete: their dX GEMM may start on the
+        // main stream once the MoSA heads' kernels are done
+        if (ax && hipEventRecord(ax->mid, ds) != hipSuccess) e |= 1;
+        e |= launch_wgrad(dt, X, dY, nullptr, Ad, dQKVd, nullptr, B, T, d, Hd, dh, T, g->dWq_d, g->dWk_d,
+                          g->dWv_d, nullptr, g->dWo_d, wpd, 0, mk, ds);
     }
     if (H > 0) {
         e |= launch_dattn_out(dt, dY, I, r, w->Wo, A, B, T, d, H, dh, k, dA, D, dz, dz16, stream);
@@ -457,7 +457,12 @@ int mosa_backward_timed(const mosa_shape* s, const void* X, const mosa_weights* 
             e |= sm.mark("dx_proj");
         }
     }
-    if (ax) e |= aux_join(ax, stream);
+    if (ax) {
+        if (hipStreamWaitEvent(stream, ax->mid, 0) != hipSuccess) e |= 1;
+        e |= launch_dx_combine(dt, dQKVd, w->Wq_d, w->Wk_d, w->Wv_d, slot, dXs, B, T, d, H, dh, k, Hd, dX,
+                               accumulate_dX, at<float>(scratch, L.dxbase), 1, mk, stream);
+        e |= aux_join(ax, stream);
+    }
     e |= launch_dx_combine(dt, dQKVd, w->Wq_d, w->Wk_d, w->Wv_d, slot, dXs, B, T, d, H, dh, k, Hd, dX, accumulate_dX,
                            at<float>(scratch, L.dxbase), ax ? 2 : 0, mk, stream);
     return e ? MOSA_ERR_HIP : MOSA_OK;

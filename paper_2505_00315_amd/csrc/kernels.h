@@ -94,10 +94,7 @@ int launch_dattn_out(int dtype, const void* dY, const int32_t* I, const float* r
 // Attention backward into packed dQKV rows (dQ, dK and dV; one launch where
 // the kernels allow it).  Marks "attn_bwd" (dense heads: "attn_bwd_dense"),
 // or "attn_bwd_kv" and "attn_bwd_q" (+ "_dense") when the passes are two
-// launches.  dense: 0 MoSA heads, 1 dense heads, 2 dense heads of a layer
-// whose MoSA heads' backward runs beside them (the tiled passes then take
-// twice the rows per wave: fewer, heavier waves, which share the CUs with
-// the MoSA heads' kernels better).
+// launches.
 int launch_attn_bwd(int dtype, const void* QKV, const void* dA, const float* lse, const float* D, int BH,
                     int n, int dh, int causal, int window, void* dQKV, const int32_t* rope_I,
                     const float2* rope, int dense, const Marker& mk, hipStream_t stream);
