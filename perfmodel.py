@@ -192,9 +192,11 @@ def _by_dispatch(rows):
 
 
 def label_dispatches(dispatches, order_info):
-    """Stage name of every library dispatch (by position in the step) and the
-    dispatches outside the library (in order).  Checks that each position
-    always runs the same kernel."""
+    """Stage name of every library dispatch of the stage-timed steps (by
+    position in the step; the warm-up steps before them are untimed steps,
+    whose launch order differs where two streams are used, and are left out)
+    and the dispatches outside the library (in order).  Checks that each
+    position always runs the same kernel."""
     lib = [x for x in dispatches if "mosa::" in x[0]]
     other = [x for x in dispatches if "mosa::" not in x[0]]
     order = order_info["order"]
@@ -202,6 +204,7 @@ def label_dispatches(dispatches, order_info):
     if len(lib) != n:
         raise ValueError(f"{len(lib)} library dispatches, expected {n} ({order_info['warmup']} + "
                          f"{order_info['steps']} steps of {len(order)} launches)")
+    lib = lib[order_info["warmup"] * len(order):]
     kern = {}
     labelled = []
     for i, x in enumerate(lib):
