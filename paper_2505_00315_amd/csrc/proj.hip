@@ -129,10 +129,10 @@ struct QkvPolicy {
 // bf16 storage: the multi-stage engine with direct-to-LDS loads (gemm2.h).
 // A: gathered token rows (k-contiguous, clamped to the last row past M);
 // B: the three weights as one m-contiguous [d][3 DH] operand.
-template <int DH>
+template <int DH, int MT_ = 128>
 struct QkvPolicy2 {
     using ST = uint16_t;
-    static constexpr int MT = 128, NT = 3 * DH, KC = DH == 64 ? 32 : 64, WM = 2, WN = 2, STAGES = 4;
+    static constexpr int MT = MT_, NT = 3 * DH, KC = DH == 64 ? 32 : 64, WM = 2, WN = 2, STAGES = 4;
     static constexpr size_t TAB_LDS = (size_t)MT * (DH / 4) * 8;  // staged rotary rows
     static constexpr size_t EPI_LDS = TAB_LDS;
     static constexpr bool A_KCONTIG = true, B_KCONTIG = false;
@@ -178,16 +178,17 @@ struct QkvPolicy2 {
 // backward pass), the same workgroup copies the tile's K and V in bf16 into
 // LDS, takes Q from the C tile, and runs the attention of its groups
 // (attn_lds.h, bit-identical to the separate attention kernel).
-template <int DH>
-struct QkvAttnPolicy : QkvPolicy2<DH> {
+template <int DH, int MT_ = 128>
+struct QkvAttnPolicy : QkvPolicy2<DH, MT_> {
     using ST = uint16_t;
-    using Base = QkvPolicy2<DH>;
+    using Base = QkvPolicy2<DH, MT_>;
     static constexpr int MT = Base::MT, U = DH / 8, KROWS = MT, VROWS = MT + 16;
     // bf16 K tile, then the V tile with 16 zero rows after it (the last
     // group's odd key block reads 16 rows past its end, at weight zero)
     static constexpr size_t KV_LDS = (size_t)(KROWS + VROWS) * DH * 2;
     static constexpr size_t EPI_LDS = KV_LDS + Base::TAB_LDS;  // then the staged rotary rows
-    static_assert(MT == 128 && Base::WM * Base::WN == 4, "two query blocks per wave");
+    static_assert((MT == 128 || MT == 64) && Base::WM * Base::WN == 4, "one or two query blocks per wave");
+    static constexpr int QBW = MT / 64;  // query blocks of 16 rows per wave
     struct Args : QkvPolicy<ST, DH>::Args {
         const float* r;  // [B, H, n] router weights of the selected rows
         ST* A;           // [B, H, n, DH]
@@ -230,11 +231,12 @@ struct QkvAttnPolicy : QkvPolicy2<DH> {
             *reinterpret_cast<uint4*>(Vs + (size_t)(MT * U + v) * 16) = make_uint4(0, 0, 0, 0);
         __syncthreads();
 
-        // MT / 16 = 8 query blocks over 4 waves: blocks w and 7 - w, so that
-        // every wave's causal key blocks add up to the same count
+        // MT / 16 query blocks over 4 waves: 128 rows, blocks w and 7 - w, so
+        // that every wave's causal key blocks add up to the same count; 64
+        // rows, block w
         const int wave = tid >> 6, lane = tid & 63, g = lane >> 4, c16 = lane & 15;
         const int n = a.n, nqb = n / 16;
-        for (int j2 = 0; j2 < 2; ++j2) {
+        for (int j2 = 0; j2 < QBW; ++j2) {
             const int j = j2 ? 7 - wave : wave, gi = j / nqb, qb = j % nqb, mg = m0 + gi * n;
             if (mg >= a.M) continue;
             const size_t bh = (size_t)(mg / n) * a.H + h;
@@ -269,9 +271,9 @@ int launch_qkv_attn(int dtype, const void* X, const int32_t* I, const void* Wq, 
                     int causal, void* A, float* lse, hipStream_t stream) {
     if (dtype != kBF16 || n < 16 || n % 16 || 128 % n || (dh != 64 && dh != 32)) return 1;
     const float scale = 1.0f / sqrtf((float)dh);
-    auto go = [&](auto tag) {
+    auto go = [&](auto tag, auto mt) {
         constexpr int DH = decltype(tag)::value;
-        using P = QkvAttnPolicy<DH>;
+        using P = QkvAttnPolicy<DH, decltype(mt)::value>;
         if (d % P::KC) return 1;
         typename P::Args a{};
         static_cast<typename QkvPolicy<uint16_t, DH>::Args&>(a) = {
@@ -284,7 +286,13 @@ int launch_qkv_attn(int dtype, const void* X, const int32_t* I, const void* Wq, 
         a.scale = scale;
         return launch_gemm2<P>(a, P::mtiles(B * n) * H, stream);
     };
-    return dh == 64 ? go(std::integral_constant<int, 64>{}) : go(std::integral_constant<int, 32>{});
+    // at most 64 rows per head (B n <= 64): 64-row tiles instead of half-empty
+    // 128-row ones (measured equal or slower for more rows)
+    if ((long long)B * n <= 64)
+        return dh == 64 ? go(std::integral_constant<int, 64>{}, std::integral_constant<int, 64>{})
+                        : go(std::integral_constant<int, 32>{}, std::integral_constant<int, 64>{});
+    return dh == 64 ? go(std::integral_constant<int, 64>{}, std::integral_constant<int, 128>{})
+                    : go(std::integral_constant<int, 32>{}, std::integral_constant<int, 128>{});
 }
 
 int launch_qkv(int dtype, const void* X, const int32_t* I, const void* Wq, const void* Wk, const void* Wv, int B,
