@@ -70,9 +70,11 @@ MOSA_HD inline ProductParts product_parts(uint32_t sx, uint32_t Mx, int Ex, uint
 // digits may be any signed values whose sum fits) to the nearest double.
 // The digits are normalised in place (carries propagated, the magnitude's
 // 32-bit words left in the slots), so no local array is needed: on the GPU the
-// digits stay in LDS and the routine uses no private (scratch) memory.
+// digits stay in LDS and the routine uses no private (scratch) memory; its
+// loops stay loops (not unrolled), so that it holds few registers.
 MOSA_HD inline double long_accumulator_round(int64_t* dig) {
     int64_t carry = 0;
+#pragma clang loop unroll(disable)
     for (int j = 0; j < kLongDigits; ++j) {
         const int64_t v = dig[j] + carry;
         dig[j] = (int64_t)((uint64_t)v & 0xffffffffull);
@@ -81,6 +83,7 @@ MOSA_HD inline double long_accumulator_round(int64_t* dig) {
     const int negative = carry < 0;
     if (negative) {  // two's-complement negation of the 640-bit word
         uint64_t c = 1;
+#pragma clang loop unroll(disable)
         for (int j = 0; j < kLongDigits; ++j) {
             const uint64_t v = (uint64_t)(uint32_t)~(uint32_t)dig[j] + c;
             dig[j] = (int64_t)(uint32_t)v;
@@ -89,6 +92,7 @@ MOSA_HD inline double long_accumulator_round(int64_t* dig) {
     }
     auto w = [dig](int j) { return (uint32_t)dig[j]; };
     int top = -1;
+#pragma clang loop unroll(disable)
     for (int j = kLongDigits - 1; j >= 0; --j)
         if (w(j)) { top = j; break; }
     if (top < 0) return 0.0;
@@ -108,6 +112,7 @@ MOSA_HD inline double long_accumulator_round(int64_t* dig) {
         uint64_t hi32 = (wi + 2 < kLongDigits) ? (uint64_t)w(wi + 2) : 0ull;
         win = (lo64 >> sb) | (sb ? (hi32 << (64 - sb)) : 0ull);
         if (sb && (lo64 & ((1ull << sb) - 1ull))) sticky = 1;
+#pragma clang loop unroll(disable)
         for (int j = 0; j < wi; ++j)
             if (w(j)) sticky = 1;
     }
