@@ -162,7 +162,7 @@ __device__ __forceinline__ void combine_tile(const float* Cs, int ldc, int tid, 
 
 // The same combination as a kernel of its own: out[b, t] (+)= base[b, t] +
 // sum over MoSA heads h (ascending) of rows[b, h, slot[b, h, t]], where base
-// (fp32, optional) holds the dense heads' part.  A
+// (storage type, like the rows; optional) holds the dense heads' part.  A
 // workgroup takes 16 tokens of one batch element and stages their slot
 // entries for every head in LDS (head-major, padded rows); each of its 16
 // waves then handles one token, with the whole d-wide row spread over its
@@ -181,7 +181,7 @@ constexpr int kCombineLdt = kCombineTokens + 2;  // padded LDS row (int16) per h
 template <typename ST, int CH, int USE>
 __global__ __launch_bounds__(kCombineThreads) void combine_rows_kernel(const int16_t* __restrict__ slot,
                                                            const ST* __restrict__ rows,
-                                                           const float* __restrict__ base, ST* __restrict__ out,
+                                                           const ST* __restrict__ base, ST* __restrict__ out,
                                                            int T, int d, int H, int k, int accumulate,
                                                            int tiles_per_b) {
     extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
@@ -218,10 +218,7 @@ __global__ __launch_bounds__(kCombineThreads) void combine_rows_kernel(const int
         for (int c = 0; c < CH; ++c) {
             const int col = 8 * (lane + 64 * c);
             if (base && col < d) {
-                const float* bp = base + ((size_t)b * T + t) * d + col;
-                const float4 u = *reinterpret_cast<const float4*>(bp), w = *reinterpret_cast<const float4*>(bp + 4);
-                acc[c][0] = u.x, acc[c][1] = u.y, acc[c][2] = u.z, acc[c][3] = u.w;
-                acc[c][4] = w.x, acc[c][5] = w.y, acc[c][6] = w.z, acc[c][7] = w.w;
+                vec8_to_f32<ST>(vec8_load<ST>(base + ((size_t)b * T + t) * d + col), acc[c]);
             } else {
 #pragma unroll
                 for (int e = 0; e < 8; ++e) acc[c][e] = 0.f;
@@ -290,12 +287,12 @@ __global__ __launch_bounds__(kCombineThreads) void combine_rows_kernel(const int
 }
 
 // out (+)= base + head-ordered sum of the MoSA rows; d a multiple of 8, base
-// [B, T, d] fp32 or nullptr.
+// [B, T, d] in the storage type, or nullptr.
 inline bool combine_rows_fits(int d, int H) {
     return d % 8 == 0 && d <= 2048 && (size_t)(H > 0 ? H : 1) * kCombineLdt * sizeof(int16_t) <= 64 * 1024;
 }
 template <typename ST, int USE>
-int launch_combine_rows(const int16_t* slot, const ST* rows, const float* base, ST* out, int B, int T, int d, int H,
+int launch_combine_rows(const int16_t* slot, const ST* rows, const ST* base, ST* out, int B, int T, int d, int H,
                         int k, int accumulate, hipStream_t stream) {
     if (B == 0 || T == 0) return 0;
     if (!combine_rows_fits(d, H)) return -1;

@@ -156,8 +156,8 @@ struct DxCombinePolicy {
     }
 };
 
-// The dense heads' part alone, kept in fp32 ([B, T, d]) for combine_rows_kernel
-// to start from.
+// The dense heads' part alone ([B, T, d] in the storage type, here fp32) for
+// combine_rows_kernel to start from.
 template <typename ST, int DH>
 struct DxDensePolicy : DxCombinePolicy<ST, DH> {
     using Base = DxCombinePolicy<ST, DH>;
@@ -193,7 +193,7 @@ struct DxDensePolicy2 {
         const ST* dQKVd;  // [B, Hd, T, 3 DH]
         const ST* Wq;     // [Hd, d, DH]
         ptrdiff_t dk, dv; // W^K_d - W^Q_d, W^V_d - W^Q_d (elements)
-        float* base;      // [B, T, d]
+        ST* base;         // [B, T, d], the dense heads' part in the storage type
         int T, d, Hd, mtiles, ntiles;
     };
     struct ARef {
@@ -225,12 +225,13 @@ struct DxDensePolicy2 {
     }
     __device__ static void epilogue(const Args& a, int b, int m0, int n0, const float* Cs, int ldc, int tid,
                                     unsigned char*) {
-        constexpr int VPR = NT / 4;
+        constexpr int VPR = NT / 8;
         for (int v = tid; v < MT * VPR; v += 256) {
-            const int ml = v / VPR, c = (v % VPR) * 4, t = m0 + ml;
+            const int ml = v / VPR, c = (v % VPR) * 8, t = m0 + ml;
             if (t >= a.T || n0 + c >= a.d) continue;
-            *reinterpret_cast<float4*>(a.base + ((size_t)b * a.T + t) * a.d + n0 + c) =
-                *reinterpret_cast<const float4*>(Cs + ml * ldc + c);
+            float x[8];
+            cs_load8(Cs, ldc, ml, c, x);
+            vec8_store<ST>(a.base + ((size_t)b * a.T + t) * a.d + n0 + c, vec8_from_f32<ST>(x));
         }
     }
 };
@@ -253,12 +254,12 @@ int run_proj(const ST* dQKV, const float* dz, const ST* Wq, const ST* Wk, const 
 
 template <typename ST, int DH>
 int run_combine(const ST* dQKVd, const ST* Wq, const ST* Wk, const ST* Wv, const int16_t* slot, const ST* dXs, int B,
-                int T, int d, int H, int k, int Hd, ST* dX, int accumulate, float* base, int part, const Marker& mk, hipStream_t stream) {
+                int T, int d, int H, int k, int Hd, ST* dX, int accumulate, ST* base, int part, const Marker& mk, hipStream_t stream) {
     using P = DxCombinePolicy<ST, DH>;
     typename P::Args a{dQKVd, Wq, Wk, Wv, slot, dXs, dX, T, d, H, k, Hd, accumulate, (T + P::MT - 1) / P::MT,
                        (d + P::NT - 1) / P::NT};
     if (combine_rows_fits(d, H) && (Hd == 0 || base)) {
-        // dense heads first (fp32 into base), then the per-token combination
+        // dense heads first (into base), then the per-token combination
         // (part 1: the first only, part 2: the second only, 0: both)
         if (Hd > 0 && part != 2) {
             int e;
@@ -305,15 +306,15 @@ int launch_dx_proj(int dtype, const void* dQKV, const float* dz, const void* Wq,
 
 int launch_dx_combine(int dtype, const void* dQKVd, const void* Wq_d, const void* Wk_d, const void* Wv_d,
                       const int16_t* slot, const void* dXs, int B, int T, int d, int H, int dh, int k, int Hd,
-                      void* dX, int accumulate, float* base, int part, const Marker& mk, hipStream_t stream) {
+                      void* dX, int accumulate, void* base, int part, const Marker& mk, hipStream_t stream) {
     if (dtype == kBF16) {
         auto f = dh == 64 ? run_combine<uint16_t, 64> : run_combine<uint16_t, 32>;
         return f((const uint16_t*)dQKVd, (const uint16_t*)Wq_d, (const uint16_t*)Wk_d, (const uint16_t*)Wv_d, slot,
-                 (const uint16_t*)dXs, B, T, d, H, k, Hd, (uint16_t*)dX, accumulate, base, part, mk, stream);
+                 (const uint16_t*)dXs, B, T, d, H, k, Hd, (uint16_t*)dX, accumulate, (uint16_t*)base, part, mk, stream);
     }
     auto f = dh == 64 ? run_combine<float, 64> : run_combine<float, 32>;
     return f((const float*)dQKVd, (const float*)Wq_d, (const float*)Wk_d, (const float*)Wv_d, slot,
-             (const float*)dXs, B, T, d, H, k, Hd, (float*)dX, accumulate, base, part, mk, stream);
+             (const float*)dXs, B, T, d, H, k, Hd, (float*)dX, accumulate, (float*)base, part, mk, stream);
 }
 
 }  // namespace mosa

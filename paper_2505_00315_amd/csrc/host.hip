@@ -94,7 +94,7 @@ Layout make_layout(const mosa_shape* s) {
     L.unc_key = fw.take(B * H * T * 8);
     L.unc_sel = fw.take(B * H * T * 4);
     L.Xo = fw.take(B * H * k * d * es);
-    L.ybase = fw.take(Hd > 0 ? B * T * d * 4 : 0);  // dense heads' part of Y (fp32)
+    L.ybase = fw.take(Hd > 0 ? B * T * d * es : 0);  // dense heads' part of Y
     {  // partial results of the attention's key splits, MoSA and dense heads
        // apart (the two chains may run at the same time)
         const int dt = s->dtype == MOSA_BF16 ? kBF16 : kF32;
@@ -111,7 +111,7 @@ Layout make_layout(const mosa_shape* s) {
     L.dAd = bw.take(B * Hd * T * dh * es);
     L.Dd = bw.take(B * Hd * T * 4);
     L.dQKVd = bw.take(B * Hd * T * 3 * dh * es);
-    L.dxbase = bw.take(Hd > 0 ? B * T * d * 4 : 0);  // dense heads' part of dX (fp32)
+    L.dxbase = bw.take(Hd > 0 ? B * T * d * es : 0);  // dense heads' part of dX
     L.dwr = bw.take(H > 0 && s->fixed_stride > 0 ? H * d * es : 0);  // dW^r sink without a router
     {
         const int dt = s->dtype == MOSA_BF16 ? kBF16 : kF32;
@@ -300,7 +300,7 @@ int forward_impl(const mosa_shape* s, const void* X, const mosa_weights* w, void
                              at<float>(scratch, L.apart_d), 1, sm.marker(), ds);
         if (ax) {
             e |= launch_out_combine(dt, Ad, w->Wo_d, slot, Xo, B, T, d, H, dh, k, Hd, Y, accumulate,
-                                    at<float>(scratch, L.ybase), 1, sm.marker(), ds);
+                                    at<void>(scratch, L.ybase), 1, sm.marker(), ds);
         }
     }
     if (H > 0) {
@@ -331,7 +331,7 @@ int forward_impl(const mosa_shape* s, const void* X, const mosa_weights* w, void
     }
     if (ax) e |= aux_join(ax, stream);
     e |= launch_out_combine(dt, Ad, w->Wo_d, slot, Xo, B, T, d, H, dh, k, Hd, Y, accumulate,
-                            at<float>(scratch, L.ybase), ax ? 2 : 0, sm.marker(), stream);
+                            at<void>(scratch, L.ybase), ax ? 2 : 0, sm.marker(), stream);
     if (H > 0 && I_out)
         e |= hipMemcpyAsync(I_out, I, (size_t)B * H * k * 4, hipMemcpyDeviceToDevice, stream) != hipSuccess;
     if (H > 0 && r_out)
@@ -460,11 +460,11 @@ int mosa_backward_timed(const mosa_shape* s, const void* X, const mosa_weights* 
     if (ax) {
         if (hipStreamWaitEvent(stream, ax->mid, 0) != hipSuccess) e |= 1;
         e |= launch_dx_combine(dt, dQKVd, w->Wq_d, w->Wk_d, w->Wv_d, slot, dXs, B, T, d, H, dh, k, Hd, dX,
-                               accumulate_dX, at<float>(scratch, L.dxbase), 1, mk, stream);
+                               accumulate_dX, at<void>(scratch, L.dxbase), 1, mk, stream);
         e |= aux_join(ax, stream);
     }
     e |= launch_dx_combine(dt, dQKVd, w->Wq_d, w->Wk_d, w->Wv_d, slot, dXs, B, T, d, H, dh, k, Hd, dX, accumulate_dX,
-                           at<float>(scratch, L.dxbase), ax ? 2 : 0, mk, stream);
+                           at<void>(scratch, L.dxbase), ax ? 2 : 0, mk, stream);
     return e ? MOSA_ERR_HIP : MOSA_OK;
 }
 

@@ -74,13 +74,13 @@ int launch_out_proj(int dtype, const void* A, const void* Wo, int B, int d, int 
                     hipStream_t stream);
 
 // Y[b,t,:] (+)= sum_hd Ad[b,hd,t,:] Wo_d[hd] + sum_h (ascending) Xo[b,h,slot[b,h,t],:].
-// base: fp32 [B, T, d] scratch for the dense heads' part (used when Hd > 0).
-// Marks "out_dense" (the dense heads' GEMM, when launched separately) and
+// base: [B, T, d] scratch in the storage type for the dense heads' part (used
+// when Hd > 0).  Marks "out_dense" (the dense heads' GEMM, when launched separately) and
 // "out_combine".  part 1: only the dense heads' GEMM into base, part 2: only
 // the combination (base written before), 0: both; parts 1 and 2 need
 // combine_split_ok(d, H) (else they return 1 and launch nothing).
 int launch_out_combine(int dtype, const void* Ad, const void* Wo_d, const int16_t* slot, const void* Xo,
-                       int B, int T, int d, int H, int dh, int k, int Hd, void* Y, int accumulate, float* base,
+                       int B, int T, int d, int H, int dh, int k, int Hd, void* Y, int accumulate, void* base,
                        int part, const Marker& mk, hipStream_t stream);
 bool combine_split_ok(int d, int H);
 
@@ -133,11 +133,11 @@ int launch_dx_proj(int dtype, const void* dQKV, const float* dz, const void* Wq,
                    hipStream_t stream);
 
 // dX[b,t,:] (+)= dense heads' (dQ Wq^T + dK Wk^T + dV Wv^T) + sum_h (ascending) dXs[b,h,slot,:].
-// base: fp32 [B, T, d] scratch for the dense heads' part (used when Hd > 0).
-// Marks "dx_dense" (when launched separately) and "dx_combine"; part as in
+// base: [B, T, d] scratch in the storage type for the dense heads' part (used
+// when Hd > 0).  Marks "dx_dense" (when launched separately) and "dx_combine"; part as in
 // launch_out_combine.
 int launch_dx_combine(int dtype, const void* dQKVd, const void* Wq_d, const void* Wk_d, const void* Wv_d,
                       const int16_t* slot, const void* dXs, int B, int T, int d, int H, int dh, int k,
-                      int Hd, void* dX, int accumulate, float* base, int part, const Marker& mk, hipStream_t stream);
+                      int Hd, void* dX, int accumulate, void* base, int part, const Marker& mk, hipStream_t stream);
 
 }  // namespace mosa

@@ -141,8 +141,8 @@ struct OutCombinePolicy {
     }
 };
 
-// The dense heads' part alone, kept in fp32 ([B, T, d]) for combine_rows_kernel
-// to start from.
+// The dense heads' part alone ([B, T, d] in the storage type, here fp32) for
+// combine_rows_kernel to start from.
 template <typename ST, int DH>
 struct OutDensePolicy : OutCombinePolicy<ST, DH> {
     using Base = OutCombinePolicy<ST, DH>;
@@ -176,7 +176,7 @@ struct OutDensePolicy2 {
     struct Args {
         const ST* Ad;   // [B, Hd, T, DH]
         const ST* Wod;  // [Hd DH, d]
-        float* base;    // [B, T, d]
+        ST* base;       // [B, T, d], the dense heads' part in the storage type
         int T, d, Hd, mtiles, ntiles;
     };
     struct ARef {
@@ -203,12 +203,13 @@ struct OutDensePolicy2 {
     }
     __device__ static void epilogue(const Args& a, int b, int m0, int n0, const float* Cs, int ldc, int tid,
                                     unsigned char*) {
-        constexpr int VPR = NT / 4;
+        constexpr int VPR = NT / 8;
         for (int v = tid; v < MT * VPR; v += 256) {
-            const int ml = v / VPR, c = (v % VPR) * 4, t = m0 + ml;
+            const int ml = v / VPR, c = (v % VPR) * 8, t = m0 + ml;
             if (t >= a.T || n0 + c >= a.d) continue;
-            *reinterpret_cast<float4*>(a.base + ((size_t)b * a.T + t) * a.d + n0 + c) =
-                *reinterpret_cast<const float4*>(Cs + ml * ldc + c);
+            float x[8];
+            cs_load8(Cs, ldc, ml, c, x);
+            vec8_store<ST>(a.base + ((size_t)b * a.T + t) * a.d + n0 + c, vec8_from_f32<ST>(x));
         }
     }
 };
@@ -267,12 +268,12 @@ int run_proj(const ST* A, const ST* Wo, int B, int d, int H, int k, ST* Xo, hipS
 
 template <typename ST, int DH>
 int run_combine(const ST* Ad, const ST* Wod, const int16_t* slot, const ST* Xo, int B, int T, int d, int H, int k,
-                int Hd, ST* Y, int accumulate, float* base, int part, const Marker& mk, hipStream_t stream) {
+                int Hd, ST* Y, int accumulate, ST* base, int part, const Marker& mk, hipStream_t stream) {
     using P = OutCombinePolicy<ST, DH>;
     typename P::Args a{Ad, Wod, slot, Xo, Y, T, d, H, k, Hd, accumulate, (T + P::MT - 1) / P::MT,
                        (d + P::NT - 1) / P::NT};
     if (combine_rows_fits(d, H) && (Hd == 0 || base)) {
-        // dense heads first (fp32 into base), then the per-token combination
+        // dense heads first (into base), then the per-token combination
         // (part 1: the first only, part 2: the second only, 0: both)
         if (Hd > 0 && part != 2) {
             int e;
@@ -314,16 +315,16 @@ int launch_out_proj(int dtype, const void* A, const void* Wo, int B, int d, int 
 }
 
 int launch_out_combine(int dtype, const void* Ad, const void* Wo_d, const int16_t* slot, const void* Xo, int B,
-                       int T, int d, int H, int dh, int k, int Hd, void* Y, int accumulate, float* base,
+                       int T, int d, int H, int dh, int k, int Hd, void* Y, int accumulate, void* base,
                        int part, const Marker& mk, hipStream_t stream) {
     if (dtype == kBF16) {
         auto f = dh == 64 ? run_combine<uint16_t, 64> : run_combine<uint16_t, 32>;
         return f((const uint16_t*)Ad, (const uint16_t*)Wo_d, slot, (const uint16_t*)Xo, B, T, d, H, k, Hd,
-                 (uint16_t*)Y, accumulate, base, part, mk, stream);
+                 (uint16_t*)Y, accumulate, (uint16_t*)base, part, mk, stream);
     }
     auto f = dh == 64 ? run_combine<float, 64> : run_combine<float, 32>;
     return f((const float*)Ad, (const float*)Wo_d, slot, (const float*)Xo, B, T, d, H, k, Hd, (float*)Y, accumulate,
-             base, part, mk, stream);
+             (float*)base, part, mk, stream);
 }
 
 }  // namespace mosa
