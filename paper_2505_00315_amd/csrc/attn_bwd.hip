@@ -211,6 +211,18 @@ struct BwdTile {
         return (size_t)(sr + TB) * LDR * sizeof(ST);
     }
     static constexpr size_t both_lds(int ob) { return kv_lds(ob) > q_lds(ob) ? kv_lds(ob) : q_lds(ob); }
+    // The 64-row tiles the loop walks are stored without padding, the 16-byte
+    // units of row r XOR-permuted by swz(r), so that the three access patterns
+    // are free of bank conflicts: 16-byte reads of one unit of 16 consecutive
+    // rows (2 or 4 rows share a 256-byte line: swz takes distinct values on the
+    // rows that share a line position), transposed 8-byte reads of two
+    // adjacent units of 8 consecutive rows (swz even and distinct on those, up
+    // to a common low bit, so the unit pairs stay distinct), and 16-byte row
+    // writes.  (The output rows after the loop keep the padded stride LDR.)
+    static constexpr int U = DH / 8, L = 16 / U;
+    __device__ static int swz(int r) { return 2 * ((r / L) % (U / 2)) + ((r >> 3) & 1); }
+    // element offset of (row r, column c) in such a tile
+    __device__ static int off(int r, int c) { return r * DH + ((((c >> 3) ^ swz(r))) << 3) + (c & 7); }
 };
 
 template <typename ST, int DH, bool WIN, int NWV, int CB>
@@ -285,8 +297,8 @@ __device__ __forceinline__ void attn_bwd_kv_tiled_body(unsigned char* smem, int 
 #pragma unroll
         for (int p = 0; p < PER; ++p) {
             const int v = tid + NT * p, r = v / VPR, dc = (v % VPR) * 8;
-            vec8_store<ST>(Qs + r * LDR + dc, qreg[p]);
-            vec8_store<ST>(dAs + r * LDR + dc, areg[p]);
+            vec8_store<ST>(Qs + TL::off(r, dc), qreg[p]);
+            vec8_store<ST>(dAs + TL::off(r, dc), areg[p]);
         }
         if (tid < TB) {
             ls[tid] = lreg;
@@ -311,8 +323,8 @@ __device__ __forceinline__ void attn_bwd_kv_tiled_body(unsigned char* smem, int 
             for (int cb = 0; cb < CB; ++cb) sv[cb] = dp[cb] = zero4();
 #pragma unroll
             for (int st = 0; st < DH / 32; ++st) {
-                const Frag8<ST> qa = frag8_load<ST>(Qs + (sb * 16 + c16) * LDR + st * 32 + 8 * g);
-                const Frag8<ST> aa = frag8_load<ST>(dAs + (sb * 16 + c16) * LDR + st * 32 + 8 * g);
+                const Frag8<ST> qa = frag8_load<ST>(Qs + TL::off(sb * 16 + c16, st * 32 + 8 * g));
+                const Frag8<ST> aa = frag8_load<ST>(dAs + TL::off(sb * 16 + c16, st * 32 + 8 * g));
 #pragma unroll
                 for (int cb = 0; cb < CB; ++cb) {
                     mma8(sv[cb], qa, kf[cb][st]);
@@ -351,10 +363,11 @@ __device__ __forceinline__ void attn_bwd_kv_tiled_body(unsigned char* smem, int 
 #pragma unroll
             for (int db = 0; db < DH / 16; ++db) {
                 const int mcol = 16 * db + 4 * (c16 & 3);
-                const unsigned char* a0 = reinterpret_cast<const unsigned char*>(dAs + r0 * LDR + mcol);
-                const unsigned char* q0p = reinterpret_cast<const unsigned char*>(Qs + r0 * LDR + mcol);
-                const u32x2 alo = lds_read_tr16(a0), ahi = lds_read_tr16(a0 + 32 * LDR);
-                const u32x2 qlo = lds_read_tr16(q0p), qhi = lds_read_tr16(q0p + 32 * LDR);
+                const int o0 = TL::off(r0, mcol), o1 = TL::off(r0 + 16, mcol);
+                const u32x2 alo = lds_read_tr16(reinterpret_cast<const unsigned char*>(dAs + o0));
+                const u32x2 ahi = lds_read_tr16(reinterpret_cast<const unsigned char*>(dAs + o1));
+                const u32x2 qlo = lds_read_tr16(reinterpret_cast<const unsigned char*>(Qs + o0));
+                const u32x2 qhi = lds_read_tr16(reinterpret_cast<const unsigned char*>(Qs + o1));
                 at[db] = u32x4{alo.x, alo.y, ahi.x, ahi.y};
                 qt[db] = u32x4{qlo.x, qlo.y, qhi.x, qhi.y};
             }
@@ -483,8 +496,8 @@ __device__ __forceinline__ void attn_bwd_q_tiled_body(unsigned char* smem, int b
 #pragma unroll
         for (int p = 0; p < PER; ++p) {
             const int v = tid + NT * p, r = v / VPR, dc = (v % VPR) * 8;
-            vec8_store<ST>(Ks + r * LDR + dc, kreg[p]);
-            vec8_store<ST>(Vs + r * LDR + dc, vreg[p]);
+            vec8_store<ST>(Ks + TL::off(r, dc), kreg[p]);
+            vec8_store<ST>(Vs + TL::off(r, dc), vreg[p]);
         }
     };
 
@@ -505,8 +518,8 @@ __device__ __forceinline__ void attn_bwd_q_tiled_body(unsigned char* smem, int b
             for (int cb = 0; cb < CB; ++cb) sv[cb] = dp[cb] = zero4();
 #pragma unroll
             for (int st = 0; st < DH / 32; ++st) {
-                const Frag8<ST> kk = frag8_load<ST>(Ks + (sb * 16 + c16) * LDR + st * 32 + 8 * g);
-                const Frag8<ST> vv = frag8_load<ST>(Vs + (sb * 16 + c16) * LDR + st * 32 + 8 * g);
+                const Frag8<ST> kk = frag8_load<ST>(Ks + TL::off(sb * 16 + c16, st * 32 + 8 * g));
+                const Frag8<ST> vv = frag8_load<ST>(Vs + TL::off(sb * 16 + c16, st * 32 + 8 * g));
 #pragma unroll
                 for (int cb = 0; cb < CB; ++cb) {
                     mma8(sv[cb], kk, qf[cb][st]);
@@ -539,9 +552,9 @@ __device__ __forceinline__ void attn_bwd_q_tiled_body(unsigned char* smem, int b
             u32x4 kt[DH / 16];
 #pragma unroll
             for (int db = 0; db < DH / 16; ++db) {
-                const unsigned char* k0p =
-                    reinterpret_cast<const unsigned char*>(Ks + r0 * LDR + 16 * db + 4 * (c16 & 3));
-                const u32x2 lo = lds_read_tr16(k0p), hi = lds_read_tr16(k0p + 32 * LDR);
+                const int mcol = 16 * db + 4 * (c16 & 3);
+                const u32x2 lo = lds_read_tr16(reinterpret_cast<const unsigned char*>(Ks + TL::off(r0, mcol)));
+                const u32x2 hi = lds_read_tr16(reinterpret_cast<const unsigned char*>(Ks + TL::off(r0 + 16, mcol)));
                 kt[db] = u32x4{lo.x, lo.y, hi.x, hi.y};
             }
             lds_wait();
