@@ -72,9 +72,10 @@ struct RowGemmShape {
     static constexpr int WAIT = (STG - 2) * (IA + IZ + NS) + NS;
     static_assert(K % 32 == 0 && (64 * K / 8) % 256 == 0 && (K * NC / 8) % 256 == 0, "K");
     static_assert(STG >= 2 && WAIT <= 63, "vmcnt range");
-    static constexpr size_t lds_bytes() {
-        return (size_t)STG * STAGE_BYTES > (size_t)W_BYTES ? (size_t)STG * STAGE_BYTES : (size_t)W_BYTES;
-    }
+    // LDS: the ring of STG tile buffers, then (m-contiguous W) the W block,
+    // apart so that the first tiles' loads are in flight while W is staged
+    static constexpr int W_OFF = STG * STAGE_BYTES;
+    static constexpr size_t lds_bytes() { return (size_t)STG * STAGE_BYTES + W_BYTES; }
 };
 
 // One workgroup's run of row tiles, logical index `logical`.
@@ -91,56 +92,6 @@ __device__ __forceinline__ void rowgemm_body(const typename P::Args& args, int l
     const int nsteps = s_end - s_beg, M = P::rows(args);
     const int wcol = n0 + 32 * S::NPAIR * wave;            // this wave's columns
     const int icol = 8 * (c16 >> 2) + (c16 & 3);           // column of MFMA row c16 in a block pair
-
-    // W fragments: wf[nb][ks] for 16-column block nb (pair nb / 2, half nb % 2)
-    // and k = 32 ks + 8 g .. + 7, MFMA row c16.
-    bf16x8 wf[NB][KS];
-    if constexpr (P::W_KCONTIG) {
-#pragma unroll
-        for (int nb = 0; nb < NB; ++nb)
-#pragma unroll
-            for (int ks = 0; ks < KS; ++ks)
-                wf[nb][ks] = __builtin_bit_cast(
-                    bf16x8, *reinterpret_cast<const uint4*>(
-                                P::w_kptr(args, h, wcol + 32 * (nb >> 1) + 4 * (nb & 1) + icol, 32 * ks + 8 * g)));
-    } else {
-        // W[0:K][n0:n0+NC] row-major in LDS, then the fragments from there.
-        ST* wl = reinterpret_cast<ST*>(smem);
-        constexpr int UPR = NC / 8;  // 16-byte units per W row
-#pragma unroll
-        for (int i = 0; i < K * UPR / 256; ++i) {
-            const int u = tid + 256 * i, k = u / UPR, c8 = (u % UPR) * 8;
-            *reinterpret_cast<uint4*>(wl + k * NC + c8) = *reinterpret_cast<const uint4*>(P::w_mptr(args, h, k, n0 + c8));
-        }
-        __syncthreads();
-#pragma unroll
-        for (int nb = 0; nb < NB; ++nb)
-#pragma unroll
-            for (int ks = 0; ks < KS; ++ks) {
-                const int col = 32 * S::NPAIR * wave + 32 * (nb >> 1) + 4 * (nb & 1) + icol;
-                uint16_t e[8];
-#pragma unroll
-                for (int j = 0; j < 8; ++j) e[j] = wl[(32 * ks + 8 * g + j) * NC + col];
-                const uint4 u = make_uint4(e[0] | ((uint32_t)e[1] << 16), e[2] | ((uint32_t)e[3] << 16),
-                                           e[4] | ((uint32_t)e[5] << 16), e[6] | ((uint32_t)e[7] << 16));
-                wf[nb][ks] = __builtin_bit_cast(bf16x8, u);
-            }
-        __syncthreads();  // the ring below reuses this LDS
-    }
-    float cv[S::NPAIR][8];
-#pragma unroll
-    for (int p = 0; p < S::NPAIR; ++p) P::col_init(args, h, wcol + 32 * p + 8 * g, cv[p]);
-    const __amdgpu_buffer_rsrc_t out = P::out_rsrc(args, h);
-    // Take the weights now: a first use inside the pipeline would make the
-    // compiler wait for every load in flight there.
-#pragma unroll
-    for (int nb = 0; nb < NB; ++nb)
-#pragma unroll
-        for (int ks = 0; ks < KS; ++ks) asm volatile("" : "+v"(wf[nb][ks]));
-#pragma unroll
-    for (int p = 0; p < S::NPAIR; ++p)
-#pragma unroll
-        for (int j = 0; j < 8; ++j) asm volatile("" : "+v"(cv[p][j]));
 
     // This lane's slot in each A load: row r of the tile, 16-byte unit.
     int arow[S::IA], acol[S::IA];
@@ -164,6 +115,63 @@ __device__ __forceinline__ void rowgemm_body(const typename P::Args& args, int l
         if constexpr (P::ROW_SCALAR)
             lds_load4(P::z_ptr(args, h, min(m0 + lane, M - 1)), lds_base + bidx * S::STAGE_BYTES + S::A_BYTES + 256 * wave_s);
     };
+    // The first STG - 1 tiles are requested before the weights, so that the
+    // two latencies overlap (the weights' own waits then also cover these
+    // loads: vector memory operations complete in issue order).
+    if (nsteps > 0) {
+#pragma unroll
+        for (int s = 0; s < STG - 1; ++s) issue(s, s);
+    }
+    // W fragments: wf[nb][ks] for 16-column block nb (pair nb / 2, half nb % 2)
+    // and k = 32 ks + 8 g .. + 7, MFMA row c16.
+    bf16x8 wf[NB][KS];
+    if constexpr (P::W_KCONTIG) {
+#pragma unroll
+        for (int nb = 0; nb < NB; ++nb)
+#pragma unroll
+            for (int ks = 0; ks < KS; ++ks)
+                wf[nb][ks] = __builtin_bit_cast(
+                    bf16x8, *reinterpret_cast<const uint4*>(
+                                P::w_kptr(args, h, wcol + 32 * (nb >> 1) + 4 * (nb & 1) + icol, 32 * ks + 8 * g)));
+    } else {
+        // W[0:K][n0:n0+NC] row-major in LDS (after the ring), then the fragments from there.
+        ST* wl = reinterpret_cast<ST*>(smem + S::W_OFF);
+        constexpr int UPR = NC / 8;  // 16-byte units per W row
+#pragma unroll
+        for (int i = 0; i < K * UPR / 256; ++i) {
+            const int u = tid + 256 * i, k = u / UPR, c8 = (u % UPR) * 8;
+            *reinterpret_cast<uint4*>(wl + k * NC + c8) = *reinterpret_cast<const uint4*>(P::w_mptr(args, h, k, n0 + c8));
+        }
+        __syncthreads();
+#pragma unroll
+        for (int nb = 0; nb < NB; ++nb)
+#pragma unroll
+            for (int ks = 0; ks < KS; ++ks) {
+                const int col = 32 * S::NPAIR * wave + 32 * (nb >> 1) + 4 * (nb & 1) + icol;
+                uint16_t e[8];
+#pragma unroll
+                for (int j = 0; j < 8; ++j) e[j] = wl[(32 * ks + 8 * g + j) * NC + col];
+                const uint4 u = make_uint4(e[0] | ((uint32_t)e[1] << 16), e[2] | ((uint32_t)e[3] << 16),
+                                           e[4] | ((uint32_t)e[5] << 16), e[6] | ((uint32_t)e[7] << 16));
+                wf[nb][ks] = __builtin_bit_cast(bf16x8, u);
+            }
+        __syncthreads();
+    }
+    float cv[S::NPAIR][8];
+#pragma unroll
+    for (int p = 0; p < S::NPAIR; ++p) P::col_init(args, h, wcol + 32 * p + 8 * g, cv[p]);
+    const __amdgpu_buffer_rsrc_t out = P::out_rsrc(args, h);
+    // Take the weights now: a first use inside the pipeline would make the
+    // compiler wait for every load in flight there.
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb)
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) asm volatile("" : "+v"(wf[nb][ks]));
+#pragma unroll
+    for (int p = 0; p < S::NPAIR; ++p)
+#pragma unroll
+        for (int j = 0; j < 8; ++j) asm volatile("" : "+v"(cv[p][j]));
+
 
     auto tile_step = [&](int s, int bidx) {
         const unsigned char* ta = smem + bidx * S::STAGE_BYTES;
@@ -236,8 +244,6 @@ __device__ __forceinline__ void rowgemm_body(const typename P::Args& args, int l
         return false;
     };
     if (nsteps > 0) {
-#pragma unroll
-        for (int s = 0; s < STG - 1; ++s) issue(s, s);
         if (!pass(0, std::true_type{}))
             for (int s0 = STG;; s0 += STG)
                 if (pass(s0, std::false_type{})) break;
