@@ -454,12 +454,15 @@ __device__ void bh_job_w3(const BhArgs& a, int h, int t0, int t1, unsigned char*
     wait_vmcnt<0>();
 }
 
-// Workgroup j: job j % 3 (W1, W2, W3 alternate, so every CU gets a mix),
-// head and tile range from j / 3.
+// Workgroups in three equal ranges: W1, then W2, then W3 (head and tile
+// range from the position in the range).  The dX rows come last so that they
+// are the freshest in the memory-side cache when the head-ordered sum reads
+// them back (hybrid_d1024: 86 -> 80 us here and 28 -> 22 us for that sum,
+// against the three jobs interleaved).
 template <int NR>
 __global__ __launch_bounds__(256) void bwd_head_kernel(const BhArgs a) {
     extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
-    const int j = blockIdx.x, job = j % 3, u = j / 3;
+    const int nu = gridDim.x / 3, j = blockIdx.x, job = j / nu, u = j % nu;
     const int h = u / a.nsplit, sp = u % a.nsplit;
     const int ntiles = a.d / 64, t0 = sp * a.tpw, t1 = min(ntiles, t0 + a.tpw);
     if (job == 0) bh_job_w1<NR>(a, h, t0, t1, smem);
