@@ -855,12 +855,154 @@ __global__ __launch_bounds__(512) void attn_bwd_lds_kernel(const uint16_t* __res
     }
 }
 
+// bf16, at most 16 rows per (b, h) (one 16-row block): both passes in one
+// wave per (b, h), no loop.  The wave loads the rows of Q, K, V and dA as
+// MFMA fragments (lane: row c16, 8 consecutive head columns), computes S and
+// dP (lane: query 4g + i, key c16), P and dS (rounded to bf16 as MFMA
+// operands, as in the other kernels), and keeps Q, K, dA and dS ([query][key])
+// in its own LDS region, from which the transposed operands of
+// dV^T += dA^T P, dK^T += Q^T dS and dQ^T += K^T dS^T are read (16 rows per
+// MFMA).  A lane ends with 4 consecutive head columns of one row of dQ, dK
+// and dV, stored 8 bytes at a time.  No value is accumulated by more than one
+// lane: reproducible.
+template <int DH>
+__global__ __launch_bounds__(256) void attn_bwd_small_kernel(const uint16_t* __restrict__ QKV,
+                                                             const uint16_t* __restrict__ dA,
+                                                             const float* __restrict__ lse,
+                                                             const float* __restrict__ D, int BH, int n, int causal,
+                                                             float scale, uint16_t* __restrict__ dQKV,
+                                                             const int32_t* __restrict__ rI,
+                                                             const float2* __restrict__ rtab) {
+    using ST = uint16_t;
+    using TL = BwdTile<ST, DH>;  // 16-byte units of a row XOR-permuted (conflict-free transposed reads)
+    constexpr int RS = 3 * DH, NS = DH / 32, NDB = DH / 16, TILE = 16 * DH;
+    __shared__ __attribute__((aligned(16))) ST lds[4][3 * TILE + 16 * 16];
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int g = lane >> 4, c16 = lane & 15;
+    const int bh = blockIdx.x * 4 + wave;
+    if (bh >= BH) return;
+    ST* Qs = lds[wave];
+    ST* Ks = Qs + TILE;
+    ST* As = Ks + TILE;
+    ST* dSs = As + TILE;
+    const size_t base = (size_t)bh * n;
+    const ST* Qp = QKV + base * RS;
+    const ST* dAp = dA + base * DH;
+    const bool rv = c16 < n;  // this lane's row (fragment row c16) exists
+
+    Frag8<ST> qf[NS], kf[NS], vf[NS], af[NS];
+#pragma unroll
+    for (int st = 0; st < NS; ++st) {
+        const size_t o = (size_t)c16 * RS + st * 32 + 8 * g;
+        qf[st] = rv ? frag8_load<ST>(Qp + o) : frag8_zero<ST>();
+        kf[st] = rv ? frag8_load<ST>(Qp + DH + o) : frag8_zero<ST>();
+        vf[st] = rv ? frag8_load<ST>(Qp + 2 * DH + o) : frag8_zero<ST>();
+        af[st] = rv ? frag8_load<ST>(dAp + (size_t)c16 * DH + st * 32 + 8 * g) : frag8_zero<ST>();
+    }
+    float l[4], dd[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        const int q = 4 * g + i;
+        l[i] = q < n ? lse[base + q] : 0.f;
+        dd[i] = q < n ? D[base + q] : 0.f;
+    }
+    // Q, K, dA rows into the wave's tiles (rows past n hold zeros)
+#pragma unroll
+    for (int st = 0; st < NS; ++st) {
+        const int o = TL::off(c16, st * 32 + 8 * g);
+        *reinterpret_cast<uint4*>(Qs + o) = __builtin_bit_cast(uint4, qf[st].v);
+        *reinterpret_cast<uint4*>(Ks + o) = __builtin_bit_cast(uint4, kf[st].v);
+        *reinterpret_cast<uint4*>(As + o) = __builtin_bit_cast(uint4, af[st].v);
+    }
+
+    f32x4 sv = zero4(), dp = zero4();
+#pragma unroll
+    for (int st = 0; st < NS; ++st) {
+        mma8(sv, qf[st], kf[st]);
+        mma8(dp, af[st], vf[st]);
+    }
+    // lane: key c16, queries 4g + i
+    float p[4], ds[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        const int q = 4 * g + i;
+        const bool ok = q < n && rv && (!causal || c16 <= q);
+        p[i] = ok ? expf(sv[i] * scale - l[i]) : 0.f;
+        ds[i] = p[i] * (dp[i] - dd[i]);
+    }
+    const Frag4<ST> pf = frag4_from<ST>(p), dsf = frag4_from<ST>(ds);
+    // dS as rounded for the MFMAs, [query][key], for its transposed use in dQ
+    {
+        const uint2 w = __builtin_bit_cast(uint2, dsf.v);
+        dSs[(4 * g + 0) * 16 + c16] = (ST)(w.x & 0xffffu);
+        dSs[(4 * g + 1) * 16 + c16] = (ST)(w.x >> 16);
+        dSs[(4 * g + 2) * 16 + c16] = (ST)(w.y & 0xffffu);
+        dSs[(4 * g + 3) * 16 + c16] = (ST)(w.y >> 16);
+    }
+    // B operand of dQ^T: dS[query c16][keys 4g .. 4g + 3] (the wave's own LDS
+    // writes above complete before this read)
+    Frag4<ST> dstf;
+    dstf.v = __builtin_bit_cast(s16x4, *reinterpret_cast<const uint2*>(dSs + c16 * 16 + 4 * g));
+
+    f32x4 dVt[NDB], dKt[NDB], dQt[NDB];
+    // transposed reads: source lane supplies row 4g + c16 / 4, 4 columns from
+    // 16 db + 4 (c16 % 4); lane receives rows 4g .. 4g + 3 of column 16 db + c16
+    const int rr = 4 * g + (c16 >> 2);
+#pragma unroll
+    for (int db = 0; db < NDB; ++db) {
+        const int o = TL::off(rr, 16 * db + 4 * (c16 & 3));
+        u32x2 at = lds_read_tr16(reinterpret_cast<const unsigned char*>(As + o));
+        u32x2 qt = lds_read_tr16(reinterpret_cast<const unsigned char*>(Qs + o));
+        u32x2 kt = lds_read_tr16(reinterpret_cast<const unsigned char*>(Ks + o));
+        lds_wait();
+        // the values exist only after the wait: tie their uses to it
+        asm volatile("" : "+v"(at), "+v"(qt), "+v"(kt));
+        Frag4<ST> fa, fq, fk;
+        fa.v = __builtin_bit_cast(s16x4, at);
+        fq.v = __builtin_bit_cast(s16x4, qt);
+        fk.v = __builtin_bit_cast(s16x4, kt);
+        dVt[db] = dKt[db] = dQt[db] = zero4();
+        mma4(dVt[db], fa, pf);
+        mma4(dKt[db], fq, dsf);
+        mma4(dQt[db], fk, dstf);
+    }
+    mfma_drain();
+    if (rv) {
+        // lane: row c16 (key for dK, dV; query for dQ), head columns 16 db + 4g .. + 3
+        const int pos = rtab ? (rI ? rI[base + c16] : c16) : 0;
+        ST* out = dQKV + (base + c16) * RS;
+#pragma unroll
+        for (int db = 0; db < NDB; ++db) {
+            const int d0 = 16 * db + 4 * g;
+            float xq[4] = {dQt[db][0] * scale, dQt[db][1] * scale, dQt[db][2] * scale, dQt[db][3] * scale};
+            float xk[4] = {dKt[db][0] * scale, dKt[db][1] * scale, dKt[db][2] * scale, dKt[db][3] * scale};
+            if (rtab) {  // back through the rotation
+                rope4_back<DH>(xq, d0, rtab, pos);
+                rope4_back<DH>(xk, d0, rtab, pos);
+            }
+            *reinterpret_cast<uint2*>(out + d0) = make_uint2(pack_bf16x2(xq[0], xq[1]), pack_bf16x2(xq[2], xq[3]));
+            *reinterpret_cast<uint2*>(out + DH + d0) =
+                make_uint2(pack_bf16x2(xk[0], xk[1]), pack_bf16x2(xk[2], xk[3]));
+            *reinterpret_cast<uint2*>(out + 2 * DH + d0) =
+                make_uint2(pack_bf16x2(dVt[db][0], dVt[db][1]), pack_bf16x2(dVt[db][2], dVt[db][3]));
+        }
+    }
+}
+
 template <typename ST>
 int launch_t(const ST* QKV, const ST* dA, const float* lse, const float* D, int BH, int n, int dh, int causal,
              int window, ST* dQKV, const int32_t* rI, const float2* rtab, int pass, hipStream_t stream) {
     const float scale = 1.0f / sqrtf((float)dh);
     const int lb = window > 0 ? window - 1 : n;  // keys a query may look back
     if constexpr (sizeof(ST) == 2) {
+      if (n <= 16 && window == 0 && (dh == 64 || dh == 32)) {
+        // both passes in one launch: the call for the dQ pass has nothing left to do
+        if (pass == 1 || BH == 0) return 0;
+        auto kern = dh == 64 ? attn_bwd_small_kernel<64> : attn_bwd_small_kernel<32>;
+        hipLaunchKernelGGL(kern, dim3((BH + 3) / 4), dim3(256), 0, stream, QKV, dA, lse, D, BH, n, causal, scale,
+                           dQKV, rI, rtab);
+        return hipGetLastError() == hipSuccess ? 0 : -1;
+      }
       if (n > 32 && n <= kAttnBwdLdsMaxN && window == 0) {
         // both passes in one launch: the call for the dQ pass has nothing left to do
         if (pass == 1) return 0;
@@ -918,11 +1060,12 @@ int launch_t(const ST* QKV, const ST* dA, const float* lse, const float* D, int 
 
 }  // namespace
 
-// One launch for both passes where a kernel does both (bf16: the LDS kernel
-// for 32 < n <= its limit, the tiled kernels otherwise), else the two passes.
+// One launch for both passes where a kernel does both (bf16: the one-wave
+// kernel for n <= 16, the LDS kernel for 32 < n <= its limit, the tiled
+// kernels otherwise), else the two passes.
 template <typename ST>
 bool both_in_one(int n, int window) {
-    if constexpr (sizeof(ST) == 2) return n > 32 || window > 0;
+    if constexpr (sizeof(ST) == 2) return n > 32 || window > 0 || n <= 16;
     return false;
 }
 
