@@ -615,17 +615,24 @@ __global__ __launch_bounds__(64 * NWV) void attn_bwd_q_tiled_kernel(MOSA_BWD_TIL
     __shared__ __attribute__((aligned(16))) unsigned char smem[BwdTile<ST, DH>::q_lds(16 * CB * NWV)];
     attn_bwd_q_tiled_body<ST, DH, WIN, NWV, CB>(smem, blockIdx.x, MOSA_BWD_TILED_ARGS);
 }
-// Both passes in one launch (they are independent): even blocks take the dK,
-// dV pass, odd blocks the dQ pass, each in its longest-first order, so the
-// short blocks of one pass fill the CUs beside the long blocks of the other.
+// Both passes in one launch (they are independent): blocks of even rank take
+// the dK, dV pass, odd ranks the dQ pass, each in its longest-first order, so
+// the short blocks of one pass fill the CUs beside the long blocks of the
+// other.  Ranks go to workgroups in rounds of one per CU (the dispatcher
+// hands workgroup b and b + 256 to the same CU), every second round in reverse,
+// so that the blocks a CU receives add up to about the same number of tiles
+// (causal, hybrid_d1024: 32 per CU instead of 24 to 40; 54 -> 48 us).
 // (register budget for 3 waves per SIMD: more of the MoSA heads' waves fit
 // beside it in the hybrid layer's backward, 0.435 -> 0.431 ms per step)
 template <typename ST, int DH, bool WIN, int NWV, int CB>
 __global__ __launch_bounds__(64 * NWV, 3) void attn_bwd_tiled_both_kernel(MOSA_BWD_TILED_PARAMS) {
     // one LDS buffer for whichever pass the block runs
     __shared__ __attribute__((aligned(16))) unsigned char smem[BwdTile<ST, DH>::both_lds(16 * CB * NWV)];
-    if (blockIdx.x & 1) attn_bwd_q_tiled_body<ST, DH, WIN, NWV, CB>(smem, blockIdx.x >> 1, MOSA_BWD_TILED_ARGS);
-    else attn_bwd_kv_tiled_body<ST, DH, WIN, NWV, CB>(smem, blockIdx.x >> 1, MOSA_BWD_TILED_ARGS);
+    constexpr int kRound = 256;
+    const int b = blockIdx.x, m = b / kRound;
+    const int s = ((m & 1) && (m + 1) * kRound <= (int)gridDim.x) ? m * kRound + (kRound - 1 - b % kRound) : b;
+    if (s & 1) attn_bwd_q_tiled_body<ST, DH, WIN, NWV, CB>(smem, s >> 1, MOSA_BWD_TILED_ARGS);
+    else attn_bwd_kv_tiled_body<ST, DH, WIN, NWV, CB>(smem, s >> 1, MOSA_BWD_TILED_ARGS);
 }
 #undef MOSA_BWD_TILED_PARAMS
 #undef MOSA_BWD_TILED_ARGS
