@@ -307,8 +307,14 @@ __device__ __forceinline__ void attn_bwd_kv_tiled_body(unsigned char* smem, int 
     };
 
     load_tile(it0 * TB);
+    const int kmax = wk0 + 16 * CB - 1;  // this wave's last key
     for (int it = it0; it < it_end; ++it) {
         const int i0 = it * TB;
+        // every (query, key) pair of the tile and this wave is allowed: all
+        // rows exist and, causal, the first query follows the wave's last key
+        // (within the window)
+        const bool full = i0 + TB <= n && kmax < n &&
+                          (!causal || (i0 >= kmax && (!WIN || i0 + TB - 1 - wk0 <= lb)));
         __syncthreads();
         store_tile();
         __syncthreads();
@@ -331,15 +337,21 @@ __device__ __forceinline__ void attn_bwd_kv_tiled_body(unsigned char* smem, int 
                     mma8(dp[cb], aa, vf[cb][st]);
                 }
             }
+            // no per-element mask where the whole tile is allowed for this wave
+            auto scores = [&](auto all_allowed) {
 #pragma unroll
-            for (int cb = 0; cb < CB; ++cb)
+                for (int cb = 0; cb < CB; ++cb)
 #pragma unroll
-                for (int i = 0; i < 4; ++i) {
-                    const int ql = sb * 16 + 4 * g + i, q = i0 + ql, kk = key[cb];
-                    const bool ok = q < n && kk < n && (!causal || (kk <= q && (!WIN || q - kk <= lb)));
-                    p[cb][sb][i] = ok ? __builtin_amdgcn_exp2f(fmaf(sv[cb][i], c2, -ls[ql])) : 0.f;
-                    ds[cb][sb][i] = p[cb][sb][i] * (dp[cb][i] - Dsh[ql]);
-                }
+                    for (int i = 0; i < 4; ++i) {
+                        const int ql = sb * 16 + 4 * g + i, q = i0 + ql, kk = key[cb];
+                        const bool ok = decltype(all_allowed)::value ||
+                                        (q < n && kk < n && (!causal || (kk <= q && (!WIN || q - kk <= lb))));
+                        p[cb][sb][i] = ok ? __builtin_amdgcn_exp2f(fmaf(sv[cb][i], c2, -ls[ql])) : 0.f;
+                        ds[cb][sb][i] = p[cb][sb][i] * (dp[cb][i] - Dsh[ql]);
+                    }
+            };
+            if (full) scores(std::true_type{});
+            else scores(std::false_type{});
         }
         // dV^T += dA^T P and dK^T += Q^T dS over 32 queries per MFMA
 #pragma unroll
@@ -502,8 +514,14 @@ __device__ __forceinline__ void attn_bwd_q_tiled_body(unsigned char* smem, int b
     };
 
     load_tile(t0 * TB);
+    const int qmax = wq0 + 16 * CB - 1;  // this wave's last query
     for (int t = t0; t < ntiles; ++t) {
         const int j0 = t * TB;
+        // every (query, key) pair of the tile and this wave is allowed: all
+        // rows exist and, causal, the tile's last key precedes the wave's
+        // first query (the last query within the window of the first key)
+        const bool full = j0 + TB <= n && qmax < n &&
+                          (!causal || (j0 + TB - 1 <= wq0 && (!WIN || qmax - j0 <= lb)));
         __syncthreads();
         store_tile();
         __syncthreads();
@@ -526,15 +544,21 @@ __device__ __forceinline__ void attn_bwd_q_tiled_body(unsigned char* smem, int b
                     mma8(dp[cb], vv, af[cb][st]);
                 }
             }
+            // no per-element mask where the whole tile is allowed for this wave
+            auto scores = [&](auto all_allowed) {
 #pragma unroll
-            for (int cb = 0; cb < CB; ++cb)
+                for (int cb = 0; cb < CB; ++cb)
 #pragma unroll
-                for (int i = 0; i < 4; ++i) {
-                    const int j = j0 + sb * 16 + 4 * g + i, qq = q[cb];
-                    const bool ok = j < n && qq < n && (!causal || (j <= qq && (!WIN || qq - j <= lb)));
-                    const float pp = ok ? __builtin_amdgcn_exp2f(fmaf(sv[cb][i], c2, -lq[cb])) : 0.f;
-                    ds[cb][sb][i] = pp * (dp[cb][i] - dq[cb]);
-                }
+                    for (int i = 0; i < 4; ++i) {
+                        const int j = j0 + sb * 16 + 4 * g + i, qq = q[cb];
+                        const bool ok = decltype(all_allowed)::value ||
+                                        (j < n && qq < n && (!causal || (j <= qq && (!WIN || qq - j <= lb))));
+                        const float pp = ok ? __builtin_amdgcn_exp2f(fmaf(sv[cb][i], c2, -lq[cb])) : 0.f;
+                        ds[cb][sb][i] = pp * (dp[cb][i] - dq[cb]);
+                    }
+            };
+            if (full) scores(std::true_type{});
+            else scores(std::false_type{});
         }
         // dQ^T += K^T dS^T over 32 keys per MFMA
 #pragma unroll
