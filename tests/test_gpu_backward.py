@@ -57,6 +57,7 @@ def test_tiny_f32_workload(orc):
     # at most 16 rows per head: the one-wave attention backward (a full block
     # of 64-wide heads, a ragged non-causal block, dense heads of 16 tokens)
     dict(batch=2, seq_len=64, heads=3, k=16, d_head=64, d_model=128),
+    dict(batch=2, seq_len=96, heads=2, k=16, d_head=64, d_model=128, rope=True, first_token=True),
     dict(seq_len=80, k=13, causal=False),
     dict(batch=2, seq_len=16, heads=0, dense_heads=2, d_head=64, d_model=128),
     dict(seq_len=70, k=70),
