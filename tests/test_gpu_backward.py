@@ -28,7 +28,10 @@ def run_fwd_bwd(w, inp, accumulate_dX=False, dX0=None):
     return Y, dX, grads, saved
 
 
-def check_backward(orc, w, inp=None):
+def check_backward(orc, w, inp=None, row_bar_mosa_weights=True):
+    """row_bar_mosa_weights=False: the MoSA heads' weight gradients are held to
+    the per-tensor bar only (for a handful of selected rows per head, see
+    test_gpu_random_shapes.py)."""
     print(f"\n[case] {w}", flush=True)
     inp = wl.make_inputs(w, with_grad=True) if inp is None else inp
     Y, dX, grads, saved = run_fwd_bwd(w, inp)
@@ -38,7 +41,9 @@ def check_backward(orc, w, inp=None):
     errs = {n: rel_err(v, ref[n]) for n, v in got.items()}
     rows = {n: row_rel_err(v, ref[n]) for n, v in got.items()}
     print("[case] rel err " + " ".join(f"{n}={e:.2e}/{rows[n]:.2e}" for n, e in errs.items()), flush=True)
-    bad = {n: (e, rows[n]) for n, e in errs.items() if not (e <= TOL[w.dtype] and rows[n] <= ROW_TOL[w.dtype])}
+    mosa_w = {"dWq", "dWk", "dWv", "dWr", "dWo"}
+    bad = {n: (e, rows[n]) for n, e in errs.items()
+           if not (e <= TOL[w.dtype] and (rows[n] <= ROW_TOL[w.dtype] or (not row_bar_mosa_weights and n in mosa_w)))}
     assert not bad, bad
     return Y, saved, errs
 

@@ -1,0 +1,65 @@
+"""GPU parity on randomly drawn small layers: batch, length, width, head counts
+and sizes, k, causality, local windows, rotary encoding, a forced first token
+and fixed sparse attention drawn from a fixed-seed generator (the same cases
+every run), each checked forward (I bit-exact, r and Y within the bar) and
+backward (dX and every weight gradient) against the oracle.  The draws cover
+combinations the hand-written cases do not pair up, and every launch path the
+shapes select (one-wave, LDS and tiled attention backward, fused or tiled
+forward attention, the per-head and grouped weight-gradient kernels).
+
+With very few selected rows per head (B k < 8) the MoSA heads' weight
+gradients are held to the per-tensor bar only: under causal masking the first
+selected row of every (b, h) attends only to itself, so its dS is zero in exact
+arithmetic and pure rounding residue (dP - D from the bf16 values of dA and A)
+on the GPU; with two or three rows per head that residue is a large share of
+some rows of dW^Q and dW^K.  A CPU emulation of only those bf16 roundings on
+the drawn B = 2, k = 2 case gives a worst-row error of 0.18 against the
+oracle (per tensor 0.005), more than the GPU's 0.09."""
+import numpy as np
+import pytest
+
+import workloads as wl
+from test_gpu_backward import check_backward
+from test_gpu_forward import check_forward
+
+pytestmark = pytest.mark.gpu
+
+N_CASES = 24
+
+
+def _draw(rng, i):
+    dtype = "f32" if rng.random() < 0.2 else "bf16"
+    d_head = int(rng.choice([32, 64]))
+    d_model = int(rng.choice([64, 128, 192]))
+    T = int(rng.integers(8, 321))
+    heads = int(rng.integers(0, 6))
+    dense = int(rng.integers(0, 3))
+    if heads + dense == 0:
+        heads = 1
+    # k: mostly small (the one-wave and fused kernels), sometimes up to T
+    k = int(min(T, rng.choice([rng.integers(1, 17), rng.integers(17, 129), rng.integers(1, T + 1)])))
+    causal = bool(rng.random() < 0.8)
+    v = {}
+    if rng.random() < 0.3:
+        v["rope"] = True
+        v["rope_base"] = float(rng.choice([50.0, 10000.0]))
+    if heads and rng.random() < 0.15 and k > 1 and (T - 1) // (k - 1) >= 1:
+        v["fixed_stride"] = int(rng.integers(1, (T - 1) // (k - 1) + 1))
+    elif heads and rng.random() < 0.2:
+        v["first_token"] = True
+    if dense and causal and rng.random() < 0.3:
+        v["window"] = int(rng.integers(1, T + 1))
+    return wl.small(name=f"random{i}", batch=int(rng.integers(1, 4)), seq_len=T, d_model=d_model, heads=heads,
+                    d_head=d_head, k=k if heads else 1, dense_heads=dense, causal=causal, dtype=dtype,
+                    seed=1000 + i, **v)
+
+
+_RNG = np.random.default_rng(2505)
+CASES = [_draw(_RNG, i) for i in range(N_CASES)]
+
+
+@pytest.mark.parametrize("w", CASES, ids=[c.name for c in CASES])
+def test_random_shape(orc, w):
+    inp = wl.make_inputs(w, with_grad=True)
+    check_forward(orc, w, inp)
+    check_backward(orc, w, inp, row_bar_mosa_weights=w.batch * w.k >= 8)
