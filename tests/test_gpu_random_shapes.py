@@ -54,8 +54,29 @@ def _draw(rng, i):
                     seed=1000 + i, **v)
 
 
+def _draw_medium(rng, i):
+    """Longer sequences and wider layers: the tiled attention passes (k > 128),
+    the LDS attention kernels (32 < k <= 128) and the grouped weight-gradient
+    launch, in random combinations."""
+    T = int(rng.integers(300, 1101))
+    heads = int(rng.integers(1, 17))
+    dense = int(rng.integers(0, 3))
+    k = int(min(T, rng.choice([rng.integers(16, 65), rng.integers(65, 129), rng.integers(129, 301)])))
+    causal = bool(rng.random() < 0.8)
+    v = {}
+    if rng.random() < 0.3:
+        v["rope"] = True
+    if rng.random() < 0.2:
+        v["first_token"] = True
+    if dense and causal and rng.random() < 0.3:
+        v["window"] = int(rng.integers(16, T + 1))
+    return wl.small(name=f"medium{i}", batch=int(rng.integers(1, 3)), seq_len=T, d_model=int(rng.choice([256, 512])),
+                    heads=heads, d_head=int(rng.choice([32, 64])), k=k, dense_heads=dense, causal=causal,
+                    dtype="bf16", seed=2000 + i, **v)
+
+
 _RNG = np.random.default_rng(2505)
-CASES = [_draw(_RNG, i) for i in range(N_CASES)]
+CASES = [_draw(_RNG, i) for i in range(N_CASES)] + [_draw_medium(_RNG, i) for i in range(8)]
 
 
 @pytest.mark.parametrize("w", CASES, ids=[c.name for c in CASES])
