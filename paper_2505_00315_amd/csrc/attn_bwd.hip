@@ -646,10 +646,11 @@ __global__ __launch_bounds__(64 * NWV) void attn_bwd_q_tiled_kernel(MOSA_BWD_TIL
 // hands workgroup b and b + 256 to the same CU), every second round in reverse,
 // so that the blocks a CU receives add up to about the same number of tiles
 // (causal, hybrid_d1024: 32 per CU instead of 24 to 40; 54 -> 48 us).
-// (register budget for 3 waves per SIMD: more of the MoSA heads' waves fit
-// beside it in the hybrid layer's backward, 0.435 -> 0.431 ms per step)
+// Register budget: 3 waves per SIMD with one column block per wave (more of
+// the MoSA heads' waves fit beside it in the hybrid layer's backward, 0.435 ->
+// 0.431 ms per step), 2 with two (254 registers, no spills).
 template <typename ST, int DH, bool WIN, int NWV, int CB>
-__global__ __launch_bounds__(64 * NWV, 3) void attn_bwd_tiled_both_kernel(MOSA_BWD_TILED_PARAMS) {
+__global__ __launch_bounds__(64 * NWV, CB == 1 ? 3 : 2) void attn_bwd_tiled_both_kernel(MOSA_BWD_TILED_PARAMS) {
     // one LDS buffer for whichever pass the block runs
     __shared__ __attribute__((aligned(16))) unsigned char smem[BwdTile<ST, DH>::both_lds(16 * CB * NWV)];
     constexpr int kRound = 256;
@@ -1045,24 +1046,30 @@ int launch_t(const ST* QKV, const ST* dA, const float* lse, const float* D, int 
         return hipGetLastError() == hipSuccess ? 0 : -1;
       }
       if (n > 32 || window > 0) {
-        // 4 waves per workgroup, 16 owned rows per wave (one column block:
-        // two, with half the LDS reads per MFMA but one wave per SIMD, were
-        // slower beside the MoSA heads' backward)
-#define MOSA_ATTN_BWD_T(KERN, DHV)                                                                     \
+        // 4 waves per workgroup, 16 CB owned rows per wave.  Two column
+        // blocks (half the LDS reads per MFMA, 2 waves per SIMD) where the
+        // rows are long (n >= 1024, no window) and the blocks still give
+        // every CU two workgroups (4 dense heads, B = 8, T = 1024: 44 -> 39.5 us); one
+        // otherwise (measured slower with two: n = 512 MoSA heads, local
+        // windows, a single head of T = 8192 that fills half the chip).
+#define MOSA_ATTN_BWD_T(KERN, DHV, CBV)                                                                \
     do {                                                                                                \
-        constexpr int NWV = 4, CB = 1, OB = 16 * CB * NWV;                                              \
+        constexpr int NWV = 4, CB = CBV, OB = 16 * CB * NWV;                                            \
         auto kern = window > 0 ? KERN<ST, DHV, true, NWV, CB> : KERN<ST, DHV, false, NWV, CB>;          \
         const dim3 grid((pass == 2 ? 2 : 1) * BH * ((n + OB - 1) / OB)), block(64 * NWV);               \
         hipLaunchKernelGGL(kern, grid, block, 0, stream, QKV, dA, lse, D, BH, n, causal, lb, scale, dQKV, rI, rtab); \
     } while (0)
-#define MOSA_ATTN_BWD_TD(KERN)                                                                         \
+#define MOSA_ATTN_BWD_TD(KERN, CBV)                                                                    \
     do {                                                                                                \
-        if (dh == 64) MOSA_ATTN_BWD_T(KERN, 64);                                                        \
-        else MOSA_ATTN_BWD_T(KERN, 32);                                                                 \
+        if (dh == 64) MOSA_ATTN_BWD_T(KERN, 64, CBV);                                                   \
+        else MOSA_ATTN_BWD_T(KERN, 32, CBV);                                                            \
     } while (0)
-        if (pass == 2) MOSA_ATTN_BWD_TD(attn_bwd_tiled_both_kernel);
-        else if (pass == 0) MOSA_ATTN_BWD_TD(attn_bwd_kv_tiled_kernel);
-        else MOSA_ATTN_BWD_TD(attn_bwd_q_tiled_kernel);
+        const bool wide = window == 0 && n >= 1024 && 2LL * BH * ((n + 127) / 128) >= 512;
+        if (pass == 2) {
+            if (wide) MOSA_ATTN_BWD_TD(attn_bwd_tiled_both_kernel, 2);
+            else MOSA_ATTN_BWD_TD(attn_bwd_tiled_both_kernel, 1);
+        } else if (pass == 0) MOSA_ATTN_BWD_TD(attn_bwd_kv_tiled_kernel, 1);
+        else MOSA_ATTN_BWD_TD(attn_bwd_q_tiled_kernel, 1);
 #undef MOSA_ATTN_BWD_TD
 #undef MOSA_ATTN_BWD_T
         return hipGetLastError() == hipSuccess ? 0 : -1;

@@ -77,6 +77,12 @@ def test_tiny_f32_workload(orc):
     dict(seq_len=200, k=100, causal=False),
     dict(batch=2, seq_len=700, heads=0, dense_heads=1, d_head=64, d_model=128, causal=False),
     dict(batch=2, seq_len=900, heads=0, dense_heads=1, d_head=64, d_model=128, window=600),
+    # rows of 1024 or more with at least 32 (b, h): the tiled attention
+    # backward with two column blocks per wave (32-wide heads; a ragged
+    # non-causal tail; selected rows with the rotation)
+    dict(batch=8, seq_len=1024, heads=0, dense_heads=4, d_head=32, d_model=128),
+    dict(batch=4, seq_len=1040, heads=1, k=8, dense_heads=8, d_head=64, d_model=128, causal=False),
+    dict(batch=4, seq_len=1100, heads=8, k=1030, d_head=64, d_model=128, rope=True),
     # 64-wide heads with at most 128 selected rows per head over the batch:
     # the per-head streaming kernel of the weight gradients and dX rows
     # (R = B k = 7, 40, 100 rows; one, two and three column tiles), and the
