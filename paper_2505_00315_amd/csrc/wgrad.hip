@@ -412,10 +412,13 @@ struct WgradODensePolicy2 : WgradOPolicy2<DH> {
     }
 };
 
-// Row ranges of the dense-head split: enough workgroups for the chip (about
-// 512 for `tiles` output tiles per range), each range at most 4096 rows.
+// Row ranges of the dense-head split: about one workgroup per CU (256 for
+// `tiles` output tiles per range), each range at most 4096 rows.  Fewer
+// ranges mean fewer fp32 partials to write and sum; with 4 dense heads,
+// d = 1024 and B T = 8192 rows, 4 ranges beat 2 and 8 (the hybrid layer's
+// step: 0.428, 0.406 and 0.410 ms cold), 16 were slower still.
 inline int dense_ranges(int R, int tiles, int kc, int& rows) {
-    int S = std::max(1, (512 + tiles - 1) / tiles);
+    int S = std::max(1, (256 + tiles - 1) / tiles);
     S = std::max(S, (R + 4095) / 4096);
     rows = (R + S - 1) / S;
     rows = (rows + kc - 1) / kc * kc;
