@@ -53,8 +53,13 @@ struct BwdOutPolicy {
     __device__ static const ST* a_fallback(const Args& a) { return a.dY; }
     __device__ static const ST* b_fallback(const Args& a) { return a.Wo; }
     __device__ static void tile(const Args& a, int logical, int& h, int& m0, int& n0) {
-        h = logical / a.mtiles;
-        m0 = (logical % a.mtiles) * MT;
+        if (a.I) {  // a head's row tiles side by side: they share its W^O rows
+            h = logical / a.mtiles;
+            m0 = (logical % a.mtiles) * MT;
+        } else {  // dense heads: the heads of a row tile side by side (its dY rows)
+            h = logical % a.H;
+            m0 = (logical / a.H) * MT;
+        }
         n0 = 0;
     }
     __device__ static int k_size(const Args& a, int) { return a.d; }

@@ -143,8 +143,13 @@ struct QkvPolicy2 {
     static int mtiles(int M) { return (M + MT - 1) / MT; }
     __device__ static void tile(const Args& a, int logical, int& batch, int& m0, int& n0) {
         const int mt = (a.M + MT - 1) / MT;
-        batch = logical / mt;
-        m0 = (logical % mt) * MT;
+        if (a.I) {  // a head's row tiles side by side: they share its weights
+            batch = logical / mt;
+            m0 = (logical % mt) * MT;
+        } else {  // dense heads: the heads of a row tile side by side (its X rows)
+            batch = logical % a.H;
+            m0 = (logical / a.H) * MT;
+        }
         n0 = 0;
     }
     __device__ static int k_size(const Args& a, int) { return a.d; }

@@ -359,9 +359,11 @@ struct WgradQkvDensePolicy2 : WgradQkvPolicy2<DH> {
     static constexpr int MT = DH == 64 ? 192 : 128;  // [dQ | dK | dV] (DH 32: zero rows past 96)
     using Args = typename WgradQkvPolicy2<DH>::Args;  // I unused, cps = rows per range
     __device__ static void tile(const Args& a, int logical, int& batch, int& m0, int& n0) {
-        batch = logical / a.mtiles;  // h S + s
+        // the heads of one (row range, column tile) side by side (its X block)
+        const int h = logical % a.H, rest = logical / a.H;
+        batch = h * a.S + rest / a.mtiles;  // h S + s
         m0 = 0;
-        n0 = (logical % a.mtiles) * WgradQkvPolicy2<DH>::NT;
+        n0 = (rest % a.mtiles) * WgradQkvPolicy2<DH>::NT;
     }
     __device__ static int k_size(const Args& a, int batch) { return min(a.cps, a.R - (batch % a.S) * a.cps); }
     __device__ static int2 k_row(const Args& a, int batch, int k, int K) {
@@ -395,8 +397,10 @@ struct WgradODensePolicy2 : WgradOPolicy2<DH> {
     using ST = uint16_t;
     using Args = typename WgradOPolicy2<DH>::Args;  // I unused, cps = rows per range
     __device__ static void tile(const Args& a, int logical, int& batch, int& m0, int& n0) {
-        batch = logical / a.ntiles;  // h S + s
-        m0 = (logical % a.ntiles) * WgradOPolicy2<DH>::MT;
+        // the heads of one (row range, column tile) side by side (its dY block)
+        const int h = logical % a.H, rest = logical / a.H;
+        batch = h * a.S + rest / a.ntiles;  // h S + s
+        m0 = (rest % a.ntiles) * WgradOPolicy2<DH>::MT;
         n0 = 0;
     }
     __device__ static int k_size(const Args& a, int batch) { return min(a.cps, a.R - (batch % a.S) * a.cps); }
