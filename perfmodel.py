@@ -11,6 +11,8 @@ is `paper_flops_*` below.
 from dataclasses import dataclass
 
 HBM_PEAK = 8.0e12  # bytes/s, MI355X HBM3E
+SIMDS = 1024  # 256 CUs x 4
+SHADER_ENGINES = 32  # 8 XCDs x 4; SQ_BUSY_CYCLES is summed over them
 MFMA_PEAK = {"bf16": 2.5e15, "f32": 157.3e12}  # dense FLOP/s by operand type
 
 
@@ -314,15 +316,22 @@ def profile_markdown(w, order_info, rows, scales, commands):
             "WRITE_SIZE per dispatch scaled by a plain copy of known size"
             + (f" (fetch x{scales['fetch']:.3f}, write x{scales['write']:.3f})" if len(scales) == 2 else "")
             + "; `HBM/alg` their ratio; `MFMA %` = 512 x SQ_INSTS_VALU_MFMA_MOPS_BF16 / `us` / 2.5 PFLOP/s; "
+            "`clk GHz` = SQ_BUSY_CYCLES / 32 shader engines / `us`, the clock the kernel ran at; `MFMA busy %` = "
+            "SQ_VALU_MFMA_BUSY_CYCLES (summed over the 1024 SIMDs) / (1024 x SQ_BUSY_CYCLES / 32), the share of "
+            "the SIMDs' cycles at that clock with the matrix core busy; "
             "`wait %` = SQ_WAIT_ANY / SQ_WAVE_CYCLES; `LDS conf %` = SQ_LDS_BANK_CONFLICT / SQ_LDS_IDX_ACTIVE.",
             "", "| stage | kernel | calls | us | event us | alg MB | alg GF | bound | frac | HBM MB | HBM/alg | "
-            "MFMA % | wait % | LDS conf % |", "|---|---|---:|---:|---:|---:|---:|---|---:|---:|---:|---:|---:|---:|"]
+            "MFMA % | clk GHz | MFMA busy % | wait % | LDS conf % |",
+            "|---|---|---:|---:|---:|---:|---:|---|---:|---:|---:|---:|---:|---:|---:|---:|"]
     total = 0.0
     for r in rows:
         total += r.get("us", 0.0)
         ratio = r["hbm_bytes"] / r["alg_bytes"] if r.get("hbm_bytes") and r.get("alg_bytes") else None
         wait = (100.0 * r["SQ_WAIT_ANY"] / r["SQ_WAVE_CYCLES"]) if r.get("SQ_WAVE_CYCLES") else None
         conf = (100.0 * r["SQ_LDS_BANK_CONFLICT"] / r["SQ_LDS_IDX_ACTIVE"]) if r.get("SQ_LDS_IDX_ACTIVE") else None
+        clk = r["SQ_BUSY_CYCLES"] / SHADER_ENGINES / (r["us"] * 1e3) if r.get("SQ_BUSY_CYCLES") and r.get("us") else None
+        busy = (100.0 * r["SQ_VALU_MFMA_BUSY_CYCLES"] * SHADER_ENGINES / (SIMDS * r["SQ_BUSY_CYCLES"])
+                if r.get("SQ_BUSY_CYCLES") and r.get("SQ_VALU_MFMA_BUSY_CYCLES") is not None else None)
         kern = r.get("kernel", "")
         if len(kern) > 60:
             kern = kern[:57] + "..."
@@ -332,7 +341,8 @@ def profile_markdown(w, order_info, rows, scales, commands):
             _fmt(r.get("alg_flops", 0) / 1e9 if r.get("alg_flops") is not None else None, ".2f"),
             r.get("bound", ""), _fmt(r.get("frac"), ".3f"),
             _fmt(r["hbm_bytes"] / 1e6 if r.get("hbm_bytes") is not None else None, ".2f"), _fmt(ratio, ".2f"),
-            _fmt(100.0 * r["mfma_util"] if r.get("mfma_util") is not None else None, ".1f"), _fmt(wait, ".0f"),
+            _fmt(100.0 * r["mfma_util"] if r.get("mfma_util") is not None else None, ".1f"), _fmt(clk, ".2f"),
+            _fmt(busy, ".1f"), _fmt(wait, ".0f"),
             _fmt(conf, ".1f")]) + " |")
     out += ["", f"Sum of the mean kernel durations of one step: {total:.1f} us."]
     return "\n".join(out) + "\n"
