@@ -461,10 +461,12 @@ int mosa_backward_timed(const mosa_shape* s, const void* X, const mosa_weights* 
         if (hipStreamWaitEvent(stream, ax->mid, 0) != hipSuccess) e |= 1;
         e |= launch_dx_combine(dt, dQKVd, w->Wq_d, w->Wk_d, w->Wv_d, slot, dXs, B, T, d, H, dh, k, Hd, dX,
                                accumulate_dX, at<void>(scratch, L.dxbase), 1, mk, stream);
-        e |= aux_join(ax, stream);
     }
     e |= launch_dx_combine(dt, dQKVd, w->Wq_d, w->Wk_d, w->Wv_d, slot, dXs, B, T, d, H, dh, k, Hd, dX, accumulate_dX,
                            at<void>(scratch, L.dxbase), ax ? 2 : 0, mk, stream);
+    // nothing on the main stream needs the auxiliary chain's last kernels (the
+    // dense heads' dW^{Q,K,V}), so the call's join comes last
+    if (ax) e |= aux_join(ax, stream);
     return e ? MOSA_ERR_HIP : MOSA_OK;
 }
 

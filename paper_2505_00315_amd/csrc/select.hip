@@ -440,10 +440,278 @@ __global__ __launch_bounds__(64 * NW) void select_rows_kernel(
     }
 }
 
+// One wave per (b, h) row for T <= 64 EPL (EPL tokens per lane at t = 64 e +
+// lane): the same certified selection as select_rows_kernel without an LDS
+// histogram or a workgroup barrier.  tau, the (k+1)-th largest key, is found
+// exactly by a binary search over the 32 key bits (each step counts the keys
+// at or above a candidate: one compare per key and a wave sum), so A and B
+// bracket tau itself; counts and in-order positions come from ballots.  The
+// uncertain tokens are re-scored as there, one token at a time by the whole
+// wave (fp64, then the long accumulator where the fp64 intervals overlap).
+// The waves of a workgroup take independent rows and never wait for each
+// other.
+constexpr int kSelectWaveRows = 4;  // rows (waves) per workgroup
+
+template <typename ST, int EPL>
+__global__ __launch_bounds__(64 * kSelectWaveRows) void select_wave_kernel(
+    const float* __restrict__ z, const float* __restrict__ xnorm, const ST* __restrict__ X,
+    const ST* __restrict__ Wr, int rows, int T, int d, int H, int k, int first, int32_t* __restrict__ I,
+    float* __restrict__ r, int16_t* __restrict__ slot, int32_t* __restrict__ unc_tok, double* __restrict__ unc_key,
+    int32_t* __restrict__ unc_sel, int32_t* __restrict__ status) {
+    __shared__ int s_utok[kSelectWaveRows][kSelectLdsUnc];
+    __shared__ double s_ukey[kSelectWaveRows][kSelectLdsUnc];
+    __shared__ int s_usel[kSelectWaveRows][kSelectLdsUnc];
+    __shared__ int64_t s_long[kSelectWaveRows][kLongDigits];
+    static_assert(EPL >= 1 && EPL <= 32 && kLongDigits <= 64, "shape");
+
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int row = blockIdx.x * kSelectWaveRows + wave;
+    if (row >= rows) return;  // the whole wave; no other wave waits for it
+    const int b = row / H, h = row % H;
+    const size_t rowT = (size_t)row * T;
+    const float* zr = z + rowT;
+    const float* xn = xnorm + (size_t)b * T;
+    const ST* w = Wr + (size_t)h * d;
+
+    // All loads first: the logits and ||x|| of this lane's tokens, a share of w.
+    float zv[EPL], xv[EPL];
+#pragma unroll
+    for (int e = 0; e < EPL; ++e) {
+        const int tc = min(64 * e + lane, T - 1);
+        zv[e] = zr[tc];
+        xv[e] = xn[tc];
+    }
+    double ss = 0.0;
+    for (int c = 8 * lane; c < d; c += 8 * 64) {  // d is a multiple of 64
+        float wv8[8];
+        vec8_to_f32<ST>(vec8_load<ST>(w + c), wv8);
+#pragma unroll
+        for (int j = 0; j < 8; ++j) ss += (double)wv8[j] * (double)wv8[j];
+    }
+    const bool all = k >= T;
+    uint32_t key[EPL];
+#pragma unroll
+    for (int e = 0; e < EPL; ++e) key[e] = 64 * e + lane < T ? order_key(zv[e]) : 0u;  // 0: below every real key
+    // forced first token: above every real key (see select_rows_kernel)
+    if (first && lane == 0) key[0] = 0xffffffffu;
+
+    // tau = the largest key v with at least k + 1 keys >= v, bit by bit
+    uint32_t tau = 0u;
+    if (!all) {
+        for (int bit = 31; bit >= 0; --bit) {
+            const uint32_t cand = tau | (1u << bit);
+            uint32_t c = 0u;
+#pragma unroll
+            for (int e = 0; e < EPL; ++e) c += key[e] >= cand ? 1u : 0u;
+            if (wave_sum_u32(c) >= (uint32_t)(k + 1)) tau = cand;
+        }
+    }
+
+    // ||w|| and the largest ||x_t|| (every xv is a real token's); the bound
+    // as in select_rows_kernel, with tau exact: A = down(tau - bmax) is at
+    // most the k-th largest lower end, B = up(tau + bmax) at least the
+    // (k+1)-th largest upper end
+    ss = wave_sum_f64(ss);
+    float xm = xv[0];
+#pragma unroll
+    for (int e = 1; e < EPL; ++e) xm = fmaxf(xm, xv[e]);
+    xm = wave_max_nonneg_f32(xm);
+    const double wn = sqrt(ss) * (1.0 + 0x1p-30);
+    const int nc = d / 32;
+    const double coef = (96.0 * 0x1p-23 + 1.01 * (double)nc * 0x1p-24) * (1.0 + 0x1p-10);
+    const double absterm = (double)(d + nc) * 0x1p-126 * (1.0 + 0x1p-10);
+    const double bmax = coef * (double)xm * wn + absterm * (1.0 + (double)xm + wn);
+    uint32_t A = 0u, Bk = 0u;
+    if (!all) {
+        const float tf = key_float(tau);
+        A = isfinite(tf) ? order_key(f32_down((double)tf - bmax)) : 0u;
+        Bk = isfinite(tf) ? order_key(f32_up((double)tf + bmax)) : 0xffffffffu;
+    }
+
+    // Classify: in (lo > B), out (hi < A) or uncertain.
+    uint32_t inm = 0u, uncm = 0u;
+    int tot_in = 0, tot_unc = 0;
+#pragma unroll
+    for (int e = 0; e < EPL; ++e) {
+        const bool ok = 64 * e + lane < T;
+        const double x = (double)xv[e];
+        const double beta = coef * x * wn + absterm * (1.0 + x + wn);
+        uint32_t lo = ok ? order_key(f32_down((double)zv[e] - beta)) : 0u;
+        uint32_t hi = ok ? order_key(f32_up((double)zv[e] + beta)) : 0u;
+        if (first && lane == 0 && e == 0) lo = hi = 0xffffffffu;
+        const bool in = ok && (all || lo > Bk);
+        const bool unc = ok && !in && !(hi < A);
+        inm |= (uint32_t)in << e;
+        uncm |= (uint32_t)unc << e;
+        tot_in += __popcll(__ballot(in));
+        tot_unc += __popcll(__ballot(unc));
+    }
+    int need = k - tot_in;  // 0 <= need <= tot_unc when the bound holds
+    if (need < 0) need = 0;
+    if (need > tot_unc) need = tot_unc;
+    const bool resolve = need > 0 && need < tot_unc;
+
+    const bool small = tot_unc <= kSelectLdsUnc;
+    int* utok = small ? s_utok[wave] : unc_tok + rowT;
+    double* ukey = small ? s_ukey[wave] : unc_key + rowT;
+    int* usel = small ? s_usel[wave] : unc_sel + rowT;
+    if (resolve) {
+        // the uncertain tokens in index order
+        int base = 0;
+#pragma unroll
+        for (int e = 0; e < EPL; ++e) {
+            const uint64_t ub = __ballot((uncm >> e) & 1u);
+            if ((uncm >> e) & 1u) utok[base + __popcll(ub & lanes_below())] = 64 * e + lane;
+            base += __popcll(ub);
+        }
+        __threadfence_block();
+        __builtin_amdgcn_wave_barrier();
+        // their logits in fp64 (bound as in select_rows_kernel)
+        for (int u = 0; u < tot_unc; ++u) {
+            const ST* xr = X + ((size_t)b * T + utok[u]) * d;
+            double acc = 0.0;
+            for (int c = 8 * lane; c < d; c += 8 * 64) {
+                float xv8[8], wv8[8];
+                vec8_to_f32<ST>(vec8_load<ST>(xr + c), xv8);
+                vec8_to_f32<ST>(vec8_load<ST>(w + c), wv8);
+#pragma unroll
+                for (int j = 0; j < 8; ++j) acc += (double)xv8[j] * (double)wv8[j];
+            }
+            acc = wave_sum_f64(acc);
+            if (lane == 0) ukey[u] = acc;
+        }
+        __threadfence_block();
+        __builtin_amdgcn_wave_barrier();
+        // decide from the fp64 intervals where they separate
+        bool unknown = false;
+        for (int u = lane; u < tot_unc; u += 64) {
+            const double vu = ukey[u];
+            const double bu = 1.01 * (double)d * 0x1p-53 * (double)xn[utok[u]] * wn + fabs(vu) * 0x1p-51;
+            int above = 0, maybe = 0;
+            for (int v = 0; v < tot_unc; ++v) {
+                if (v == u) continue;
+                const double vv = ukey[v];
+                const double bv = 1.01 * (double)d * 0x1p-53 * (double)xn[utok[v]] * wn + fabs(vv) * 0x1p-51;
+                if (vv - bv > vu + bu) ++above;         // certainly above u
+                else if (!(vv + bv < vu - bu)) ++maybe;  // order unknown
+            }
+            int sel = -1;
+            if (above + maybe < need) sel = 1;
+            else if (above >= need) sel = 0;
+            else unknown = true;
+            usel[u] = sel;
+        }
+        const bool exact = __ballot(unknown) != 0ull;
+        __threadfence_block();
+        __builtin_amdgcn_wave_barrier();
+        if (exact) {
+            // exact keys, one token at a time (long accumulator in the wave's LDS digits)
+            for (int u = 0; u < tot_unc; ++u) {
+                if (lane < kLongDigits) s_long[wave][lane] = 0;
+                __threadfence_block();
+                __builtin_amdgcn_wave_barrier();
+                const ST* xr = X + ((size_t)b * T + utok[u]) * d;
+                for (int c = lane; c < d; c += 64) {
+                    uint32_t sx, Mx, sw, Mw;
+                    int Ex, Ew;
+                    split_elem<ST>(xr + c, sx, Mx, Ex);
+                    split_elem<ST>(w + c, sw, Mw, Ew);
+                    const ProductParts p = product_parts(sx, Mx, Ex, sw, Mw, Ew);
+                    if (!p.zero) {
+#pragma unroll
+                        for (int q = 0; q < 3; ++q) {
+                            if (p.v[q]) {
+                                const uint64_t add = p.negative ? (uint64_t)(-(int64_t)p.v[q]) : p.v[q];
+                                atomicAdd(reinterpret_cast<unsigned long long*>(&s_long[wave][p.j + q]),
+                                          (unsigned long long)add);
+                            }
+                        }
+                    }
+                }
+                __threadfence_block();
+                __builtin_amdgcn_wave_barrier();
+                if (lane == 0) ukey[u] = long_accumulator_round(&s_long[wave][0]);
+                __threadfence_block();
+                __builtin_amdgcn_wave_barrier();
+            }
+            // exact rank among the uncertain tokens (key desc, index asc)
+            for (int u = lane; u < tot_unc; u += 64) {
+                const double ku = ukey[u];
+                const int tu = utok[u];
+                int rank = 0;
+                for (int v = 0; v < tot_unc; ++v) {
+                    const double kv = ukey[v];
+                    const int tv = utok[v];
+                    rank += (kv > ku) || (kv == ku && tv < tu);
+                }
+                usel[u] = rank < need;
+            }
+            __threadfence_block();
+            __builtin_amdgcn_wave_barrier();
+        }
+    }
+
+    // Compact the chosen tokens in index order: I ascending, r, and the slot map.
+    uint32_t selm = inm;
+    {
+        int base = 0;
+#pragma unroll
+        for (int e = 0; e < EPL; ++e) {
+            const bool unc = (uncm >> e) & 1u;
+            const uint64_t ub = __ballot(unc);
+            if (unc && (resolve ? (usel[base + __popcll(ub & lanes_below())] > 0) : (need == tot_unc)))
+                selm |= 1u << e;
+            base += __popcll(ub);
+        }
+    }
+    int pos0 = 0;
+#pragma unroll
+    for (int e = 0; e < EPL; ++e) {
+        const bool sel = (selm >> e) & 1u;
+        const uint64_t sb = __ballot(sel);
+        const int t = 64 * e + lane;
+        const int pos = pos0 + __popcll(sb & lanes_below());
+        int16_t sl = -1;
+        if (sel && pos < k) {
+            I[(size_t)row * k + pos] = t;
+            r[(size_t)row * k + pos] = 1.0f / (1.0f + expf(-zv[e]));
+            sl = (int16_t)pos;
+        }
+        if (t < T) slot[rowT + t] = sl;
+        pos0 += __popcll(sb);
+    }
+    // exactly k tokens unless the logit error bound was violated (then as in
+    // select_rows_kernel: the row is flagged and every slot kept defined)
+    if (lane == 0) status[row] = pos0 == k ? 0 : 1;
+    for (int pos = pos0 + lane; pos < k; pos += 64) {
+        I[(size_t)row * k + pos] = 0;
+        r[(size_t)row * k + pos] = 0.f;
+    }
+}
+
 template <typename ST>
 int launch_select_t(const float* z, const float* xnorm, const ST* X, const ST* Wr, int B, int T, int d, int H,
                     int k, int first, int32_t* I, float* r, int16_t* slot, int32_t* unc_tok, double* unc_key,
                     int32_t* unc_sel, int32_t* status, hipStream_t stream) {
+    if (T <= 1024 && B * H >= 2048) {
+        // one wave per row where the rows give every SIMD two waves: each row
+        // then takes longer than with the workgroup kernel (one wave does all
+        // of its steps), but the launch as a whole does not, and it holds a
+        // quarter of the LDS, which leaves more room to the dense QKV GEMM
+        // beside it (hybrid_d1024's 2048 rows: the two-stream step 0.400 ->
+        // 0.398 ms cold; with 256 or 512 rows it is slower, 11 -> 22 and 13
+        // -> 25 us)
+        const int rows = B * H;
+        const dim3 g((rows + kSelectWaveRows - 1) / kSelectWaveRows), blk(64 * kSelectWaveRows);
+#define MOSA_SELECT_WAVE(E)                                                                                    \
+    hipLaunchKernelGGL((select_wave_kernel<ST, E>), g, blk, 0, stream, z, xnorm, X, Wr, rows, T, d, H, k, first, I, \
+                       r, slot, unc_tok, unc_key, unc_sel, status)
+        if (T <= 256) MOSA_SELECT_WAVE(4);
+        else if (T <= 512) MOSA_SELECT_WAVE(8);
+        else MOSA_SELECT_WAVE(16);
+#undef MOSA_SELECT_WAVE
+        return hipGetLastError() == hipSuccess ? 0 : -1;
+    }
     const dim3 grid(B * H);
 #define MOSA_SELECT_ROWS(NW, E)                                                                                \
     hipLaunchKernelGGL((select_rows_kernel<ST, NW, E>), grid, dim3(64 * NW), 0, stream, z, xnorm, X, Wr, T, d, H, \

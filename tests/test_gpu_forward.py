@@ -100,6 +100,40 @@ def test_duplicate_rows_tie_to_lower_index(orc):
     check_forward(orc, w, inp)
 
 
+# 2048 or more routed rows of T <= 1024: the one-wave selection (4, 8 and 16
+# tokens per lane, a forced first token, k = 1 and k = T, fp32 storage)
+@pytest.mark.parametrize("kw", [
+    dict(batch=8, seq_len=64, heads=256, k=8, d_head=32, d_model=64),
+    dict(batch=4, seq_len=300, heads=512, k=37, d_head=32, d_model=64, first_token=True),
+    dict(batch=2, seq_len=1000, heads=1024, k=1, d_head=32, d_model=64, causal=False),
+    dict(batch=8, seq_len=40, heads=256, k=40, d_head=32, d_model=64),
+    dict(batch=8, seq_len=96, heads=256, k=20, d_head=32, d_model=64, dtype="f32"),
+])
+def test_wave_select_shapes(orc, kw):
+    check_forward(orc, wl.small(**kw))
+
+
+@pytest.mark.parametrize("T", [64, 200])
+def test_wave_select_all_ties(orc, T):
+    """Every key equal (W^r = 0) over 2048 rows: all tokens uncertain, decided
+    by the exact keys and the index; the lists in LDS (T = 64) or in the
+    global scratch (T = 200)."""
+    w = wl.small(batch=8, seq_len=T, heads=256, k=T // 4, d_head=32, d_model=64)
+    inp = wl.make_inputs(w)
+    inp["Wr"][:] = 0
+    out, ref = check_forward(orc, w, inp)
+    assert (out["I"] == np.arange(w.k)).all()
+
+
+def test_wave_select_duplicate_rows(orc):
+    w = wl.small(batch=8, seq_len=128, heads=256, k=16, d_head=32, d_model=64)
+    inp = wl.make_inputs(w)
+    for b in range(w.batch):
+        for src, dst in [(5, 90), (17, 3), (40, 41), (100, 7)]:
+            inp["X"][b, dst] = inp["X"][b, src]
+    check_forward(orc, w, inp)
+
+
 def test_unselected_rows_exactly_zero(orc):
     w = wl.small(seq_len=256, k=8, heads=2)
     out, ref = check_forward(orc, w)
