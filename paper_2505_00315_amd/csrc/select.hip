@@ -442,14 +442,15 @@ __global__ __launch_bounds__(64 * NW) void select_rows_kernel(
 
 // One wave per (b, h) row for T <= 64 EPL (EPL tokens per lane at t = 64 e +
 // lane): the same certified selection as select_rows_kernel without an LDS
-// histogram or a workgroup barrier.  tau, the (k+1)-th largest key, is found
-// exactly by a binary search over the 32 key bits (each step counts the keys
-// at or above a candidate: one compare per key and a wave sum), so A and B
-// bracket tau itself; counts and in-order positions come from ballots.  The
-// uncertain tokens are re-scored as there, one token at a time by the whole
-// wave (fp64, then the long accumulator where the fp64 intervals overlap).
-// The waves of a workgroup take independent rows and never wait for each
-// other.
+// histogram or a workgroup barrier.  tau, the (k+1)-th largest key, is
+// located to within 1024 keys as there, here by a binary search over its top
+// 22 bits (each step counts the keys at or above a candidate: one compare per
+// key and a wave sum).  Most tokens are classified by one compare of their
+// key against row-wide thresholds; counts and in-order positions come from
+// wave sums and ballots.  The uncertain tokens are re-scored as there, one
+// token at a time by the whole wave (fp64, then the long accumulator where
+// the fp64 intervals overlap).  The waves of a workgroup take independent
+// rows and never wait for each other.
 constexpr int kSelectWaveRows = 4;  // rows (waves) per workgroup
 
 template <typename ST, int EPL>
@@ -495,22 +496,22 @@ __global__ __launch_bounds__(64 * kSelectWaveRows) void select_wave_kernel(
     // forced first token: above every real key (see select_rows_kernel)
     if (first && lane == 0) key[0] = 0xffffffffu;
 
-    // tau = the largest key v with at least k + 1 keys >= v, bit by bit
-    uint32_t tau = 0u;
+    // tau, the largest key v with at least k + 1 keys >= v, to within 1024
+    // consecutive keys: its top 22 bits, bit by bit (a compare per key and a
+    // wave sum per bit); tlo <= tau <= thi are the ends of that range
+    uint32_t pref = 0u;
     if (!all) {
-        for (int bit = 31; bit >= 0; --bit) {
-            const uint32_t cand = tau | (1u << bit);
+        for (int bit = 31; bit >= 10; --bit) {
+            const uint32_t cand = pref | (1u << bit);
             uint32_t c = 0u;
 #pragma unroll
             for (int e = 0; e < EPL; ++e) c += key[e] >= cand ? 1u : 0u;
-            if (wave_sum_u32(c) >= (uint32_t)(k + 1)) tau = cand;
+            if (wave_sum_u32(c) >= (uint32_t)(k + 1)) pref = cand;
         }
     }
 
-    // ||w|| and the largest ||x_t|| (every xv is a real token's); the bound
-    // as in select_rows_kernel, with tau exact: A = down(tau - bmax) is at
-    // most the k-th largest lower end, B = up(tau + bmax) at least the
-    // (k+1)-th largest upper end
+    // ||w|| and the largest ||x_t|| (every xv is a real token's); the bound,
+    // A and B as in select_rows_kernel
     ss = wave_sum_f64(ss);
     float xm = xv[0];
 #pragma unroll
@@ -523,29 +524,60 @@ __global__ __launch_bounds__(64 * kSelectWaveRows) void select_wave_kernel(
     const double bmax = coef * (double)xm * wn + absterm * (1.0 + (double)xm + wn);
     uint32_t A = 0u, Bk = 0u;
     if (!all) {
-        const float tf = key_float(tau);
-        A = isfinite(tf) ? order_key(f32_down((double)tf - bmax)) : 0u;
-        Bk = isfinite(tf) ? order_key(f32_up((double)tf + bmax)) : 0xffffffffu;
+        const float tlo = key_float(pref), thi = key_float(pref | 0x3ffu);
+        A = isfinite(tlo) ? order_key(f32_down((double)tlo - bmax)) : 0u;
+        Bk = isfinite(thi) ? order_key(f32_up((double)thi + bmax)) : 0xffffffffu;
     }
 
-    // Classify: in (lo > B), out (hi < A) or uncertain.
-    uint32_t inm = 0u, uncm = 0u;
-    int tot_in = 0, tot_unc = 0;
+    // Classify: in (lo > B), out (hi < A) or uncertain.  Most tokens are
+    // decided by one key compare against the row's thresholds with bmax in
+    // place of their own beta: z~ <= Lo (the float below next_down(A) - bmax,
+    // one float lower for the fp64 rounding of the difference) gives
+    // hi <= next_down(A) < A, and z~ >= Hi (likewise above next_up(B) +
+    // bmax) gives lo >= next_up(B) > B.  The others (and a forced token)
+    // take the per-token bounds.
+    uint32_t lo_key = 0u, hi_key = 0xffffffffu;
+    bool lo_ok = false, hi_ok = false;
+    if (!all) {
+        const float af = key_float(A), bf = key_float(Bk);
+        if (A != 0u && isfinite(af)) {
+            const float lf = next_down(f32_down((double)next_down(af) - bmax));
+            lo_ok = isfinite(lf);
+            lo_key = order_key(lf);
+        }
+        if (Bk != 0xffffffffu && isfinite(bf)) {
+            const float hf = next_up(f32_up((double)next_up(bf) + bmax));
+            hi_ok = isfinite(hf);
+            hi_key = order_key(hf);
+        }
+    }
+    uint32_t inm = 0u, uncm = 0u, bandm = 0u;
 #pragma unroll
     for (int e = 0; e < EPL; ++e) {
         const bool ok = 64 * e + lane < T;
-        const double x = (double)xv[e];
-        const double beta = coef * x * wn + absterm * (1.0 + x + wn);
-        uint32_t lo = ok ? order_key(f32_down((double)zv[e] - beta)) : 0u;
-        uint32_t hi = ok ? order_key(f32_up((double)zv[e] + beta)) : 0u;
-        if (first && lane == 0 && e == 0) lo = hi = 0xffffffffu;
-        const bool in = ok && (all || lo > Bk);
-        const bool unc = ok && !in && !(hi < A);
-        inm |= (uint32_t)in << e;
-        uncm |= (uint32_t)unc << e;
-        tot_in += __popcll(__ballot(in));
-        tot_unc += __popcll(__ballot(unc));
+        const bool forced = first && lane == 0 && e == 0;
+        const bool fin = ok && !forced && (all || (hi_ok && key[e] >= hi_key));
+        const bool fout = ok && !forced && !all && lo_ok && key[e] <= lo_key;
+        inm |= (uint32_t)fin << e;
+        bandm |= (uint32_t)(ok && !fin && !fout) << e;
     }
+    if (__ballot(bandm != 0u)) {
+#pragma unroll
+        for (int e = 0; e < EPL; ++e) {
+            if ((bandm >> e) & 1u) {
+                const double x = (double)xv[e];
+                const double beta = coef * x * wn + absterm * (1.0 + x + wn);
+                uint32_t lo = order_key(f32_down((double)zv[e] - beta));
+                uint32_t hi = order_key(f32_up((double)zv[e] + beta));
+                if (first && lane == 0 && e == 0) lo = hi = 0xffffffffu;
+                const bool in = all || lo > Bk;
+                inm |= (uint32_t)in << e;
+                uncm |= (uint32_t)(!in && !(hi < A)) << e;
+            }
+        }
+    }
+    const int tot_in = (int)wave_sum_u32((uint32_t)__popc(inm));
+    const int tot_unc = (int)wave_sum_u32((uint32_t)__popc(uncm));
     int need = k - tot_in;  // 0 <= need <= tot_unc when the bound holds
     if (need < 0) need = 0;
     if (need > tot_unc) need = tot_unc;
@@ -653,14 +685,15 @@ __global__ __launch_bounds__(64 * kSelectWaveRows) void select_wave_kernel(
 
     // Compact the chosen tokens in index order: I ascending, r, and the slot map.
     uint32_t selm = inm;
-    {
+    if (!resolve) {
+        if (need == tot_unc) selm |= uncm;
+    } else {
         int base = 0;
 #pragma unroll
         for (int e = 0; e < EPL; ++e) {
             const bool unc = (uncm >> e) & 1u;
             const uint64_t ub = __ballot(unc);
-            if (unc && (resolve ? (usel[base + __popcll(ub & lanes_below())] > 0) : (need == tot_unc)))
-                selm |= 1u << e;
+            if (unc && usel[base + __popcll(ub & lanes_below())] > 0) selm |= 1u << e;
             base += __popcll(ub);
         }
     }
