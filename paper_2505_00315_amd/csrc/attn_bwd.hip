@@ -629,16 +629,6 @@ __device__ __forceinline__ void attn_bwd_q_tiled_body(unsigned char* smem, int b
         const int32_t *__restrict__ rI, const float2 *__restrict__ rtab
 #define MOSA_BWD_TILED_ARGS QKV, dA, lse, D, BH, n, causal, lb, scale, dQKV, rI, rtab
 
-template <typename ST, int DH, bool WIN, int NWV, int CB>
-__global__ __launch_bounds__(64 * NWV) void attn_bwd_kv_tiled_kernel(MOSA_BWD_TILED_PARAMS) {
-    __shared__ __attribute__((aligned(16))) unsigned char smem[BwdTile<ST, DH>::kv_lds(16 * CB * NWV)];
-    attn_bwd_kv_tiled_body<ST, DH, WIN, NWV, CB>(smem, blockIdx.x, MOSA_BWD_TILED_ARGS);
-}
-template <typename ST, int DH, bool WIN, int NWV, int CB>
-__global__ __launch_bounds__(64 * NWV) void attn_bwd_q_tiled_kernel(MOSA_BWD_TILED_PARAMS) {
-    __shared__ __attribute__((aligned(16))) unsigned char smem[BwdTile<ST, DH>::q_lds(16 * CB * NWV)];
-    attn_bwd_q_tiled_body<ST, DH, WIN, NWV, CB>(smem, blockIdx.x, MOSA_BWD_TILED_ARGS);
-}
 // Both passes in one launch (they are independent): blocks of even rank take
 // the dK, dV pass, odd ranks the dQ pass, each in its longest-first order, so
 // the short blocks of one pass fill the CUs beside the long blocks of the
@@ -1052,24 +1042,23 @@ int launch_t(const ST* QKV, const ST* dA, const float* lse, const float* D, int 
         // every CU two workgroups (4 dense heads, B = 8, T = 1024: 44 -> 39.5 us); one
         // otherwise (measured slower with two: n = 512 MoSA heads, local
         // windows, a single head of T = 8192 that fills half the chip).
-#define MOSA_ATTN_BWD_T(KERN, DHV, CBV)                                                                \
+        if (pass != 2) return -1;  // both passes are one launch here
+#define MOSA_ATTN_BWD_T(DHV, CBV)                                                                      \
     do {                                                                                                \
         constexpr int NWV = 4, CB = CBV, OB = 16 * CB * NWV;                                            \
-        auto kern = window > 0 ? KERN<ST, DHV, true, NWV, CB> : KERN<ST, DHV, false, NWV, CB>;          \
-        const dim3 grid((pass == 2 ? 2 : 1) * BH * ((n + OB - 1) / OB)), block(64 * NWV);               \
+        auto kern = window > 0 ? attn_bwd_tiled_both_kernel<ST, DHV, true, NWV, CB>                     \
+                               : attn_bwd_tiled_both_kernel<ST, DHV, false, NWV, CB>;                   \
+        const dim3 grid(2 * BH * ((n + OB - 1) / OB)), block(64 * NWV);                                 \
         hipLaunchKernelGGL(kern, grid, block, 0, stream, QKV, dA, lse, D, BH, n, causal, lb, scale, dQKV, rI, rtab); \
     } while (0)
-#define MOSA_ATTN_BWD_TD(KERN, CBV)                                                                    \
+#define MOSA_ATTN_BWD_TD(CBV)                                                                          \
     do {                                                                                                \
-        if (dh == 64) MOSA_ATTN_BWD_T(KERN, 64, CBV);                                                   \
-        else MOSA_ATTN_BWD_T(KERN, 32, CBV);                                                            \
+        if (dh == 64) MOSA_ATTN_BWD_T(64, CBV);                                                         \
+        else MOSA_ATTN_BWD_T(32, CBV);                                                                  \
     } while (0)
         const bool wide = window == 0 && n >= 1024 && 2LL * BH * ((n + 127) / 128) >= 512;
-        if (pass == 2) {
-            if (wide) MOSA_ATTN_BWD_TD(attn_bwd_tiled_both_kernel, 2);
-            else MOSA_ATTN_BWD_TD(attn_bwd_tiled_both_kernel, 1);
-        } else if (pass == 0) MOSA_ATTN_BWD_TD(attn_bwd_kv_tiled_kernel, 1);
-        else MOSA_ATTN_BWD_TD(attn_bwd_q_tiled_kernel, 1);
+        if (wide) MOSA_ATTN_BWD_TD(2);
+        else MOSA_ATTN_BWD_TD(1);
 #undef MOSA_ATTN_BWD_TD
 #undef MOSA_ATTN_BWD_T
         return hipGetLastError() == hipSuccess ? 0 : -1;
