@@ -5,7 +5,8 @@ every run), each checked forward (I bit-exact, r and Y within the bar) and
 backward (dX and every weight gradient) against the oracle.  The draws cover
 combinations the hand-written cases do not pair up, and every launch path the
 shapes select (one-wave, LDS and tiled attention backward, fused or tiled
-forward attention, the per-head and grouped weight-gradient kernels).
+forward attention, the per-head and grouped weight-gradient kernels, the
+workgroup and the one-wave selection).
 
 With very few selected rows per head (B k < 8) the MoSA heads' weight
 gradients are held to the per-tensor bar only: under causal masking the first
@@ -75,8 +76,26 @@ def _draw_medium(rng, i):
                     dtype="bf16", seed=2000 + i, **v)
 
 
+def _draw_many_rows(rng, i):
+    """2048 or more (b, h) rows of T <= 512: the one-wave selection, with
+    every option it handles drawn at random."""
+    heads = int(rng.choice([256, 512]))
+    batch = int(rng.integers(2048 // heads, 2048 // heads + 3))
+    T = int(rng.integers(40, 513))
+    k = int(min(T, rng.choice([rng.integers(1, 17), rng.integers(17, 65), T])))
+    v = {}
+    if rng.random() < 0.3:
+        v["rope"] = True
+    if rng.random() < 0.3 and k > 1:
+        v["first_token"] = True
+    return wl.small(name=f"rows{i}", batch=batch, seq_len=T, d_model=64, heads=heads, d_head=32, k=k,
+                    causal=bool(rng.random() < 0.8), dtype="f32" if rng.random() < 0.2 else "bf16",
+                    seed=3000 + i, **v)
+
+
 _RNG = np.random.default_rng(2505)
-CASES = [_draw(_RNG, i) for i in range(N_CASES)] + [_draw_medium(_RNG, i) for i in range(8)]
+CASES = ([_draw(_RNG, i) for i in range(N_CASES)] + [_draw_medium(_RNG, i) for i in range(8)]
+         + [_draw_many_rows(_RNG, i) for i in range(4)])
 
 
 @pytest.mark.parametrize("w", CASES, ids=[c.name for c in CASES])
