@@ -46,10 +46,11 @@ int launch_rope_table(int T, int dh, float base, float2* tab, hipStream_t stream
 
 // QKV[b,h,i,:] = X[b, I[b,h,i], :] . [Wq | Wk | Wv][h]  (packed rows of 3*dh)
 // for i < n (I == nullptr: identity, i.e. a dense head with n = T); with a
-// rotary table, q and k rotated at position I[b,h,i] (or i).
+// rotary table, q and k rotated at position I[b,h,i] (or i).  narrow: tiles
+// of 64 rows instead of 128 (bf16).
 int launch_qkv(int dtype, const void* X, const int32_t* I, const void* Wq, const void* Wk,
                const void* Wv, int B, int T, int d, int H, int dh, int n, void* QKV, const float2* rope,
-               hipStream_t stream);
+               int narrow, hipStream_t stream);
 
 // A = diag(r) softmax(Q K^T / sqrt(dh) + causal mask in slot order) V per
 // (b,h) (r == nullptr: r = 1); lse = log-sum-exp of the scaled scores

@@ -260,10 +260,12 @@ struct QkvAttnPolicy : QkvPolicy2<DH, MT_> {
 
 template <typename ST, int DH>
 int run(const ST* X, const int32_t* I, const ST* Wq, const ST* Wk, const ST* Wv, int B, int T, int d, int H, int n,
-        ST* out, const float2* rope, hipStream_t stream) {
+        ST* out, const float2* rope, int narrow, hipStream_t stream) {
     using P = QkvPolicy<ST, DH>;
     typename P::Args a{X, I, Wq, Wk, Wv, out, T, d, H, n, B * n, (B * n + P::MT - 1) / P::MT, rope};
     if constexpr (sizeof(ST) == 2) {
+        using N2 = QkvPolicy2<DH, 64>;
+        if (narrow && d % N2::KC == 0) return launch_gemm2<N2>(a, N2::mtiles(B * n) * H, stream);
         if (d % QkvPolicy2<DH>::KC == 0) return launch_gemm2<QkvPolicy2<DH>>(a, QkvPolicy2<DH>::mtiles(B * n) * H, stream);
     }
     return launch_gemm<ST, P>(a, a.mtiles * H, stream);
@@ -301,15 +303,15 @@ int launch_qkv_attn(int dtype, const void* X, const int32_t* I, const void* Wq, 
 }
 
 int launch_qkv(int dtype, const void* X, const int32_t* I, const void* Wq, const void* Wk, const void* Wv, int B,
-               int T, int d, int H, int dh, int n, void* QKV, const float2* rope, hipStream_t stream) {
+               int T, int d, int H, int dh, int n, void* QKV, const float2* rope, int narrow, hipStream_t stream) {
     if (dtype == kBF16) {
         auto f = dh == 64 ? run<uint16_t, 64> : run<uint16_t, 32>;
         return f((const uint16_t*)X, I, (const uint16_t*)Wq, (const uint16_t*)Wk, (const uint16_t*)Wv, B, T, d, H, n,
-                 (uint16_t*)QKV, rope, stream);
+                 (uint16_t*)QKV, rope, narrow, stream);
     }
     auto f = dh == 64 ? run<float, 64> : run<float, 32>;
     return f((const float*)X, I, (const float*)Wq, (const float*)Wk, (const float*)Wv, B, T, d, H, n, (float*)QKV,
-             rope, stream);
+             rope, 0, stream);
 }
 
 }  // namespace mosa
